@@ -1,0 +1,172 @@
+"""CPU oracle for the prefix-cache-aware router -- TEST INFRASTRUCTURE ONLY.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package.  The product library never calls it and
+shares no code with it.
+
+The oracle computes the plain definition of the paper's routing rule
+(System Design; Algorithm 1): for every peer p, m[q][p] is the longest common
+prefix of q with any sequence inserted into p's tree, and the chosen peer is the
+lowest id attaining the maximum.  See ``prefix_oracle.c``.
+
+Every function here is pinned by ``tests/test_oracle_pins.py`` against
+independent formulations (hand-worked examples, the prefix-set definition of a
+trie, numpy brute force, invariants the paper states).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import Optional, Sequence, Tuple
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "prefix_oracle.c")
+LIB_PATH = os.path.join(_HERE, "liboracle.so")
+
+_i32p = ctypes.POINTER(ctypes.c_int32)
+_i64p = ctypes.POINTER(ctypes.c_int64)
+
+
+def build(plant: Optional[str] = None, out: Optional[str] = None) -> str:
+    """Compile the oracle with gcc.  ``plant`` names a deliberate mistake
+    (PLANT_* macro) for the tests that check the pins catch it."""
+    out = out or (LIB_PATH if plant is None else os.path.join(_HERE, f"liboracle_{plant.lower()}.so"))
+    cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-pthread", _SRC, "-o", out + ".tmp"]
+    if plant:
+        cmd.insert(1, f"-D{plant}")
+    subprocess.run(cmd, check=True)
+    os.replace(out + ".tmp", out)
+    return out
+
+
+def _load(path: str) -> ctypes.CDLL:
+    lib = ctypes.CDLL(path)
+    lib.or_create.restype = ctypes.c_void_p
+    lib.or_create.argtypes = [ctypes.c_int32]
+    lib.or_destroy.restype = None
+    lib.or_destroy.argtypes = [ctypes.c_void_p]
+    lib.or_load.restype = ctypes.c_int
+    lib.or_load.argtypes = [ctypes.c_void_p, ctypes.c_int32, _i32p, _i64p, ctypes.c_int64]
+    lib.or_merge.restype = ctypes.c_int
+    lib.or_merge.argtypes = [ctypes.c_void_p, _i32p, _i32p, _i64p, ctypes.c_int64]
+    lib.or_route.restype = ctypes.c_int
+    lib.or_route.argtypes = [ctypes.c_void_p, _i32p, _i64p, ctypes.c_int64, _i32p, _i32p, ctypes.c_int32]
+    lib.or_lcp.restype = ctypes.c_int64
+    lib.or_lcp.argtypes = [_i32p, ctypes.c_int64, _i32p, ctypes.c_int64]
+    lib.or_prefix_match.restype = ctypes.c_int64
+    lib.or_prefix_match.argtypes = [ctypes.c_void_p, ctypes.c_int32, _i32p, ctypes.c_int64]
+    lib.or_set_size.restype = ctypes.c_int64
+    lib.or_set_size.argtypes = [ctypes.c_void_p, ctypes.c_int32]
+    return lib
+
+
+_LIBS = {}
+
+
+def lib(path: Optional[str] = None) -> ctypes.CDLL:
+    path = path or LIB_PATH
+    if path not in _LIBS:
+        if not os.path.exists(path):
+            if path == LIB_PATH:
+                build()
+            else:
+                raise FileNotFoundError(path)
+        _LIBS[path] = _load(path)
+    return _LIBS[path]
+
+
+def _p32(a: np.ndarray):
+    return a.ctypes.data_as(_i32p)
+
+
+def _p64(a: np.ndarray):
+    return a.ctypes.data_as(_i64p)
+
+
+def _csr(tokens, offsets) -> Tuple[np.ndarray, np.ndarray]:
+    t = np.ascontiguousarray(tokens, dtype=np.int32)
+    o = np.ascontiguousarray(offsets, dtype=np.int64)
+    if t.size == 0:
+        t = np.zeros(1, np.int32)  # valid pointer for empty batches
+    return t, o
+
+
+class Oracle:
+    """Per-peer multisets S_p with load (replace), merge (insert) and route."""
+
+    def __init__(self, num_peers: int, lib_path: Optional[str] = None):
+        self._lib = lib(lib_path)
+        self.num_peers = int(num_peers)
+        self._h = self._lib.or_create(self.num_peers)
+        if not self._h:
+            raise ValueError("or_create failed")
+
+    def close(self):
+        if self._h:
+            self._lib.or_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def load(self, peer: int, tokens, offsets) -> None:
+        t, o = _csr(tokens, offsets)
+        r = self._lib.or_load(self._h, int(peer), _p32(t), _p64(o), o.shape[0] - 1)
+        if r:
+            raise ValueError(f"or_load failed ({r})")
+
+    def load_seqset(self, ss) -> None:
+        """Load every peer's snapshot from a peer-major SeqSet."""
+        for p in range(self.num_peers):
+            lo, hi = ss.peer_range(p)
+            o = ss.offsets[lo:hi + 1] - ss.offsets[lo]
+            self.load(p, ss.tokens[ss.offsets[lo]:ss.offsets[hi]], o)
+
+    def merge(self, peer_of, tokens, offsets) -> None:
+        t, o = _csr(tokens, offsets)
+        po = np.ascontiguousarray(peer_of, dtype=np.int32)
+        if po.size == 0:
+            po = np.zeros(1, np.int32)
+        r = self._lib.or_merge(self._h, _p32(po), _p32(t), _p64(o), o.shape[0] - 1)
+        if r:
+            raise ValueError(f"or_merge failed ({r})")
+
+    def route(self, tokens, offsets, nthreads: int = 0) -> Tuple[np.ndarray, np.ndarray]:
+        t, o = _csr(tokens, offsets)
+        nq = o.shape[0] - 1
+        m = np.zeros((max(nq, 1), self.num_peers), dtype=np.int32)
+        c = np.zeros(max(nq, 1), dtype=np.int32)
+        nt = nthreads or (os.cpu_count() or 1)
+        r = self._lib.or_route(self._h, _p32(t), _p64(o), nq, _p32(m), _p32(c), nt)
+        if r:
+            raise ValueError(f"or_route failed ({r})")
+        return m[:nq], c[:nq]
+
+    def route_seqset(self, qs, idx: Optional[Sequence[int]] = None, nthreads: int = 0):
+        """Route all queries of a SeqSet, or only the sampled indices ``idx``."""
+        if idx is None:
+            return self.route(qs.tokens, qs.offsets, nthreads)
+        sub = qs.subset(np.asarray(idx))
+        return self.route(sub.tokens, sub.offsets, nthreads)
+
+    def prefix_match(self, peer: int, q) -> int:
+        qa = np.ascontiguousarray(q, dtype=np.int32)
+        if qa.size == 0:
+            return int(self._lib.or_prefix_match(self._h, int(peer), _p32(np.zeros(1, np.int32)), 0))
+        return int(self._lib.or_prefix_match(self._h, int(peer), _p32(qa), qa.shape[0]))
+
+    def set_size(self, peer: int) -> int:
+        return int(self._lib.or_set_size(self._h, int(peer)))
+
+    def lcp(self, a, b) -> int:
+        a = np.ascontiguousarray(a, dtype=np.int32)
+        b = np.ascontiguousarray(b, dtype=np.int32)
+        pa = _p32(a if a.size else np.zeros(1, np.int32))
+        pb = _p32(b if b.size else np.zeros(1, np.int32))
+        return int(self._lib.or_lcp(pa, a.shape[0], pb, b.shape[0]))

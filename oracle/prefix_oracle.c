@@ -1,0 +1,221 @@
+/*
+ * prefix_oracle.c -- CPU oracle for the prefix-cache-aware router.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product library links, calls or
+ * includes this file; only the tests, the smoke check and the benchmark's CPU
+ * baseline leg use it.  It shares no code, header or table with the device
+ * path.
+ *
+ * What it computes is the plain definition behind the paper's routing rule
+ * (System Design: every node keeps one prefix tree per node and sends a request
+ * to the node whose tree has the largest prefix match; Algorithm 1, the argmax
+ * of PrefixMatch over all N trees including the node's own):
+ *
+ *   S_p        the multiset of token sequences inserted into peer p's tree:
+ *              the last full snapshot loaded for p (a snapshot replaces the
+ *              estimate, Section "Trie-broadcast loss") plus every sequence
+ *              merged into p since (updateTrie / updateTrieEstimate).
+ *   LCP(a, b)  length of the longest common prefix of two token sequences.
+ *   m[q][p]    = max over s in S_p of LCP(q, s)        (0 when S_p is empty).
+ *              A radix tree over S_p holds exactly the prefixes of its members
+ *              as root paths, so this is the tree's longest prefix match.
+ *   chosen[q]  = the smallest p with m[q][p] = max_j m[q][j]  (ties go to the
+ *              lowest peer id; the paper leaves the tie rule open).
+ *
+ * It is deliberately a linear scan over every stored sequence: slow, and
+ * checkable by eye.  Threads only split the query list into contiguous ranges.
+ */
+#include <pthread.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+typedef struct {
+    int64_t n, cap;
+    int32_t **seq;
+    int64_t *len;
+} or_set;
+
+typedef struct {
+    int32_t num_peers;
+    or_set *sets;
+} or_forest;
+
+/* ---- the definition ---------------------------------------------------- */
+
+/* Length of the longest common prefix of a[0..na) and b[0..nb). */
+int64_t or_lcp(const int32_t *a, int64_t na, const int32_t *b, int64_t nb) {
+    int64_t n = na < nb ? na : nb;
+    int64_t i = 0;
+#ifdef PLANT_LCP_OFF_BY_ONE
+    while (i < n && a[i] == b[i]) i++;
+    return i > 0 ? i - 1 : 0;
+#else
+    while (i < n && a[i] == b[i]) i++;
+    return i;
+#endif
+}
+
+/* PrefixMatch(q, T_p): the longest prefix of q shared with any s in S_p. */
+int64_t or_prefix_match(const or_forest *f, int32_t peer, const int32_t *q, int64_t qlen) {
+    const or_set *s = &f->sets[peer];
+    int64_t best = 0;
+    for (int64_t i = 0; i < s->n; i++) {
+        int64_t l = or_lcp(q, qlen, s->seq[i], s->len[i]);
+#ifdef PLANT_MIN_NOT_MAX
+        if (i == 0 || l < best) best = l;
+#else
+        if (l > best) best = l;
+#endif
+    }
+    return best;
+}
+
+/* getBestNode: argmax over peers, lowest id among equal maxima. */
+static int32_t argmax_lowest(const int32_t *m, int32_t P) {
+    int32_t best = 0;
+    for (int32_t p = 1; p < P; p++) {
+#ifdef PLANT_TIE_HIGHEST
+        if (m[p] >= m[best]) best = p;
+#else
+        if (m[p] > m[best]) best = p;
+#endif
+    }
+    return best;
+}
+
+/* ---- sets --------------------------------------------------------------- */
+
+or_forest *or_create(int32_t num_peers) {
+    if (num_peers <= 0) return NULL;
+    or_forest *f = (or_forest *)calloc(1, sizeof(or_forest));
+    if (!f) return NULL;
+    f->num_peers = num_peers;
+    f->sets = (or_set *)calloc((size_t)num_peers, sizeof(or_set));
+    if (!f->sets) { free(f); return NULL; }
+    return f;
+}
+
+static void set_clear(or_set *s) {
+    for (int64_t i = 0; i < s->n; i++) free(s->seq[i]);
+    free(s->seq);
+    free(s->len);
+    memset(s, 0, sizeof(*s));
+}
+
+void or_destroy(or_forest *f) {
+    if (!f) return;
+    for (int32_t p = 0; p < f->num_peers; p++) set_clear(&f->sets[p]);
+    free(f->sets);
+    free(f);
+}
+
+static int set_add(or_set *s, const int32_t *tok, int64_t len) {
+    if (s->n == s->cap) {
+        int64_t nc = s->cap ? 2 * s->cap : 16;
+        int32_t **ns = (int32_t **)realloc(s->seq, (size_t)nc * sizeof(int32_t *));
+        if (!ns) return -2;
+        s->seq = ns;
+        int64_t *nl = (int64_t *)realloc(s->len, (size_t)nc * sizeof(int64_t));
+        if (!nl) return -2;
+        s->len = nl;
+        s->cap = nc;
+    }
+    int32_t *c = (int32_t *)malloc((size_t)(len > 0 ? len : 1) * sizeof(int32_t));
+    if (!c) return -2;
+    if (len > 0) memcpy(c, tok, (size_t)len * sizeof(int32_t));
+    s->seq[s->n] = c;
+    s->len[s->n] = len;
+    s->n++;
+    return 0;
+}
+
+static int check_csr(const int64_t *offsets, int64_t n) {
+    if (n < 0 || !offsets || offsets[0] != 0) return -1;
+    for (int64_t i = 0; i < n; i++)
+        if (offsets[i + 1] < offsets[i]) return -1;
+    return 0;
+}
+
+/* sendTrie receive: the snapshot REPLACES peer's set. */
+int or_load(or_forest *f, int32_t peer, const int32_t *tokens, const int64_t *offsets, int64_t n) {
+    if (!f || peer < 0 || peer >= f->num_peers || check_csr(offsets, n)) return -1;
+#ifndef PLANT_LOAD_APPENDS
+    set_clear(&f->sets[peer]);
+#endif
+    for (int64_t i = 0; i < n; i++) {
+        int r = set_add(&f->sets[peer], tokens + offsets[i], offsets[i + 1] - offsets[i]);
+        if (r) return r;
+    }
+    return 0;
+}
+
+/* updateTrie / updateTrieEstimate: insert sequence i into peer_of[i]'s set. */
+int or_merge(or_forest *f, const int32_t *peer_of, const int32_t *tokens, const int64_t *offsets, int64_t n) {
+    if (!f || check_csr(offsets, n)) return -1;
+    for (int64_t i = 0; i < n; i++)
+        if (peer_of[i] < 0 || peer_of[i] >= f->num_peers) return -1;
+    for (int64_t i = 0; i < n; i++) {
+        int32_t p = peer_of[i];
+#ifdef PLANT_MERGE_WRONG_PEER
+        p = (p + 1) % f->num_peers;
+#endif
+        int r = set_add(&f->sets[p], tokens + offsets[i], offsets[i + 1] - offsets[i]);
+        if (r) return r;
+    }
+    return 0;
+}
+
+int64_t or_set_size(const or_forest *f, int32_t peer) {
+    if (!f || peer < 0 || peer >= f->num_peers) return -1;
+    return f->sets[peer].n;
+}
+
+/* ---- batched route ------------------------------------------------------ */
+
+typedef struct {
+    const or_forest *f;
+    const int32_t *qt;
+    const int64_t *qo;
+    int64_t lo, hi;
+    int32_t *match_len, *chosen;
+} route_job;
+
+static void *route_range(void *arg) {
+    route_job *j = (route_job *)arg;
+    int32_t P = j->f->num_peers;
+    for (int64_t q = j->lo; q < j->hi; q++) {
+        const int32_t *qs = j->qt + j->qo[q];
+        int64_t ql = j->qo[q + 1] - j->qo[q];
+        int32_t *row = j->match_len + q * (int64_t)P;
+        for (int32_t p = 0; p < P; p++) row[p] = (int32_t)or_prefix_match(j->f, p, qs, ql);
+        j->chosen[q] = argmax_lowest(row, P);
+    }
+    return NULL;
+}
+
+/* Route queries [0, nq): match_len is [nq][P] row-major, chosen is [nq]. */
+int or_route(const or_forest *f, const int32_t *q_tokens, const int64_t *q_offsets, int64_t nq,
+             int32_t *match_len, int32_t *chosen, int32_t nthreads) {
+    if (!f || check_csr(q_offsets, nq)) return -1;
+    if (nthreads < 1) nthreads = 1;
+    if (nthreads > nq) nthreads = nq > 0 ? (int32_t)nq : 1;
+    route_job *jobs = (route_job *)calloc((size_t)nthreads, sizeof(route_job));
+    pthread_t *th = (pthread_t *)calloc((size_t)nthreads, sizeof(pthread_t));
+    if (!jobs || !th) { free(jobs); free(th); return -2; }
+    for (int32_t t = 0; t < nthreads; t++) {
+        jobs[t].f = f;
+        jobs[t].qt = q_tokens;
+        jobs[t].qo = q_offsets;
+        jobs[t].lo = nq * t / nthreads;
+        jobs[t].hi = nq * (t + 1) / nthreads;
+        jobs[t].match_len = match_len;
+        jobs[t].chosen = chosen;
+    }
+    for (int32_t t = 1; t < nthreads; t++) pthread_create(&th[t], NULL, route_range, &jobs[t]);
+    route_range(&jobs[0]);
+    for (int32_t t = 1; t < nthreads; t++) pthread_join(th[t], NULL);
+    free(jobs);
+    free(th);
+    return 0;
+}

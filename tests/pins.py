@@ -1,0 +1,271 @@
+"""Pins for the CPU oracle: independent ways to know the right answer.
+
+Each check takes a factory ``make(num_peers) -> oracle-like object`` (with
+load / merge / route) and returns a list of failure strings, so the same checks
+run against the real oracle and against builds with a planted mistake.
+
+* hand-worked examples (tests/golden/hand_examples.txt, derived by hand from the
+  paper's definitions: System Design, Algorithm 1, "Trie-broadcast loss");
+* the prefix-set formulation of a trie: a tree over S holds exactly the
+  prefixes of S's members, so m = the largest k with q[:k] among them;
+* numpy brute force of max_s LCP(q, s) by padded-matrix comparison;
+* numpy's argmax, which returns the first (lowest-index) maximum;
+* invariants: m <= |q|; a cached prompt used as a query matches its owner in
+  full; merging never lowers a match and yields the union's match; set
+  semantics under permutation / duplication / repeated loads (a snapshot is a
+  complete state, so applying it twice is applying it once).
+"""
+from __future__ import annotations
+
+import os
+import re
+from dataclasses import dataclass, field
+from typing import Callable, List, Sequence, Tuple
+
+import numpy as np
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "hand_examples.txt")
+
+
+# --------------------------------------------------------------------------
+# golden examples
+# --------------------------------------------------------------------------
+@dataclass
+class Example:
+    name: str
+    peers: int = 0
+    ops: List[Tuple] = field(default_factory=list)  # ("load", p, seqs) | ("merge", [(p, seq)]) | ("query", q, m, c)
+
+
+def _toks(s: str) -> List[int]:
+    s = s.strip()
+    if s == "[]":
+        return []
+    return [int(x) for x in s.split()] if s else []
+
+
+def parse_golden(path: str = GOLDEN) -> List[Example]:
+    exs: List[Example] = []
+    cur = None
+    for raw in open(path):
+        line = raw.strip()
+        if not line or line.startswith("#"):
+            continue
+        kw, _, rest = line.partition(" ")
+        if kw == "example":
+            cur = Example(rest.strip())
+            exs.append(cur)
+        elif kw == "peers":
+            cur.peers = int(rest)
+        elif kw == "load":
+            p, _, seqs = rest.partition("|")
+            items = [x for x in seqs.split(";")] if seqs.strip() else []
+            cur.ops.append(("load", int(p), [_toks(x) for x in items]))
+        elif kw == "merge":
+            items = []
+            for it in rest.split(";"):
+                p, _, s = it.partition(":")
+                items.append((int(p), _toks(s)))
+            cur.ops.append(("merge", items))
+        elif kw == "query":
+            q, _, res = rest.partition("->") if rest.strip() != "" else ("", "", "")
+            if line.startswith("query ->"):
+                q, res = "", line[len("query ->"):]
+            ms, _, c = res.partition(";")
+            cur.ops.append(("query", _toks(q), [int(x) for x in ms.split()], int(c)))
+        else:
+            raise ValueError(f"bad golden line: {line}")
+    return exs
+
+
+def _csr(seqs: Sequence[Sequence[int]]):
+    offs = np.zeros(len(seqs) + 1, dtype=np.int64)
+    if seqs:
+        np.cumsum([len(s) for s in seqs], out=offs[1:])
+    toks = np.array([t for s in seqs for t in s], dtype=np.int32)
+    return toks, offs
+
+
+def check_golden(make: Callable) -> List[str]:
+    fails = []
+    for ex in parse_golden():
+        o = make(ex.peers)
+        for op in ex.ops:
+            if op[0] == "load":
+                t, off = _csr(op[2])
+                o.load(op[1], t, off)
+            elif op[0] == "merge":
+                t, off = _csr([s for _, s in op[1]])
+                o.merge(np.array([p for p, _ in op[1]], np.int32), t, off)
+            else:
+                _, q, m_exp, c_exp = op
+                t, off = _csr([q])
+                m, c = o.route(t, off, 1)
+                if list(m[0]) != m_exp or int(c[0]) != c_exp:
+                    fails.append(f"{ex.name}: q={q} got m={list(m[0])} c={int(c[0])}, want m={m_exp} c={c_exp}")
+    return fails
+
+
+# --------------------------------------------------------------------------
+# independent formulations
+# --------------------------------------------------------------------------
+def prefix_set_match(seqs: Sequence[np.ndarray], q: np.ndarray) -> int:
+    """Largest k such that q[:k] is a prefix of some stored sequence."""
+    prefixes = set()
+    for s in seqs:
+        s = tuple(int(x) for x in s)
+        for k in range(len(s) + 1):
+            prefixes.add(s[:k])
+    if not prefixes:
+        return 0
+    qt = tuple(int(x) for x in q)
+    best = 0
+    for k in range(len(qt) + 1):
+        if qt[:k] in prefixes:
+            best = k
+    return best
+
+
+def numpy_lcp_match(seqs: Sequence[np.ndarray], q: np.ndarray) -> int:
+    """max over s of LCP(q, s) with a padded matrix compare (no loops over tokens)."""
+    if len(seqs) == 0:
+        return 0
+    L = max([len(s) for s in seqs] + [len(q)])
+    if L == 0:
+        return 0
+    M = np.zeros((len(seqs), L), dtype=np.int64)
+    valid = np.zeros((len(seqs), L), dtype=bool)
+    for i, s in enumerate(seqs):
+        M[i, :len(s)] = s
+        valid[i, :len(s)] = True
+    qq = np.zeros(L, dtype=np.int64)
+    qv = np.zeros(L, dtype=bool)
+    qq[:len(q)] = q
+    qv[:len(q)] = True
+    eq = (M == qq[None, :]) & valid & qv[None, :]
+    # first False per row (or L if none) = LCP
+    notq = ~eq
+    first = np.where(notq.any(axis=1), notq.argmax(axis=1), L)
+    return int(first.max())
+
+
+def reference_matrix(peer_sets: List[List[np.ndarray]], queries: List[np.ndarray], fn=numpy_lcp_match):
+    m = np.array([[fn(S, q) for S in peer_sets] for q in queries], dtype=np.int64)
+    if m.size == 0:
+        return m.reshape(len(queries), len(peer_sets)), np.zeros(len(queries), np.int64)
+    return m, np.argmax(m, axis=1)
+
+
+def _peer_lists(w) -> List[List[np.ndarray]]:
+    out = []
+    for p in range(w.num_peers):
+        lo, hi = w.snapshot.peer_range(p)
+        out.append([w.snapshot.seq(i) for i in range(lo, hi)])
+    return out
+
+
+def load_all(o, ss, num_peers):
+    for p in range(num_peers):
+        lo, hi = ss.peer_range(p)
+        o.load(p, ss.tokens[ss.offsets[lo]:ss.offsets[hi]], ss.offsets[lo:hi + 1] - ss.offsets[lo])
+
+
+def check_tiny_random(make: Callable, seeds: Sequence[int], vocabs=(2, 3, 8)) -> List[str]:
+    import workloads as W
+    fails = []
+    for v in vocabs:
+        for sd in seeds:
+            w = W.tiny_random(sd, num_peers=2 + sd % 4, vocab=v, n_queries=40)
+            o = make(w.num_peers)
+            load_all(o, w.snapshot, w.num_peers)
+            m, c = o.route(w.queries.tokens, w.queries.offsets, 2)
+            sets = _peer_lists(w)
+            qs = [w.queries.seq(i) for i in range(len(w.queries))]
+            m_ps, c_ps = reference_matrix(sets, qs, prefix_set_match)
+            m_np, c_np = reference_matrix(sets, qs, numpy_lcp_match)
+            if not np.array_equal(m, m_ps) or not np.array_equal(m, m_np):
+                bad = np.nonzero((m != m_ps).any(axis=1))[0][:3]
+                fails.append(f"vocab={v} seed={sd}: match mismatch at queries {bad.tolist()}")
+            if not np.array_equal(c, c_np):
+                fails.append(f"vocab={v} seed={sd}: chosen differs from numpy argmax")
+    return fails
+
+
+def check_merge_semantics(make: Callable, seeds: Sequence[int]) -> List[str]:
+    """Merging a batch gives exactly max(before, batch alone); permuting or
+    duplicating the batch changes nothing; loading twice equals loading once."""
+    import workloads as W
+    fails = []
+    for sd in seeds:
+        base = W.tiny_random(sd, num_peers=3, vocab=3, n_queries=50)
+        extra = W.tiny_random(sd + 1000, num_peers=3, vocab=3, n_queries=1)
+        qt, qo = base.queries.tokens, base.queries.offsets
+        P = 3
+        a = make(P)
+        load_all(a, base.snapshot, P)
+        m0, _ = a.route(qt, qo, 1)
+        ins = extra.snapshot
+        a.merge(ins.peer, ins.tokens, ins.offsets)
+        m1, c1 = a.route(qt, qo, 1)
+        b = make(P)
+        load_all(b, ins, P)
+        mb, _ = b.route(qt, qo, 1)
+        if (m1 < m0).any():
+            fails.append(f"seed {sd}: merge lowered a match")
+        if not np.array_equal(m1, np.maximum(m0, mb)):
+            fails.append(f"seed {sd}: merge result != max(before, batch alone)")
+        # permuted + duplicated batch, and a doubled snapshot load
+        perm = np.random.default_rng(sd).permutation(len(ins))
+        dup = np.concatenate([perm, perm[: len(perm) // 2]])
+        sub = ins.subset(dup)
+        d = make(P)
+        load_all(d, base.snapshot, P)
+        load_all(d, base.snapshot, P)
+        d.merge(sub.peer, sub.tokens, sub.offsets)
+        m2, c2 = d.route(qt, qo, 1)
+        if not np.array_equal(m1, m2) or not np.array_equal(c1, c2):
+            fails.append(f"seed {sd}: order/duplicate/reload changed the result")
+    return fails
+
+
+def check_config_invariants(make: Callable, w, idx: np.ndarray, nthreads: int = 4) -> List[str]:
+    """Invariants and generator closed forms on a real configuration sample."""
+    fails = []
+    o = make(w.num_peers)
+    load_all(o, w.snapshot, w.num_peers)
+    sub = w.queries.subset(idx)
+    m, c = o.route(sub.tokens, sub.offsets, nthreads)
+    qlen = sub.lengths()
+    if (m > qlen[:, None]).any():
+        fails.append("m exceeds |q|")
+    if not np.array_equal(c, np.argmax(m, axis=1)):
+        fails.append("chosen != first argmax")
+    # closed forms of the generator: a peer caching the query's topic matches at
+    # least the whole shared head; a peer not caching it matches less than that;
+    # any peer with a cached prompt matches at least the system prefix.
+    meta = w.meta
+    head = meta["query_head"][idx]
+    hl = meta["head_len"][head]
+    cached = [set() for _ in range(w.num_peers)]
+    for t, p in zip(meta["cache_topic"].tolist(), w.snapshot.peer.tolist()):
+        cached[p].add(t)
+    for i in range(len(idx)):
+        for p in range(w.num_peers):
+            has = int(head[i]) in cached[p]
+            if has and m[i, p] < hl[i]:
+                fails.append(f"q{idx[i]} p{p}: caches the topic but m={m[i, p]} < {hl[i]}")
+            if not has and m[i, p] >= hl[i]:
+                fails.append(f"q{idx[i]} p{p}: lacks the topic but m={m[i, p]} >= {hl[i]}")
+            if cached[p] and m[i, p] < meta["sys_len"]:
+                fails.append(f"q{idx[i]} p{p}: below the system prefix")
+        if len(fails) > 5:
+            break
+    # a cached prompt used as a query matches its owner in full
+    rng = np.random.default_rng(7)
+    pick = rng.choice(len(w.snapshot), size=min(32, len(w.snapshot)), replace=False)
+    ps = w.snapshot.subset(pick)
+    mp, _ = o.route(ps.tokens, ps.offsets, nthreads)
+    own = w.snapshot.peer[pick]
+    if not np.array_equal(mp[np.arange(len(pick)), own], ps.lengths()):
+        fails.append("a cached prompt does not match its owner in full")
+    return fails

@@ -1,0 +1,105 @@
+"""The CPU oracle checked against things other than itself (runs without a GPU)."""
+import numpy as np
+import pytest
+
+import oracle
+import pins
+import workloads as W
+
+
+def make(P):
+    return oracle.Oracle(P)
+
+
+def test_golden_hand_examples():
+    assert pins.check_golden(make) == []
+
+
+def test_golden_file_is_nontrivial():
+    exs = pins.parse_golden()
+    assert len(exs) >= 5
+    nq = sum(1 for e in exs for op in e.ops if op[0] == "query")
+    assert nq >= 25
+    # the examples exercise a tie that is not at peer 0 and a merge
+    assert any(op[0] == "merge" for e in exs for op in e.ops)
+
+
+@pytest.mark.parametrize("vocab", [2, 3, 8])
+def test_tiny_random_vs_prefix_set_and_numpy(vocab):
+    assert pins.check_tiny_random(make, seeds=range(12), vocabs=(vocab,)) == []
+
+
+def test_merge_union_order_duplicates_reload():
+    assert pins.check_merge_semantics(make, seeds=range(8)) == []
+
+
+def test_config1_invariants_and_closed_forms():
+    w = W.make_config(1)
+    idx = np.arange(len(w.queries))
+    assert pins.check_config_invariants(make, w, idx) == []
+
+
+def test_config2_sample_invariants_and_closed_forms():
+    w = W.make_config(2, n_queries=512, prompts_per_peer=400)
+    idx = np.arange(0, 512, 4)
+    assert pins.check_config_invariants(make, w, idx) == []
+
+
+def test_config1_full_vs_numpy_bruteforce_sample():
+    """All of config 1's peers against numpy brute force on a query sample."""
+    w = W.make_config(1)
+    o = make(w.num_peers)
+    pins.load_all(o, w.snapshot, w.num_peers)
+    idx = np.arange(0, len(w.queries), 16)
+    sub = w.queries.subset(idx)
+    m, c = o.route(sub.tokens, sub.offsets, 4)
+    sets = pins._peer_lists(w)
+    m_np, c_np = pins.reference_matrix(sets, [sub.seq(i) for i in range(len(sub))])
+    assert np.array_equal(m, m_np)
+    assert np.array_equal(c, c_np)
+
+
+def test_stale_replicas_never_exceed_true_trees():
+    """Estimates hold a subset of each peer's inserts, so they never match more
+    (Section "Stale trie estimates": staleness can only cost cache hits)."""
+    w = W.make_config(3, n_queries=96, prompts_per_peer=60)
+    est, tru = make(w.num_peers), make(w.num_peers)
+    pins.load_all(est, w.snapshot, w.num_peers)
+    pins.load_all(tru, w.true_snapshot, w.num_peers)
+    me, _ = est.route(w.queries.tokens, w.queries.offsets, 4)
+    mt, _ = tru.route(w.queries.tokens, w.queries.offsets, 4)
+    assert (me <= mt).all()
+    assert np.array_equal(me[:, 0], mt[:, 0])  # observer 0's own tree is exact
+    assert (me < mt).any()  # the drops matter for some query
+
+
+def test_edge_cases():
+    o = make(3)
+    e = np.zeros(0, np.int32)
+    m, c = o.route(e, np.zeros(1, np.int64))  # no queries
+    assert m.shape == (0, 3) and c.shape == (0,)
+    m, c = o.route(e, np.zeros(2, np.int64))  # one empty query, empty forest
+    assert m.tolist() == [[0, 0, 0]] and c.tolist() == [0]
+    with pytest.raises(ValueError):
+        o.load(3, e, np.zeros(1, np.int64))  # bad peer
+    with pytest.raises(ValueError):
+        o.load(0, np.zeros(2, np.int32), np.array([0, 2, 1], np.int64))  # non-monotone
+    with pytest.raises(ValueError):
+        o.merge(np.array([-1], np.int32), np.zeros(1, np.int32), np.array([0, 1], np.int64))
+
+
+PLANTS = ["PLANT_LCP_OFF_BY_ONE", "PLANT_MIN_NOT_MAX", "PLANT_TIE_HIGHEST",
+          "PLANT_LOAD_APPENDS", "PLANT_MERGE_WRONG_PEER"]
+
+
+@pytest.mark.parametrize("plant", PLANTS)
+def test_planted_mistake_is_caught(plant, tmp_path):
+    """A plausible mistake planted in the oracle fails at least one pin."""
+    path = oracle.build(plant=plant, out=str(tmp_path / f"lib_{plant}.so"))
+
+    def mk(P):
+        return oracle.Oracle(P, lib_path=path)
+
+    fails = pins.check_golden(mk) + pins.check_tiny_random(mk, seeds=range(3), vocabs=(3,)) \
+        + pins.check_merge_semantics(mk, seeds=range(2))
+    assert fails, f"{plant} slipped through every pin"

@@ -1,0 +1,190 @@
+#!/usr/bin/env python3
+"""Throughput of the batched prefix-cache-aware router on one MI355X.
+
+One step = one pr_route over a full query batch of the workload: every query's
+longest-prefix match against every peer's tree plus the argmax over peers
+(walk, child locate, label compare, per-peer lengths, argmax, output write).
+Queries, offsets, outputs and the forest are resident in HBM before the timed
+region; two device copies of the query batch alternate so that the 256 MB
+last-level cache cannot serve the query stream from one step to the next.
+
+Prints one JSON line (rank 0 = the only rank).  Algorithmic bytes per query:
+  B_q = 4*min(|q|, M_q + 1) + 4*(P + 1) + 8
+(the query tokens a walk must read, including the mismatching one; the output
+row plus the chosen peer; the int64 query offset).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_HBM_GBPS = 8000.0  # MI355X HBM3E, AMD public specification
+
+WORKLOADS = {
+    1: "tiny: 4 peers x 200 prompts (64 sys + 16 topics x 256 + 32-128 suffix), 2,048 queries Zipf(1.0), 10% unseen",
+    2: "medium: 16 peers x 2,000 prompts (128 sys + 64 topics x 1,024 + 64-256 suffix, 2 homes/topic), "
+       "65,536 queries Zipf(1.1), 5% unseen",
+    3: "stale: 64 peers x 4,000 prompts (256 sys + 512 tasks x 512-2,048 + suffix, <= 4,096 tokens), "
+       "observer-0 estimates with Bernoulli(0.2) drops of the last 1,000 inserts, 262,144 queries Zipf(1.2)",
+    4: "long: 32 peers x 500 prompts (256 prefixes x 8,192-32,768 + 128-1,024 suffix), 32,768 queries Zipf(1.0)",
+    5: "stream: 128 peers x 2,000 prompts (128 sys + 512 topics x 1,024 + 64-256 suffix), 1,048,576-query lookup batch",
+}
+
+
+def log(msg: str) -> None:
+    sys.stderr.write(msg + "\n")
+    sys.stderr.flush()
+
+
+def cpu_threads() -> int:
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
+
+
+def cpu_baseline(w, queries, target_s: float):
+    """Time the CPU oracle, as it stands, on a bounded sample of the same batch."""
+    import oracle
+    o = oracle.Oracle(w.num_peers)
+    ss = w.snapshot
+    for p in range(w.num_peers):
+        lo, hi = ss.peer_range(p)
+        o.load(p, ss.tokens[ss.offsets[lo]:ss.offsets[hi]], ss.offsets[lo:hi + 1] - ss.offsets[lo])
+    T = cpu_threads()
+    rng = np.random.default_rng(12345)
+    n = min(len(queries), 4 * T)
+    while True:
+        idx = np.sort(rng.choice(len(queries), n, replace=False))
+        sub = queries.subset(idx)
+        t0 = time.perf_counter()
+        o.route(sub.tokens, sub.offsets, T)
+        dt = time.perf_counter() - t0
+        if dt >= 0.25 * target_s or n >= len(queries):
+            break
+        n = int(min(len(queries), max(2 * n, n * target_s / max(dt, 1e-3))))
+    o.close()
+    return {"value": n / dt, "unit": "queries/s", "cores": T, "kind": "oracle",
+            "sample": f"{n} of {len(queries)} queries drawn uniformly (seed 12345), {dt:.1f} s with {T} threads"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=2, choices=sorted(WORKLOADS))
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU time of the oracle sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copies", type=int, default=2, help="device copies of the query batch to rotate")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        sys.stderr.write("bench.py: this build measures one GPU only; multi-GPU runs are not part of it "
+                         "(queries would shard across GPUs with the forest replicated)\n")
+        return 2
+
+    import torch
+
+    import workloads as W
+    from paper_2606_17059_amd import Forest
+
+    if not torch.cuda.is_available():
+        sys.stderr.write("bench.py needs a HIP device\n")
+        return 1
+    dev = torch.device("cuda:0")
+    t0 = time.perf_counter()
+    w = W.make_config(args.config)
+    queries = w.queries if args.config != 5 else w.phase("zipf", 0).queries
+    log(f"[bench] generated config {args.config} in {time.perf_counter() - t0:.1f} s: "
+        f"{len(w.snapshot)} cached prompts, {len(queries)} queries")
+
+    f = Forest(w.num_peers)
+    f.load_seqset(w.snapshot)
+    qt = [torch.from_numpy(queries.tokens).to(dev) for _ in range(max(1, args.copies))]
+    qo = [torch.from_numpy(queries.offsets).to(dev) for _ in range(max(1, args.copies))]
+    nq = len(queries)
+    P = w.num_peers
+    ml = torch.empty((nq, P), dtype=torch.int32, device=dev)
+    ch = torch.empty(nq, dtype=torch.int32, device=dev)
+    t0 = time.perf_counter()
+    f.route(qt[0], qo[0], ml, ch)  # first route builds and uploads the forest
+    torch.cuda.synchronize()
+    log(f"[bench] forest build + upload + first route {time.perf_counter() - t0:.2f} s; {f.info()}")
+
+    for i in range(args.warmup):
+        f.route(qt[i % len(qt)], qo[i % len(qo)], ml, ch)
+    torch.cuda.synchronize()
+
+    K = args.steps
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+    all0, all1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    all0.record()
+    for k in range(K):
+        ev[k][0].record()
+        f.route(qt[k % len(qt)], qo[k % len(qo)], ml, ch)
+        ev[k][1].record()
+    all1.record()
+    torch.cuda.synchronize()
+    total_ms = all0.elapsed_time(all1)
+    kern_ms = np.array([a.elapsed_time(b) for a, b in ev])
+    f.check()
+
+    m = ml.cpu().numpy()
+    M = m.max(axis=1).astype(np.int64)
+    qlen = queries.lengths()
+    needed = np.minimum(qlen, M + 1)
+    bytes_q = 4 * needed + 4 * (P + 1) + 8
+    total_bytes = float(bytes_q.sum())
+    avg_kernel_s = float(kern_ms.mean()) / 1e3
+    achieved = total_bytes / avg_kernel_s / 1e9
+    value = nq * K / (total_ms / 1e3)
+    log(f"[bench] per-launch ms: mean {kern_ms.mean():.4f} median {np.median(kern_ms):.4f} "
+        f"min {kern_ms.min():.4f} max {kern_ms.max():.4f}; algorithmic bytes/launch {total_bytes / 1e6:.1f} MB")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(w, queries, args.cpu_seconds)
+        log(f"[bench] cpu baseline: {cpu}")
+
+    out = {
+        "metric": "routed queries/sec (batched LPM over all peer trees) + achieved HBM GB/s",
+        "value": value,
+        "unit": "queries/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": total_ms / K,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int32",
+        "data": "synthetic",
+        "config": {"workload": WORKLOADS[args.config], "config_index": args.config, "peers": P,
+                   "queries_per_step": nq, "query_tokens": int(qlen.sum()), "parallelism": "single GPU"},
+        "hbm_gbps": achieved,
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                     "frac": achieved / PEAK_HBM_GBPS, "traffic": None,
+                     "kernel": "route_kernel", "kernel_ms": float(kern_ms.mean()),
+                     "algorithmic_bytes_per_launch": total_bytes},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+    f.close()
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

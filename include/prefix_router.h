@@ -1,0 +1,175 @@
+/*
+ * prefix_router.h -- C ABI of the MI355X (gfx950) prefix-cache-aware router.
+ *
+ * The library keeps, on one GPU, a node's view of every peer's prefix cache:
+ * its own exact radix tree plus one read-only estimate per other peer
+ * (paper, System Design).  It answers getBestNode for a whole batch of
+ * requests at once (Algorithm 1, the argmax of PrefixMatch over all N trees),
+ * and applies the tree updates the paper names: full-snapshot replacement
+ * (sendTrie received; Section "Trie-broadcast loss") and per-request inserts
+ * (updateTrie / updateTrieEstimate).
+ *
+ * Conventions shared by every call
+ *   - Status: every call returns pr_status; 0 is success, negative is an error.
+ *     Nothing is thrown across the ABI.  pr_last_error() gives a message for
+ *     the calling thread's last failure.
+ *   - Peers are 0 .. num_peers-1; peer p's tree is "slot p".  Which slot is
+ *     the local node's own tree is the caller's business: routing treats all
+ *     slots alike (the argmax runs over every tree, the node's own included).
+ *   - Tokens are int32; every int32 value is a legal token.  Sequence batches
+ *     are CSR: sequence i is tokens[offsets[i] .. offsets[i+1]), offsets are
+ *     int64, offsets[0] == 0 and non-decreasing.
+ *   - Match semantics: match_len[q][p] is the length of the longest prefix of
+ *     query q that is also a prefix of some sequence inserted into peer p's
+ *     tree (0 for an empty tree or query).  chosen[q] is the lowest peer id
+ *     whose match length is the largest (so an all-zero row chooses peer 0).
+ *   - Single writer: calls on one forest must be serialised by the caller
+ *     (each tree has one writer, paper Section 1).  pr_route only reads the
+ *     forest.
+ *   - Device calls (pr_merge, pr_route) take device pointers and a HIP stream
+ *     (NULL = the legacy default stream), are ordered on that stream and return
+ *     without waiting for the GPU.  Input buffers must stay valid, and output
+ *     buffers untouched, until the stream has passed the call.
+ *   - A forest lives on the HIP device that is current when it first touches
+ *     the GPU; later calls switch to that device for their duration.
+ */
+#ifndef PREFIX_ROUTER_H
+#define PREFIX_ROUTER_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t pr_status;
+
+#define PR_OK 0
+#define PR_EINVAL (-1)  /* bad argument; the forest is unchanged, no output is written */
+#define PR_ENOMEM (-2)  /* host or device allocation failed; the forest is unchanged */
+#define PR_EDEVICE (-3) /* a HIP call failed; destroy the forest */
+#define PR_ESTATE (-4)  /* call not valid in the forest's current state */
+
+#define PR_MAX_PEERS 1024
+
+typedef struct pr_forest pr_forest;
+
+/* ABI version of this header (incremented on incompatible changes). */
+int32_t pr_abi_version(void);
+
+/* Message describing the calling thread's last failed call ("" if none). */
+const char *pr_last_error(void);
+
+/*
+ * Create an empty forest of num_peers trees (1 <= num_peers <= PR_MAX_PEERS).
+ * Every tree starts empty.  No GPU work happens here.
+ * Errors: PR_EINVAL (num_peers out of range, out == NULL), PR_ENOMEM.
+ * Ownership: the caller owns *out and releases it with pr_forest_destroy.
+ */
+pr_status pr_forest_create(int32_t num_peers, pr_forest **out);
+
+/* Release a forest and all its host and device memory.  NULL is a no-op.
+ * Waits for the forest's device to finish outstanding work first. */
+void pr_forest_destroy(pr_forest *f);
+
+/*
+ * sendTrie, receive side (paper: sendTrie broadcasts the local trie; Section
+ * "Trie-broadcast loss": every broadcast is a complete snapshot, so receiving
+ * it replaces the estimate, and a duplicated broadcast changes nothing).
+ * REPLACES peer's tree by the set of num_seqs sequences given as a HOST CSR
+ * batch.  Any merges into that peer since its last snapshot are dropped with
+ * the old tree; other peers are untouched.  An empty snapshot (num_seqs == 0)
+ * empties the tree, e.g. a peer that crashed and lost its cache.
+ * The data is copied before the call returns; the device copy of the forest is
+ * rebuilt before the next pr_merge or pr_route on this forest runs (that call
+ * then blocks the host for the rebuild and upload).
+ * Errors: PR_EINVAL (peer out of range, num_seqs < 0, NULL offsets, NULL tokens
+ * with a non-empty batch, offsets[0] != 0 or decreasing offsets), PR_ENOMEM.
+ */
+pr_status pr_load_snapshot(pr_forest *f, int32_t peer, const int32_t *tokens,
+                           const int64_t *offsets, int64_t num_seqs);
+
+/*
+ * updateTrie / updateTrieEstimate (paper, System Design; Algorithm 1 inserts a
+ * request into the local tree after serving it, or into the estimate of the
+ * peer it was forwarded to once that peer acknowledges).
+ * Inserts DEVICE sequence i (tokens[offsets[i] .. offsets[i+1]), offsets within
+ * [0, num_tokens]) into peer peer_of[i]'s tree, for every i < num_seqs, on the
+ * given stream.  The result depends only on the set of inserts (order and
+ * duplicates do not matter).  Entries with a peer out of range or offsets
+ * outside [0, num_tokens] or decreasing are skipped and counted; see
+ * pr_forest_check.
+ * Errors (host side, nothing enqueued): PR_EINVAL (NULL pointers with
+ * num_seqs > 0, num_seqs < 0, num_tokens < 0), PR_ENOMEM (the forest's device
+ * capacity could not grow), PR_EDEVICE.
+ */
+pr_status pr_merge(pr_forest *f, const int32_t *peer_of, const int32_t *tokens,
+                   int64_t num_tokens, const int64_t *offsets, int64_t num_seqs,
+                   void *hip_stream);
+
+/*
+ * getBestNode for a batch (paper, System Design; Algorithm 1: the node picks
+ * k = argmax over all N trees of PrefixMatch(r, tree_j)).
+ * DEVICE inputs: query q is q_tokens[q_offsets[q] .. q_offsets[q+1]), offsets
+ * within [0, num_tokens].  DEVICE outputs, caller-allocated:
+ *   match_len  int32 [num_queries][num_peers], row-major;
+ *   chosen     int32 [num_queries].
+ * A query whose offsets are outside [0, num_tokens], decreasing, or span more
+ * than INT32_MAX tokens gets match_len -1 in every column and chosen -1.
+ * num_queries == 0 is a no-op.  Reads the forest only.
+ * Errors (host side, nothing enqueued): PR_EINVAL (NULL pointers with
+ * num_queries > 0, negative counts), PR_ENOMEM / PR_EDEVICE (rebuild after a
+ * snapshot load failed).
+ */
+pr_status pr_route(pr_forest *f, const int32_t *q_tokens, int64_t num_tokens,
+                   const int64_t *q_offsets, int64_t num_queries, int32_t *match_len,
+                   int32_t *chosen, void *hip_stream);
+
+/*
+ * Wait for the forest's device work and report inputs that device calls
+ * skipped since the last check: returns PR_OK if none, else PR_EINVAL with the
+ * count in the message (and resets the count).
+ */
+pr_status pr_forest_check(pr_forest *f);
+
+/* Sizes of the forest's current device layout (for reports and tests). */
+typedef struct {
+    int32_t num_peers;
+    int32_t mask_words;      /* 64-bit peer-mask words per node */
+    int64_t num_nodes;       /* union-tree nodes, root included */
+    int64_t num_child_slots; /* child-table entries */
+    int64_t pool_tokens;     /* edge-label tokens */
+    int64_t device_bytes;    /* device memory held by the forest */
+    int64_t host_seq_tokens; /* tokens of the host-side snapshot copies */
+} pr_forest_info;
+
+pr_status pr_forest_info_get(pr_forest *f, pr_forest_info *out);
+
+/*
+ * Host-side image of the union layout built from the forest's host snapshot
+ * copies, for inspection without a GPU (layout tests).  No GPU work.  The
+ * pointers stay valid until the next call on f.  Layout:
+ *   nodes  int32 [num_nodes][4]: label offset in pool (uint32 bits), label
+ *          length, first child-table slot, child count; node 0 is the root;
+ *   masks  uint64 [num_nodes][mask_words]: bit p set if peer p's tree holds
+ *          the path from the root through this node's whole label;
+ *   ctab   int32 [num_child_slots][2]: (first label token, child node), sorted
+ *          by first token within each node's slots;
+ *   pool   int32 [pool_tokens]: label tokens.
+ */
+typedef struct {
+    int32_t mask_words;
+    int64_t num_nodes, num_child_slots, pool_tokens;
+    const int32_t *nodes;
+    const uint64_t *masks;
+    const int32_t *ctab;
+    const int32_t *pool;
+} pr_image_view;
+
+pr_status pr_forest_host_image(pr_forest *f, pr_image_view *out);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PREFIX_ROUTER_H */

@@ -1,0 +1,254 @@
+"""Python binding of libprefix_router.so (ctypes; argument marshalling only).
+
+Function names follow the C ABI in include/prefix_router.h.  Every routing and
+merge step runs in the library's HIP kernels; this module only checks shapes,
+dtypes and devices of torch tensors and passes raw pointers and the current HIP
+stream.  If the library is not built, loading it raises: there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Tuple
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libprefix_router.so")
+
+PR_OK, PR_EINVAL, PR_ENOMEM, PR_EDEVICE, PR_ESTATE = 0, -1, -2, -3, -4
+PR_MAX_PEERS = 1024
+
+EXPORTED = ("pr_abi_version", "pr_last_error", "pr_forest_create", "pr_forest_destroy",
+            "pr_load_snapshot", "pr_merge", "pr_route", "pr_forest_check", "pr_forest_info_get",
+            "pr_forest_host_image")
+
+
+class RouterError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"status {status}: {msg}")
+        self.status = status
+
+
+class ForestInfo(ctypes.Structure):
+    _fields_ = [("num_peers", ctypes.c_int32), ("mask_words", ctypes.c_int32),
+                ("num_nodes", ctypes.c_int64), ("num_child_slots", ctypes.c_int64),
+                ("pool_tokens", ctypes.c_int64), ("device_bytes", ctypes.c_int64),
+                ("host_seq_tokens", ctypes.c_int64)]
+
+
+class ImageView(ctypes.Structure):
+    _fields_ = [("mask_words", ctypes.c_int32), ("num_nodes", ctypes.c_int64),
+                ("num_child_slots", ctypes.c_int64), ("pool_tokens", ctypes.c_int64),
+                ("nodes", ctypes.POINTER(ctypes.c_int32)), ("masks", ctypes.POINTER(ctypes.c_uint64)),
+                ("ctab", ctypes.POINTER(ctypes.c_int32)), ("pool", ctypes.POINTER(ctypes.c_int32))]
+
+
+_lib_handle = None
+_vp = ctypes.c_void_p
+_i32p = ctypes.POINTER(ctypes.c_int32)
+_i64p = ctypes.POINTER(ctypes.c_int64)
+
+
+def lib() -> ctypes.CDLL:
+    """Load the library (import torch first so that one HIP runtime serves both)."""
+    global _lib_handle
+    if _lib_handle is not None:
+        return _lib_handle
+    try:
+        import torch  # noqa: F401  (binds libamdhip64 to torch's copy)
+    except ImportError:
+        pass
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is not built; run paper_2606_17059_amd.build.build()")
+    L = ctypes.CDLL(LIB_PATH)
+    L.pr_abi_version.restype = ctypes.c_int32
+    L.pr_last_error.restype = ctypes.c_char_p
+    L.pr_forest_create.argtypes = [ctypes.c_int32, ctypes.POINTER(_vp)]
+    L.pr_forest_create.restype = ctypes.c_int32
+    L.pr_forest_destroy.argtypes = [_vp]
+    L.pr_forest_destroy.restype = None
+    L.pr_load_snapshot.argtypes = [_vp, ctypes.c_int32, _vp, _vp, ctypes.c_int64]
+    L.pr_load_snapshot.restype = ctypes.c_int32
+    L.pr_merge.argtypes = [_vp, _vp, _vp, ctypes.c_int64, _vp, ctypes.c_int64, _vp]
+    L.pr_merge.restype = ctypes.c_int32
+    L.pr_route.argtypes = [_vp, _vp, ctypes.c_int64, _vp, ctypes.c_int64, _vp, _vp, _vp]
+    L.pr_route.restype = ctypes.c_int32
+    L.pr_forest_check.argtypes = [_vp]
+    L.pr_forest_check.restype = ctypes.c_int32
+    L.pr_forest_info_get.argtypes = [_vp, ctypes.POINTER(ForestInfo)]
+    L.pr_forest_info_get.restype = ctypes.c_int32
+    L.pr_forest_host_image.argtypes = [_vp, ctypes.POINTER(ImageView)]
+    L.pr_forest_host_image.restype = ctypes.c_int32
+    if L.pr_abi_version() != 1:
+        raise RuntimeError("libprefix_router ABI version mismatch")
+    _lib_handle = L
+    return L
+
+
+def _check(status: int) -> None:
+    if status != PR_OK:
+        raise RouterError(status, lib().pr_last_error().decode())
+
+
+def pr_last_error() -> str:
+    return lib().pr_last_error().decode()
+
+
+# ---- thin wrappers with the C names -----------------------------------------
+def pr_forest_create(num_peers: int) -> int:
+    h = _vp()
+    _check(lib().pr_forest_create(int(num_peers), ctypes.byref(h)))
+    return h.value
+
+
+def pr_forest_destroy(f: int) -> None:
+    lib().pr_forest_destroy(f)
+
+
+def pr_load_snapshot(f: int, peer: int, tokens: np.ndarray, offsets: np.ndarray) -> None:
+    t = np.ascontiguousarray(tokens, dtype=np.int32)
+    o = np.ascontiguousarray(offsets, dtype=np.int64)
+    if o.ndim != 1 or o.shape[0] < 1:
+        raise ValueError("offsets must be 1-D with at least one entry")
+    _check(lib().pr_load_snapshot(f, int(peer), t.ctypes.data if t.size else None, o.ctypes.data,
+                                  o.shape[0] - 1))
+
+
+def _dev(t, dtype, name):
+    import torch
+    if not isinstance(t, torch.Tensor) or t.device.type != "cuda":
+        raise TypeError(f"{name} must be a CUDA (HIP) torch tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t
+
+
+def _stream_ptr(stream, device) -> int:
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream(device)
+    return int(s.cuda_stream)
+
+
+def pr_merge(f: int, peer_of, tokens, offsets, stream=None) -> None:
+    import torch
+    _dev(peer_of, torch.int32, "peer_of")
+    _dev(tokens, torch.int32, "tokens")
+    _dev(offsets, torch.int64, "offsets")
+    n = offsets.numel() - 1
+    if n < 0 or peer_of.numel() != n:
+        raise ValueError("peer_of must have len(offsets) - 1 entries")
+    _check(lib().pr_merge(f, peer_of.data_ptr() or None, tokens.data_ptr() or None, tokens.numel(),
+                          offsets.data_ptr(), n, _stream_ptr(stream, offsets.device)))
+
+
+def pr_route(f: int, q_tokens, q_offsets, match_len, chosen, num_peers: int, stream=None) -> None:
+    import torch
+    _dev(q_tokens, torch.int32, "q_tokens")
+    _dev(q_offsets, torch.int64, "q_offsets")
+    _dev(match_len, torch.int32, "match_len")
+    _dev(chosen, torch.int32, "chosen")
+    nq = q_offsets.numel() - 1
+    if nq < 0:
+        raise ValueError("q_offsets must have at least one entry")
+    if match_len.numel() != nq * num_peers or chosen.numel() != nq:
+        raise ValueError("match_len must hold [num_queries][num_peers] and chosen [num_queries]")
+    _check(lib().pr_route(f, q_tokens.data_ptr() or None, q_tokens.numel(), q_offsets.data_ptr(), nq,
+                          match_len.data_ptr() or None, chosen.data_ptr() or None,
+                          _stream_ptr(stream, q_offsets.device)))
+
+
+def pr_forest_check(f: int) -> None:
+    _check(lib().pr_forest_check(f))
+
+
+def pr_forest_info_get(f: int) -> dict:
+    info = ForestInfo()
+    _check(lib().pr_forest_info_get(f, ctypes.byref(info)))
+    return {k: getattr(info, k) for k, _ in ForestInfo._fields_}
+
+
+def pr_forest_host_image(f: int) -> dict:
+    """Copy of the host-side layout image (numpy arrays)."""
+    v = ImageView()
+    _check(lib().pr_forest_host_image(f, ctypes.byref(v)))
+
+    def arr(ptr, n, dt):
+        if n == 0:
+            return np.zeros(0, dtype=dt)
+        return np.ctypeslib.as_array(ptr, shape=(n,)).astype(dt, copy=True)
+
+    W = v.mask_words
+    return dict(mask_words=W,
+                nodes=arr(v.nodes, v.num_nodes * 4, np.int32).reshape(-1, 4),
+                masks=arr(v.masks, v.num_nodes * W, np.uint64).reshape(-1, W),
+                ctab=arr(v.ctab, v.num_child_slots * 2, np.int32).reshape(-1, 2),
+                pool=arr(v.pool, v.pool_tokens, np.int32))
+
+
+# ---- convenience object ------------------------------------------------------
+class Forest:
+    """Owning handle of a pr_forest (one node's view of all peers' trees)."""
+
+    def __init__(self, num_peers: int):
+        self.num_peers = int(num_peers)
+        self._h = pr_forest_create(self.num_peers)
+
+    @property
+    def handle(self) -> int:
+        if not self._h:
+            raise RuntimeError("forest is closed")
+        return self._h
+
+    def close(self) -> None:
+        if getattr(self, "_h", None):
+            pr_forest_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc):
+        self.close()
+
+    def load_snapshot(self, peer: int, tokens, offsets) -> None:
+        pr_load_snapshot(self.handle, peer, tokens, offsets)
+
+    def load_seqset(self, ss) -> None:
+        """Load every peer's snapshot from a peer-major CSR batch (workloads.SeqSet)."""
+        for p in range(self.num_peers):
+            lo = int(np.searchsorted(ss.peer, p, side="left"))
+            hi = int(np.searchsorted(ss.peer, p, side="right"))
+            o = ss.offsets[lo:hi + 1] - ss.offsets[lo]
+            self.load_snapshot(p, ss.tokens[ss.offsets[lo]:ss.offsets[hi]], o)
+
+    def merge(self, peer_of, tokens, offsets, stream=None) -> None:
+        pr_merge(self.handle, peer_of, tokens, offsets, stream)
+
+    def route(self, q_tokens, q_offsets, match_len=None, chosen=None, stream=None) -> Tuple:
+        import torch
+        nq = q_offsets.numel() - 1
+        dev = q_offsets.device
+        if match_len is None:
+            match_len = torch.empty((nq, self.num_peers), dtype=torch.int32, device=dev)
+        if chosen is None:
+            chosen = torch.empty(nq, dtype=torch.int32, device=dev)
+        pr_route(self.handle, q_tokens, q_offsets, match_len, chosen, self.num_peers, stream)
+        return match_len, chosen
+
+    def check(self) -> None:
+        pr_forest_check(self.handle)
+
+    def info(self) -> dict:
+        return pr_forest_info_get(self.handle)
+
+    def host_image(self) -> dict:
+        return pr_forest_host_image(self.handle)

@@ -1,0 +1,39 @@
+"""The C-ABI library loads and exports every entry point its header declares
+(no GPU calls)."""
+import ctypes
+import os
+import re
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    src = open(os.path.join(ROOT, "include", "prefix_router.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(pr_[a-z_]+)\s*\(", src)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for must in ("pr_forest_create", "pr_forest_destroy", "pr_load_snapshot", "pr_merge", "pr_route"):
+        assert must in names
+
+
+def test_library_exports_every_declared_symbol():
+    from paper_2606_17059_amd import router as R
+    L = R.lib()
+    for name in declared_functions():
+        assert hasattr(L, name), f"{name} not exported"
+        assert isinstance(getattr(L, name), ctypes._CFuncPtr)
+    assert set(declared_functions()) == set(R.EXPORTED)
+
+
+def test_binding_refuses_missing_library(monkeypatch, tmp_path):
+    from paper_2606_17059_amd import router as R
+    monkeypatch.setattr(R, "_lib_handle", None)
+    monkeypatch.setattr(R, "LIB_PATH", str(tmp_path / "missing.so"))
+    try:
+        R.lib()
+        raise AssertionError("loading a missing library must raise")
+    except RuntimeError as e:
+        assert "not built" in str(e)

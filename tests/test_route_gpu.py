@@ -1,0 +1,151 @@
+"""Route parity on the GPU: the HIP path through the C ABI versus the CPU oracle.
+
+Integer outputs, so the bar is bit-exact: every match length and every chosen
+peer.  Small cases compare every row; full-size configurations compare a
+sampled set of rows exactly and check properties on all rows.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import pins
+import workloads as W
+from gpu_util import (announce, assert_properties, assert_rows_equal, device, gpu_route, nthreads,
+                      oracle_for, to_dev)
+
+pytestmark = pytest.mark.gpu
+
+
+def _forest(snapshot, P):
+    from paper_2606_17059_amd import Forest
+    f = Forest(P)
+    f.load_seqset(snapshot)
+    return f
+
+
+def test_golden_examples_on_gpu():
+    from paper_2606_17059_amd import Forest
+    import torch
+    dev = device()
+    for ex in pins.parse_golden():
+        if any(op[0] == "merge" for op in ex.ops):
+            continue  # examples with merges run in the merge tests
+        f = Forest(ex.peers)
+        for op in ex.ops:
+            if op[0] == "load":
+                t, o = pins._csr(op[2])
+                f.load_snapshot(op[1], t, o)
+            else:
+                _, q, m_exp, c_exp = op
+                t, o = pins._csr([q])
+                announce(f"golden {ex.name} q={q}")
+                m, c = f.route(torch.from_numpy(t).to(dev), torch.from_numpy(o).to(dev))
+                assert m.cpu().numpy()[0].tolist() == m_exp and int(c.cpu()[0]) == c_exp, (ex.name, q)
+        f.close()
+
+
+@pytest.mark.parametrize("vocab", [2, 3, 8])
+def test_tiny_random_all_rows(vocab):
+    for sd in range(16):
+        P = [1, 2, 3, 5, 64, 65, 130][sd % 7]
+        w = W.tiny_random(sd, num_peers=P, vocab=vocab, max_seqs=6 if P > 10 else 12, n_queries=67)
+        f = _forest(w.snapshot, P)
+        m, c = gpu_route(f, w.queries, f"tiny vocab={vocab} seed={sd} P={P}")
+        o = oracle_for(w.snapshot, P)
+        m_or, c_or = o.route(w.queries.tokens, w.queries.offsets, 2)
+        assert_rows_equal(m, c, m_or, c_or, what=f"tiny vocab={vocab} seed={sd}")
+        f.close()
+
+
+def test_max_peers_1024():
+    w = W.tiny_random(77, num_peers=1024, vocab=3, max_seqs=2, n_queries=40)
+    f = _forest(w.snapshot, 1024)
+    m, c = gpu_route(f, w.queries, "P=1024")
+    o = oracle_for(w.snapshot, 1024)
+    m_or, c_or = o.route(w.queries.tokens, w.queries.offsets, 2)
+    assert_rows_equal(m, c, m_or, c_or, what="P=1024")
+
+
+def test_config1_tiny_all_rows():
+    w = W.make_config(1)
+    f = _forest(w.snapshot, w.num_peers)
+    m, c = gpu_route(f, w.queries, "config 1 tiny")
+    o = oracle_for(w.snapshot, w.num_peers)
+    m_or, c_or = o.route(w.queries.tokens, w.queries.offsets, nthreads())
+    assert_rows_equal(m, c, m_or, c_or, what="config 1")
+
+
+@pytest.mark.timeout(900)
+def test_config2_medium_full_batch():
+    """The benchmark's workload and launch (65,536 queries, 16 peers): exact on
+    a 4,096-row sample plus a ragged tail, properties on every row."""
+    w = W.make_config(2)
+    f = _forest(w.snapshot, w.num_peers)
+    m, c = gpu_route(f, w.queries, "config 2 medium full")
+    assert_properties(m, c, w.queries, "config 2")
+    rng = np.random.default_rng(2)
+    idx = np.unique(np.concatenate([rng.choice(len(w.queries), 4096, replace=False),
+                                    np.arange(len(w.queries) - 37, len(w.queries))]))
+    o = oracle_for(w.snapshot, w.num_peers)
+    m_or, c_or = o.route_seqset(w.queries, idx, nthreads())
+    assert_rows_equal(m, c, m_or, c_or, idx, "config 2 sample")
+    # determinism: a second launch gives identical bytes
+    m2, c2 = gpu_route(f, w.queries, "config 2 medium repeat")
+    assert np.array_equal(m, m2) and np.array_equal(c, c2)
+
+
+def test_small_batches_ragged():
+    """Batch sizes around the 4-waves-per-block boundary, several tiles."""
+    w = W.make_config(2, n_queries=1031, prompts_per_peer=150)
+    f = _forest(w.snapshot, w.num_peers)
+    o = oracle_for(w.snapshot, w.num_peers)
+    for n in (1, 2, 3, 4, 5, 7, 8, 9, 63, 64, 65, 1031):
+        sub = w.queries.subset(np.arange(n))
+        m, c = gpu_route(f, sub, f"ragged n={n}")
+        m_or, c_or = o.route(sub.tokens, sub.offsets, nthreads())
+        assert_rows_equal(m, c, m_or, c_or, what=f"ragged n={n}")
+
+
+def test_edge_cases():
+    import torch
+    from paper_2606_17059_amd import Forest
+    dev = device()
+    f = Forest(5)
+    # empty forest, empty query, ordinary query
+    qs = W.from_lists([[], [1, 2, 3], [7]])
+    m, c = gpu_route(f, qs, "empty forest")
+    assert m.tolist() == [[0] * 5] * 3 and c.tolist() == [0, 0, 0]
+    f.load_snapshot(3, np.array([1, 2, 3, 4], np.int32), np.array([0, 4]))
+    f.load_snapshot(1, np.array([1, 2], np.int32), np.array([0, 2]))
+    m, c = gpu_route(f, qs, "two peers loaded")
+    assert m.tolist() == [[0] * 5, [0, 2, 0, 3, 0], [0] * 5] and c.tolist() == [0, 3, 0]
+    # zero queries is a no-op
+    e = torch.zeros(0, dtype=torch.int32, device=dev)
+    mo, co = f.route(e, torch.zeros(1, dtype=torch.int64, device=dev))
+    assert mo.shape == (0, 5)
+    # offsets outside the token buffer or decreasing: row of -1, nothing read
+    toks = torch.tensor([1, 2, 3], dtype=torch.int32, device=dev)
+    offs = torch.tensor([0, 3, 2, 9, -1, 3], dtype=torch.int64, device=dev)
+    announce("invalid offsets")
+    m, c = f.route(toks, offs)
+    m, c = m.cpu().numpy(), c.cpu().numpy()
+    assert m[0].tolist() == [0, 2, 0, 3, 0] and c[0] == 3
+    assert (m[1:] == -1).all() and (c[1:] == -1).all()
+    f.close()
+
+
+def test_reload_replaces_on_device():
+    """A new snapshot replaces a peer's tree for the next route (the device
+    image is rebuilt), and a duplicate load changes nothing."""
+    w = W.make_config(1, n_queries=300, prompts_per_peer=50)
+    f = _forest(w.snapshot, w.num_peers)
+    m1, c1 = gpu_route(f, w.queries, "before reload")
+    f.load_snapshot(1, np.zeros(0, np.int32), np.zeros(1, np.int64))  # peer 1 crashed
+    m2, c2 = gpu_route(f, w.queries, "peer 1 emptied")
+    assert (m2[:, 1] == 0).all()
+    lo, hi = w.snapshot.peer_range(1)
+    for _ in range(2):  # recovered, and the broadcast duplicated
+        f.load_snapshot(1, w.snapshot.tokens[w.snapshot.offsets[lo]:w.snapshot.offsets[hi]],
+                        w.snapshot.offsets[lo:hi + 1] - w.snapshot.offsets[lo])
+    m3, c3 = gpu_route(f, w.queries, "peer 1 reloaded")
+    assert np.array_equal(m1, m3) and np.array_equal(c1, c3)

@@ -154,6 +154,26 @@ def main() -> int:
     log(f"[bench] per-launch ms: mean {kern_ms.mean():.4f} median {np.median(kern_ms):.4f} "
         f"min {kern_ms.min():.4f} max {kern_ms.max():.4f}; algorithmic bytes/launch {total_bytes / 1e6:.1f} MB")
 
+    extra = {}
+    if args.config == 3:
+        # the same batch routed on the peers' true trees: how often the stale
+        # estimates pick the same peer, and the prefill reuse they predict vs get
+        ft = Forest(P)
+        ft.load_seqset(w.true_snapshot)
+        mt, ct = ft.route(qt[0], qo[0])
+        torch.cuda.synchronize()
+        ft.close()
+        mt, ct = mt.cpu().numpy(), ct.cpu().numpy()
+        ce = ch.cpu().numpy()
+        rows = np.arange(nq)
+        tot = float(qlen.sum())
+        extra["stale_report"] = {
+            "route_agreement": float((ce == ct).mean()),
+            "expected_hit": float(m[rows, ce].sum() / tot),
+            "actual_hit": float(mt[rows, ce].sum() / tot),
+            "oracle_true_hit": float(mt[rows, ct].sum() / tot)}
+        log(f"[bench] stale report: {extra['stale_report']}")
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(w, queries, args.cpu_seconds)
@@ -181,6 +201,7 @@ def main() -> int:
                      "algorithmic_bytes_per_launch": total_bytes},
         "cpu_baseline": cpu,
     }
+    out.update(extra)
     print(json.dumps(out), flush=True)
     f.close()
     return 0

@@ -136,9 +136,8 @@ pr_status pr_forest_check(pr_forest *f);
 typedef struct {
     int32_t num_peers;
     int32_t mask_words;      /* 64-bit peer-mask words per node */
-    int64_t num_nodes;       /* union-tree nodes, root included */
-    int64_t num_child_slots; /* child-table entries */
-    int64_t pool_tokens;     /* edge-label tokens */
+    int64_t num_nodes;       /* union-tree node records in use, root included */
+    int64_t pool_tokens;     /* edge-label tokens in use */
     int64_t device_bytes;    /* device memory held by the forest */
     int64_t host_seq_tokens; /* tokens of the host-side snapshot copies */
 } pr_forest_info;
@@ -149,20 +148,23 @@ pr_status pr_forest_info_get(pr_forest *f, pr_forest_info *out);
  * Host-side image of the union layout built from the forest's host snapshot
  * copies, for inspection without a GPU (layout tests).  No GPU work.  The
  * pointers stay valid until the next call on f.  Layout:
- *   nodes  int32 [num_nodes][4]: label offset in pool (uint32 bits), label
- *          length, first child-table slot, child count; node 0 is the root;
- *   masks  uint64 [num_nodes][mask_words]: bit p set if peer p's tree holds
- *          the path from the root through this node's whole label;
- *   ctab   int32 [num_child_slots][2]: (first label token, child node), sorted
- *          by first token within each node's slots;
+ *   nodes  int32 [num_nodes][8]: first label token, label offset in pool
+ *          (uint32 bits), label length, first child id, child count, 0,
+ *          peer-mask word 0 (low 32 bits, high 32 bits).  Node 0 is the root;
+ *          the children of a node are the contiguous ids [first child id,
+ *          first child id + child count), sorted by first label token.
+ *          Bit p of the mask is set if peer p's tree holds the path from the
+ *          root through the node's whole label;
+ *   ntok   int32 [num_nodes]: first label token of every node;
+ *   mext   uint64 [num_nodes][mask_words - 1]: peer-mask words 1.. ;
  *   pool   int32 [pool_tokens]: label tokens.
  */
 typedef struct {
     int32_t mask_words;
-    int64_t num_nodes, num_child_slots, pool_tokens;
+    int64_t num_nodes, pool_tokens;
     const int32_t *nodes;
-    const uint64_t *masks;
-    const int32_t *ctab;
+    const int32_t *ntok;
+    const uint64_t *mext;
     const int32_t *pool;
 } pr_image_view;
 

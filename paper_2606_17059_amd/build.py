@@ -31,18 +31,21 @@ def _run(cmd):
     return out
 
 
-def build(verbose: bool = False) -> str:
+def build(verbose: bool = False, defines=(), out_path: str = LIB_PATH) -> str:
+    """Compile the library.  ``defines`` (e.g. "PR_LCP_VECTORS=16") override the
+    kernels' compile-time tile constants."""
     os.makedirs(BUILD_DIR, exist_ok=True)
     host_obj = os.path.join(BUILD_DIR, "forest_host.o")
     out = _run(["g++", *HOST_FLAGS, "-I", CSRC, "-c", os.path.join(CSRC, "forest_host.cpp"), "-o", host_obj])
     dev_obj = os.path.join(BUILD_DIR, "router.o")
-    out += _run([HIPCC, *HIP_FLAGS, "-I", INCLUDE, "-I", CSRC, "-c", os.path.join(CSRC, "router.hip"), "-o", dev_obj])
-    tmp = LIB_PATH + ".tmp"
+    out += _run([HIPCC, *HIP_FLAGS, *["-D" + d for d in defines], "-I", INCLUDE, "-I", CSRC, "-c",
+                 os.path.join(CSRC, "router.hip"), "-o", dev_obj])
+    tmp = out_path + ".tmp"
     out += _run([HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC", dev_obj, host_obj, "-o", tmp])
-    os.replace(tmp, LIB_PATH)
+    os.replace(tmp, out_path)
     if verbose and out.strip():
         print(out)
-    return LIB_PATH
+    return out_path
 
 
 if __name__ == "__main__":

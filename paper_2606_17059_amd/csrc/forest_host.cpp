@@ -10,8 +10,8 @@
 //
 // Afterwards chains are compressed: a node with a single child whose peer mask
 // equals its own absorbs that child, since no match length can end between
-// them.  The flattened image lists nodes in depth-first preorder with the
-// labels of each path laid out contiguously in the pool.
+// them.  The flattened image gives the children of every node one contiguous
+// block of ids, sorted by first token.
 #include "forest_host.h"
 
 #include <algorithm>
@@ -94,59 +94,57 @@ class Builder {
     }
 
     bool flatten(HostImage *out, std::string *err) {
-        // depth-first preorder, children in first-token order
-        std::vector<int32_t> order;
-        order.reserve(nodes_.size());
-        std::vector<int32_t> stack{0};
-        while (!stack.empty()) {
-            const int32_t x = stack.back();
-            stack.pop_back();
-            order.push_back(x);
-            const auto &K = nodes_[x].kids;
-            for (size_t j = K.size(); j-- > 0;) stack.push_back(K[j]);
-        }
-        if (order.size() > (size_t)std::numeric_limits<int32_t>::max()) {
+        // Ids: the root is 0; when a node is visited, its children receive one
+        // contiguous block of ids in first-token order; children are then
+        // visited depth first.  Labels are laid out in id order.
+        const size_t n = nodes_.size();
+        if (n > (size_t)std::numeric_limits<int32_t>::max()) {
             *err = "too many nodes";
             return false;
         }
-        std::vector<int32_t> new_id(nodes_.size(), -1);
-        for (size_t j = 0; j < order.size(); j++) new_id[order[j]] = (int32_t)j;
-        uint64_t pool_len = 0, slots = 0;
-        for (int32_t x : order) {
-            pool_len += (uint64_t)nodes_[x].len;
-            slots += nodes_[x].kids.size();
+        // nodes absorbed by compression are unreachable and get no id
+        std::vector<int32_t> order;  // order[id] = builder node
+        order.reserve(n);
+        order.push_back(0);
+        std::vector<int32_t> stack{0};
+        std::vector<int32_t> first_child_id(n, -1);
+        while (!stack.empty()) {
+            const int32_t x = stack.back();
+            stack.pop_back();
+            const auto &K = nodes_[x].kids;
+            first_child_id[x] = (int32_t)order.size();
+            for (int32_t k : K) order.push_back(k);
+            for (size_t j = K.size(); j-- > 0;) stack.push_back(K[j]);
         }
+        uint64_t pool_len = 0;
+        for (int32_t x : order) pool_len += (uint64_t)nodes_[x].len;
         if (pool_len > (uint64_t)std::numeric_limits<uint32_t>::max()) {
             *err = "label pool exceeds 2^32 tokens";
             return false;
         }
-        if (slots > (uint64_t)std::numeric_limits<int32_t>::max()) {
-            *err = "too many child slots";
-            return false;
-        }
+        const size_t m = order.size();
         out->W = W_;
-        out->nodes.resize(order.size());
-        out->masks.resize(order.size() * (size_t)W_);
-        out->ctab.resize((size_t)slots);
+        out->nodes.assign(m, Node{});
+        out->ntok.assign(m, 0);
+        out->mext.assign(m * (size_t)(W_ - 1), 0ull);
         out->pool.resize((size_t)pool_len);
         uint64_t po = 0;
-        int32_t co = 0;
-        for (size_t j = 0; j < order.size(); j++) {
-            const BNode &b = nodes_[order[j]];
-            Node &nd = out->nodes[j];
+        for (size_t id = 0; id < m; id++) {
+            const int32_t x = order[id];
+            const BNode &b = nodes_[x];
+            Node &nd = out->nodes[id];
+            nd.tok = b.len ? b.lab[0] : 0;
             nd.lab_off = (uint32_t)po;
             nd.lab_len = (int32_t)b.len;
             if (b.len) std::memcpy(out->pool.data() + po, b.lab, (size_t)b.len * sizeof(int32_t));
             po += (uint64_t)b.len;
-            nd.ct_beg = co;
+            nd.ct_beg = b.kids.empty() ? 0 : first_child_id[x];
             nd.ct_cnt = (int32_t)b.kids.size();
-            for (int32_t k : b.kids) {
-                out->ctab[(size_t)co].tok = nodes_[k].lab[0];
-                out->ctab[(size_t)co].node = new_id[k];
-                co++;
-            }
-            for (int w = 0; w < W_; w++)
-                out->masks[j * (size_t)W_ + w] = masks_[(size_t)order[j] * W_ + w];
+            nd.aux = 0;
+            nd.mask0 = masks_[(size_t)x * W_];
+            out->ntok[id] = nd.tok;
+            for (int w = 1; w < W_; w++)
+                out->mext[id * (size_t)(W_ - 1) + (w - 1)] = masks_[(size_t)x * W_ + w];
         }
         return true;
     }

@@ -22,8 +22,8 @@ struct PeerSeqs {
 struct HostImage {
     int W = 1;
     std::vector<Node> nodes;
-    std::vector<uint64_t> masks;
-    std::vector<ChildSlot> ctab;
+    std::vector<int32_t> ntok;
+    std::vector<uint64_t> mext;  // words 1..W-1 per node
     std::vector<int32_t> pool;
 };
 

@@ -1,15 +1,20 @@
 // route_kernels.h -- gfx950 kernels of the batched router (device code).
 //
-// One wavefront (64 lanes) serves one query.  The wave walks the union forest
-// from the root:
-//   child locate  : lanes load the node's sorted (first token, child) slots and
-//                   a ballot finds the slot equal to the next query token; wide
-//                   tables are first narrowed by a 64-ary separator search;
-//   mask narrowing: the wave-uniform set of peers still matching is ANDed with
-//                   the child's peer mask; every peer that drops out records
-//                   the depth reached so far (lane i owns peers i, i+64, ...);
-//   label compare : lanes compare label and query tokens 64 x U per step and a
-//                   ballot of mismatches gives the common-prefix length.
+// One wavefront (64 lanes) serves one query and walks the union forest from
+// the root.  Per tree level the wave
+//   1. locates the child whose first label token is the next query token:
+//      the node's child block was already loaded into the lanes (one child
+//      record per lane for blocks of <= 64 children, 8 first tokens per lane
+//      for blocks of <= 512, a 64-ary separator search beyond that), so a
+//      ballot finds the child and the lanes already hold its record;
+//   2. issues, in one batch, the loads of the child's label, of the matching
+//      query tokens (64 x kLcpVectors per step), of the query token after the
+//      label and of the child's own child block (speculatively, for the next
+//      level), so one memory round trip serves the whole level;
+//   3. narrows the wave-uniform set of peers still matching by the child's peer
+//      mask; every peer that drops out records the depth reached so far (lane
+//      i owns peers i, i+64, ...), and takes the common-prefix length of label
+//      and query from a ballot of mismatches.
 // Peers still in the set at the end matched the whole walked depth.  A wave
 // reduction then takes the largest match and the lowest peer id holding it
 // (the argmax of Algorithm 1, ties to the lowest id).
@@ -23,12 +28,28 @@
 
 namespace pr {
 
+#ifndef PR_ROUTE_WAVES_PER_BLOCK
+#define PR_ROUTE_WAVES_PER_BLOCK 4
+#endif
+#ifndef PR_LCP_VECTORS
+#define PR_LCP_VECTORS 8
+#endif
+#ifndef PR_WIDE_VECTORS
+#define PR_WIDE_VECTORS 8
+#endif
+
 constexpr int kWave = 64;
-constexpr int kRouteWavesPerBlock = 4;
-constexpr int kLcpVectors = 4;   // 64-token vectors compared per step (256 tokens)
-constexpr int kScanVectors = 4;  // child slots scanned per step: 64 x 4 = 256
+constexpr int kRouteWavesPerBlock = PR_ROUTE_WAVES_PER_BLOCK;
+constexpr int kLcpVectors = PR_LCP_VECTORS;    // 64-token vectors compared per step
+constexpr int kWideVectors = PR_WIDE_VECTORS;  // first tokens held per lane for wide blocks
 
 __device__ __forceinline__ int32_t uniform(int32_t v) { return __builtin_amdgcn_readfirstlane(v); }
+
+__device__ __forceinline__ uint64_t readlane64(uint64_t v, int src) {
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, src);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), src);
+    return ((uint64_t)hi << 32) | lo;
+}
 
 // Length of the common prefix of a[0..n) and b[0..n): the first i < n with
 // a[i] != b[i], or n.  Wave-cooperative; every lane returns the same value.
@@ -50,54 +71,115 @@ __device__ __forceinline__ int64_t wave_lcp(const int32_t *__restrict__ a, const
         for (int j = 0; j < kLcpVectors; j++) {
             const int64_t i = base + j * kWave + lane;
             const uint64_t bal = __ballot(i < n && va[j] != vb[j]);
-            if (bal) {
-                const int64_t r = base + j * kWave + (__ffsll((unsigned long long)bal) - 1);
-                return r;
-            }
+            if (bal) return base + j * kWave + (__ffsll((unsigned long long)bal) - 1);
         }
     }
     return n;
 }
 
-// Child of a node whose first label token is t, or -1.  ct[0..cnt) is sorted
-// by token (distinct tokens).
-__device__ __forceinline__ int32_t find_child(const ChildSlot *__restrict__ ct, int32_t cnt, int32_t t, int lane) {
-    int32_t lo = 0, hi = cnt;
-    while (hi - lo > kWave * kScanVectors) {
-        const int32_t stride = (hi - lo + kWave - 1) / kWave;
-        const int32_t idx = lo + lane * stride;
-        bool le = false;
-        if (idx < hi) le = ct[idx].tok <= t;
-        const uint64_t b = __ballot(le);
-        if (!b) return -1;  // t is below every token
-        const int32_t k = __popcll(b) - 1;  // separators ascend, so set lanes are a prefix
-        lo = lo + k * stride;
-        hi = min(lo + stride, hi);
-    }
-    int32_t tok[kScanVectors], node[kScanVectors];
+// A node's child block as held by the wave.
+struct ChildBlock {
+    int32_t beg, cnt;  // uniform
+    // cnt <= 64: lane j holds the record of child beg + j
+    int32_t tok, lab_off, lab_len, ct_beg, ct_cnt;
+    uint64_t mask0;
+    // 64 < cnt <= 64 * kWideVectors: lane j holds ntok[beg + 64 v + j]
+    int32_t wt[kWideVectors];
+};
+
+// Uniform view of the located child.
+struct Child {
+    int32_t id, lab_off, lab_len, ct_beg, ct_cnt;
+    uint64_t mask0;
+};
+
+__device__ __forceinline__ void load_block(ChildBlock &cb, const Node *__restrict__ nodes,
+                                           const int32_t *__restrict__ ntok, int32_t beg, int32_t cnt, int lane) {
+    cb.beg = beg;
+    cb.cnt = cnt;
+    cb.tok = 0;
+    cb.lab_off = 0;
+    cb.lab_len = 0;
+    cb.ct_beg = 0;
+    cb.ct_cnt = 0;
+    cb.mask0 = 0ull;
+    if (cnt <= kWave) {
+        if (lane < cnt) {
+            const Node r = nodes[beg + lane];
+            cb.tok = r.tok;
+            cb.lab_off = (int32_t)r.lab_off;
+            cb.lab_len = r.lab_len;
+            cb.ct_beg = r.ct_beg;
+            cb.ct_cnt = r.ct_cnt;
+            cb.mask0 = r.mask0;
+        }
+    } else if (cnt <= kWave * kWideVectors) {
 #pragma unroll
-    for (int j = 0; j < kScanVectors; j++) {
-        const int32_t idx = lo + j * kWave + lane;
-        tok[j] = 0;
-        node[j] = -1;
-        if (idx < hi) {
-            const ChildSlot s = ct[idx];
-            tok[j] = s.tok;
-            node[j] = s.node;
+        for (int v = 0; v < kWideVectors; v++) {
+            const int32_t j = v * kWave + lane;
+            cb.wt[v] = j < cnt ? ntok[beg + j] : 0;
         }
     }
-#pragma unroll
-    for (int j = 0; j < kScanVectors; j++) {
-        const int32_t idx = lo + j * kWave + lane;
-        const uint64_t b = __ballot(idx < hi && tok[j] == t);
-        if (b) return __builtin_amdgcn_readlane(node[j], (int)(__ffsll((unsigned long long)b) - 1));
+}
+
+// Find the child whose first token is t.  Returns false if there is none.
+__device__ __forceinline__ bool locate(const ChildBlock &cb, int32_t t, const Node *__restrict__ nodes,
+                                       const int32_t *__restrict__ ntok, int lane, Child &c) {
+    if (cb.cnt <= kWave) {
+        const uint64_t b = __ballot(lane < cb.cnt && cb.tok == t);
+        if (!b) return false;
+        const int src = (int)(__ffsll((unsigned long long)b) - 1);
+        c.id = cb.beg + src;
+        c.lab_off = __builtin_amdgcn_readlane(cb.lab_off, src);
+        c.lab_len = __builtin_amdgcn_readlane(cb.lab_len, src);
+        c.ct_beg = __builtin_amdgcn_readlane(cb.ct_beg, src);
+        c.ct_cnt = __builtin_amdgcn_readlane(cb.ct_cnt, src);
+        c.mask0 = readlane64(cb.mask0, src);
+        return true;
     }
-    return -1;
+    int32_t idx = -1;
+    if (cb.cnt <= kWave * kWideVectors) {
+#pragma unroll
+        for (int v = 0; v < kWideVectors; v++) {
+            const uint64_t b = __ballot(v * kWave + lane < cb.cnt && cb.wt[v] == t);
+            if (b) {
+                idx = v * kWave + (int32_t)(__ffsll((unsigned long long)b) - 1);
+                break;
+            }
+        }
+    } else {
+        // 64-ary search: separators ascend, so the lanes with sep <= t form a prefix
+        int32_t lo = 0, hi = cb.cnt;
+        while (hi - lo > kWave) {
+            const int32_t stride = (hi - lo + kWave - 1) / kWave;
+            const int32_t j = lo + lane * stride;
+            bool le = false;
+            if (j < hi) le = ntok[cb.beg + j] <= t;
+            const uint64_t b = __ballot(le);
+            if (!b) return false;
+            lo = lo + (__popcll(b) - 1) * stride;
+            hi = min(lo + stride, hi);
+        }
+        const int32_t j = lo + lane;
+        bool eq = false;
+        if (j < hi) eq = ntok[cb.beg + j] == t;
+        const uint64_t b = __ballot(eq);
+        if (b) idx = lo + (int32_t)(__ffsll((unsigned long long)b) - 1);
+    }
+    if (idx < 0) return false;
+    const Node r = nodes[cb.beg + idx];
+    c.id = cb.beg + idx;
+    c.lab_off = (int32_t)r.lab_off;
+    c.lab_len = r.lab_len;
+    c.ct_beg = r.ct_beg;
+    c.ct_cnt = r.ct_cnt;
+    c.mask0 = r.mask0;
+    return true;
 }
 
 template <int W>
 __global__ __launch_bounds__(kWave *kRouteWavesPerBlock) void route_kernel(
-    const Node *__restrict__ nodes, const uint64_t *__restrict__ masks, const ChildSlot *__restrict__ ctab,
+    const Node *__restrict__ nodes, const int32_t *__restrict__ ntok, const uint64_t *__restrict__ mext,
     const int32_t *__restrict__ pool, const int32_t *__restrict__ qtok, int64_t num_tokens,
     const int64_t *__restrict__ qoff, int64_t nq, int32_t P, int32_t *__restrict__ match_len,
     int32_t *__restrict__ chosen) {
@@ -124,27 +206,39 @@ __global__ __launch_bounds__(kWave *kRouteWavesPerBlock) void route_kernel(
     }
 
     int64_t d = 0;
-    Node nx = nodes[0];
-    while (d < qlen && nx.ct_cnt > 0) {
-        const int32_t t = qs[d];
-        const int32_t c = find_child(ctab + nx.ct_beg, nx.ct_cnt, t, lane);
-        if (c < 0) break;
-        const Node nc = nodes[c];
-        if (nc.lab_len <= 0) break;  // only the root has an empty label
+    ChildBlock cb;
+    {
+        const Node root = nodes[0];
+        load_block(cb, nodes, ntok, root.ct_beg, root.ct_cnt, lane);
+    }
+    int32_t t = qlen > 0 ? qs[0] : 0;
+    while (d < qlen) {
+        Child c;
+        if (!locate(cb, t, nodes, ntok, lane, c)) break;
+        if (c.lab_len <= 0) break;  // only the root has an empty label
+        // one batch of loads per level: next token, ext mask words, the next
+        // child block (used if the label matches in full) and the label compare
+        const int64_t end = d + c.lab_len;
+        const int32_t tnext = end < qlen ? qs[end] : 0;
+        uint64_t mx[W];
+        mx[0] = c.mask0;
+#pragma unroll
+        for (int w = 1; w < W; w++) mx[w] = mext[(int64_t)c.id * (W - 1) + (w - 1)];
+        load_block(cb, nodes, ntok, c.ct_beg, c.ct_cnt, lane);
+        const int64_t n = min((int64_t)c.lab_len, qlen - d);
+        const int64_t l = wave_lcp(pool + (uint32_t)c.lab_off, qs + d, n, lane);
         bool any = false;
 #pragma unroll
         for (int w = 0; w < W; w++) {
-            const uint64_t nm = alive[w] & masks[(int64_t)c * W + w];
+            const uint64_t nm = alive[w] & mx[w];
             if (((alive[w] & ~nm) >> lane) & 1ull) m[w] = (int32_t)d;
             alive[w] = nm;
             any |= nm != 0ull;
         }
         if (!any) break;  // no peer holds this edge (left behind by a replaced snapshot)
-        const int64_t n = min((int64_t)nc.lab_len, qlen - d);
-        const int64_t l = wave_lcp(pool + nc.lab_off, qs + d, n, lane);
         d += l;
-        if (l < nc.lab_len) break;
-        nx = nc;
+        if (l < c.lab_len) break;
+        t = tnext;
     }
 
     // peers still holding the walked path matched all of it

@@ -17,7 +17,6 @@
 #include "prefix_router.h"
 #include "route_kernels.h"
 
-using pr::ChildSlot;
 using pr::Node;
 
 namespace {
@@ -36,10 +35,10 @@ pr_status ok() {
 
 struct DevImage {
     Node *nodes = nullptr;
-    uint64_t *masks = nullptr;
-    ChildSlot *ctab = nullptr;
+    int32_t *ntok = nullptr;
+    uint64_t *mext = nullptr;
     int32_t *pool = nullptr;
-    int64_t n_nodes = 0, n_ctab = 0, n_pool = 0;
+    int64_t n_nodes = 0, n_pool = 0;
     int64_t bytes = 0;
 };
 
@@ -85,8 +84,8 @@ class DeviceScope {
 
 void free_image(DevImage *d) {
     (void)hipFree(d->nodes);
-    (void)hipFree(d->masks);
-    (void)hipFree(d->ctab);
+    (void)hipFree(d->ntok);
+    (void)hipFree(d->mext);
     (void)hipFree(d->pool);
     *d = DevImage();
 }
@@ -129,13 +128,12 @@ pr_status commit(pr_forest *f) {
     if (f->has_dev && hipDeviceSynchronize() != hipSuccess) return fail(PR_EDEVICE, "hipDeviceSynchronize failed");
     DevImage d;
     const pr::HostImage &h = f->host_img;
-    if ((s = upload(&d.nodes, h.nodes, &d.bytes)) || (s = upload(&d.masks, h.masks, &d.bytes)) ||
-        (s = upload(&d.ctab, h.ctab, &d.bytes)) || (s = upload(&d.pool, h.pool, &d.bytes))) {
+    if ((s = upload(&d.nodes, h.nodes, &d.bytes)) || (s = upload(&d.ntok, h.ntok, &d.bytes)) ||
+        (s = upload(&d.mext, h.mext, &d.bytes)) || (s = upload(&d.pool, h.pool, &d.bytes))) {
         free_image(&d);
         return s;
     }
     d.n_nodes = (int64_t)h.nodes.size();
-    d.n_ctab = (int64_t)h.ctab.size();
     d.n_pool = (int64_t)h.pool.size();
     if (f->has_dev) free_image(&f->dev);
     f->dev = d;
@@ -152,7 +150,7 @@ hipError_t launch_route(const pr_forest *f, const int32_t *qt, int64_t ntok, con
                         int32_t *ml, int32_t *ch, hipStream_t s) {
     const int64_t blocks = (nq + pr::kRouteWavesPerBlock - 1) / pr::kRouteWavesPerBlock;
     hipLaunchKernelGGL(pr::route_kernel<W>, dim3((unsigned)blocks), dim3(pr::kWave * pr::kRouteWavesPerBlock), 0, s,
-                       f->dev.nodes, f->dev.masks, f->dev.ctab, f->dev.pool, qt, ntok, qo, nq, f->P, ml, ch);
+                       f->dev.nodes, f->dev.ntok, f->dev.mext, f->dev.pool, qt, ntok, qo, nq, f->P, ml, ch);
     return hipGetLastError();
 }
 
@@ -275,11 +273,9 @@ pr_status pr_forest_info_get(pr_forest *f, pr_forest_info *out) {
     out->mask_words = f->W;
     if (f->has_dev && !f->dirty) {
         out->num_nodes = f->dev.n_nodes;
-        out->num_child_slots = f->dev.n_ctab;
         out->pool_tokens = f->dev.n_pool;
     } else if (f->host_img_valid) {
         out->num_nodes = (int64_t)f->host_img.nodes.size();
-        out->num_child_slots = (int64_t)f->host_img.ctab.size();
         out->pool_tokens = (int64_t)f->host_img.pool.size();
     }
     out->device_bytes = f->has_dev ? f->dev.bytes : 0;
@@ -296,11 +292,10 @@ pr_status pr_forest_host_image(pr_forest *f, pr_image_view *out) {
     const pr::HostImage &h = f->host_img;
     out->mask_words = h.W;
     out->num_nodes = (int64_t)h.nodes.size();
-    out->num_child_slots = (int64_t)h.ctab.size();
     out->pool_tokens = (int64_t)h.pool.size();
     out->nodes = reinterpret_cast<const int32_t *>(h.nodes.data());
-    out->masks = h.masks.data();
-    out->ctab = reinterpret_cast<const int32_t *>(h.ctab.data());
+    out->ntok = h.ntok.data();
+    out->mext = h.mext.data();
     out->pool = h.pool.data();
     return ok();
 }

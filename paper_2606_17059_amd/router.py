@@ -32,16 +32,16 @@ class RouterError(RuntimeError):
 
 class ForestInfo(ctypes.Structure):
     _fields_ = [("num_peers", ctypes.c_int32), ("mask_words", ctypes.c_int32),
-                ("num_nodes", ctypes.c_int64), ("num_child_slots", ctypes.c_int64),
+                ("num_nodes", ctypes.c_int64),
                 ("pool_tokens", ctypes.c_int64), ("device_bytes", ctypes.c_int64),
                 ("host_seq_tokens", ctypes.c_int64)]
 
 
 class ImageView(ctypes.Structure):
     _fields_ = [("mask_words", ctypes.c_int32), ("num_nodes", ctypes.c_int64),
-                ("num_child_slots", ctypes.c_int64), ("pool_tokens", ctypes.c_int64),
-                ("nodes", ctypes.POINTER(ctypes.c_int32)), ("masks", ctypes.POINTER(ctypes.c_uint64)),
-                ("ctab", ctypes.POINTER(ctypes.c_int32)), ("pool", ctypes.POINTER(ctypes.c_int32))]
+                ("pool_tokens", ctypes.c_int64),
+                ("nodes", ctypes.POINTER(ctypes.c_int32)), ("ntok", ctypes.POINTER(ctypes.c_int32)),
+                ("mext", ctypes.POINTER(ctypes.c_uint64)), ("pool", ctypes.POINTER(ctypes.c_int32))]
 
 
 _lib_handle = None
@@ -181,11 +181,12 @@ def pr_forest_host_image(f: int) -> dict:
         return np.ctypeslib.as_array(ptr, shape=(n,)).astype(dt, copy=True)
 
     W = v.mask_words
-    return dict(mask_words=W,
-                nodes=arr(v.nodes, v.num_nodes * 4, np.int32).reshape(-1, 4),
-                masks=arr(v.masks, v.num_nodes * W, np.uint64).reshape(-1, W),
-                ctab=arr(v.ctab, v.num_child_slots * 2, np.int32).reshape(-1, 2),
-                pool=arr(v.pool, v.pool_tokens, np.int32))
+    nodes = arr(v.nodes, v.num_nodes * 8, np.int32).reshape(-1, 8)
+    mask0 = nodes[:, 6].astype(np.uint32).astype(np.uint64) | (nodes[:, 7].astype(np.uint32).astype(np.uint64) << np.uint64(32))
+    mext = arr(v.mext, v.num_nodes * (W - 1), np.uint64).reshape(-1, W - 1) if W > 1 \
+        else np.zeros((v.num_nodes, 0), np.uint64)
+    return dict(mask_words=W, nodes=nodes, ntok=arr(v.ntok, v.num_nodes, np.int32),
+                masks=np.concatenate([mask0[:, None], mext], axis=1), pool=arr(v.pool, v.pool_tokens, np.int32))
 
 
 # ---- convenience object ------------------------------------------------------

@@ -25,18 +25,21 @@ def _mask_int(row):
 
 
 def walk(img, P, q):
-    nodes, masks, ctab, pool = img["nodes"], img["masks"], img["ctab"], img["pool"]
+    """Walk the image as the layout contract states: the children of node x are
+    ids [ct_beg, ct_beg + ct_cnt) sorted by first token; masks are uniform
+    along each edge."""
+    nodes, masks, pool = img["nodes"], img["masks"], img["pool"]
     alive = (1 << P) - 1
     m = [0] * P
     d, x = 0, 0
     q = [int(t) for t in q]
-    while d < len(q) and nodes[x, 3] > 0:
-        beg, cnt = int(nodes[x, 2]), int(nodes[x, 3])
-        toks = ctab[beg:beg + cnt, 0]
+    while d < len(q) and nodes[x, 4] > 0:
+        beg, cnt = int(nodes[x, 3]), int(nodes[x, 4])
+        toks = nodes[beg:beg + cnt, 0]
         j = int(np.searchsorted(toks, q[d]))
         if j >= cnt or int(toks[j]) != q[d]:
             break
-        c = int(ctab[beg + j, 1])
+        c = beg + j
         nm = alive & _mask_int(masks[c])
         dead = alive & ~nm
         for p in range(P):
@@ -45,7 +48,7 @@ def walk(img, P, q):
         alive = nm
         if not alive:
             break
-        off, ln = int(np.uint32(nodes[c, 0])), int(nodes[c, 1])
+        off, ln = int(np.uint32(nodes[c, 1])), int(nodes[c, 2])
         lab = pool[off:off + ln].tolist()
         l = 0
         while l < ln and d + l < len(q) and lab[l] == q[d + l]:
@@ -61,27 +64,26 @@ def walk(img, P, q):
 
 
 def check_structure(img, P):
-    nodes, masks, ctab, pool = img["nodes"], img["masks"], img["ctab"], img["pool"]
+    nodes, masks, pool, ntok = img["nodes"], img["masks"], img["pool"], img["ntok"]
     n = nodes.shape[0]
-    assert nodes[0, 1] == 0  # root label empty
-    seen_parent = np.zeros(n, dtype=np.int64)
+    assert nodes[0, 2] == 0  # root label empty
+    assert np.array_equal(ntok, nodes[:, 0])
+    parents = np.zeros(n, dtype=np.int64)
     for x in range(n):
-        beg, cnt = int(nodes[x, 2]), int(nodes[x, 3])
-        toks = ctab[beg:beg + cnt, 0]
-        assert (np.diff(toks.astype(np.int64)) > 0).all(), "child slots must be strictly sorted"
+        beg, cnt = int(nodes[x, 3]), int(nodes[x, 4])
+        toks = nodes[beg:beg + cnt, 0]
+        assert (np.diff(toks.astype(np.int64)) > 0).all(), "child blocks must be strictly sorted"
         mx = _mask_int(masks[x])
-        for j in range(cnt):
-            c = int(ctab[beg + j, 1])
-            seen_parent[c] += 1
-            assert nodes[c, 1] >= 1
-            assert int(pool[int(np.uint32(nodes[c, 0]))]) == int(toks[j]), "slot token = label's first token"
+        for c in range(beg, beg + cnt):
+            parents[c] += 1
+            assert nodes[c, 2] >= 1
+            assert int(pool[int(np.uint32(nodes[c, 1]))]) == int(nodes[c, 0]), "tok = label's first token"
             mc = _mask_int(masks[c])
             assert mc & ~mx == 0, "a child's peers are a subset of its parent's"
         if x != 0 and cnt == 1:
-            c = int(ctab[beg, 1])
-            assert _mask_int(masks[c]) != mx, "single-child chains with equal masks are compressed"
+            assert _mask_int(masks[beg]) != mx, "single-child chains with equal masks are compressed"
         assert mx >> P == 0
-    assert seen_parent[0] == 0 and (seen_parent[1:] == 1).all(), "every non-root node has one parent"
+    assert parents[0] == 0 and (parents[1:] == 1).all(), "every non-root node has one parent"
 
 
 def build_forest(w, snapshot=None):
@@ -137,7 +139,7 @@ def test_snapshot_replace_and_duplicate_load():
     f.load_snapshot(2, w.snapshot.tokens[w.snapshot.offsets[lo]:w.snapshot.offsets[hi]],
                     w.snapshot.offsets[lo:hi + 1] - w.snapshot.offsets[lo])
     b = f.host_image()
-    for k in ("nodes", "masks", "ctab", "pool"):
+    for k in ("nodes", "masks", "ntok", "pool"):
         assert np.array_equal(a[k], b[k])
     # an empty snapshot (crashed peer) removes that peer everywhere
     f.load_snapshot(2, np.zeros(0, np.int32), np.zeros(1, np.int64))

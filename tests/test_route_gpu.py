@@ -149,3 +149,47 @@ def test_reload_replaces_on_device():
                         w.snapshot.offsets[lo:hi + 1] - w.snapshot.offsets[lo])
     m3, c3 = gpu_route(f, w.queries, "peer 1 reloaded")
     assert np.array_equal(m1, m3) and np.array_equal(c1, c3)
+
+
+def _sample(n, k, seed):
+    rng = np.random.default_rng(seed)
+    return np.unique(np.concatenate([rng.choice(n, min(k, n), replace=False), np.arange(max(0, n - 13), n)]))
+
+
+@pytest.mark.timeout(1200)
+def test_config3_stale_estimates_and_truth_full_batch():
+    """64 peers, 262,144 queries: the estimated forest (stale replicas) and the
+    true forest, each exact against the oracle on a sample and checked on every
+    row; estimates never match more than the truth (Section "Stale trie
+    estimates")."""
+    announce("config 3: generating")
+    w = W.make_config(3)
+    fe = _forest(w.snapshot, w.num_peers)
+    me, ce = gpu_route(fe, w.queries, "config 3 estimated forest")
+    fe.close()
+    ft = _forest(w.true_snapshot, w.num_peers)
+    mt, ct = gpu_route(ft, w.queries, "config 3 true forest")
+    ft.close()
+    assert_properties(me, ce, w.queries, "config 3 est")
+    assert_properties(mt, ct, w.queries, "config 3 true")
+    assert (me <= mt).all() and np.array_equal(me[:, 0], mt[:, 0])
+    idx = _sample(len(w.queries), 768, 3)
+    for snap, m, c, what in ((w.snapshot, me, ce, "est"), (w.true_snapshot, mt, ct, "true")):
+        o = oracle_for(snap, w.num_peers)
+        m_or, c_or = o.route_seqset(w.queries, idx, nthreads())
+        assert_rows_equal(m, c, m_or, c_or, idx, f"config 3 {what} sample")
+        o.close()
+
+
+@pytest.mark.timeout(900)
+def test_config4_long_context_full_batch():
+    """32 peers, 8K-33K-token shared prefixes, 32,768 queries."""
+    announce("config 4: generating")
+    w = W.make_config(4)
+    f = _forest(w.snapshot, w.num_peers)
+    m, c = gpu_route(f, w.queries, "config 4 long")
+    assert_properties(m, c, w.queries, "config 4")
+    idx = _sample(len(w.queries), 2048, 4)
+    o = oracle_for(w.snapshot, w.num_peers)
+    m_or, c_or = o.route_seqset(w.queries, idx, nthreads())
+    assert_rows_equal(m, c, m_or, c_or, idx, "config 4 sample")

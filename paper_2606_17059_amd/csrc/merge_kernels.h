@@ -1,0 +1,463 @@
+// merge_kernels.h -- gfx950 kernels that insert a batch of sequences into the
+// union forest (updateTrie / updateTrieEstimate applied to a batch).
+//
+// The batch is applied in rounds.  Every round each unfinished insert walks the
+// current forest (one wave per insert) and ends in one of three states:
+//   DONE   the sequence ends exactly at a node: nothing structural is missing;
+//   ADD    at node x no child starts with the next token: a leaf must be hung
+//          below x;
+//   SPLIT  the sequence leaves (or ends inside) the label of child c of x
+//          after l tokens: c's edge must be cut there.
+// If any insert needs a SPLIT, the round cuts edges: per child c the insert
+// with the lowest batch index wins (an atomic max claim), rewrites c's record
+// in place as the upper part of the edge and gives it a new child block
+// holding the lower part (c's old record, label advanced) and, if the winner's
+// sequence goes on, a leaf with the winner's remaining tokens.  Otherwise the
+// round adds leaves: ADD inserts are radix-sorted by (x, next token); per slot
+// the lowest batch index wins, and one wave per node x writes a new, sorted
+// child block holding x's old children and one leaf per winning slot.  Records
+// that move are stamped with their new position so that a parent rebuilt in
+// the same round can be pointed at its new block wherever its record lives.
+// Losers walk again in the next round and find the structure the winners
+// built.  When every insert is DONE, a last pass ORs each insert's peer bit
+// into the mask of every node on its path.  The match function afterwards is
+// that of the old sets plus the batch; it does not depend on the batch order.
+#ifndef PR_MERGE_KERNELS_H
+#define PR_MERGE_KERNELS_H
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "forest_layout.h"
+#include "wave_ops.h"
+
+namespace pr {
+
+enum InsKind : int32_t { kInsSkip = 0, kInsActive = 1, kInsDone = 2, kInsAdd = 3, kInsSplit = 4 };
+
+struct InsState {
+    int32_t kind;
+    int32_t x;  // node the walk stopped at (ADD, SPLIT) or ended at (DONE)
+    int32_t c;  // SPLIT: the child whose label is cut
+    int32_t l;  // SPLIT: tokens of c's label shared with the insert
+    int32_t d;  // depth of x
+    int32_t t;  // next token below x (ADD, SPLIT)
+};
+
+// Device-side counters of one merge call; the host reads them between rounds.
+struct MergeCounters {
+    unsigned long long n_nodes;   // node records in use
+    unsigned long long n_pool;    // pool tokens in use
+    unsigned long long n_add;     // inserts in state ADD after the last walk
+    unsigned long long n_split;   // inserts in state SPLIT after the last walk
+    unsigned long long pool_need; // upper bound of pool tokens the next round adds
+    unsigned long long node_need; // add round: exact node records the next round adds
+    unsigned long long overflow;  // allocations refused for lack of capacity
+    unsigned long long skipped;   // inserts with invalid peer or offsets
+    unsigned long long bad_path;  // mask pass found a sequence not ending at a node
+};
+
+struct DevForest {
+    Node *nodes;
+    int32_t *ntok;
+    uint64_t *mext;
+    int32_t *pool;
+    long long *moved;  // (stamp << 32) | new position, per node id
+    int64_t cap_nodes, cap_pool;
+    int32_t W;
+};
+
+struct Batch {
+    const int32_t *peer_of;
+    const int32_t *tokens;
+    const int64_t *offsets;
+    int64_t num_tokens;
+    int64_t n;
+    int32_t P;
+};
+
+constexpr int kMergeWavesPerBlock = 4;
+
+__device__ __forceinline__ int64_t m_wave_index() {
+    return (int64_t)blockIdx.x * kMergeWavesPerBlock + uniform((int32_t)(threadIdx.x / 64));
+}
+
+// Atomic add by lane 0, result broadcast to the wave.
+__device__ __forceinline__ unsigned long long wave_atomic_add(unsigned long long *p, unsigned long long v, int lane) {
+    unsigned long long r = 0;
+    if (lane == 0) r = atomicAdd(p, v);
+    return (unsigned long long)readlane64((uint64_t)r, 0);
+}
+
+// First i < n with a[i] != b[i], or n (wave-cooperative).
+__device__ __forceinline__ int64_t m_lcp(const int32_t *a, const int32_t *b, int64_t n, int lane) {
+    for (int64_t base = 0; base < n; base += 256) {
+        uint64_t bal[4];
+#pragma unroll
+        for (int j = 0; j < 4; j++) {
+            const int64_t i = base + j * 64 + lane;
+            bool mis = false;
+            if (i < n) mis = a[i] != b[i];
+            bal[j] = __ballot(mis);
+        }
+#pragma unroll
+        for (int j = 0; j < 4; j++)
+            if (bal[j]) return base + j * 64 + (__ffsll((unsigned long long)bal[j]) - 1);
+    }
+    return n;
+}
+
+// Child of node x whose first token is t, or -1 (wave-cooperative scan).
+__device__ __forceinline__ int32_t m_find_child(const DevForest &F, const Node &x, int32_t t, int lane) {
+    for (int32_t base = 0; base < x.ct_cnt; base += 64) {
+        const int32_t j = base + lane;
+        bool eq = false;
+        if (j < x.ct_cnt) eq = F.ntok[x.ct_beg + j] == t;
+        const uint64_t b = __ballot(eq);
+        if (b) return x.ct_beg + base + (int32_t)(__ffsll((unsigned long long)b) - 1);
+    }
+    return -1;
+}
+
+__global__ void merge_validate_kernel(Batch B, InsState *st, MergeCounters *ctr) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= B.n) return;
+    const int64_t b = B.offsets[i], e = B.offsets[i + 1];
+    const int32_t p = B.peer_of[i];
+    const bool ok = p >= 0 && p < B.P && b >= 0 && e >= b && e <= B.num_tokens && e - b <= (int64_t)INT32_MAX;
+    st[i].kind = ok ? kInsActive : kInsSkip;
+    if (!ok) atomicAdd(&ctr->skipped, 1ull);
+}
+
+// Walk every active insert; classify it as DONE, ADD or SPLIT.
+__global__ __launch_bounds__(64 *kMergeWavesPerBlock) void merge_walk_kernel(DevForest F, Batch B, InsState *st,
+                                                                            MergeCounters *ctr) {
+    const int lane = (int)(threadIdx.x & 63);
+    const int64_t i = m_wave_index();
+    if (i >= B.n) return;
+    const int32_t kind = st[i].kind;
+    if (kind == kInsSkip || kind == kInsDone) return;
+    const int32_t *s = B.tokens + B.offsets[i];
+    const int64_t len = B.offsets[i + 1] - B.offsets[i];
+    int32_t x = 0;
+    int64_t d = 0;
+    InsState r;
+    r.c = -1;
+    r.l = 0;
+    r.t = 0;
+    while (true) {
+        if (d == len) {
+            r.kind = kInsDone;
+            break;
+        }
+        const Node nx = F.nodes[x];
+        const int32_t t = s[d];
+        const int32_t c = m_find_child(F, nx, t, lane);
+        if (c < 0) {
+            r.kind = kInsAdd;
+            r.t = t;
+            break;
+        }
+        const Node nc = F.nodes[c];
+        const int64_t n = min((int64_t)nc.lab_len, len - d);
+        const int64_t l = m_lcp(F.pool + nc.lab_off, s + d, n, lane);
+        if (l == nc.lab_len && nc.lab_len > 0) {
+            x = c;
+            d += l;
+            continue;
+        }
+        r.kind = kInsSplit;
+        r.c = c;
+        r.l = (int32_t)l;
+        r.t = t;
+        break;
+    }
+    r.x = x;
+    r.d = (int32_t)d;
+    if (lane == 0) {
+        st[i] = r;
+        if (r.kind == kInsAdd) {
+            atomicAdd(&ctr->n_add, 1ull);
+            atomicAdd(&ctr->pool_need, (unsigned long long)(len - d));
+        } else if (r.kind == kInsSplit) {
+            atomicAdd(&ctr->n_split, 1ull);
+            atomicAdd(&ctr->pool_need, (unsigned long long)(len - d));
+        }
+    }
+}
+
+__global__ void split_claim_kernel(DevForest F, Batch B, const InsState *st) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= B.n || st[i].kind != kInsSplit) return;
+    atomicMax(&F.nodes[st[i].c].aux, (int32_t)(INT32_MAX - i));
+}
+
+__device__ __forceinline__ void copy_mext(const DevForest &F, int64_t dst, int64_t src, int lane) {
+    for (int w = lane; w < F.W - 1; w += 64) F.mext[dst * (F.W - 1) + w] = F.mext[src * (F.W - 1) + w];
+}
+
+__device__ __forceinline__ void zero_mext(const DevForest &F, int64_t dst, int lane) {
+    for (int w = lane; w < F.W - 1; w += 64) F.mext[dst * (F.W - 1) + w] = 0ull;
+}
+
+// Copy n tokens into freshly allocated pool space (wave-cooperative).
+__device__ __forceinline__ void copy_tokens(int32_t *dst, const int32_t *src, int64_t n, int lane) {
+    for (int64_t k = lane; k < n; k += 64) dst[k] = src[k];
+}
+
+// Cut child c's edge after l tokens; the winning insert's rest becomes a leaf.
+__global__ __launch_bounds__(64 *kMergeWavesPerBlock) void split_apply_kernel(DevForest F, Batch B,
+                                                                             const InsState *st,
+                                                                             MergeCounters *ctr) {
+    const int lane = (int)(threadIdx.x & 63);
+    const int64_t i = m_wave_index();
+    if (i >= B.n || st[i].kind != kInsSplit) return;
+    const InsState r = st[i];
+    if (F.nodes[r.c].aux != (int32_t)(INT32_MAX - i)) return;  // another insert cuts c this round
+    const int32_t *s = B.tokens + B.offsets[i];
+    const int64_t len = B.offsets[i + 1] - B.offsets[i];
+    const int64_t rest = len - (int64_t)r.d - r.l;  // tokens after the cut (0: ends at the cut)
+    const int32_t k = rest > 0 ? 2 : 1;
+    if (r.l <= 0) {  // a first-token match guarantees l >= 1; refuse anything else
+        if (lane == 0) atomicAdd(&ctr->overflow, 1ull);
+        return;
+    }
+    const int64_t nb = (int64_t)wave_atomic_add(&ctr->n_nodes, (unsigned long long)k, lane);
+    const int64_t pb = rest > 0 ? (int64_t)wave_atomic_add(&ctr->n_pool, (unsigned long long)rest, lane) : 0;
+    if (nb + k > F.cap_nodes || pb + rest > F.cap_pool) {
+        if (lane == 0) atomicAdd(&ctr->overflow, 1ull);
+        return;
+    }
+    const Node old = F.nodes[r.c];
+    Node lower = old;
+    lower.tok = F.pool[old.lab_off + r.l];
+    lower.lab_off = old.lab_off + (uint32_t)r.l;
+    lower.lab_len = old.lab_len - r.l;
+    lower.aux = 0;
+    int64_t pos_lower = nb, pos_leaf = nb + 1;
+    if (rest > 0 && s[r.d + r.l] < lower.tok) {
+        pos_leaf = nb;
+        pos_lower = nb + 1;
+    }
+    if (rest > 0) copy_tokens(F.pool + pb, s + r.d + r.l, rest, lane);
+    copy_mext(F, pos_lower, r.c, lane);
+    if (rest > 0) zero_mext(F, pos_leaf, lane);
+    if (lane == 0) {
+        F.nodes[pos_lower] = lower;
+        F.ntok[pos_lower] = lower.tok;
+        if (rest > 0) {
+            Node leaf;
+            leaf.tok = s[r.d + r.l];
+            leaf.lab_off = (uint32_t)pb;
+            leaf.lab_len = (int32_t)rest;
+            leaf.ct_beg = 0;
+            leaf.ct_cnt = 0;
+            leaf.aux = 0;
+            leaf.mask0 = 0ull;
+            F.nodes[pos_leaf] = leaf;
+            F.ntok[pos_leaf] = leaf.tok;
+        }
+        Node upper = old;  // keeps tok, label start, peers and c's slot in its parent
+        upper.lab_len = r.l;
+        upper.ct_beg = (int32_t)nb;
+        upper.ct_cnt = k;
+        upper.aux = 0;
+        F.nodes[r.c] = upper;
+    }
+}
+
+// Sort keys of ADD inserts: (parent, next token) in (unsigned, signed) order;
+// other inserts sort last.  A stable sort keeps batch order inside a slot.
+__global__ void add_keys_kernel(Batch B, const InsState *st, unsigned long long *keys, int32_t *vals) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= B.n) return;
+    const InsState r = st[i];
+    keys[i] = r.kind == kInsAdd ? (((unsigned long long)(uint32_t)r.x << 32) | (uint32_t)(r.t ^ (int32_t)0x80000000))
+                                : ~0ull;
+    vals[i] = (int32_t)i;
+}
+
+__device__ __forceinline__ int32_t key_parent(unsigned long long k) { return (int32_t)(k >> 32); }
+
+// For each group of sorted ADD entries with one parent: the records its new
+// child block needs (old children + one leaf per distinct token).
+// The group's winners (first entry of each distinct key) are compacted, in
+// token order, to win_tok / win_ins [k, k + nw) for the build kernel.
+__global__ void add_count_kernel(DevForest F, const unsigned long long *keys, const int32_t *vals, int64_t n_add,
+                                 const InsState *st, Batch B, int32_t *grp_nw, int32_t *win_tok, int32_t *win_ins,
+                                 MergeCounters *ctr) {
+    const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (k >= n_add) return;
+    if (k > 0 && key_parent(keys[k - 1]) == key_parent(keys[k])) return;  // not a group head
+    const int32_t x = key_parent(keys[k]);
+    int32_t nw = 0;
+    unsigned long long pool = 0;
+    for (int64_t e = k; e < n_add && key_parent(keys[e]) == x; e++) {
+        if (e == k || keys[e] != keys[e - 1]) {
+            const int32_t i = vals[e];
+            win_tok[k + nw] = st[i].t;
+            win_ins[k + nw] = i;
+            pool += (unsigned long long)(B.offsets[i + 1] - B.offsets[i] - st[i].d);
+            nw++;
+        }
+    }
+    grp_nw[k] = nw;
+    atomicAdd(&ctr->node_need, (unsigned long long)(F.nodes[x].ct_cnt + nw));
+    atomicAdd(&ctr->pool_need, pool);
+}
+
+// Number of entries of the sorted int32 array a[0..n) that are < v.
+__device__ __forceinline__ int32_t lower_count(const int32_t *a, int32_t n, int32_t v) {
+    int32_t lo = 0, hi = n;
+    while (lo < hi) {
+        const int32_t mid = (lo + hi) >> 1;
+        if (a[mid] < v)
+            lo = mid + 1;
+        else
+            hi = mid;
+    }
+    return lo;
+}
+
+// One wave per group head: write the parent's new child block.
+__global__ __launch_bounds__(64 *kMergeWavesPerBlock) void add_build_kernel(
+    DevForest F, Batch B, const unsigned long long *keys, int64_t n_add, const InsState *st,
+    const int32_t *grp_nw, const int32_t *win_tok, const int32_t *win_ins, int32_t *grp_nb, long long stamp,
+    MergeCounters *ctr) {
+    const int lane = (int)(threadIdx.x & 63);
+    const int64_t k = m_wave_index();
+    if (k >= n_add) return;
+    if (k > 0 && key_parent(keys[k - 1]) == key_parent(keys[k])) return;  // not a group head
+    const int32_t x = key_parent(keys[k]);
+    const int32_t nw = grp_nw[k];
+    const Node nx = F.nodes[x];
+    const int32_t old_cnt = nx.ct_cnt, old_beg = nx.ct_beg;
+    const int32_t cnt = old_cnt + nw;
+    // label tokens of all leaves of the group, allocated in one span
+    int64_t group_pool = 0;
+    for (int32_t w = 0; w < nw; w++) {
+        const int32_t i = win_ins[k + w];
+        group_pool += B.offsets[i + 1] - B.offsets[i] - st[i].d;
+    }
+    const int64_t nb = (int64_t)wave_atomic_add(&ctr->n_nodes, (unsigned long long)cnt, lane);
+    const int64_t pb0 = (int64_t)wave_atomic_add(&ctr->n_pool, (unsigned long long)group_pool, lane);
+    if (nb + cnt > F.cap_nodes || pb0 + group_pool > F.cap_pool) {
+        // nothing written: the parent keeps its old, consistent block
+        if (lane == 0) {
+            atomicAdd(&ctr->overflow, 1ull);
+            grp_nb[k] = -1;
+        }
+        return;
+    }
+    // old children keep their order; each moves up by the winners below it
+    for (int32_t j = lane; j < old_cnt; j += 64) {
+        const int32_t src = old_beg + j;
+        const int64_t dst = nb + j + lower_count(win_tok + k, nw, F.ntok[src]);
+        F.nodes[dst] = F.nodes[src];
+        F.ntok[dst] = F.ntok[src];
+        F.moved[src] = (stamp << 32) | (long long)(uint32_t)dst;
+    }
+    if (F.W > 1)
+        for (int32_t j = 0; j < old_cnt; j++) {
+            const int32_t src = old_beg + j;
+            const int64_t dst = nb + j + lower_count(win_tok + k, nw, F.ntok[src]);
+            copy_mext(F, dst, src, lane);
+        }
+    // one leaf per winner, holding the rest of its sequence
+    int64_t pb = pb0;
+    for (int32_t w = 0; w < nw; w++) {
+        const int32_t i = win_ins[k + w];
+        const int32_t *s = B.tokens + B.offsets[i];
+        const int64_t len = B.offsets[i + 1] - B.offsets[i];
+        const int32_t d = st[i].d;
+        const int64_t rest = len - d;  // >= 1: an ADD insert has a next token
+        const int64_t dst = nb + w + lower_count(F.ntok + old_beg, old_cnt, win_tok[k + w]);
+        copy_tokens(F.pool + pb, s + d, rest, lane);
+        zero_mext(F, dst, lane);
+        if (lane == 0) {
+            Node leaf;
+            leaf.tok = s[d];
+            leaf.lab_off = (uint32_t)pb;
+            leaf.lab_len = (int32_t)rest;
+            leaf.ct_beg = 0;
+            leaf.ct_cnt = 0;
+            leaf.aux = 0;
+            leaf.mask0 = 0ull;
+            F.nodes[dst] = leaf;
+            F.ntok[dst] = leaf.tok;
+        }
+        pb += rest;
+    }
+    if (lane == 0) grp_nb[k] = (int32_t)nb;
+}
+
+// Point every rebuilt parent at its new block, wherever its record lives now.
+__global__ void add_fix_kernel(DevForest F, const unsigned long long *keys, int64_t n_add, const int32_t *grp_nw,
+                               const int32_t *grp_nb, long long stamp) {
+    const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (k >= n_add) return;
+    if (k > 0 && key_parent(keys[k - 1]) == key_parent(keys[k])) return;
+    if (grp_nb[k] < 0) return;  // the build of this group was refused
+    const int32_t x = key_parent(keys[k]);
+    const long long mv = F.moved[x];
+    const int64_t pos = (mv >> 32) == stamp ? (int64_t)(uint32_t)mv : (int64_t)x;
+    F.nodes[pos].ct_cnt = F.nodes[pos].ct_cnt + grp_nw[k];
+    F.nodes[pos].ct_beg = grp_nb[k];
+}
+
+// OR each insert's peer bit into every node on its path (the root included).
+__global__ __launch_bounds__(64 *kMergeWavesPerBlock) void merge_mask_kernel(DevForest F, Batch B,
+                                                                            const InsState *st,
+                                                                            MergeCounters *ctr) {
+    const int lane = (int)(threadIdx.x & 63);
+    const int64_t i = m_wave_index();
+    if (i >= B.n || st[i].kind != kInsDone) return;
+    const int32_t p = B.peer_of[i];
+    const int32_t w = p >> 6;
+    const unsigned long long bit = 1ull << (p & 63);
+    const int32_t *s = B.tokens + B.offsets[i];
+    const int64_t len = B.offsets[i + 1] - B.offsets[i];
+    int32_t x = 0;
+    int64_t d = 0;
+    while (true) {
+        if (lane == 0) {
+            if (w == 0)
+                atomicOr((unsigned long long *)&F.nodes[x].mask0, bit);
+            else
+                atomicOr((unsigned long long *)&F.mext[(int64_t)x * (F.W - 1) + (w - 1)], bit);
+        }
+        if (d == len) break;
+        const Node nx = F.nodes[x];
+        const int32_t c = m_find_child(F, nx, s[d], lane);
+        const int32_t ll = c < 0 ? 0 : F.nodes[c].lab_len;
+        if (c < 0 || ll <= 0 || d + ll > len) {
+            if (lane == 0) atomicAdd(&ctr->bad_path, 1ull);
+            break;
+        }
+        x = c;
+        d += ll;
+    }
+}
+
+// A replaced snapshot: remove peer p from every mask (its old paths stay as
+// structure that no peer holds until something is inserted there again).
+__global__ void clear_peer_kernel(DevForest F, int64_t n_nodes, int32_t p) {
+    const int64_t x = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (x >= n_nodes) return;
+    const int32_t w = p >> 6;
+    const unsigned long long keep = ~(1ull << (p & 63));
+    if (w == 0)
+        F.nodes[x].mask0 &= keep;
+    else
+        F.mext[x * (F.W - 1) + (w - 1)] &= keep;
+}
+
+// Fill a peer id array (snapshot loads insert every sequence into one peer).
+__global__ void fill_peer_kernel(int32_t *peer_of, int64_t n, int32_t p) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) peer_of[i] = p;
+}
+
+}  // namespace pr
+
+#endif

@@ -25,6 +25,7 @@
 #include <stdint.h>
 
 #include "forest_layout.h"
+#include "wave_ops.h"
 
 namespace pr {
 
@@ -42,14 +43,6 @@ constexpr int kWave = 64;
 constexpr int kRouteWavesPerBlock = PR_ROUTE_WAVES_PER_BLOCK;
 constexpr int kLcpVectors = PR_LCP_VECTORS;    // 64-token vectors compared per step
 constexpr int kWideVectors = PR_WIDE_VECTORS;  // first tokens held per lane for wide blocks
-
-__device__ __forceinline__ int32_t uniform(int32_t v) { return __builtin_amdgcn_readfirstlane(v); }
-
-__device__ __forceinline__ uint64_t readlane64(uint64_t v, int src) {
-    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, src);
-    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), src);
-    return ((uint64_t)hi << 32) | lo;
-}
 
 // Length of the common prefix of a[0..n) and b[0..n): the first i < n with
 // a[i] != b[i], or n.  Wave-cooperative; every lane returns the same value.

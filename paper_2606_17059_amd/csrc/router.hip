@@ -1,19 +1,22 @@
 // router.hip -- C ABI of the gfx950 prefix-cache-aware router (see
 // include/prefix_router.h for the contract of every entry point).
 //
-// Host side: per-peer snapshot copies, the union-forest build, device memory,
-// argument checks and launches.  Device side: route_kernels.h.
+// Host side: per-peer snapshot copies, the union-forest build, device memory
+// with spare capacity for merges, argument checks, the merge round loop and
+// launches.  Device side: route_kernels.h, merge_kernels.h.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
 #include <cstdio>
 #include <cstring>
 #include <new>
+#include <rocprim/device/device_radix_sort.hpp>
 #include <string>
 #include <vector>
 
 #include "forest_host.h"
 #include "forest_layout.h"
+#include "merge_kernels.h"
 #include "prefix_router.h"
 #include "route_kernels.h"
 
@@ -33,13 +36,31 @@ pr_status ok() {
     return PR_OK;
 }
 
+// Device arrays of the forest.  Node ids and pool offsets never move: growing
+// a capacity copies the arrays into larger ones.
 struct DevImage {
     Node *nodes = nullptr;
     int32_t *ntok = nullptr;
     uint64_t *mext = nullptr;
     int32_t *pool = nullptr;
-    int64_t n_nodes = 0, n_pool = 0;
-    int64_t bytes = 0;
+    long long *moved = nullptr;
+    int64_t cap_nodes = 0, cap_pool = 0;
+    int64_t n_nodes = 0, n_pool = 0;  // host mirror of the device counters
+};
+
+// Scratch of one merge call, kept between calls and grown on demand.
+struct MergeScratch {
+    pr::InsState *st = nullptr;
+    unsigned long long *keys_in = nullptr, *keys_out = nullptr;
+    int32_t *vals_in = nullptr, *vals_out = nullptr;
+    int32_t *grp_nw = nullptr, *grp_nb = nullptr, *win_tok = nullptr, *win_ins = nullptr;
+    int64_t cap = 0;
+    void *sort_tmp = nullptr;
+    size_t sort_tmp_bytes = 0;
+    // snapshot loads on the device path stage their host batch here
+    int32_t *load_tok = nullptr, *load_peer = nullptr;
+    int64_t *load_off = nullptr;
+    int64_t load_tok_cap = 0, load_seq_cap = 0;
 };
 
 }  // namespace
@@ -49,12 +70,17 @@ struct pr_forest {
     int32_t W = 1;
     int device = -1;
     std::vector<pr::PeerSeqs> sets;
-    bool dirty = true;  // host sets changed since the device image was built
+    bool dirty = true;            // host sets changed since the device image was built
+    bool merged = false;          // the device image holds merges the host sets lack
     pr::HostImage host_img;
     bool host_img_valid = false;
     DevImage dev;
     bool has_dev = false;
+    pr::MergeCounters *d_ctr = nullptr;
     unsigned long long *d_skipped = nullptr;  // inputs skipped by device calls
+    MergeScratch ms;
+    long long stamp = 0;          // add-round counter (stamps of moved records)
+    int64_t device_bytes = 0;
 };
 
 namespace {
@@ -82,12 +108,55 @@ class DeviceScope {
     bool switched_ = false;
 };
 
-void free_image(DevImage *d) {
-    (void)hipFree(d->nodes);
-    (void)hipFree(d->ntok);
-    (void)hipFree(d->mext);
-    (void)hipFree(d->pool);
-    *d = DevImage();
+template <typename T>
+bool dalloc(pr_forest *f, T **p, int64_t count) {
+    const size_t n = (size_t)std::max<int64_t>(count, 1) * sizeof(T);
+    if (hipMalloc((void **)p, n) != hipSuccess) {
+        (void)hipGetLastError();
+        *p = nullptr;
+        return false;
+    }
+    f->device_bytes += (int64_t)n;
+    return true;
+}
+
+template <typename T>
+void dfree(pr_forest *f, T **p, int64_t count) {
+    if (*p) {
+        (void)hipFree(*p);
+        f->device_bytes -= (int64_t)((size_t)std::max<int64_t>(count, 1) * sizeof(T));
+    }
+    *p = nullptr;
+}
+
+void free_image(pr_forest *f) {
+    DevImage &d = f->dev;
+    dfree(f, &d.nodes, d.cap_nodes);
+    dfree(f, &d.ntok, d.cap_nodes);
+    dfree(f, &d.mext, d.cap_nodes * (f->W - 1));
+    dfree(f, &d.moved, d.cap_nodes);
+    dfree(f, &d.pool, d.cap_pool);
+    d = DevImage();
+    f->has_dev = false;
+}
+
+void free_scratch(pr_forest *f) {
+    MergeScratch &m = f->ms;
+    dfree(f, &m.st, m.cap);
+    dfree(f, &m.keys_in, m.cap);
+    dfree(f, &m.keys_out, m.cap);
+    dfree(f, &m.vals_in, m.cap);
+    dfree(f, &m.vals_out, m.cap);
+    dfree(f, &m.grp_nw, m.cap);
+    dfree(f, &m.grp_nb, m.cap);
+    dfree(f, &m.win_tok, m.cap);
+    dfree(f, &m.win_ins, m.cap);
+    if (m.sort_tmp) (void)hipFree(m.sort_tmp);
+    f->device_bytes -= (int64_t)m.sort_tmp_bytes;
+    dfree(f, &m.load_tok, m.load_tok_cap);
+    dfree(f, &m.load_peer, m.load_seq_cap);
+    dfree(f, &m.load_off, m.load_seq_cap + 1);
+    m = MergeScratch();
 }
 
 pr_status ensure_host_image(pr_forest *f) {
@@ -100,16 +169,57 @@ pr_status ensure_host_image(pr_forest *f) {
     return PR_OK;
 }
 
-template <typename T>
-pr_status upload(T **dst, const std::vector<T> &src, int64_t *bytes) {
-    const size_t n = std::max<size_t>(src.size(), 1) * sizeof(T);
-    if (hipMalloc((void **)dst, n) != hipSuccess) {
-        (void)hipGetLastError();
-        return fail(PR_ENOMEM, "hipMalloc failed for the forest image");
+// Grow the node and pool capacities to hold at least the given totals.
+pr_status ensure_capacity(pr_forest *f, int64_t need_nodes, int64_t need_pool, hipStream_t s) {
+    DevImage &d = f->dev;
+    if (need_pool > (int64_t)UINT32_MAX) return fail(PR_ENOMEM, "label pool would exceed 2^32 tokens");
+    if (need_nodes > (int64_t)INT32_MAX) return fail(PR_ENOMEM, "node count would exceed 2^31");
+    if (need_nodes > d.cap_nodes) {
+        const int64_t cap = std::min<int64_t>(std::max<int64_t>(need_nodes, d.cap_nodes + d.cap_nodes / 2),
+                                              (int64_t)INT32_MAX);
+        Node *nn = nullptr;
+        int32_t *nt = nullptr;
+        uint64_t *nm = nullptr;
+        long long *mv = nullptr;
+        if (!dalloc(f, &nn, cap) || !dalloc(f, &nt, cap) || !dalloc(f, &nm, cap * (f->W - 1)) ||
+            !dalloc(f, &mv, cap)) {
+            dfree(f, &nn, cap);
+            dfree(f, &nt, cap);
+            dfree(f, &nm, cap * (f->W - 1));
+            dfree(f, &mv, cap);
+            return fail(PR_ENOMEM, "hipMalloc failed while growing the forest");
+        }
+        const int64_t n = d.n_nodes;
+        if (hipMemcpyAsync(nn, d.nodes, n * sizeof(Node), hipMemcpyDeviceToDevice, s) != hipSuccess ||
+            hipMemcpyAsync(nt, d.ntok, n * sizeof(int32_t), hipMemcpyDeviceToDevice, s) != hipSuccess ||
+            (f->W > 1 && hipMemcpyAsync(nm, d.mext, n * (f->W - 1) * sizeof(uint64_t), hipMemcpyDeviceToDevice,
+                                        s) != hipSuccess) ||
+            hipMemcpyAsync(mv, d.moved, d.cap_nodes * sizeof(long long), hipMemcpyDeviceToDevice, s) != hipSuccess ||
+            hipMemsetAsync(mv + d.cap_nodes, 0, (cap - d.cap_nodes) * sizeof(long long), s) != hipSuccess ||
+            hipStreamSynchronize(s) != hipSuccess)
+            return fail(PR_EDEVICE, "device copy failed while growing the forest");
+        dfree(f, &d.nodes, d.cap_nodes);
+        dfree(f, &d.ntok, d.cap_nodes);
+        dfree(f, &d.mext, d.cap_nodes * (f->W - 1));
+        dfree(f, &d.moved, d.cap_nodes);
+        d.nodes = nn;
+        d.ntok = nt;
+        d.mext = nm;
+        d.moved = mv;
+        d.cap_nodes = cap;
     }
-    *bytes += (int64_t)n;
-    if (!src.empty() && hipMemcpy(*dst, src.data(), src.size() * sizeof(T), hipMemcpyHostToDevice) != hipSuccess)
-        return fail(PR_EDEVICE, "hipMemcpy of the forest image failed");
+    if (need_pool > d.cap_pool) {
+        const int64_t cap = std::min<int64_t>(std::max<int64_t>(need_pool, d.cap_pool + d.cap_pool / 2),
+                                              (int64_t)UINT32_MAX);
+        int32_t *np = nullptr;
+        if (!dalloc(f, &np, cap)) return fail(PR_ENOMEM, "hipMalloc failed while growing the label pool");
+        if (hipMemcpyAsync(np, d.pool, d.n_pool * sizeof(int32_t), hipMemcpyDeviceToDevice, s) != hipSuccess ||
+            hipStreamSynchronize(s) != hipSuccess)
+            return fail(PR_EDEVICE, "device copy failed while growing the label pool");
+        dfree(f, &d.pool, d.cap_pool);
+        d.pool = np;
+        d.cap_pool = cap;
+    }
     return PR_OK;
 }
 
@@ -119,26 +229,44 @@ pr_status commit(pr_forest *f) {
     pr_status s = ensure_host_image(f);
     if (s) return s;
     if (!f->d_skipped) {
-        if (hipMalloc((void **)&f->d_skipped, sizeof(unsigned long long)) != hipSuccess)
-            return fail(PR_ENOMEM, "hipMalloc failed");
+        if (!dalloc(f, &f->d_skipped, 1) || !dalloc(f, &f->d_ctr, 1)) return fail(PR_ENOMEM, "hipMalloc failed");
         if (hipMemset(f->d_skipped, 0, sizeof(unsigned long long)) != hipSuccess)
             return fail(PR_EDEVICE, "hipMemset failed");
     }
     // earlier launches may still read the old image
     if (f->has_dev && hipDeviceSynchronize() != hipSuccess) return fail(PR_EDEVICE, "hipDeviceSynchronize failed");
-    DevImage d;
+    if (f->has_dev) free_image(f);
     const pr::HostImage &h = f->host_img;
-    if ((s = upload(&d.nodes, h.nodes, &d.bytes)) || (s = upload(&d.ntok, h.ntok, &d.bytes)) ||
-        (s = upload(&d.mext, h.mext, &d.bytes)) || (s = upload(&d.pool, h.pool, &d.bytes))) {
-        free_image(&d);
-        return s;
+    DevImage &d = f->dev;
+    const int64_t n = (int64_t)h.nodes.size(), np = (int64_t)h.pool.size();
+    d.cap_nodes = std::max<int64_t>(n + n / 8, 1024);
+    d.cap_pool = std::max<int64_t>(np + np / 8, 4096);
+    if (!dalloc(f, &d.nodes, d.cap_nodes) || !dalloc(f, &d.ntok, d.cap_nodes) ||
+        !dalloc(f, &d.mext, d.cap_nodes * (f->W - 1)) || !dalloc(f, &d.moved, d.cap_nodes) ||
+        !dalloc(f, &d.pool, d.cap_pool)) {
+        free_image(f);
+        return fail(PR_ENOMEM, "hipMalloc failed for the forest image");
     }
-    d.n_nodes = (int64_t)h.nodes.size();
-    d.n_pool = (int64_t)h.pool.size();
-    if (f->has_dev) free_image(&f->dev);
-    f->dev = d;
+    if (hipMemcpy(d.nodes, h.nodes.data(), n * sizeof(Node), hipMemcpyHostToDevice) != hipSuccess ||
+        hipMemcpy(d.ntok, h.ntok.data(), n * sizeof(int32_t), hipMemcpyHostToDevice) != hipSuccess ||
+        (f->W > 1 && hipMemcpy(d.mext, h.mext.data(), h.mext.size() * sizeof(uint64_t), hipMemcpyHostToDevice) !=
+                         hipSuccess) ||
+        (np > 0 && hipMemcpy(d.pool, h.pool.data(), np * sizeof(int32_t), hipMemcpyHostToDevice) != hipSuccess) ||
+        hipMemset(d.moved, 0, d.cap_nodes * sizeof(long long)) != hipSuccess) {
+        free_image(f);
+        return fail(PR_EDEVICE, "upload of the forest image failed");
+    }
+    d.n_nodes = n;
+    d.n_pool = np;
+    pr::MergeCounters c;
+    std::memset(&c, 0, sizeof(c));
+    c.n_nodes = (unsigned long long)n;
+    c.n_pool = (unsigned long long)np;
+    if (hipMemcpy(f->d_ctr, &c, sizeof(c), hipMemcpyHostToDevice) != hipSuccess)
+        return fail(PR_EDEVICE, "counter upload failed");
     f->has_dev = true;
     f->dirty = false;
+    f->merged = false;
     // the device image is the state of record now; drop the host copy of it
     f->host_img = pr::HostImage();
     f->host_img_valid = false;
@@ -152,6 +280,190 @@ hipError_t launch_route(const pr_forest *f, const int32_t *qt, int64_t ntok, con
     hipLaunchKernelGGL(pr::route_kernel<W>, dim3((unsigned)blocks), dim3(pr::kWave * pr::kRouteWavesPerBlock), 0, s,
                        f->dev.nodes, f->dev.ntok, f->dev.mext, f->dev.pool, qt, ntok, qo, nq, f->P, ml, ch);
     return hipGetLastError();
+}
+
+// ---- merge ------------------------------------------------------------------
+
+pr_status ensure_merge_scratch(pr_forest *f, int64_t n, hipStream_t s) {
+    MergeScratch &m = f->ms;
+    if (n > m.cap) {
+        const int64_t cap = std::max<int64_t>(n, m.cap * 2);
+        dfree(f, &m.st, m.cap);
+        dfree(f, &m.keys_in, m.cap);
+        dfree(f, &m.keys_out, m.cap);
+        dfree(f, &m.vals_in, m.cap);
+        dfree(f, &m.vals_out, m.cap);
+        dfree(f, &m.grp_nw, m.cap);
+        dfree(f, &m.grp_nb, m.cap);
+        dfree(f, &m.win_tok, m.cap);
+        dfree(f, &m.win_ins, m.cap);
+        m.cap = 0;
+        if (!dalloc(f, &m.st, cap) || !dalloc(f, &m.keys_in, cap) || !dalloc(f, &m.keys_out, cap) ||
+            !dalloc(f, &m.vals_in, cap) || !dalloc(f, &m.vals_out, cap) || !dalloc(f, &m.grp_nw, cap) ||
+            !dalloc(f, &m.grp_nb, cap) || !dalloc(f, &m.win_tok, cap) || !dalloc(f, &m.win_ins, cap)) {
+            free_scratch(f);
+            return fail(PR_ENOMEM, "hipMalloc failed for merge scratch");
+        }
+        m.cap = cap;
+    }
+    size_t need = 0;
+    if (rocprim::radix_sort_pairs(nullptr, need, m.keys_in, m.keys_out, m.vals_in, m.vals_out, n, 0, 64, s) !=
+        hipSuccess)
+        return fail(PR_EDEVICE, "radix sort size query failed");
+    if (need > m.sort_tmp_bytes) {
+        if (m.sort_tmp) (void)hipFree(m.sort_tmp);
+        f->device_bytes -= (int64_t)m.sort_tmp_bytes;
+        m.sort_tmp_bytes = 0;
+        m.sort_tmp = nullptr;
+        if (hipMalloc(&m.sort_tmp, need) != hipSuccess) {
+            (void)hipGetLastError();
+            return fail(PR_ENOMEM, "hipMalloc failed for sort scratch");
+        }
+        m.sort_tmp_bytes = need;
+        f->device_bytes += (int64_t)need;
+    }
+    return PR_OK;
+}
+
+__global__ void reset_round_kernel(pr::MergeCounters *c) {
+    c->n_add = 0;
+    c->n_split = 0;
+    c->pool_need = 0;
+    c->node_need = 0;
+}
+
+__global__ void reset_call_kernel(pr::MergeCounters *c) {
+    c->n_add = 0;
+    c->n_split = 0;
+    c->pool_need = 0;
+    c->node_need = 0;
+    c->overflow = 0;
+    c->skipped = 0;
+    c->bad_path = 0;
+}
+
+__global__ void add_skipped_kernel(unsigned long long *acc, const pr::MergeCounters *c) { *acc += c->skipped; }
+
+pr_status read_counters(pr_forest *f, pr::MergeCounters *c, hipStream_t s) {
+    if (hipMemcpyAsync(c, f->d_ctr, sizeof(*c), hipMemcpyDeviceToHost, s) != hipSuccess ||
+        hipStreamSynchronize(s) != hipSuccess)
+        return fail(PR_EDEVICE, "reading merge counters failed");
+    return PR_OK;
+}
+
+pr::DevForest dev_view(const pr_forest *f) {
+    pr::DevForest F;
+    F.nodes = f->dev.nodes;
+    F.ntok = f->dev.ntok;
+    F.mext = f->dev.mext;
+    F.pool = f->dev.pool;
+    F.moved = f->dev.moved;
+    F.cap_nodes = f->dev.cap_nodes;
+    F.cap_pool = f->dev.cap_pool;
+    F.W = f->W;
+    return F;
+}
+
+unsigned grid_threads(int64_t n, int bs) { return (unsigned)((n + bs - 1) / bs); }
+unsigned grid_waves(int64_t n) { return (unsigned)((n + pr::kMergeWavesPerBlock - 1) / pr::kMergeWavesPerBlock); }
+
+// Insert a device batch into the device forest (see merge_kernels.h).
+pr_status run_merge(pr_forest *f, const int32_t *peer_of, const int32_t *tokens, int64_t num_tokens,
+                    const int64_t *offsets, int64_t n, hipStream_t s) {
+    pr_status r = ensure_merge_scratch(f, n, s);
+    if (r) return r;
+    MergeScratch &m = f->ms;
+    pr::Batch B{peer_of, tokens, offsets, num_tokens, n, f->P};
+    const int bs = 256, wb = 64 * pr::kMergeWavesPerBlock;
+    hipLaunchKernelGGL(reset_call_kernel, dim3(1), dim3(1), 0, s, f->d_ctr);
+    hipLaunchKernelGGL(pr::merge_validate_kernel, dim3(grid_threads(n, bs)), dim3(bs), 0, s, B, m.st, f->d_ctr);
+    pr::MergeCounters c;
+    const int max_rounds = 100000;
+    int round = 0;
+    for (; round < max_rounds; round++) {
+        hipLaunchKernelGGL(reset_round_kernel, dim3(1), dim3(1), 0, s, f->d_ctr);
+        hipLaunchKernelGGL(pr::merge_walk_kernel, dim3(grid_waves(n)), dim3(wb), 0, s, dev_view(f), B, m.st,
+                           f->d_ctr);
+        if ((r = read_counters(f, &c, s))) return r;
+        if (c.overflow) break;  // reported below; the forest stays consistent
+        if (c.n_split > 0) {
+            if ((r = ensure_capacity(f, (int64_t)c.n_nodes + 2 * (int64_t)c.n_split,
+                                     (int64_t)c.n_pool + (int64_t)c.pool_need, s)))
+                return r;
+            const pr::DevForest F = dev_view(f);
+            hipLaunchKernelGGL(pr::split_claim_kernel, dim3(grid_threads(n, bs)), dim3(bs), 0, s, F, B, m.st);
+            hipLaunchKernelGGL(pr::split_apply_kernel, dim3(grid_waves(n)), dim3(wb), 0, s, F, B, m.st, f->d_ctr);
+        } else if (c.n_add > 0) {
+            const int64_t n_add = (int64_t)c.n_add;
+            hipLaunchKernelGGL(pr::add_keys_kernel, dim3(grid_threads(n, bs)), dim3(bs), 0, s, B, m.st, m.keys_in,
+                               m.vals_in);
+            size_t tmp = m.sort_tmp_bytes;
+            if (rocprim::radix_sort_pairs(m.sort_tmp, tmp, m.keys_in, m.keys_out, m.vals_in, m.vals_out, n, 0, 64,
+                                          s) != hipSuccess)
+                return fail(PR_EDEVICE, "radix sort failed");
+            hipLaunchKernelGGL(reset_round_kernel, dim3(1), dim3(1), 0, s, f->d_ctr);
+            hipLaunchKernelGGL(pr::add_count_kernel, dim3(grid_threads(n_add, bs)), dim3(bs), 0, s, dev_view(f),
+                               m.keys_out, m.vals_out, n_add, m.st, B, m.grp_nw, m.win_tok, m.win_ins, f->d_ctr);
+            if ((r = read_counters(f, &c, s))) return r;
+            if ((r = ensure_capacity(f, (int64_t)c.n_nodes + (int64_t)c.node_need,
+                                     (int64_t)c.n_pool + (int64_t)c.pool_need, s)))
+                return r;
+            const long long stamp = ++f->stamp;
+            const pr::DevForest F = dev_view(f);
+            hipLaunchKernelGGL(pr::add_build_kernel, dim3(grid_waves(n_add)), dim3(wb), 0, s, F, B, m.keys_out,
+                               n_add, m.st, m.grp_nw, m.win_tok, m.win_ins, m.grp_nb, stamp, f->d_ctr);
+            hipLaunchKernelGGL(pr::add_fix_kernel, dim3(grid_threads(n_add, bs)), dim3(bs), 0, s, F, m.keys_out,
+                               n_add, m.grp_nw, m.grp_nb, stamp);
+        } else {
+            break;
+        }
+        if (hipGetLastError() != hipSuccess) return fail(PR_EDEVICE, "merge launch failed");
+    }
+    if (round == max_rounds) return fail(PR_EDEVICE, "merge did not converge");
+    hipLaunchKernelGGL(pr::merge_mask_kernel, dim3(grid_waves(n)), dim3(wb), 0, s, dev_view(f), B, m.st, f->d_ctr);
+    hipLaunchKernelGGL(add_skipped_kernel, dim3(1), dim3(1), 0, s, f->d_skipped, f->d_ctr);
+    if (hipGetLastError() != hipSuccess) return fail(PR_EDEVICE, "merge launch failed");
+    if ((r = read_counters(f, &c, s))) return r;
+    f->dev.n_nodes = (int64_t)c.n_nodes;
+    f->dev.n_pool = (int64_t)c.n_pool;
+    if (c.overflow || c.bad_path)
+        return fail(PR_EDEVICE, "merge invariant broken (overflow " + std::to_string(c.overflow) + ", bad paths " +
+                                    std::to_string(c.bad_path) + "); destroy the forest");
+    f->merged = true;
+    return PR_OK;
+}
+
+// Snapshot load once merges have run: the host copies no longer describe the
+// device forest, so the replacement happens on the device: clear the peer from
+// every mask, then insert the snapshot for it.
+pr_status device_load(pr_forest *f, int32_t peer, const pr::PeerSeqs &S) {
+    MergeScratch &m = f->ms;
+    const int64_t ns = S.count(), nt = (int64_t)S.tokens.size();
+    if (nt > m.load_tok_cap) {
+        dfree(f, &m.load_tok, m.load_tok_cap);
+        m.load_tok_cap = 0;
+        if (!dalloc(f, &m.load_tok, nt)) return fail(PR_ENOMEM, "hipMalloc failed for the snapshot");
+        m.load_tok_cap = nt;
+    }
+    if (ns > m.load_seq_cap) {
+        dfree(f, &m.load_peer, m.load_seq_cap);
+        dfree(f, &m.load_off, m.load_seq_cap + 1);
+        m.load_seq_cap = 0;
+        if (!dalloc(f, &m.load_peer, ns) || !dalloc(f, &m.load_off, ns + 1))
+            return fail(PR_ENOMEM, "hipMalloc failed for the snapshot");
+        m.load_seq_cap = ns;
+    }
+    hipStream_t s = nullptr;
+    if ((nt > 0 && hipMemcpy(m.load_tok, S.tokens.data(), nt * sizeof(int32_t), hipMemcpyHostToDevice) != hipSuccess) ||
+        hipMemcpy(m.load_off, S.offsets.data(), (ns + 1) * sizeof(int64_t), hipMemcpyHostToDevice) != hipSuccess)
+        return fail(PR_EDEVICE, "snapshot upload failed");
+    hipLaunchKernelGGL(pr::clear_peer_kernel, dim3(grid_threads(f->dev.n_nodes, 256)), dim3(256), 0, s,
+                       dev_view(f), f->dev.n_nodes, peer);
+    if (ns > 0)
+        hipLaunchKernelGGL(pr::fill_peer_kernel, dim3(grid_threads(ns, 256)), dim3(256), 0, s, m.load_peer, ns, peer);
+    if (hipGetLastError() != hipSuccess) return fail(PR_EDEVICE, "snapshot kernels failed to launch");
+    if (ns == 0) return hipStreamSynchronize(s) == hipSuccess ? PR_OK : fail(PR_EDEVICE, "sync failed");
+    return run_merge(f, m.load_peer, m.load_tok, nt, m.load_off, ns, s);
 }
 
 }  // namespace
@@ -186,8 +498,10 @@ void pr_forest_destroy(pr_forest *f) {
     if (f->device >= 0) {
         DeviceScope ds(f);
         (void)hipDeviceSynchronize();
-        if (f->has_dev) free_image(&f->dev);
-        (void)hipFree(f->d_skipped);
+        free_image(f);
+        free_scratch(f);
+        dfree(f, &f->d_skipped, 1);
+        dfree(f, &f->d_ctr, 1);
     }
     delete f;
 }
@@ -201,14 +515,23 @@ pr_status pr_load_snapshot(pr_forest *f, int32_t peer, const int32_t *tokens, co
     if (offsets[0] != 0) return fail(PR_EINVAL, "offsets[0] != 0");
     for (int64_t i = 0; i < num_seqs; i++)
         if (offsets[i + 1] < offsets[i]) return fail(PR_EINVAL, "offsets decrease at sequence " + std::to_string(i));
+    if (offsets[num_seqs] > 0 && !tokens) return fail(PR_EINVAL, "tokens is NULL");
+    if (num_seqs > (int64_t)INT32_MAX) return fail(PR_EINVAL, "too many sequences");
     const int64_t ntok = offsets[num_seqs];
-    if (ntok > 0 && !tokens) return fail(PR_EINVAL, "tokens is NULL");
     pr::PeerSeqs S;
     try {
         S.tokens.assign(tokens, tokens + ntok);
         S.offsets.assign(offsets, offsets + num_seqs + 1);
     } catch (const std::bad_alloc &) {
         return fail(PR_ENOMEM, "host allocation failed");
+    }
+    if (f->has_dev && f->merged) {
+        DeviceScope ds(f);
+        if (!ds.ok()) return fail(PR_EDEVICE, "cannot select the forest's device");
+        pr_status r = device_load(f, peer, S);
+        if (r) return r;
+        f->sets[(size_t)peer] = std::move(S);
+        return ok();
     }
     f->sets[(size_t)peer] = std::move(S);
     f->dirty = true;
@@ -218,14 +541,19 @@ pr_status pr_load_snapshot(pr_forest *f, int32_t peer, const int32_t *tokens, co
 
 pr_status pr_merge(pr_forest *f, const int32_t *peer_of, const int32_t *tokens, int64_t num_tokens,
                    const int64_t *offsets, int64_t num_seqs, void *hip_stream) {
-    (void)peer_of;
-    (void)tokens;
-    (void)num_tokens;
-    (void)offsets;
-    (void)hip_stream;
     if (!f) return fail(PR_EINVAL, "forest is NULL");
-    if (num_seqs < 0) return fail(PR_EINVAL, "num_seqs < 0");
-    return fail(PR_ESTATE, "pr_merge is not available in this build");
+    if (num_seqs < 0 || num_tokens < 0) return fail(PR_EINVAL, "negative count");
+    if (num_seqs == 0) return ok();
+    if (!peer_of || !offsets) return fail(PR_EINVAL, "NULL device pointer");
+    if (num_tokens > 0 && !tokens) return fail(PR_EINVAL, "tokens is NULL");
+    if (num_seqs > (int64_t)INT32_MAX) return fail(PR_EINVAL, "too many sequences");
+    DeviceScope ds(f);
+    if (!ds.ok()) return fail(PR_EDEVICE, "cannot select the forest's device");
+    pr_status s = commit(f);
+    if (s) return s;
+    s = run_merge(f, peer_of, tokens, num_tokens, offsets, num_seqs, (hipStream_t)hip_stream);
+    if (s) return s;
+    return ok();
 }
 
 pr_status pr_route(pr_forest *f, const int32_t *q_tokens, int64_t num_tokens, const int64_t *q_offsets,
@@ -278,7 +606,7 @@ pr_status pr_forest_info_get(pr_forest *f, pr_forest_info *out) {
         out->num_nodes = (int64_t)f->host_img.nodes.size();
         out->pool_tokens = (int64_t)f->host_img.pool.size();
     }
-    out->device_bytes = f->has_dev ? f->dev.bytes : 0;
+    out->device_bytes = f->device_bytes;
     int64_t t = 0;
     for (const auto &S : f->sets) t += (int64_t)S.tokens.size();
     out->host_seq_tokens = t;
@@ -287,6 +615,7 @@ pr_status pr_forest_info_get(pr_forest *f, pr_forest_info *out) {
 
 pr_status pr_forest_host_image(pr_forest *f, pr_image_view *out) {
     if (!f || !out) return fail(PR_EINVAL, "NULL argument");
+    if (f->merged) return fail(PR_ESTATE, "the device forest holds merges; the host copies do not describe it");
     pr_status s = ensure_host_image(f);
     if (s) return s;
     const pr::HostImage &h = f->host_img;

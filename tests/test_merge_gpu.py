@@ -1,0 +1,212 @@
+"""Delta-merge parity on the GPU: batches of inserts applied by the HIP merge
+kernels (updateTrie / updateTrieEstimate), then routed, versus the CPU oracle
+given the same snapshots and inserts.  Bit-exact on every output."""
+import numpy as np
+import pytest
+
+import oracle
+import pins
+import workloads as W
+from gpu_util import (announce, assert_properties, assert_rows_equal, device, gpu_route, nthreads,
+                      oracle_for, to_dev)
+
+pytestmark = pytest.mark.gpu
+
+
+def _merge(f, ins, label=""):
+    import torch
+    dev = device()
+    announce(f"merge {label}: {len(ins)} inserts")
+    peer = torch.from_numpy(np.ascontiguousarray(ins.peer, dtype=np.int32)).to(dev)
+    t, o = to_dev(ins)
+    f.merge(peer, t, o)
+    torch.cuda.synchronize()
+
+
+def _forest(snapshot, P):
+    from paper_2606_17059_amd import Forest
+    f = Forest(P)
+    if snapshot is not None:
+        f.load_seqset(snapshot)
+    return f
+
+
+def test_golden_examples_with_merges():
+    from paper_2606_17059_amd import Forest
+    import torch
+    dev = device()
+    for ex in pins.parse_golden():
+        f = Forest(ex.peers)
+        for op in ex.ops:
+            if op[0] == "load":
+                t, o = pins._csr(op[2])
+                f.load_snapshot(op[1], t, o)
+            elif op[0] == "merge":
+                t, o = pins._csr([s for _, s in op[1]])
+                ins = W.SeqSet(t, o, np.array([p for p, _ in op[1]], np.int32))
+                _merge(f, ins, ex.name)
+            else:
+                _, q, m_exp, c_exp = op
+                t, o = pins._csr([q])
+                announce(f"golden {ex.name} q={q}")
+                m, c = f.route(torch.from_numpy(t).to(dev), torch.from_numpy(o).to(dev))
+                assert m.cpu().numpy()[0].tolist() == m_exp and int(c.cpu()[0]) == c_exp, (ex.name, q)
+        f.close()
+
+
+def _random_batch(seed, P, vocab, n):
+    w = W.tiny_random(seed, num_peers=P, vocab=vocab, max_seqs=max(1, n // P), n_queries=1)
+    return w.snapshot
+
+
+@pytest.mark.parametrize("vocab", [2, 3, 8])
+def test_tiny_random_merge_sequences(vocab):
+    """Snapshots, then three merge batches; every route compared with the oracle."""
+    for sd in range(12):
+        P = [1, 3, 5, 64, 65, 130][sd % 6]
+        base = W.tiny_random(sd, num_peers=P, vocab=vocab, max_seqs=8 if P < 10 else 2, n_queries=60)
+        f = _forest(base.snapshot if sd % 3 else None, P)  # every third case starts empty
+        o = oracle.Oracle(P)
+        if sd % 3:
+            pins.load_all(o, base.snapshot, P)
+        for r in range(3):
+            ins = _random_batch(1000 * sd + r, P, vocab, 24)
+            if len(ins) == 0:
+                continue
+            _merge(f, ins, f"vocab={vocab} seed={sd} batch={r}")
+            o.merge(ins.peer, ins.tokens, ins.offsets)
+            m, c = gpu_route(f, base.queries, f"after batch {r}")
+            m_or, c_or = o.route(base.queries.tokens, base.queries.offsets, 2)
+            assert_rows_equal(m, c, m_or, c_or, what=f"vocab={vocab} seed={sd} batch={r}")
+            # cached prompts as queries: every inserted sequence matches its owner in full
+            mi, _ = gpu_route(f, ins, "inserted sequences as queries")
+            assert np.array_equal(mi[np.arange(len(ins)), ins.peer], ins.lengths())
+        f.check()
+        f.close()
+
+
+def test_duplicates_prefixes_and_shared_new_prefixes_in_one_batch():
+    """Inserts that duplicate each other, are prefixes of each other, or share a
+    long new prefix, all in one batch (several rounds of splits and adds)."""
+    rng = np.random.default_rng(5)
+    P = 4
+    shared = rng.integers(0, 50, 300).astype(np.int32)
+    seqs, owners = [], []
+    for i in range(200):
+        k = int(rng.integers(0, 300))
+        tail = rng.integers(0, 50, int(rng.integers(0, 40))).astype(np.int32)
+        seqs.append(np.concatenate([shared[:k], tail]))
+        owners.append(int(rng.integers(0, P)))
+    seqs += [shared.copy(), shared[:10].copy(), shared[:10].copy(), np.zeros(0, np.int32)]
+    owners += [0, 1, 1, 2]
+    ins = W.from_lists(seqs, owners)
+    qs = W.from_lists([s for s in seqs] + [shared[:k] for k in range(0, 300, 7)])
+    f = _forest(None, P)
+    _merge(f, ins, "shared prefixes")
+    o = oracle.Oracle(P)
+    o.merge(ins.peer, ins.tokens, ins.offsets)
+    m, c = gpu_route(f, qs, "shared prefixes")
+    m_or, c_or = o.route(qs.tokens, qs.offsets, 2)
+    assert_rows_equal(m, c, m_or, c_or, what="shared prefixes")
+
+
+def test_batch_order_does_not_matter():
+    w = W.make_config(1, n_queries=400, prompts_per_peer=60)
+    extra = W.make_config(1, seed_base=W.SEED_BASE + 9, n_queries=1, prompts_per_peer=60).snapshot
+    perm = np.random.default_rng(3).permutation(len(extra))
+    f1, f2 = _forest(w.snapshot, 4), _forest(w.snapshot, 4)
+    _merge(f1, extra, "in order")
+    _merge(f2, extra.subset(perm), "shuffled")
+    m1, c1 = gpu_route(f1, w.queries, "in order")
+    m2, c2 = gpu_route(f2, w.queries, "shuffled")
+    assert np.array_equal(m1, m2) and np.array_equal(c1, c2)
+    o = oracle_for(w.snapshot, 4)
+    o.merge(extra.peer, extra.tokens, extra.offsets)
+    m_or, c_or = o.route(w.queries.tokens, w.queries.offsets, nthreads())
+    assert_rows_equal(m1, c1, m_or, c_or, what="merged config 1")
+
+
+def test_invalid_inserts_are_skipped_and_reported():
+    import torch
+    from paper_2606_17059_amd import RouterError
+    dev = device()
+    f = _forest(None, 3)
+    toks = torch.tensor([1, 2, 3, 4, 5], dtype=torch.int32, device=dev)
+    offs = torch.tensor([0, 2, 5, 4, 9, 5], dtype=torch.int64, device=dev)  # [0,2) [2,5) bad bad [9,5)bad
+    peer = torch.tensor([0, 7, 1, 2, 0], dtype=torch.int32, device=dev)  # peer 7 out of range
+    announce("invalid inserts")
+    f.merge(peer, toks, offs)
+    with pytest.raises(RouterError):
+        f.check()
+    f.check()  # the count was reset
+    qs = W.from_lists([[1, 2, 3], [3, 4, 5]])
+    m, c = gpu_route(f, qs, "after invalid inserts")
+    assert m.tolist() == [[2, 0, 0], [0, 0, 0]]
+
+
+def test_snapshot_load_after_merges():
+    """Once merges ran, a snapshot load replaces the peer's tree on the device."""
+    w = W.make_config(1, n_queries=300, prompts_per_peer=40)
+    extra = W.make_config(1, seed_base=W.SEED_BASE + 4, n_queries=1, prompts_per_peer=30).snapshot
+    f = _forest(w.snapshot, 4)
+    o = oracle_for(w.snapshot, 4)
+    _merge(f, extra, "before reload")
+    o.merge(extra.peer, extra.tokens, extra.offsets)
+    # peer 2 receives a new snapshot (the extra prompts of peer 3), peer 1 crashes
+    lo, hi = extra.peer_range(3)
+    t = extra.tokens[extra.offsets[lo]:extra.offsets[hi]]
+    off = extra.offsets[lo:hi + 1] - extra.offsets[lo]
+    for peer, tt, oo in ((2, t, off), (1, np.zeros(0, np.int32), np.zeros(1, np.int64))):
+        announce(f"device load peer {peer}")
+        f.load_snapshot(peer, tt, oo)
+        o.load(peer, tt, oo)
+        m, c = gpu_route(f, w.queries, f"after load of peer {peer}")
+        m_or, c_or = o.route(w.queries.tokens, w.queries.offsets, nthreads())
+        assert_rows_equal(m, c, m_or, c_or, what=f"load after merge, peer {peer}")
+    # a merge after the reload still composes
+    _merge(f, extra, "after reload")
+    o.merge(extra.peer, extra.tokens, extra.offsets)
+    m, c = gpu_route(f, w.queries, "after reload + merge")
+    m_or, c_or = o.route(w.queries.tokens, w.queries.offsets, nthreads())
+    assert_rows_equal(m, c, m_or, c_or, what="merge after reload")
+
+
+def _stream_phases(w, dist, f, o, sample, label):
+    for ph in w.phases(dist):
+        _merge(f, ph.inserts, f"{label} {dist} round {ph.round}")
+        o.merge(ph.inserts.peer, ph.inserts.tokens, ph.inserts.offsets)
+        m, c = gpu_route(f, ph.queries, f"{label} {dist} round {ph.round}")
+        assert_properties(m, c, ph.queries, f"{label} {dist} {ph.round}")
+        idx = np.arange(len(ph.queries)) if sample is None else \
+            np.unique(np.random.default_rng(ph.round).choice(len(ph.queries), sample, replace=False))
+        m_or, c_or = o.route_seqset(ph.queries, idx, nthreads())
+        assert_rows_equal(m, c, m_or, c_or, idx if sample is not None else None, f"{label} {dist} {ph.round}")
+        # the inserted prompts now match their replicas in full
+        k = min(64, len(ph.inserts))
+        sub = ph.inserts.subset(np.arange(k))
+        mi, _ = gpu_route(f, sub, "inserts as queries")
+        assert np.array_equal(mi[np.arange(k), sub.peer], sub.lengths())
+
+
+def test_stream_config_small():
+    w = W.make_config(5, prompts_per_peer=30, rounds=2, phase_queries=3000, phase_inserts=1500)
+    for dist in ("uniform", "zipf"):
+        f = _forest(w.snapshot, 128)
+        o = oracle_for(w.snapshot, 128)
+        _stream_phases(w, dist, f, o, None, "stream small")
+        f.close()
+        o.close()
+
+
+@pytest.mark.timeout(1500)
+def test_stream_config_full():
+    """128 peers x 2,000 prompts; 4 rounds of (10,000 inserts, 1,048,576 lookups)
+    per topic distribution; exact on 384 sampled lookups per phase."""
+    announce("stream full: generating")
+    w = W.make_config(5)
+    for dist in ("uniform", "zipf"):
+        f = _forest(w.snapshot, 128)
+        o = oracle_for(w.snapshot, 128)
+        _stream_phases(w, dist, f, o, 384, "stream full")
+        f.close()
+        o.close()

@@ -81,6 +81,7 @@ struct pr_forest {
     MergeScratch ms;
     long long stamp = 0;          // add-round counter (stamps of moved records)
     int64_t device_bytes = 0;
+    bool broken = false;          // a device update failed; only destroy is valid
 };
 
 namespace {
@@ -344,10 +345,14 @@ __global__ void reset_call_kernel(pr::MergeCounters *c) {
 
 __global__ void add_skipped_kernel(unsigned long long *acc, const pr::MergeCounters *c) { *acc += c->skipped; }
 
+// Read the device counters and refresh the host mirror of the used sizes
+// (growing the arrays copies exactly the used part).
 pr_status read_counters(pr_forest *f, pr::MergeCounters *c, hipStream_t s) {
     if (hipMemcpyAsync(c, f->d_ctr, sizeof(*c), hipMemcpyDeviceToHost, s) != hipSuccess ||
         hipStreamSynchronize(s) != hipSuccess)
         return fail(PR_EDEVICE, "reading merge counters failed");
+    f->dev.n_nodes = (int64_t)c->n_nodes;
+    f->dev.n_pool = (int64_t)c->n_pool;
     return PR_OK;
 }
 
@@ -424,8 +429,6 @@ pr_status run_merge(pr_forest *f, const int32_t *peer_of, const int32_t *tokens,
     hipLaunchKernelGGL(add_skipped_kernel, dim3(1), dim3(1), 0, s, f->d_skipped, f->d_ctr);
     if (hipGetLastError() != hipSuccess) return fail(PR_EDEVICE, "merge launch failed");
     if ((r = read_counters(f, &c, s))) return r;
-    f->dev.n_nodes = (int64_t)c.n_nodes;
-    f->dev.n_pool = (int64_t)c.n_pool;
     if (c.overflow || c.bad_path)
         return fail(PR_EDEVICE, "merge invariant broken (overflow " + std::to_string(c.overflow) + ", bad paths " +
                                     std::to_string(c.bad_path) + "); destroy the forest");
@@ -439,6 +442,11 @@ pr_status run_merge(pr_forest *f, const int32_t *peer_of, const int32_t *tokens,
 pr_status device_load(pr_forest *f, int32_t peer, const pr::PeerSeqs &S) {
     MergeScratch &m = f->ms;
     const int64_t ns = S.count(), nt = (int64_t)S.tokens.size();
+    hipStream_t s = nullptr;
+    hipLaunchKernelGGL(pr::clear_peer_kernel, dim3(grid_threads(f->dev.n_nodes, 256)), dim3(256), 0, s,
+                       dev_view(f), f->dev.n_nodes, peer);
+    if (hipGetLastError() != hipSuccess) return fail(PR_EDEVICE, "snapshot kernels failed to launch");
+    if (ns == 0) return hipStreamSynchronize(s) == hipSuccess ? PR_OK : fail(PR_EDEVICE, "sync failed");
     if (nt > m.load_tok_cap) {
         dfree(f, &m.load_tok, m.load_tok_cap);
         m.load_tok_cap = 0;
@@ -453,16 +461,11 @@ pr_status device_load(pr_forest *f, int32_t peer, const pr::PeerSeqs &S) {
             return fail(PR_ENOMEM, "hipMalloc failed for the snapshot");
         m.load_seq_cap = ns;
     }
-    hipStream_t s = nullptr;
     if ((nt > 0 && hipMemcpy(m.load_tok, S.tokens.data(), nt * sizeof(int32_t), hipMemcpyHostToDevice) != hipSuccess) ||
         hipMemcpy(m.load_off, S.offsets.data(), (ns + 1) * sizeof(int64_t), hipMemcpyHostToDevice) != hipSuccess)
         return fail(PR_EDEVICE, "snapshot upload failed");
-    hipLaunchKernelGGL(pr::clear_peer_kernel, dim3(grid_threads(f->dev.n_nodes, 256)), dim3(256), 0, s,
-                       dev_view(f), f->dev.n_nodes, peer);
-    if (ns > 0)
-        hipLaunchKernelGGL(pr::fill_peer_kernel, dim3(grid_threads(ns, 256)), dim3(256), 0, s, m.load_peer, ns, peer);
+    hipLaunchKernelGGL(pr::fill_peer_kernel, dim3(grid_threads(ns, 256)), dim3(256), 0, s, m.load_peer, ns, peer);
     if (hipGetLastError() != hipSuccess) return fail(PR_EDEVICE, "snapshot kernels failed to launch");
-    if (ns == 0) return hipStreamSynchronize(s) == hipSuccess ? PR_OK : fail(PR_EDEVICE, "sync failed");
     return run_merge(f, m.load_peer, m.load_tok, nt, m.load_off, ns, s);
 }
 
@@ -525,11 +528,15 @@ pr_status pr_load_snapshot(pr_forest *f, int32_t peer, const int32_t *tokens, co
     } catch (const std::bad_alloc &) {
         return fail(PR_ENOMEM, "host allocation failed");
     }
+    if (f->broken) return fail(PR_ESTATE, "an earlier device update failed; destroy the forest");
     if (f->has_dev && f->merged) {
         DeviceScope ds(f);
         if (!ds.ok()) return fail(PR_EDEVICE, "cannot select the forest's device");
         pr_status r = device_load(f, peer, S);
-        if (r) return r;
+        if (r) {
+            f->broken = true;
+            return r;
+        }
         f->sets[(size_t)peer] = std::move(S);
         return ok();
     }
@@ -547,12 +554,16 @@ pr_status pr_merge(pr_forest *f, const int32_t *peer_of, const int32_t *tokens, 
     if (!peer_of || !offsets) return fail(PR_EINVAL, "NULL device pointer");
     if (num_tokens > 0 && !tokens) return fail(PR_EINVAL, "tokens is NULL");
     if (num_seqs > (int64_t)INT32_MAX) return fail(PR_EINVAL, "too many sequences");
+    if (f->broken) return fail(PR_ESTATE, "an earlier device update failed; destroy the forest");
     DeviceScope ds(f);
     if (!ds.ok()) return fail(PR_EDEVICE, "cannot select the forest's device");
     pr_status s = commit(f);
     if (s) return s;
     s = run_merge(f, peer_of, tokens, num_tokens, offsets, num_seqs, (hipStream_t)hip_stream);
-    if (s) return s;
+    if (s) {
+        f->broken = true;
+        return s;
+    }
     return ok();
 }
 
@@ -564,6 +575,7 @@ pr_status pr_route(pr_forest *f, const int32_t *q_tokens, int64_t num_tokens, co
     if (!q_offsets || !match_len || !chosen) return fail(PR_EINVAL, "NULL device pointer");
     if (num_tokens > 0 && !q_tokens) return fail(PR_EINVAL, "q_tokens is NULL");
     if (num_queries > (int64_t)0x7fffffff * pr::kRouteWavesPerBlock) return fail(PR_EINVAL, "too many queries");
+    if (f->broken) return fail(PR_ESTATE, "an earlier device update failed; destroy the forest");
     DeviceScope ds(f);
     if (!ds.ok()) return fail(PR_EDEVICE, "cannot select the forest's device");
     pr_status s = commit(f);

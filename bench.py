@@ -40,6 +40,20 @@ WORKLOADS = {
 }
 
 
+def measured_traffic(workload: str):
+    """HBM bytes per launch of the route kernel from the committed rocprofv3
+    FETCH_SIZE / WRITE_SIZE summary, or None if it does not cover this workload
+    or the kernel source changed since it was taken."""
+    import hashlib
+    try:
+        rec = json.load(open(os.path.join(ROOT, "profiles", "route_kernel_traffic.json")))[workload]
+        src = os.path.join(ROOT, "paper_2606_17059_amd", "csrc", "route_kernels.h")
+        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    except (OSError, KeyError, ValueError):
+        return None
+    return rec["traffic_bytes_per_launch"] if rec.get("kernel_source_sha256_16") == sha else None
+
+
 def log(msg: str) -> None:
     sys.stderr.write(msg + "\n")
     sys.stderr.flush()
@@ -78,6 +92,105 @@ def cpu_baseline(w, queries, target_s: float):
             "sample": f"{n} of {len(queries)} queries drawn uniformly (seed 12345), {dt:.1f} s with {T} threads"}
 
 
+def bench_stream(args, w, dev):
+    """Streaming configuration: per round, one delta-merge of the insert batch
+    into the replica trees, then lookups of the round's query batch."""
+    import torch
+    from paper_2606_17059_amd import Forest
+    P = w.num_peers
+    phases_out = []
+    tot_ins = tot_merge_s = tot_q = tot_route_s = tot_bytes = 0.0
+    kern_all = []
+    cpu = None
+    for dist in ("uniform", "zipf"):
+        f = Forest(P)
+        f.load_seqset(w.snapshot)
+        for rnd in range(w.meta["rounds"]):
+            t0 = time.perf_counter()
+            ph = w.phase(dist, rnd)
+            gen_s = time.perf_counter() - t0
+            ins, qs = ph.inserts, ph.queries
+            ip = torch.from_numpy(ins.peer).to(dev)
+            it = torch.from_numpy(ins.tokens).to(dev)
+            io = torch.from_numpy(ins.offsets).to(dev)
+            qt = torch.from_numpy(qs.tokens).to(dev)
+            qo = torch.from_numpy(qs.offsets).to(dev)
+            nq = len(qs)
+            ml = torch.empty((nq, P), dtype=torch.int32, device=dev)
+            ch = torch.empty(nq, dtype=torch.int32, device=dev)
+            if rnd == 0:
+                f.route(qt, qo, ml, ch)  # builds and uploads the base forest
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            t0 = time.perf_counter()
+            e0.record()
+            f.merge(ip, it, io)
+            e1.record()
+            torch.cuda.synchronize()
+            merge_s = time.perf_counter() - t0
+            ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                  for _ in range(args.steps)]
+            for a, b in ev:
+                a.record()
+                f.route(qt, qo, ml, ch)
+                b.record()
+            torch.cuda.synchronize()
+            f.check()
+            km = np.array([a.elapsed_time(b) for a, b in ev])
+            m = ml.cpu().numpy()
+            M = m.max(axis=1).astype(np.int64)
+            bq = float((4 * np.minimum(qs.lengths(), M + 1) + 4 * (P + 1) + 8).sum())
+            kern_all.extend(km.tolist())
+            tot_ins += len(ins)
+            tot_merge_s += merge_s
+            tot_q += nq * len(km)
+            tot_route_s += km.sum() / 1e3
+            tot_bytes += bq * len(km)
+            ph_rec = {"dist": dist, "round": rnd, "inserts": len(ins), "merge_ms": merge_s * 1e3,
+                      "merge_inserts_per_s": len(ins) / merge_s, "lookups": nq,
+                      "route_ms": float(km.mean()), "route_gbps": bq / (km.mean() / 1e3) / 1e9,
+                      "forest_nodes": f.info()["num_nodes"]}
+            phases_out.append(ph_rec)
+            log(f"[bench] stream {dist} round {rnd}: gen {gen_s:.1f} s; {ph_rec}")
+            if cpu is None and not args.no_cpu_baseline:
+                import oracle
+                o = oracle.Oracle(P)
+                ss = w.snapshot
+                for p in range(P):
+                    lo, hi = ss.peer_range(p)
+                    o.load(p, ss.tokens[ss.offsets[lo]:ss.offsets[hi]], ss.offsets[lo:hi + 1] - ss.offsets[lo])
+                t0 = time.perf_counter()
+                o.merge(ins.peer, ins.tokens, ins.offsets)
+                o_merge_s = time.perf_counter() - t0
+                T = cpu_threads()
+                rng = np.random.default_rng(12345)
+                n = 4 * T
+                while True:
+                    sub = qs.subset(np.sort(rng.choice(nq, n, replace=False)))
+                    t0 = time.perf_counter()
+                    o.route(sub.tokens, sub.offsets, T)
+                    dt = time.perf_counter() - t0
+                    if dt >= 0.25 * args.cpu_seconds or n >= nq:
+                        break
+                    n = int(min(nq, max(2 * n, n * args.cpu_seconds / max(dt, 1e-3))))
+                o.close()
+                cpu = {"value": n / dt, "unit": "queries/s", "cores": T, "kind": "oracle",
+                       "sample": f"{n} of {nq} lookups of the first uniform round, {dt:.1f} s with {T} threads; "
+                                 f"oracle merge of that round's {len(ins)} inserts: "
+                                 f"{len(ins) / o_merge_s:.0f} inserts/s (1 thread)"}
+                log(f"[bench] cpu baseline: {cpu}")
+            del qt, qo, ml, ch
+        f.close()
+    kern = np.array(kern_all)
+    achieved = tot_bytes / tot_route_s / 1e9
+    return {
+        "value": tot_q / tot_route_s, "ms_per_step": float(kern.mean()), "kernel_ms": float(kern.mean()),
+        "achieved": achieved, "bytes_per_launch": tot_bytes / len(kern),
+        "merge": {"inserts_per_s": tot_ins / tot_merge_s, "inserts": tot_ins, "seconds": tot_merge_s,
+                  "note": "wall time of pr_merge calls (host-synchronous), 8 rounds x 10,000 inserts"},
+        "phases": phases_out, "cpu": cpu}
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -87,6 +200,9 @@ def main() -> int:
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU time of the oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copies", type=int, default=2, help="device copies of the query batch to rotate")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="first copy a buffer of this size device-to-device three times (a plain copy kernel "
+                         "of known size for scaling profiler byte counters)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -104,9 +220,35 @@ def main() -> int:
         sys.stderr.write("bench.py needs a HIP device\n")
         return 1
     dev = torch.device("cuda:0")
+    if args.copy_probe_mib > 0:
+        a = torch.empty(args.copy_probe_mib << 18, dtype=torch.int32, device=dev)
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        log(f"[bench] copy probe: 3 copies of {args.copy_probe_mib} MiB")
+        del a, b
     t0 = time.perf_counter()
     w = W.make_config(args.config)
-    queries = w.queries if args.config != 5 else w.phase("zipf", 0).queries
+    if args.config == 5:
+        r = bench_stream(args, w, dev)
+        out = {
+            "metric": "routed queries/sec (batched LPM over all peer trees) + achieved HBM GB/s",
+            "value": r["value"], "unit": "queries/s", "n_gpus": 1, "steps": args.steps, "warmup": 0,
+            "ms_per_step": r["ms_per_step"], "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+            "dtype": "int32", "data": "synthetic",
+            "config": {"workload": WORKLOADS[5], "config_index": 5, "peers": w.num_peers,
+                       "queries_per_step": w.meta["phase_queries"], "parallelism": "single GPU"},
+            "hbm_gbps": r["achieved"],
+            "roofline": {"bound": "hbm", "achieved": r["achieved"], "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                         "frac": r["achieved"] / PEAK_HBM_GBPS, "traffic": measured_traffic("stream"),
+                         "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
+                         "kernel": "route_kernel",
+                         "kernel_ms": r["kernel_ms"], "algorithmic_bytes_per_launch": r["bytes_per_launch"]},
+            "cpu_baseline": r["cpu"], "merge": r["merge"], "phases": r["phases"]}
+        print(json.dumps(out), flush=True)
+        return 0
+    queries = w.queries
     log(f"[bench] generated config {args.config} in {time.perf_counter() - t0:.1f} s: "
         f"{len(w.snapshot)} cached prompts, {len(queries)} queries")
 
@@ -196,7 +338,8 @@ def main() -> int:
                    "queries_per_step": nq, "query_tokens": int(qlen.sum()), "parallelism": "single GPU"},
         "hbm_gbps": achieved,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
-                     "frac": achieved / PEAK_HBM_GBPS, "traffic": None,
+                     "frac": achieved / PEAK_HBM_GBPS, "traffic": measured_traffic(W.CONFIG_NAMES[args.config]),
+                     "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
                      "kernel": "route_kernel", "kernel_ms": float(kern_ms.mean()),
                      "algorithmic_bytes_per_launch": total_bytes},
         "cpu_baseline": cpu,

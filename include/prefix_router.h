@@ -27,9 +27,11 @@
  *     (each tree has one writer, paper Section 1).  pr_route only reads the
  *     forest.
  *   - Device calls (pr_merge, pr_route) take device pointers and a HIP stream
- *     (NULL = the legacy default stream), are ordered on that stream and return
- *     without waiting for the GPU.  Input buffers must stay valid, and output
- *     buffers untouched, until the stream has passed the call.
+ *     (NULL = the legacy default stream) and are ordered on that stream after
+ *     the work already queued there.  pr_route returns without waiting for the
+ *     GPU: its inputs must stay valid, and its outputs untouched, until the
+ *     stream has passed the call.  pr_merge returns when the merge is complete
+ *     (it reads small counters back between its insert rounds).
  *   - A forest lives on the HIP device that is current when it first touches
  *     the GPU; later calls switch to that device for their duration.
  */
@@ -80,11 +82,15 @@ void pr_forest_destroy(pr_forest *f);
  * batch.  Any merges into that peer since its last snapshot are dropped with
  * the old tree; other peers are untouched.  An empty snapshot (num_seqs == 0)
  * empties the tree, e.g. a peer that crashed and lost its cache.
- * The data is copied before the call returns; the device copy of the forest is
- * rebuilt before the next pr_merge or pr_route on this forest runs (that call
- * then blocks the host for the rebuild and upload).
+ * The data is copied before the call returns.  Until the first pr_merge on
+ * this forest, the device copy of the forest is rebuilt from the host copies
+ * of all snapshots before the next pr_merge or pr_route runs (that call then
+ * blocks the host for the rebuild and upload).  Once merges have run, the
+ * replacement happens on the device within this call: the peer is removed
+ * from every node, then the snapshot is inserted as by pr_merge.
  * Errors: PR_EINVAL (peer out of range, num_seqs < 0, NULL offsets, NULL tokens
- * with a non-empty batch, offsets[0] != 0 or decreasing offsets), PR_ENOMEM.
+ * with a non-empty batch, offsets[0] != 0 or decreasing offsets), PR_ENOMEM,
+ * PR_ESTATE (an earlier device update failed), PR_EDEVICE.
  */
 pr_status pr_load_snapshot(pr_forest *f, int32_t peer, const int32_t *tokens,
                            const int64_t *offsets, int64_t num_seqs);
@@ -95,13 +101,15 @@ pr_status pr_load_snapshot(pr_forest *f, int32_t peer, const int32_t *tokens,
  * peer it was forwarded to once that peer acknowledges).
  * Inserts DEVICE sequence i (tokens[offsets[i] .. offsets[i+1]), offsets within
  * [0, num_tokens]) into peer peer_of[i]'s tree, for every i < num_seqs, on the
- * given stream.  The result depends only on the set of inserts (order and
- * duplicates do not matter).  Entries with a peer out of range or offsets
- * outside [0, num_tokens] or decreasing are skipped and counted; see
- * pr_forest_check.
- * Errors (host side, nothing enqueued): PR_EINVAL (NULL pointers with
- * num_seqs > 0, num_seqs < 0, num_tokens < 0), PR_ENOMEM (the forest's device
- * capacity could not grow), PR_EDEVICE.
+ * given stream, and returns when the forest holds them.  The result depends
+ * only on the set of inserts (order and duplicates do not matter).  Entries
+ * with a peer out of range or offsets outside [0, num_tokens] or decreasing
+ * are skipped and counted; see pr_forest_check.
+ * Errors: PR_EINVAL (NULL pointers with num_seqs > 0, negative counts; nothing
+ * is enqueued), PR_ESTATE (an earlier device update failed), PR_ENOMEM (the
+ * forest's device capacity could not grow) and PR_EDEVICE (a HIP call failed
+ * or an internal invariant check tripped); after PR_ENOMEM or PR_EDEVICE the
+ * forest refuses every call but destroy.
  */
 pr_status pr_merge(pr_forest *f, const int32_t *peer_of, const int32_t *tokens,
                    int64_t num_tokens, const int64_t *offsets, int64_t num_seqs,
@@ -147,7 +155,8 @@ pr_status pr_forest_info_get(pr_forest *f, pr_forest_info *out);
 /*
  * Host-side image of the union layout built from the forest's host snapshot
  * copies, for inspection without a GPU (layout tests).  No GPU work.  The
- * pointers stay valid until the next call on f.  Layout:
+ * pointers stay valid until the next call on f.  PR_ESTATE once merges have
+ * run (the host copies no longer describe the forest).  Layout:
  *   nodes  int32 [num_nodes][8]: first label token, label offset in pool
  *          (uint32 bits), label length, first child id, child count, 0,
  *          peer-mask word 0 (low 32 bits, high 32 bits).  Node 0 is the root;

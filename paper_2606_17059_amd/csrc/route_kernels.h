@@ -38,14 +38,35 @@ namespace pr {
 #ifndef PR_WIDE_VECTORS
 #define PR_WIDE_VECTORS 8
 #endif
+#ifndef PR_ROUTE_LDS
+#define PR_ROUTE_LDS 1
+#endif
+#ifndef PR_QUERY_NT
+#define PR_QUERY_NT 1
+#endif
+#ifndef PR_NARROW_RECORDS
+#define PR_NARROW_RECORDS 0
+#endif
 
 constexpr int kWave = 64;
 constexpr int kRouteWavesPerBlock = PR_ROUTE_WAVES_PER_BLOCK;
 constexpr int kLcpVectors = PR_LCP_VECTORS;    // 64-token vectors compared per step
 constexpr int kWideVectors = PR_WIDE_VECTORS;  // first tokens held per lane for wide blocks
 
-// Length of the common prefix of a[0..n) and b[0..n): the first i < n with
-// a[i] != b[i], or n.  Wave-cooperative; every lane returns the same value.
+
+// Query tokens are read once: mark their loads non-temporal so they stream
+// through the caches that hold the forest's labels.
+__device__ __forceinline__ int32_t load_stream(const int32_t *p) {
+#if PR_QUERY_NT
+    return __builtin_nontemporal_load(p);
+#else
+    return *p;
+#endif
+}
+
+// Length of the common prefix of a[0..n) (a label) and b[0..n) (query
+// tokens): the first i < n with a[i] != b[i], or n.  Wave-cooperative; every
+// lane returns the same value.
 __device__ __forceinline__ int64_t wave_lcp(const int32_t *__restrict__ a, const int32_t *__restrict__ b,
                                             int64_t n, int lane) {
     for (int64_t base = 0; base < n; base += (int64_t)kWave * kLcpVectors) {
@@ -57,7 +78,7 @@ __device__ __forceinline__ int64_t wave_lcp(const int32_t *__restrict__ a, const
             vb[j] = 0;
             if (i < n) {
                 va[j] = a[i];
-                vb[j] = b[i];
+                vb[j] = load_stream(b + i);
             }
         }
 #pragma unroll
@@ -96,7 +117,7 @@ __device__ __forceinline__ void load_block(ChildBlock &cb, const Node *__restric
     cb.ct_beg = 0;
     cb.ct_cnt = 0;
     cb.mask0 = 0ull;
-    if (cnt <= kWave) {
+    if (PR_NARROW_RECORDS && cnt <= kWave) {
         if (lane < cnt) {
             const Node r = nodes[beg + lane];
             cb.tok = r.tok;
@@ -118,7 +139,7 @@ __device__ __forceinline__ void load_block(ChildBlock &cb, const Node *__restric
 // Find the child whose first token is t.  Returns false if there is none.
 __device__ __forceinline__ bool locate(const ChildBlock &cb, int32_t t, const Node *__restrict__ nodes,
                                        const int32_t *__restrict__ ntok, int lane, Child &c) {
-    if (cb.cnt <= kWave) {
+    if (PR_NARROW_RECORDS && cb.cnt <= kWave) {
         const uint64_t b = __ballot(lane < cb.cnt && cb.tok == t);
         if (!b) return false;
         const int src = (int)(__ffsll((unsigned long long)b) - 1);
@@ -170,6 +191,33 @@ __device__ __forceinline__ bool locate(const ChildBlock &cb, int32_t t, const No
     return true;
 }
 
+// The query is staged in a per-wave LDS ring of kRing tokens: position p of
+// the query lives at ring[p % kRing].  Direct global->LDS loads (one dword per
+// lane, 64 consecutive positions per instruction) fill it without passing
+// through VGPRs, so a whole edge's worth of query tokens can be in flight while
+// the wave holds only the label tokens it compares.  Only positions the walk
+// may read are fetched, and never more than kRing ahead of the current depth.
+constexpr int kRing = 1024;
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+typedef const __attribute__((address_space(1))) void global_void_t;
+
+// Issue the loads of query positions [from, to) into the ring (to <= query
+// length, to - from <= kRing).  Lanes outside the range do not load.
+__device__ __forceinline__ void ring_fetch(int32_t *ring, const int32_t *__restrict__ qs, int64_t from, int64_t to,
+                                           int lane) {
+    for (int64_t v = from & ~(int64_t)(kWave - 1); v < to; v += kWave) {
+        const int64_t p = v + lane;
+        if (p >= from && p < to)
+            __builtin_amdgcn_global_load_lds((global_void_t *)(qs + p), (lds_void_t *)(ring + (v & (kRing - 1))), 4,
+                                             0, 0);
+    }
+}
+
+// Wait until every vector memory operation of the wave, the ring loads
+// included, has completed (s_waitcnt vmcnt(0) expcnt(7) lgkmcnt(15)).
+__device__ __forceinline__ void wait_vm_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
 template <int W>
 __global__ __launch_bounds__(kWave *kRouteWavesPerBlock) void route_kernel(
     const Node *__restrict__ nodes, const int32_t *__restrict__ ntok, const uint64_t *__restrict__ mext,
@@ -198,6 +246,98 @@ __global__ __launch_bounds__(kWave *kRouteWavesPerBlock) void route_kernel(
         alive[w] = rem >= 64 ? ~0ull : (rem > 0 ? ((1ull << rem) - 1ull) : 0ull);
     }
 
+#if PR_ROUTE_LDS
+    __shared__ int32_t ring_all[kRouteWavesPerBlock][kRing];
+    int32_t *ring = ring_all[threadIdx.x / kWave];
+    int64_t d = 0;
+    int64_t fetched = 0;  // query positions [0, fetched) have ring loads issued
+    ChildBlock cb;
+    // the first positions of the query are fetched speculatively, beside the root block
+    {
+        const int64_t f0 = min(qlen, (int64_t)kLcpVectors * kWave);
+        ring_fetch(ring, qs, 0, f0, lane);
+        fetched = f0;
+        const Node root = nodes[0];
+        load_block(cb, nodes, ntok, root.ct_beg, root.ct_cnt, lane);
+        wait_vm_all();
+    }
+    int32_t t = qlen > 0 ? ring[0] : 0;
+    while (d < qlen) {
+        Child c;
+        if (!locate(cb, t, nodes, ntok, lane, c)) break;
+        if (c.lab_len <= 0) break;  // only the root has an empty label
+        const int64_t eend = d + c.lab_len;          // depth at the child
+        const int64_t want = min(qlen, eend + 1);     // positions this level may read
+        const int64_t lend = min(eend, qlen);         // compared positions: [d, lend)
+        // one batch per level: the query tokens of the whole label (as far as
+        // the ring allows), the child's mask words and child block, and the
+        // first segment's labels
+        {
+            const int64_t to = min(want, d + kRing);
+            if (to > fetched) {
+                ring_fetch(ring, qs, fetched, to, lane);
+                fetched = to;
+            }
+        }
+        uint64_t mx[W];
+        mx[0] = c.mask0;
+#pragma unroll
+        for (int wi = 1; wi < W; wi++) mx[wi] = mext[(int64_t)c.id * (W - 1) + (wi - 1)];
+        load_block(cb, nodes, ntok, c.ct_beg, c.ct_cnt, lane);
+        const int32_t *lab = pool + (uint32_t)c.lab_off;
+        int64_t l = lend - d;
+        for (int64_t base = d; base < lend; base += (int64_t)kWave * kLcpVectors) {
+            if (base > d) {  // later segments: top the ring up to what it can hold
+                const int64_t to = min(want, base + kRing);
+                if (to > fetched) {
+                    ring_fetch(ring, qs, fetched, to, lane);
+                    fetched = to;
+                }
+            }
+            int32_t lv[kLcpVectors];
+#pragma unroll
+            for (int j = 0; j < kLcpVectors; j++) {
+                const int64_t p = base + j * kWave + lane;
+                lv[j] = 0;
+                if (p < lend) lv[j] = lab[p - d];
+            }
+            wait_vm_all();
+            int64_t found = -1;
+#pragma unroll
+            for (int j = 0; j < kLcpVectors; j++) {
+                const int64_t p = base + j * kWave + lane;
+                bool mis = false;
+                if (p < lend) mis = ring[p & (kRing - 1)] != lv[j];
+                const uint64_t b = __ballot(mis);
+                if (b && found < 0) found = base + j * kWave + (__ffsll((unsigned long long)b) - 1);
+            }
+            if (found >= 0) {
+                l = found - d;
+                break;
+            }
+        }
+        bool any = false;
+#pragma unroll
+        for (int wi = 0; wi < W; wi++) {
+            const uint64_t nm = alive[wi] & mx[wi];
+            if (((alive[wi] & ~nm) >> lane) & 1ull) m[wi] = (int32_t)d;
+            alive[wi] = nm;
+            any |= nm != 0ull;
+        }
+        if (!any) break;  // no peer holds this edge (left behind by a replaced snapshot)
+        d += l;
+        if (l < c.lab_len || d >= qlen) break;
+        // next token: in the ring (fetched with the label) unless the label ran
+        // past the ring's reach
+        if (d >= fetched) {
+            const int64_t to = min(qlen, d + (int64_t)kLcpVectors * kWave);
+            ring_fetch(ring, qs, d, to, lane);
+            fetched = to;
+        }
+        wait_vm_all();
+        t = ring[d & (kRing - 1)];
+    }
+#else
     int64_t d = 0;
     ChildBlock cb;
     {
@@ -233,6 +373,8 @@ __global__ __launch_bounds__(kWave *kRouteWavesPerBlock) void route_kernel(
         if (l < c.lab_len) break;
         t = tnext;
     }
+
+#endif
 
     // peers still holding the walked path matched all of it
     int32_t bm = -1, bp = INT32_MAX;

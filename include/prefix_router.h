@@ -165,6 +165,8 @@ pr_status pr_forest_info_get(pr_forest *f, pr_forest_info *out);
  *          Bit p of the mask is set if peer p's tree holds the path from the
  *          root through the node's whole label;
  *   ntok   int32 [num_nodes]: first label token of every node;
+ *   nsep   int32 [num_nodes]: for a child block [b, b + cnt) with cnt > 64,
+ *          nsep[b + k] = ntok[b + (k * cnt) / 64] for k < 64 (other entries 0);
  *   mext   uint64 [num_nodes][mask_words - 1]: peer-mask words 1.. ;
  *   pool   int32 [pool_tokens]: label tokens.
  */
@@ -173,6 +175,7 @@ typedef struct {
     int64_t num_nodes, pool_tokens;
     const int32_t *nodes;
     const int32_t *ntok;
+    const int32_t *nsep;
     const uint64_t *mext;
     const int32_t *pool;
 } pr_image_view;

@@ -126,6 +126,7 @@ class Builder {
         out->W = W_;
         out->nodes.assign(m, Node{});
         out->ntok.assign(m, 0);
+        out->nsep.assign(m, 0);
         out->mext.assign(m * (size_t)(W_ - 1), 0ull);
         out->pool.resize((size_t)pool_len);
         uint64_t po = 0;
@@ -145,6 +146,12 @@ class Builder {
             out->ntok[id] = nd.tok;
             for (int w = 1; w < W_; w++)
                 out->mext[id * (size_t)(W_ - 1) + (w - 1)] = masks_[(size_t)x * W_ + w];
+        }
+        for (size_t id = 0; id < m; id++) {  // separators of wide child blocks
+            const Node &nd = out->nodes[id];
+            if (nd.ct_cnt <= kSepCount) continue;
+            for (int k = 0; k < kSepCount; k++)
+                out->nsep[(size_t)nd.ct_beg + k] = out->ntok[(size_t)nd.ct_beg + PR_SEP_INDEX(k, nd.ct_cnt)];
         }
         return true;
     }

@@ -23,6 +23,7 @@ struct HostImage {
     int W = 1;
     std::vector<Node> nodes;
     std::vector<int32_t> ntok;
+    std::vector<int32_t> nsep;   // separators of wide child blocks
     std::vector<uint64_t> mext;  // words 1..W-1 per node
     std::vector<int32_t> pool;
 };

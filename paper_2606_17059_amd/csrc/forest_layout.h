@@ -13,11 +13,16 @@
 // Arrays (device resident):
 //   nodes[n]  32-byte Node records.  The children of a node are one contiguous
 //             block nodes[ct_beg .. ct_beg + ct_cnt), sorted by first label
-//             token (signed int32 order), so a wave that loads the block finds
-//             the child for a token with one ballot and already holds the
-//             child's record.  Node 0 is the root (empty label).
+//             token (signed int32 order), so the position of a child in the
+//             first-token array is its id.  Node 0 is the root (empty label).
 //   ntok[n]   first label token of node n (= nodes[n].tok), dense, for
-//             scanning wide child blocks with coalesced 4-byte loads.
+//             scanning child blocks with coalesced 4-byte loads.
+//   nsep[n]   separators of wide child blocks: for a block [b, b + cnt) with
+//             cnt > 64, nsep[b + k] = ntok[b + PR_SEP_INDEX(k, cnt)] for
+//             k < 64 (ascending).  A wave loads the 64 separators (two cache
+//             lines), a ballot picks the sub-range that can hold a token, and
+//             one more load of at most ceil(cnt / 64) first tokens settles it.
+//             Entries outside the first 64 of a wide block are unused.
 //   mext[n*(W-1) + w-1]  peer-mask words 1..W-1 of node n (W > 1 only);
 //             word 0 lives in the record.
 //   pool[t]   int32 label tokens; node n's label is pool[lab_off .. +lab_len).
@@ -39,6 +44,12 @@ struct alignas(32) Node {
 };
 
 static_assert(sizeof(Node) == 32, "Node is one 32-byte record");
+
+// Child blocks with more than this many children carry separators.
+constexpr int kSepCount = 64;
+
+// Position in a wide block of cnt children of its k-th separator (k < 64).
+#define PR_SEP_INDEX(k, cnt) ((int32_t)(((int64_t)(k) * (int64_t)(cnt)) / 64))
 
 // Mask words per node for a peer count (template instances exist for these).
 inline int mask_words_for(int num_peers) {

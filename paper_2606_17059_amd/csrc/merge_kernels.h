@@ -60,6 +60,7 @@ struct MergeCounters {
 struct DevForest {
     Node *nodes;
     int32_t *ntok;
+    int32_t *nsep;
     uint64_t *mext;
     int32_t *pool;
     long long *moved;  // (stamp << 32) | new position, per node id
@@ -389,6 +390,24 @@ __global__ __launch_bounds__(64 *kMergeWavesPerBlock) void add_build_kernel(
         pb += rest;
     }
     if (lane == 0) grp_nb[k] = (int32_t)nb;
+}
+
+// Separators of every rebuilt wide block (runs after the build, before the
+// parents are pointed at their new blocks; the old record of x still holds the
+// old child count).
+__global__ __launch_bounds__(64 *kMergeWavesPerBlock) void add_sep_kernel(DevForest F,
+                                                                         const unsigned long long *keys,
+                                                                         int64_t n_add, const int32_t *grp_nw,
+                                                                         const int32_t *grp_nb) {
+    const int lane = (int)(threadIdx.x & 63);
+    const int64_t k = m_wave_index();
+    if (k >= n_add) return;
+    if (k > 0 && key_parent(keys[k - 1]) == key_parent(keys[k])) return;
+    const int32_t nb = grp_nb[k];
+    if (nb < 0) return;
+    const int32_t cnt = F.nodes[key_parent(keys[k])].ct_cnt + grp_nw[k];
+    if (cnt <= kSepCount) return;
+    F.nsep[nb + lane] = F.ntok[nb + PR_SEP_INDEX(lane, cnt)];
 }
 
 // Point every rebuilt parent at its new block, wherever its record lives now.

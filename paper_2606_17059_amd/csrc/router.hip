@@ -41,6 +41,7 @@ pr_status ok() {
 struct DevImage {
     Node *nodes = nullptr;
     int32_t *ntok = nullptr;
+    int32_t *nsep = nullptr;
     uint64_t *mext = nullptr;
     int32_t *pool = nullptr;
     long long *moved = nullptr;
@@ -134,6 +135,7 @@ void free_image(pr_forest *f) {
     DevImage &d = f->dev;
     dfree(f, &d.nodes, d.cap_nodes);
     dfree(f, &d.ntok, d.cap_nodes);
+    dfree(f, &d.nsep, d.cap_nodes);
     dfree(f, &d.mext, d.cap_nodes * (f->W - 1));
     dfree(f, &d.moved, d.cap_nodes);
     dfree(f, &d.pool, d.cap_pool);
@@ -179,13 +181,14 @@ pr_status ensure_capacity(pr_forest *f, int64_t need_nodes, int64_t need_pool, h
         const int64_t cap = std::min<int64_t>(std::max<int64_t>(need_nodes, d.cap_nodes + d.cap_nodes / 2),
                                               (int64_t)INT32_MAX);
         Node *nn = nullptr;
-        int32_t *nt = nullptr;
+        int32_t *nt = nullptr, *ns = nullptr;
         uint64_t *nm = nullptr;
         long long *mv = nullptr;
-        if (!dalloc(f, &nn, cap) || !dalloc(f, &nt, cap) || !dalloc(f, &nm, cap * (f->W - 1)) ||
-            !dalloc(f, &mv, cap)) {
+        if (!dalloc(f, &nn, cap) || !dalloc(f, &nt, cap) || !dalloc(f, &ns, cap) ||
+            !dalloc(f, &nm, cap * (f->W - 1)) || !dalloc(f, &mv, cap)) {
             dfree(f, &nn, cap);
             dfree(f, &nt, cap);
+            dfree(f, &ns, cap);
             dfree(f, &nm, cap * (f->W - 1));
             dfree(f, &mv, cap);
             return fail(PR_ENOMEM, "hipMalloc failed while growing the forest");
@@ -193,6 +196,7 @@ pr_status ensure_capacity(pr_forest *f, int64_t need_nodes, int64_t need_pool, h
         const int64_t n = d.n_nodes;
         if (hipMemcpyAsync(nn, d.nodes, n * sizeof(Node), hipMemcpyDeviceToDevice, s) != hipSuccess ||
             hipMemcpyAsync(nt, d.ntok, n * sizeof(int32_t), hipMemcpyDeviceToDevice, s) != hipSuccess ||
+            hipMemcpyAsync(ns, d.nsep, n * sizeof(int32_t), hipMemcpyDeviceToDevice, s) != hipSuccess ||
             (f->W > 1 && hipMemcpyAsync(nm, d.mext, n * (f->W - 1) * sizeof(uint64_t), hipMemcpyDeviceToDevice,
                                         s) != hipSuccess) ||
             hipMemcpyAsync(mv, d.moved, d.cap_nodes * sizeof(long long), hipMemcpyDeviceToDevice, s) != hipSuccess ||
@@ -201,10 +205,12 @@ pr_status ensure_capacity(pr_forest *f, int64_t need_nodes, int64_t need_pool, h
             return fail(PR_EDEVICE, "device copy failed while growing the forest");
         dfree(f, &d.nodes, d.cap_nodes);
         dfree(f, &d.ntok, d.cap_nodes);
+        dfree(f, &d.nsep, d.cap_nodes);
         dfree(f, &d.mext, d.cap_nodes * (f->W - 1));
         dfree(f, &d.moved, d.cap_nodes);
         d.nodes = nn;
         d.ntok = nt;
+        d.nsep = ns;
         d.mext = nm;
         d.moved = mv;
         d.cap_nodes = cap;
@@ -242,7 +248,7 @@ pr_status commit(pr_forest *f) {
     const int64_t n = (int64_t)h.nodes.size(), np = (int64_t)h.pool.size();
     d.cap_nodes = std::max<int64_t>(n + n / 8, 1024);
     d.cap_pool = std::max<int64_t>(np + np / 8, 4096);
-    if (!dalloc(f, &d.nodes, d.cap_nodes) || !dalloc(f, &d.ntok, d.cap_nodes) ||
+    if (!dalloc(f, &d.nodes, d.cap_nodes) || !dalloc(f, &d.ntok, d.cap_nodes) || !dalloc(f, &d.nsep, d.cap_nodes) ||
         !dalloc(f, &d.mext, d.cap_nodes * (f->W - 1)) || !dalloc(f, &d.moved, d.cap_nodes) ||
         !dalloc(f, &d.pool, d.cap_pool)) {
         free_image(f);
@@ -250,6 +256,7 @@ pr_status commit(pr_forest *f) {
     }
     if (hipMemcpy(d.nodes, h.nodes.data(), n * sizeof(Node), hipMemcpyHostToDevice) != hipSuccess ||
         hipMemcpy(d.ntok, h.ntok.data(), n * sizeof(int32_t), hipMemcpyHostToDevice) != hipSuccess ||
+        hipMemcpy(d.nsep, h.nsep.data(), n * sizeof(int32_t), hipMemcpyHostToDevice) != hipSuccess ||
         (f->W > 1 && hipMemcpy(d.mext, h.mext.data(), h.mext.size() * sizeof(uint64_t), hipMemcpyHostToDevice) !=
                          hipSuccess) ||
         (np > 0 && hipMemcpy(d.pool, h.pool.data(), np * sizeof(int32_t), hipMemcpyHostToDevice) != hipSuccess) ||
@@ -279,7 +286,8 @@ hipError_t launch_route(const pr_forest *f, const int32_t *qt, int64_t ntok, con
                         int32_t *ml, int32_t *ch, hipStream_t s) {
     const int64_t blocks = (nq + pr::kRouteWavesPerBlock - 1) / pr::kRouteWavesPerBlock;
     hipLaunchKernelGGL(pr::route_kernel<W>, dim3((unsigned)blocks), dim3(pr::kWave * pr::kRouteWavesPerBlock), 0, s,
-                       f->dev.nodes, f->dev.ntok, f->dev.mext, f->dev.pool, qt, ntok, qo, nq, f->P, ml, ch);
+                       f->dev.nodes, f->dev.ntok, f->dev.nsep, f->dev.mext, f->dev.pool, qt, ntok, qo, nq, f->P,
+                       ml, ch);
     return hipGetLastError();
 }
 
@@ -360,6 +368,7 @@ pr::DevForest dev_view(const pr_forest *f) {
     pr::DevForest F;
     F.nodes = f->dev.nodes;
     F.ntok = f->dev.ntok;
+    F.nsep = f->dev.nsep;
     F.mext = f->dev.mext;
     F.pool = f->dev.pool;
     F.moved = f->dev.moved;
@@ -417,6 +426,8 @@ pr_status run_merge(pr_forest *f, const int32_t *peer_of, const int32_t *tokens,
             const pr::DevForest F = dev_view(f);
             hipLaunchKernelGGL(pr::add_build_kernel, dim3(grid_waves(n_add)), dim3(wb), 0, s, F, B, m.keys_out,
                                n_add, m.st, m.grp_nw, m.win_tok, m.win_ins, m.grp_nb, stamp, f->d_ctr);
+            hipLaunchKernelGGL(pr::add_sep_kernel, dim3(grid_waves(n_add)), dim3(wb), 0, s, F, m.keys_out, n_add,
+                               m.grp_nw, m.grp_nb);
             hipLaunchKernelGGL(pr::add_fix_kernel, dim3(grid_threads(n_add, bs)), dim3(bs), 0, s, F, m.keys_out,
                                n_add, m.grp_nw, m.grp_nb, stamp);
         } else {
@@ -473,7 +484,7 @@ pr_status device_load(pr_forest *f, int32_t peer, const pr::PeerSeqs &S) {
 
 extern "C" {
 
-int32_t pr_abi_version(void) { return 1; }
+int32_t pr_abi_version(void) { return 2; }
 
 const char *pr_last_error(void) { return g_err.c_str(); }
 
@@ -636,6 +647,7 @@ pr_status pr_forest_host_image(pr_forest *f, pr_image_view *out) {
     out->pool_tokens = (int64_t)h.pool.size();
     out->nodes = reinterpret_cast<const int32_t *>(h.nodes.data());
     out->ntok = h.ntok.data();
+    out->nsep = h.nsep.data();
     out->mext = h.mext.data();
     out->pool = h.pool.data();
     return ok();

@@ -41,7 +41,8 @@ class ImageView(ctypes.Structure):
     _fields_ = [("mask_words", ctypes.c_int32), ("num_nodes", ctypes.c_int64),
                 ("pool_tokens", ctypes.c_int64),
                 ("nodes", ctypes.POINTER(ctypes.c_int32)), ("ntok", ctypes.POINTER(ctypes.c_int32)),
-                ("mext", ctypes.POINTER(ctypes.c_uint64)), ("pool", ctypes.POINTER(ctypes.c_int32))]
+                ("nsep", ctypes.POINTER(ctypes.c_int32)), ("mext", ctypes.POINTER(ctypes.c_uint64)),
+                ("pool", ctypes.POINTER(ctypes.c_int32))]
 
 
 _lib_handle = None
@@ -80,7 +81,7 @@ def lib() -> ctypes.CDLL:
     L.pr_forest_info_get.restype = ctypes.c_int32
     L.pr_forest_host_image.argtypes = [_vp, ctypes.POINTER(ImageView)]
     L.pr_forest_host_image.restype = ctypes.c_int32
-    if L.pr_abi_version() != 1:
+    if L.pr_abi_version() != 2:
         raise RuntimeError("libprefix_router ABI version mismatch")
     _lib_handle = L
     return L
@@ -186,6 +187,7 @@ def pr_forest_host_image(f: int) -> dict:
     mext = arr(v.mext, v.num_nodes * (W - 1), np.uint64).reshape(-1, W - 1) if W > 1 \
         else np.zeros((v.num_nodes, 0), np.uint64)
     return dict(mask_words=W, nodes=nodes, ntok=arr(v.ntok, v.num_nodes, np.int32),
+                nsep=arr(v.nsep, v.num_nodes, np.int32),
                 masks=np.concatenate([mask0[:, None], mext], axis=1), pool=arr(v.pool, v.pool_tokens, np.int32))
 
 

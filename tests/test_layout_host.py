@@ -82,6 +82,10 @@ def check_structure(img, P):
             assert mc & ~mx == 0, "a child's peers are a subset of its parent's"
         if x != 0 and cnt == 1:
             assert _mask_int(masks[beg]) != mx, "single-child chains with equal masks are compressed"
+        if cnt > 64:  # separators of wide blocks
+            seps = img["nsep"][beg:beg + 64]
+            want = ntok[beg + (np.arange(64) * cnt) // 64]
+            assert np.array_equal(seps, want), "separators of a wide child block"
         assert mx >> P == 0
     assert parents[0] == 0 and (parents[1:] == 1).all(), "every non-root node has one parent"
 
@@ -117,6 +121,17 @@ def test_many_peers_mask_words():
     # 130 peers -> 4 mask words (3 used); peers share sequences heavily
     w = W.tiny_random(5, num_peers=130, vocab=3, max_seqs=3, n_queries=60)
     _compare(w)
+
+
+def test_wide_blocks_carry_separators():
+    """Blocks of more than 64 children (up to a few thousand) carry separators."""
+    rng = np.random.default_rng(11)
+    for n_children in (65, 100, 513, 4097, 5000):
+        first = rng.choice(np.arange(-100000, 100000), size=n_children, replace=False)
+        seqs = [[int(a), int(rng.integers(0, 9))] for a in first]
+        ss = W.from_lists(seqs, sorted(int(rng.integers(0, 3)) for _ in seqs))
+        w = W.Workload(0, "wide", 3, 0, ss, W.from_lists([[int(first[0]), 1], [int(first[-1])], [7777777]]))
+        _compare(w)
 
 
 def test_config1_image():

@@ -11,8 +11,9 @@
 //   2. issues, in one batch, the loads of the query token after the label, of
 //      the child's mask words, of the child's own first-token array
 //      (speculatively, for the next level), and of the label and query tokens
-//      it compares (64 x kLcpVectors per step); query tokens are read once, so
-//      their loads are non-temporal;
+//      it compares: raw buffer loads ranged to the step, 64 tokens per
+//      instruction, all of a step in flight at once; query tokens are read
+//      once, so their loads are non-temporal;
 //   3. narrows the wave-uniform set of peers still matching by the child's peer
 //      mask; every peer that drops out records the depth reached so far (lane
 //      i owns peers i, i+64, ...), and takes the common-prefix length of label
@@ -33,51 +34,88 @@
 #define PR_ROUTE_WAVES_PER_BLOCK 1
 #endif
 #ifndef PR_LCP_VECTORS
-#define PR_LCP_VECTORS 8
+#define PR_LCP_VECTORS 16
+#endif
+#ifndef PR_LCP_FIRST_VECTORS
+#define PR_LCP_FIRST_VECTORS 8
 #endif
 #ifndef PR_QUERY_NT
 #define PR_QUERY_NT 1
+#endif
+#ifndef PR_ROUTE_WAVES_PER_EU
+#define PR_ROUTE_WAVES_PER_EU 8
 #endif
 
 namespace pr {
 
 constexpr int kWave = 64;
 constexpr int kRouteWavesPerBlock = PR_ROUTE_WAVES_PER_BLOCK;
-constexpr int kLcpVectors = PR_LCP_VECTORS;    // 64-token vectors compared per step
+constexpr int kLcpVectors = PR_LCP_VECTORS;               // 64-token vectors per compare step
+constexpr int kLcpFirstVectors = PR_LCP_FIRST_VECTORS;    // ... in a label's first step
 
-// Query tokens are read once: mark their loads non-temporal so they stream
-// through the caches that hold the forest's labels.
-__device__ __forceinline__ int32_t load_stream(const int32_t *p) {
-#if PR_QUERY_NT
-    return __builtin_nontemporal_load(p);
-#else
-    return *p;
-#endif
+// Raw buffer resource over bytes [p, p + bytes): loads past the end return 0
+// without touching memory (the hardware range check of stride-0 buffers).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t token_rsrc(const int32_t *p, int32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<int32_t *>(p), (short)0, bytes, 0x00020000);
+}
+
+// Cache policy of the query loads: non-temporal (read once).
+constexpr int kQueryPolicy = PR_QUERY_NT ? 2 : 0;
+
+// One compare step over cnt <= 64 * NV tokens: ra holds the label tokens,
+// rb the query tokens, both ranged to cnt tokens so that lanes past the end
+// read 0 on both sides and compare equal.  Returns the first mismatch, or -1.
+template <int NV>
+__device__ __forceinline__ int32_t lcp_step(__amdgpu_buffer_rsrc_t ra, __amdgpu_buffer_rsrc_t rb, int lane) {
+    int32_t va[NV], vb[NV];
+    // opaque lane offset: with its range unknown the per-vector constant stays
+    // an add, which folds into the loads' immediate offsets; and as each step
+    // size gets its own opaque value, the compiler cannot merge the first loads
+    // of the short and the long step into one block that waits before the long
+    // step issues the rest
+    int32_t off = lane * 4;
+    asm volatile("" : "+v"(off));
+#pragma unroll
+    for (int j = 0; j < NV; j++) {
+        va[j] = __builtin_amdgcn_raw_buffer_load_b32(ra, off + j * kWave * 4, 0, 0);
+        vb[j] = __builtin_amdgcn_raw_buffer_load_b32(rb, off + j * kWave * 4, 0, kQueryPolicy);
+    }
+    // fold every vector's mismatches into a lane mask before branching, so
+    // that no load of the step can be deferred behind an early exit
+    uint32_t mm = 0;
+#pragma unroll
+    for (int j = 0; j < NV; j++) mm |= (uint32_t)(va[j] != vb[j]) << j;
+    if (!__ballot(mm != 0)) return -1;
+#pragma unroll
+    for (int j = 0; j < NV; j++) {
+        const uint64_t bal = __ballot((mm >> j) & 1u);
+        if (bal) return j * kWave + (int32_t)(__ffsll((unsigned long long)bal) - 1);
+    }
+    return -1;
 }
 
 // Length of the common prefix of a[0..n) (a label) and b[0..n) (query
 // tokens): the first i < n with a[i] != b[i], or n.  Wave-cooperative; every
-// lane returns the same value.
+// lane returns the same value.  A label's first step compares up to
+// 64 * kLcpFirstVectors tokens, which bounds what a mismatch early in a long
+// label reads in vain; later steps compare up to 64 * kLcpVectors, which halves
+// the round trips over long labels that match in full.  A step of at most 128
+// tokens takes a two-vector form.
 __device__ __forceinline__ int64_t wave_lcp(const int32_t *__restrict__ a, const int32_t *__restrict__ b,
                                             int64_t n, int lane) {
-    for (int64_t base = 0; base < n; base += (int64_t)kWave * kLcpVectors) {
-        int32_t va[kLcpVectors], vb[kLcpVectors];
-#pragma unroll
-        for (int j = 0; j < kLcpVectors; j++) {
-            const int64_t i = base + j * kWave + lane;
-            va[j] = 0;
-            vb[j] = 0;
-            if (i < n) {
-                va[j] = a[i];
-                vb[j] = load_stream(b + i);
-            }
-        }
-#pragma unroll
-        for (int j = 0; j < kLcpVectors; j++) {
-            const int64_t i = base + j * kWave + lane;
-            const uint64_t bal = __ballot(i < n && va[j] != vb[j]);
-            if (bal) return base + j * kWave + (__ffsll((unsigned long long)bal) - 1);
-        }
+    int64_t step = (int64_t)kWave * kLcpFirstVectors;
+    for (int64_t base = 0; base < n; base += step, step = (int64_t)kWave * kLcpVectors) {
+        const int32_t cnt = (int32_t)min(n - base, step);
+        const __amdgpu_buffer_rsrc_t ra = token_rsrc(a + base, cnt * 4);
+        const __amdgpu_buffer_rsrc_t rb = token_rsrc(b + base, cnt * 4);
+        int32_t r;
+        if (cnt <= 2 * kWave)
+            r = lcp_step<2>(ra, rb, lane);
+        else if (kLcpVectors > kLcpFirstVectors && cnt <= kWave * kLcpFirstVectors)
+            r = lcp_step<kLcpFirstVectors>(ra, rb, lane);
+        else
+            r = lcp_step<kLcpVectors>(ra, rb, lane);
+        if (r >= 0 && r < cnt) return base + r;
     }
     return n;
 }
@@ -148,7 +186,8 @@ __device__ __forceinline__ bool locate(const ChildBlock &cb, int32_t t, const No
 }
 
 template <int W>
-__global__ __launch_bounds__(kWave *kRouteWavesPerBlock) void route_kernel(
+__global__ __launch_bounds__(kWave *kRouteWavesPerBlock)
+__attribute__((amdgpu_waves_per_eu(PR_ROUTE_WAVES_PER_EU))) void route_kernel(
     const Node *__restrict__ nodes, const int32_t *__restrict__ ntok, const int32_t *__restrict__ nsep,
     const uint64_t *__restrict__ mext,
     const int32_t *__restrict__ pool, const int32_t *__restrict__ qtok, int64_t num_tokens,

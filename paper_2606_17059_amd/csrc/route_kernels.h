@@ -13,7 +13,8 @@
 //      (speculatively, for the next level), and of the label and query tokens
 //      it compares: raw buffer loads ranged to the step, 64 tokens per
 //      instruction, all of a step in flight at once; query tokens are read
-//      once, so their loads are non-temporal;
+//      once, so their loads are non-temporal (except the first level's, which
+//      come with the query's first token, before the walk starts);
 //   3. narrows the wave-uniform set of peers still matching by the child's peer
 //      mask; every peer that drops out records the depth reached so far (lane
 //      i owns peers i, i+64, ...), and takes the common-prefix length of label
@@ -26,6 +27,8 @@
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+#include <type_traits>
 
 #include "forest_layout.h"
 #include "wave_ops.h"
@@ -41,6 +44,12 @@
 #endif
 #ifndef PR_QUERY_NT
 #define PR_QUERY_NT 1
+#endif
+#ifndef PR_FIRST_WINDOW
+#define PR_FIRST_WINDOW 1
+#endif
+#ifndef PR_WIN_VECTORS
+#define PR_WIN_VECTORS 2
 #endif
 #ifndef PR_ROUTE_WAVES_PER_EU
 #define PR_ROUTE_WAVES_PER_EU 8
@@ -95,16 +104,15 @@ __device__ __forceinline__ int32_t lcp_step(__amdgpu_buffer_rsrc_t ra, __amdgpu_
 }
 
 // Length of the common prefix of a[0..n) (a label) and b[0..n) (query
-// tokens): the first i < n with a[i] != b[i], or n.  Wave-cooperative; every
-// lane returns the same value.  A label's first step compares up to
-// 64 * kLcpFirstVectors tokens, which bounds what a mismatch early in a long
-// label reads in vain; later steps compare up to 64 * kLcpVectors, which halves
-// the round trips over long labels that match in full.  A step of at most 128
-// tokens takes a two-vector form.
+// tokens), from position base on: the first i in [base, n) with a[i] != b[i],
+// or n.  Wave-cooperative; every lane returns the same value.  The first step
+// compares up to `first` tokens (a label's first step: 64 * kLcpFirstVectors,
+// which bounds what a mismatch early in a long label reads in vain), later
+// steps up to 64 * kLcpVectors, which halves the round trips over long labels
+// that match in full.  A step of at most 128 tokens takes a two-vector form.
 __device__ __forceinline__ int64_t wave_lcp(const int32_t *__restrict__ a, const int32_t *__restrict__ b,
-                                            int64_t n, int lane) {
-    int64_t step = (int64_t)kWave * kLcpFirstVectors;
-    for (int64_t base = 0; base < n; base += step, step = (int64_t)kWave * kLcpVectors) {
+                                            int64_t n, int64_t base, int64_t first, int lane) {
+    for (int64_t step = first; base < n; base += step, step = (int64_t)kWave * kLcpVectors) {
         const int32_t cnt = (int32_t)min(n - base, step);
         const __amdgpu_buffer_rsrc_t ra = token_rsrc(a + base, cnt * 4);
         const __amdgpu_buffer_rsrc_t rb = token_rsrc(b + base, cnt * 4);
@@ -119,6 +127,62 @@ __device__ __forceinline__ int64_t wave_lcp(const int32_t *__restrict__ a, const
     }
     return n;
 }
+
+#if PR_FIRST_WINDOW
+// First-level window: the query's first 64 * kWinVectors tokens are loaded
+// into registers together with its first token, whose HBM round trip the walk
+// waits for anyway, so that the first level's compare waits only on its label,
+// which the L2 holds.  Lane l of vector j holds token 64 j + l (0 past the
+// query).  The loads use the default cache policy: they also bring the lines
+// that the first level's next-token load reads.  A wider window reads more
+// tokens that the second level reads again.
+constexpr int kWinVectors = PR_WIN_VECTORS;
+constexpr int kWinTokens = kWave * kWinVectors;
+static_assert(kWinVectors >= 2 && kWinVectors <= 16, "window of 2 to 16 vectors");
+
+__device__ __forceinline__ void load_window(int32_t (&win)[kWinVectors], const int32_t *p, int32_t cnt, int lane) {
+    const __amdgpu_buffer_rsrc_t r = token_rsrc(p, cnt * 4);
+    int32_t off = lane * 4;  // opaque, as in lcp_step
+    asm volatile("" : "+v"(off));
+#pragma unroll
+    for (int j = 0; j < kWinVectors; j++)
+        win[j] = __builtin_amdgcn_raw_buffer_load_b32(r, off + j * kWave * 4, 0, 0);
+}
+
+// Label tokens [0, cnt) (ra, cnt <= 64 * NL) against the window, which
+// may hold query tokens past cnt: only lanes below cnt count.  Returns the
+// first mismatch, or -1.
+template <int NL>
+__device__ __forceinline__ int32_t lcp_step_win(__amdgpu_buffer_rsrc_t ra, const int32_t (&win)[kWinVectors],
+                                                int32_t cnt, int lane) {
+    int32_t va[NL];
+    int32_t off = lane * 4;  // opaque, as in lcp_step
+    asm volatile("" : "+v"(off));
+#pragma unroll
+    for (int j = 0; j < NL; j++) va[j] = __builtin_amdgcn_raw_buffer_load_b32(ra, off + j * kWave * 4, 0, 0);
+    uint32_t mm = 0;
+#pragma unroll
+    for (int j = 0; j < NL; j++) mm |= (uint32_t)(j * kWave + lane < cnt && va[j] != win[j]) << j;
+    if (!__ballot(mm != 0)) return -1;
+#pragma unroll
+    for (int j = 0; j < NL; j++) {
+        const uint64_t bal = __ballot((mm >> j) & 1u);
+        if (bal) return j * kWave + (int32_t)(__ffsll((unsigned long long)bal) - 1);
+    }
+    return -1;
+}
+
+// wave_lcp for the first level, whose first query tokens are in win.
+__device__ __forceinline__ int64_t wave_lcp_first(const int32_t *__restrict__ a, const int32_t *__restrict__ b,
+                                                  int64_t n, const int32_t (&win)[kWinVectors], int lane) {
+    const int32_t cnt = (int32_t)min(n, (int64_t)kWinTokens);
+    const __amdgpu_buffer_rsrc_t ra = token_rsrc(a, cnt * 4);
+    const int32_t r =
+        cnt <= 2 * kWave ? lcp_step_win<2>(ra, win, cnt, lane) : lcp_step_win<kWinVectors>(ra, win, cnt, lane);
+    if (r >= 0 && r < cnt) return r;
+    return wave_lcp(a, b, n, kWinTokens, (int64_t)kWave * kLcpVectors, lane);
+}
+#endif
 
 // A node's child block as held by the wave: lane j holds the first token of
 // child beg + j (cnt <= 64) or the block's separator j (cnt > 64).
@@ -222,10 +286,13 @@ __attribute__((amdgpu_waves_per_eu(PR_ROUTE_WAVES_PER_EU))) void route_kernel(
         load_block(cb, ntok, nsep, root.ct_beg, root.ct_cnt, lane);
     }
     int32_t t = qlen > 0 ? qs[0] : 0;
-    while (d < qlen) {
+    // One tree level; returns whether the walk goes on.  The first level is a
+    // separate instance (FIRST), so that the window's registers die after it.
+    auto level = [&](auto first_tag, const auto &win) __attribute__((always_inline)) -> bool {
+        constexpr bool FIRST = decltype(first_tag)::value;
         Child c;
-        if (!locate(cb, t, nodes, ntok, lane, c)) break;
-        if (c.lab_len <= 0) break;  // only the root has an empty label
+        if (!locate(cb, t, nodes, ntok, lane, c)) return false;
+        if (c.lab_len <= 0) return false;  // only the root has an empty label
         // one batch of loads per level: next token, ext mask words, the next
         // child block (used if the label matches in full) and the label compare
         const int64_t end = d + c.lab_len;
@@ -236,7 +303,11 @@ __attribute__((amdgpu_waves_per_eu(PR_ROUTE_WAVES_PER_EU))) void route_kernel(
         for (int w = 1; w < W; w++) mx[w] = mext[(int64_t)c.id * (W - 1) + (w - 1)];
         load_block(cb, ntok, nsep, c.ct_beg, c.ct_cnt, lane);
         const int64_t n = min((int64_t)c.lab_len, qlen - d);
-        const int64_t l = wave_lcp(pool + (uint32_t)c.lab_off, qs + d, n, lane);
+        int64_t l;
+        if constexpr (FIRST)
+            l = wave_lcp_first(pool + (uint32_t)c.lab_off, qs, n, win, lane);
+        else
+            l = wave_lcp(pool + (uint32_t)c.lab_off, qs + d, n, 0, (int64_t)kWave * kLcpFirstVectors, lane);
         bool any = false;
 #pragma unroll
         for (int w = 0; w < W; w++) {
@@ -245,11 +316,21 @@ __attribute__((amdgpu_waves_per_eu(PR_ROUTE_WAVES_PER_EU))) void route_kernel(
             alive[w] = nm;
             any |= nm != 0ull;
         }
-        if (!any) break;  // no peer holds this edge (left behind by a replaced snapshot)
+        if (!any) return false;  // no peer holds this edge (left behind by a replaced snapshot)
         d += l;
-        if (l < c.lab_len) break;
+        if (l < c.lab_len) return false;
         t = tnext;
-    }
+        return d < qlen;
+    };
+    struct NoWindow {};
+#if PR_FIRST_WINDOW
+    int32_t win[kWinVectors];
+    load_window(win, qs, (int32_t)min(qlen, (int64_t)kWinTokens), lane);
+    bool more = qlen > 0 && level(std::true_type{}, win);
+#else
+    bool more = qlen > 0 && level(std::false_type{}, NoWindow{});
+#endif
+    while (more) more = level(std::false_type{}, NoWindow{});
 
     // peers still holding the walked path matched all of it
     int32_t bm = -1, bp = INT32_MAX;

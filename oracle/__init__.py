@@ -7,7 +7,9 @@ shares no code with it.
 The oracle computes the plain definition of the paper's routing rule
 (System Design; Algorithm 1): for every peer p, m[q][p] is the longest common
 prefix of q with any sequence inserted into p's tree, and the chosen peer is the
-lowest id attaining the maximum.  See ``prefix_oracle.c``.
+lowest id attaining the maximum.  ``route_select`` adds the push-back and
+failover selection (best and second-best eligible peer).  See
+``prefix_oracle.c``.
 
 Every function here is pinned by ``tests/test_oracle_pins.py`` against
 independent formulations (hand-worked examples, the prefix-set definition of a
@@ -54,6 +56,9 @@ def _load(path: str) -> ctypes.CDLL:
     lib.or_merge.argtypes = [ctypes.c_void_p, _i32p, _i32p, _i64p, ctypes.c_int64]
     lib.or_route.restype = ctypes.c_int
     lib.or_route.argtypes = [ctypes.c_void_p, _i32p, _i64p, ctypes.c_int64, _i32p, _i32p, ctypes.c_int32]
+    lib.or_route_select.restype = ctypes.c_int
+    lib.or_route_select.argtypes = [ctypes.c_void_p, _i32p, _i64p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int32,
+                                    ctypes.c_int32, _i32p, _i32p, _i32p, ctypes.c_int32]
     lib.or_lcp.restype = ctypes.c_int64
     lib.or_lcp.argtypes = [_i32p, ctypes.c_int64, _i32p, ctypes.c_int64]
     lib.or_prefix_match.restype = ctypes.c_int64
@@ -147,6 +152,27 @@ class Oracle:
         if r:
             raise ValueError(f"or_route failed ({r})")
         return m[:nq], c[:nq]
+
+    def route_select(self, tokens, offsets, eligible=None, local: int = -1, prefer_local: bool = False,
+                     nthreads: int = 0) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
+        """Match lengths, best and second-best eligible peer (push-back and
+        failover selection; see or_route_select in prefix_oracle.c)."""
+        t, o = _csr(tokens, offsets)
+        nq = o.shape[0] - 1
+        m = np.zeros((max(nq, 1), self.num_peers), dtype=np.int32)
+        b1 = np.zeros(max(nq, 1), dtype=np.int32)
+        b2 = np.zeros(max(nq, 1), dtype=np.int32)
+        el = None
+        if eligible is not None:
+            el = np.ascontiguousarray(eligible, dtype=np.uint8)
+            if el.shape != (self.num_peers,):
+                raise ValueError("eligible must hold one flag per peer")
+        nt = nthreads or (os.cpu_count() or 1)
+        r = self._lib.or_route_select(self._h, _p32(t), _p64(o), nq, el.ctypes.data if el is not None else None,
+                                      int(local), int(bool(prefer_local)), _p32(m), _p32(b1), _p32(b2), nt)
+        if r:
+            raise ValueError(f"or_route_select failed ({r})")
+        return m[:nq], b1[:nq], b2[:nq]
 
     def route_seqset(self, qs, idx: Optional[Sequence[int]] = None, nthreads: int = 0):
         """Route all queries of a SeqSet, or only the sampled indices ``idx``."""

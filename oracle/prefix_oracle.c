@@ -219,3 +219,108 @@ int or_route(const or_forest *f, const int32_t *q_tokens, const int64_t *q_offse
     free(th);
     return 0;
 }
+
+/* ---- selection with push-back and failover ------------------------------
+ *
+ * Section "Hot specialist push-back": a node whose queue is too deep
+ * advertises back-pressure, and originating nodes stop routing to it for a
+ * while; the request then runs locally or on a slightly inferior peer.
+ * Section "In-flight forwarded request failure": when a forward times out the
+ * originating node falls back to the next-best target, which may be itself.
+ *
+ *   eligible[p]   nonzero if p may receive requests (zero: pushed back or
+ *                 suspected failed).  NULL means every peer.  The local peer
+ *                 (local >= 0) is always eligible: the originating node can
+ *                 always run the request itself.
+ *   order         larger m first; among equal m the local peer first when
+ *                 prefer_local is set, then the lower peer id.
+ *   best[q]       the first eligible peer in that order, -1 if none;
+ *   second[q]     the first eligible peer after best[q], -1 if none.
+ *
+ * m[q][p] is the same matrix as in or_route, over every peer.
+ */
+static int is_eligible(const uint8_t *eligible, int32_t p, int32_t local) {
+#ifdef PLANT_IGNORE_ELIGIBLE
+    (void)eligible; (void)p; (void)local;
+    return 1;
+#else
+    return p == local || !eligible || eligible[p] != 0;
+#endif
+}
+
+/* Does peer a come before peer b in the selection order? */
+static int comes_before(int32_t a, int32_t b, const int32_t *m, int32_t local, int32_t prefer_local) {
+#ifdef PLANT_LOCAL_ALWAYS_FIRST
+    if (prefer_local && a == local) return 1;
+    if (prefer_local && b == local) return 0;
+#endif
+    if (m[a] != m[b]) return m[a] > m[b];
+    if (prefer_local && a == local) return 1;
+    if (prefer_local && b == local) return 0;
+    return a < b;
+}
+
+typedef struct {
+    const or_forest *f;
+    const int32_t *qt;
+    const int64_t *qo;
+    int64_t lo, hi;
+    const uint8_t *eligible;
+    int32_t local, prefer_local;
+    int32_t *match_len, *best, *second;
+} select_job;
+
+static void *select_range(void *arg) {
+    select_job *j = (select_job *)arg;
+    int32_t P = j->f->num_peers;
+    for (int64_t q = j->lo; q < j->hi; q++) {
+        const int32_t *qs = j->qt + j->qo[q];
+        int64_t ql = j->qo[q + 1] - j->qo[q];
+        int32_t *row = j->match_len + q * (int64_t)P;
+        for (int32_t p = 0; p < P; p++) row[p] = (int32_t)or_prefix_match(j->f, p, qs, ql);
+        int32_t b1 = -1, b2 = -1;
+        for (int32_t p = 0; p < P; p++) {
+            if (!is_eligible(j->eligible, p, j->local)) continue;
+            if (b1 < 0 || comes_before(p, b1, row, j->local, j->prefer_local)) {
+                b2 = b1;
+                b1 = p;
+            } else if (b2 < 0 || comes_before(p, b2, row, j->local, j->prefer_local)) {
+                b2 = p;
+            }
+        }
+        j->best[q] = b1;
+        j->second[q] = b2;
+    }
+    return NULL;
+}
+
+/* Route queries [0, nq) with the selection above.  local in [-1, P). */
+int or_route_select(const or_forest *f, const int32_t *q_tokens, const int64_t *q_offsets, int64_t nq,
+                    const uint8_t *eligible, int32_t local, int32_t prefer_local, int32_t *match_len,
+                    int32_t *best, int32_t *second, int32_t nthreads) {
+    if (!f || check_csr(q_offsets, nq) || local < -1 || local >= f->num_peers) return -1;
+    if (nthreads < 1) nthreads = 1;
+    if (nthreads > nq) nthreads = nq > 0 ? (int32_t)nq : 1;
+    select_job *jobs = (select_job *)calloc((size_t)nthreads, sizeof(select_job));
+    pthread_t *th = (pthread_t *)calloc((size_t)nthreads, sizeof(pthread_t));
+    if (!jobs || !th) { free(jobs); free(th); return -2; }
+    for (int32_t t = 0; t < nthreads; t++) {
+        jobs[t].f = f;
+        jobs[t].qt = q_tokens;
+        jobs[t].qo = q_offsets;
+        jobs[t].lo = nq * t / nthreads;
+        jobs[t].hi = nq * (t + 1) / nthreads;
+        jobs[t].eligible = eligible;
+        jobs[t].local = local;
+        jobs[t].prefer_local = prefer_local;
+        jobs[t].match_len = match_len;
+        jobs[t].best = best;
+        jobs[t].second = second;
+    }
+    for (int32_t t = 1; t < nthreads; t++) pthread_create(&th[t], NULL, select_range, &jobs[t]);
+    select_range(&jobs[0]);
+    for (int32_t t = 1; t < nthreads; t++) pthread_join(th[t], NULL);
+    free(jobs);
+    free(th);
+    return 0;
+}

@@ -269,3 +269,98 @@ def check_config_invariants(make: Callable, w, idx: np.ndarray, nthreads: int = 
     if not np.array_equal(mp[np.arange(len(pick)), own], ps.lengths()):
         fails.append("a cached prompt does not match its owner in full")
     return fails
+
+
+# ---- selection with push-back and failover ----------------------------------
+SELECT_GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "select_examples.txt")
+
+
+def parse_select_golden(path: str = SELECT_GOLDEN):
+    """[(name, P, loads {p: [seqs]}, [(eligible, local, prefer, query, best, second)])]."""
+    out, cur = [], None
+    sel = None
+    for raw in open(path):
+        line = raw.split("#", 1)[0].strip()
+        if not line:
+            continue
+        kw, _, rest = line.partition(" ")
+        if kw == "example":
+            cur = [rest.strip(), 0, {}, []]
+            out.append(cur)
+        elif kw == "peers":
+            cur[1] = int(rest)
+        elif kw == "load":
+            p, _, body = rest.partition("|")
+            body = body.strip()
+            cur[2][int(p)] = [] if not body else [_toks(x) for x in body.split(";")]
+        elif kw == "select":
+            bits, local, prefer = rest.split()
+            sel = (np.array([int(c) for c in bits], np.uint8), int(local), bool(int(prefer)))
+        elif kw == "query":
+            q, _, res = rest.partition("->")
+            b1, b2 = (int(x) for x in res.split())
+            cur[3].append((sel[0], sel[1], sel[2], _toks(q), b1, b2))
+        else:
+            raise ValueError(f"bad directive {kw!r}")
+    return out
+
+
+def select_order(m_row: np.ndarray, eligible, local: int, prefer: bool) -> List[int]:
+    """The candidate order written as a sort: key (-m, local-first flag, id),
+    keeping eligible peers and the local one."""
+    P = m_row.shape[0]
+    ids = np.arange(P)
+    loc_key = np.where(prefer & (ids == local), 0, 1)
+    order = np.lexsort((ids, loc_key, -m_row.astype(np.int64)))
+    keep = np.ones(P, bool) if eligible is None else np.asarray(eligible).astype(bool).copy()
+    if local >= 0:
+        keep[local] = True
+    return [int(p) for p in order if keep[p]]
+
+
+def check_select_golden(make: Callable) -> List[str]:
+    fails = []
+    for name, P, loads, cases in parse_select_golden():
+        o = make(P)
+        for p, seqs in loads.items():
+            t, off = _csr(seqs)
+            o.load(p, t, off)
+        for el, local, prefer, q, b1, b2 in cases:
+            t, off = _csr([q])
+            _, g1, g2 = o.route_select(t, off, el, local, prefer, 1)
+            if (int(g1[0]), int(g2[0])) != (b1, b2):
+                fails.append(f"{name}: q={q} eligible={el.tolist()} local={local} prefer={prefer}: "
+                             f"got ({int(g1[0])}, {int(g2[0])}) want ({b1}, {b2})")
+    return fails
+
+
+def check_select_random(make: Callable, seeds: Sequence[int]) -> List[str]:
+    """Random eligibility, local peer and prefer flag over tiny random forests:
+    the oracle's best and second equal the first two of the sorted order, and
+    its match matrix equals route()'s."""
+    import workloads as W
+    fails = []
+    for sd in seeds:
+        rng = np.random.default_rng(1000 + sd)
+        w = W.tiny_random(sd, num_peers=2 + sd % 5, vocab=3, n_queries=40)
+        P = w.num_peers
+        o = make(P)
+        load_all(o, w.snapshot, P)
+        m0, c0 = o.route(w.queries.tokens, w.queries.offsets, 2)
+        for trial in range(6):
+            el = (rng.random(P) < 0.6).astype(np.uint8)
+            local = int(rng.integers(-1, P))
+            prefer = bool(rng.integers(0, 2))
+            m, b1, b2 = o.route_select(w.queries.tokens, w.queries.offsets, el, local, prefer, 2)
+            if not np.array_equal(m, m0):
+                fails.append(f"seed={sd}: route_select match matrix differs from route")
+            for i in range(len(w.queries)):
+                order = select_order(m0[i], el, local, prefer) + [-1, -1]
+                if (int(b1[i]), int(b2[i])) != (order[0], order[1]):
+                    fails.append(f"seed={sd} trial={trial} q={i}: got ({b1[i]}, {b2[i]}) want {order[:2]}")
+                    break
+        # everyone eligible, no local peer: best is route()'s chosen
+        _, b1, _ = o.route_select(w.queries.tokens, w.queries.offsets, None, -1, False, 2)
+        if not np.array_equal(b1, c0):
+            fails.append(f"seed={sd}: unrestricted best differs from chosen")
+    return fails

@@ -88,8 +88,35 @@ def test_edge_cases():
         o.merge(np.array([-1], np.int32), np.zeros(1, np.int32), np.array([0, 1], np.int64))
 
 
+def test_select_golden_hand_examples():
+    assert pins.check_select_golden(make) == []
+
+
+def test_select_golden_file_is_nontrivial():
+    exs = pins.parse_select_golden()
+    cases = [c for e in exs for c in e[3]]
+    assert len(cases) >= 10
+    assert any(c[1] >= 0 and c[2] for c in cases)          # prefer-local with a local peer
+    assert any(c[5] == -1 for c in cases)                   # no second choice
+    assert any(not c[0].any() for c in cases)               # nothing eligible
+
+
+def test_select_random_vs_sorted_order():
+    assert pins.check_select_random(make, seeds=range(10)) == []
+
+
+def test_select_rejects_bad_local():
+    o = oracle.Oracle(3)
+    t, off = np.array([1], np.int32), np.array([0, 1], np.int64)
+    with pytest.raises(ValueError):
+        o.route_select(t, off, None, 3, False)
+    with pytest.raises(ValueError):
+        o.route_select(t, off, np.ones(2, np.uint8), -1, False)
+
+
 PLANTS = ["PLANT_LCP_OFF_BY_ONE", "PLANT_MIN_NOT_MAX", "PLANT_TIE_HIGHEST",
-          "PLANT_LOAD_APPENDS", "PLANT_MERGE_WRONG_PEER"]
+          "PLANT_LOAD_APPENDS", "PLANT_MERGE_WRONG_PEER", "PLANT_IGNORE_ELIGIBLE",
+          "PLANT_LOCAL_ALWAYS_FIRST"]
 
 
 @pytest.mark.parametrize("plant", PLANTS)
@@ -101,5 +128,6 @@ def test_planted_mistake_is_caught(plant, tmp_path):
         return oracle.Oracle(P, lib_path=path)
 
     fails = pins.check_golden(mk) + pins.check_tiny_random(mk, seeds=range(3), vocabs=(3,)) \
-        + pins.check_merge_semantics(mk, seeds=range(2))
+        + pins.check_merge_semantics(mk, seeds=range(2)) + pins.check_select_golden(mk) \
+        + pins.check_select_random(mk, seeds=range(2))
     assert fails, f"{plant} slipped through every pin"

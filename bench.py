@@ -191,6 +191,42 @@ def bench_stream(args, w, dev):
         "phases": phases_out, "cpu": cpu}
 
 
+def bench_select(f, w, qt, qo, needed, K, warmup, dev) -> dict:
+    """Time pr_route_select on the same batch: 75% of peers eligible (seeded),
+    local peer 0 preferred on ties, best and second-best written; once with the
+    match-length matrix and once with the two picks only."""
+    import torch
+    from paper_2606_17059_amd import eligible_words
+    P = w.num_peers
+    nq = len(w.queries)
+    el = (np.random.default_rng(20261202).random(P) < 0.75).astype(np.uint8)
+    elw = torch.from_numpy(eligible_words(el)).to(dev)
+    ml = torch.empty((nq, P), dtype=torch.int32, device=dev)
+    b1 = torch.empty(nq, dtype=torch.int32, device=dev)
+    b2 = torch.empty(nq, dtype=torch.int32, device=dev)
+    out = {"eligible_peers": int(el.sum()), "local_peer": 0, "prefer_local": True}
+    for name, mlx, extra_bytes in (("with_match_len", ml, 4 * (P + 2)), ("picks_only", None, 8)):
+        for i in range(warmup):
+            f.route_select(qt[i % len(qt)], qo[i % len(qo)], elw, 0, True, mlx, b1, b2, want_match_len=mlx is not None)
+        torch.cuda.synchronize()
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+        for k in range(K):
+            ev[k][0].record()
+            f.route_select(qt[k % len(qt)], qo[k % len(qo)], elw, 0, True, mlx, b1, b2,
+                           want_match_len=mlx is not None)
+            ev[k][1].record()
+        torch.cuda.synchronize()
+        ms = np.array([a.elapsed_time(b) for a, b in ev])
+        byts = float((4 * needed + extra_bytes + 8).sum())
+        out[name] = {"kernel_ms": float(ms.mean()), "kernel_ms_median": float(np.median(ms)),
+                     "queries_per_s": nq / (float(ms.mean()) / 1e3),
+                     "algorithmic_bytes_per_launch": byts,
+                     "hbm_gbps": byts / (float(ms.mean()) / 1e3) / 1e9,
+                     "frac": byts / (float(ms.mean()) / 1e3) / 1e9 / PEAK_HBM_GBPS}
+    f.check()
+    return out
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -199,6 +235,8 @@ def main() -> int:
     ap.add_argument("--config", type=int, default=2, choices=sorted(WORKLOADS))
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU time of the oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-select", action="store_true",
+                    help="skip timing pr_route_select (push-back / failover selection)")
     ap.add_argument("--copies", type=int, default=2, help="device copies of the query batch to rotate")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="first copy a buffer of this size device-to-device three times (a plain copy kernel "
@@ -315,6 +353,10 @@ def main() -> int:
             "actual_hit": float(mt[rows, ce].sum() / tot),
             "oracle_true_hit": float(mt[rows, ct].sum() / tot)}
         log(f"[bench] stale report: {extra['stale_report']}")
+
+    if not args.no_select:
+        extra["select"] = bench_select(f, w, qt, qo, needed, K, args.warmup, dev)
+        log(f"[bench] select: {extra['select']}")
 
     cpu = None
     if not args.no_cpu_baseline:

@@ -134,6 +134,43 @@ pr_status pr_route(pr_forest *f, const int32_t *q_tokens, int64_t num_tokens,
                    int32_t *chosen, void *hip_stream);
 
 /*
+ * Peer selection under push-back and failover (paper, Section "Hot specialist
+ * push-back": originating nodes stop routing to a node that advertised
+ * back-pressure, and such a request runs locally or on a slightly inferior
+ * peer; Section "In-flight forwarded request failure": on a forward timeout
+ * the originating node falls back to the next-best target, which may be
+ * itself).  Same walk as pr_route; then the candidates are ordered by larger
+ * match length, then (flag PR_SELECT_PREFER_LOCAL) the local peer, then the
+ * lower peer id, and
+ *   best[q]    = the first eligible candidate, -1 if none;
+ *   second[q]  = the next eligible candidate, -1 if none.
+ * Arguments:
+ *   eligible    DEVICE uint64 [ceil(num_peers / 64)]: bit p % 64 of word
+ *               p / 64 set if peer p may receive requests (clear: pushed back
+ *               or suspected failed); NULL means every peer.
+ *   local_peer  the calling node's own peer id, or -1.  It is always eligible:
+ *               the originating node can always run a request itself.
+ *   flags       0 or PR_SELECT_PREFER_LOCAL (on equal match the local peer
+ *               comes first; with 0, ties go to the lowest id as in pr_route).
+ *   match_len   DEVICE int32 [num_queries][num_peers] as in pr_route, or NULL
+ *               to skip writing it (the selection still uses every peer's match).
+ *   best        DEVICE int32 [num_queries], required.
+ *   second      DEVICE int32 [num_queries], or NULL.
+ * With eligible NULL, local_peer -1 and flags 0, best equals pr_route's chosen.
+ * A query with invalid offsets gets match_len -1, best -1 and second -1.
+ * Errors (host side, nothing enqueued): PR_EINVAL (local_peer outside
+ * [-1, num_peers), unknown flags, NULL q_offsets or best with num_queries > 0,
+ * negative counts), PR_ENOMEM / PR_EDEVICE as in pr_route.
+ */
+#define PR_SELECT_PREFER_LOCAL 1u
+
+pr_status pr_route_select(pr_forest *f, const int32_t *q_tokens, int64_t num_tokens,
+                          const int64_t *q_offsets, int64_t num_queries,
+                          const uint64_t *eligible, int32_t local_peer, uint32_t flags,
+                          int32_t *match_len, int32_t *best, int32_t *second,
+                          void *hip_stream);
+
+/*
  * Wait for the forest's device work and report inputs that device calls
  * skipped since the last check: returns PR_OK if none, else PR_EINVAL with the
  * count in the message (and resets the count).

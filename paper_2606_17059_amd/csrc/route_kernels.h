@@ -249,13 +249,74 @@ __device__ __forceinline__ bool locate(const ChildBlock &cb, int32_t t, const No
     return true;
 }
 
+// Peer selection (the argmax of Algorithm 1, with the push-back and failover
+// rules of Sections "Hot specialist push-back" and "In-flight forwarded
+// request failure").  Candidates are ordered by larger match, then, when
+// prefer_local is set, the local peer, then the lower id; best is the first
+// eligible candidate and second the next (-1 when there is none).  The local
+// peer is always eligible.  Plain routing is the case "every peer eligible,
+// no local peer, no second".
+struct Select {
+    const uint64_t *eligible;  // ceil(P / 64) words, bit p % 64 of word p / 64; nullptr: every peer
+    int32_t local;             // -1: none
+    int32_t prefer_local;
+    int32_t *second;           // nullptr: not wanted
+};
+
+// Order key of a candidate: larger is earlier; 0 for peers that are not
+// candidates (every real key is above 2^32 - 1026).
+__device__ __forceinline__ uint64_t select_key(int32_t m, int32_t p, const Select &sel) {
+    const uint32_t tie = (sel.prefer_local && p == sel.local) ? 0u : (uint32_t)p + 1u;
+    return ((uint64_t)(uint32_t)m << 32) | (uint64_t)(0xFFFFFFFFu - tie);
+}
+
+__device__ __forceinline__ int32_t select_decode(uint64_t key, const Select &sel) {
+    if (key == 0) return -1;
+    const uint32_t tie = 0xFFFFFFFFu - (uint32_t)key;
+    return tie == 0 ? sel.local : (int32_t)(tie - 1u);
+}
+
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+        const uint64_t o = __shfl_xor(v, off);
+        v = o > v ? o : v;
+    }
+    return v;
+}
+
+template <int W>
+__device__ __forceinline__ int32_t select_peers(const int32_t (&m)[W], int32_t P, int lane, const Select &sel,
+                                                bool want_second, int32_t &second) {
+    uint64_t key[W];
+#pragma unroll
+    for (int w = 0; w < W; w++) {
+        const int p = lane + 64 * w;
+        bool ok = p < P;
+        if (ok && sel.eligible) ok = ((sel.eligible[w] >> lane) & 1ull) || p == sel.local;
+        key[w] = ok ? select_key(m[w], p, sel) : 0ull;
+    }
+    uint64_t k1 = 0;
+#pragma unroll
+    for (int w = 0; w < W; w++) k1 = key[w] > k1 ? key[w] : k1;
+    k1 = wave_max_u64(k1);
+    second = -1;
+    if (want_second) {
+        uint64_t k2 = 0;
+#pragma unroll
+        for (int w = 0; w < W; w++) k2 = (key[w] != k1 && key[w] > k2) ? key[w] : k2;
+        second = select_decode(wave_max_u64(k2), sel);
+    }
+    return select_decode(k1, sel);
+}
+
 template <int W>
 __global__ __launch_bounds__(kWave *kRouteWavesPerBlock)
 __attribute__((amdgpu_waves_per_eu(PR_ROUTE_WAVES_PER_EU))) void route_kernel(
     const Node *__restrict__ nodes, const int32_t *__restrict__ ntok, const int32_t *__restrict__ nsep,
     const uint64_t *__restrict__ mext,
     const int32_t *__restrict__ pool, const int32_t *__restrict__ qtok, int64_t num_tokens,
-    const int64_t *__restrict__ qoff, int64_t nq, int32_t P, int32_t *__restrict__ match_len,
+    const int64_t *__restrict__ qoff, int64_t nq, int32_t P, const Select sel, int32_t *__restrict__ match_len,
     int32_t *__restrict__ chosen) {
     const int lane = (int)(threadIdx.x & (kWave - 1));
     const int64_t q = (int64_t)blockIdx.x * kRouteWavesPerBlock + uniform((int32_t)(threadIdx.x / kWave));
@@ -263,8 +324,12 @@ __attribute__((amdgpu_waves_per_eu(PR_ROUTE_WAVES_PER_EU))) void route_kernel(
     int32_t *row = match_len + q * (int64_t)P;
     const int64_t qb = qoff[q], qe = qoff[q + 1];
     if (qb < 0 || qe < qb || qe > num_tokens || qe - qb > (int64_t)INT32_MAX) {
-        for (int p = lane; p < P; p += kWave) row[p] = -1;
-        if (lane == 0) chosen[q] = -1;
+        if (match_len)
+            for (int p = lane; p < P; p += kWave) row[p] = -1;
+        if (lane == 0) {
+            chosen[q] = -1;
+            if (sel.second) sel.second[q] = -1;
+        }
         return;
     }
     const int32_t *qs = qtok + qb;
@@ -333,30 +398,23 @@ __attribute__((amdgpu_waves_per_eu(PR_ROUTE_WAVES_PER_EU))) void route_kernel(
     while (more) more = level(std::false_type{}, NoWindow{});
 
     // peers still holding the walked path matched all of it
-    int32_t bm = -1, bp = INT32_MAX;
 #pragma unroll
-    for (int w = 0; w < W; w++) {
+    for (int w = 0; w < W; w++)
         if ((alive[w] >> lane) & 1ull) m[w] = (int32_t)d;
-        const int p = lane + 64 * w;
-        if (p < P && m[w] > bm) {
-            bm = m[w];
-            bp = p;
+
+    if (match_len) {
+#pragma unroll
+        for (int w = 0; w < W; w++) {
+            const int p = lane + 64 * w;
+            if (p < P) row[p] = m[w];
         }
     }
-    // argmax over peers: the largest match, then the lowest peer id holding it
-    int32_t M = bm;
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) M = max(M, __shfl_xor(M, off));
-    int32_t cand = (bm == M) ? bp : INT32_MAX;
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) cand = min(cand, __shfl_xor(cand, off));
-
-#pragma unroll
-    for (int w = 0; w < W; w++) {
-        const int p = lane + 64 * w;
-        if (p < P) row[p] = m[w];
+    int32_t second;
+    const int32_t best = select_peers<W>(m, P, lane, sel, sel.second != nullptr, second);
+    if (lane == 0) {
+        chosen[q] = best;
+        if (sel.second) sel.second[q] = second;
     }
-    if (lane == 0) chosen[q] = cand;
 }
 
 }  // namespace pr

@@ -283,11 +283,11 @@ pr_status commit(pr_forest *f) {
 
 template <int W>
 hipError_t launch_route(const pr_forest *f, const int32_t *qt, int64_t ntok, const int64_t *qo, int64_t nq,
-                        int32_t *ml, int32_t *ch, hipStream_t s) {
+                        const pr::Select &sel, int32_t *ml, int32_t *ch, hipStream_t s) {
     const int64_t blocks = (nq + pr::kRouteWavesPerBlock - 1) / pr::kRouteWavesPerBlock;
     hipLaunchKernelGGL(pr::route_kernel<W>, dim3((unsigned)blocks), dim3(pr::kWave * pr::kRouteWavesPerBlock), 0, s,
                        f->dev.nodes, f->dev.ntok, f->dev.nsep, f->dev.mext, f->dev.pool, qt, ntok, qo, nq, f->P,
-                       ml, ch);
+                       sel, ml, ch);
     return hipGetLastError();
 }
 
@@ -484,7 +484,7 @@ pr_status device_load(pr_forest *f, int32_t peer, const pr::PeerSeqs &S) {
 
 extern "C" {
 
-int32_t pr_abi_version(void) { return 2; }
+int32_t pr_abi_version(void) { return 3; }
 
 const char *pr_last_error(void) { return g_err.c_str(); }
 
@@ -578,13 +578,9 @@ pr_status pr_merge(pr_forest *f, const int32_t *peer_of, const int32_t *tokens, 
     return ok();
 }
 
-pr_status pr_route(pr_forest *f, const int32_t *q_tokens, int64_t num_tokens, const int64_t *q_offsets,
-                   int64_t num_queries, int32_t *match_len, int32_t *chosen, void *hip_stream) {
-    if (!f) return fail(PR_EINVAL, "forest is NULL");
-    if (num_queries < 0 || num_tokens < 0) return fail(PR_EINVAL, "negative count");
-    if (num_queries == 0) return ok();
-    if (!q_offsets || !match_len || !chosen) return fail(PR_EINVAL, "NULL device pointer");
-    if (num_tokens > 0 && !q_tokens) return fail(PR_EINVAL, "q_tokens is NULL");
+static pr_status route_impl(pr_forest *f, const int32_t *q_tokens, int64_t num_tokens, const int64_t *q_offsets,
+                            int64_t num_queries, const pr::Select &sel, int32_t *match_len, int32_t *chosen,
+                            void *hip_stream) {
     if (num_queries > (int64_t)0x7fffffff * pr::kRouteWavesPerBlock) return fail(PR_EINVAL, "too many queries");
     if (f->broken) return fail(PR_ESTATE, "an earlier device update failed; destroy the forest");
     DeviceScope ds(f);
@@ -594,14 +590,39 @@ pr_status pr_route(pr_forest *f, const int32_t *q_tokens, int64_t num_tokens, co
     hipStream_t st = (hipStream_t)hip_stream;
     hipError_t e;
     switch (f->W) {
-        case 1: e = launch_route<1>(f, q_tokens, num_tokens, q_offsets, num_queries, match_len, chosen, st); break;
-        case 2: e = launch_route<2>(f, q_tokens, num_tokens, q_offsets, num_queries, match_len, chosen, st); break;
-        case 4: e = launch_route<4>(f, q_tokens, num_tokens, q_offsets, num_queries, match_len, chosen, st); break;
-        case 8: e = launch_route<8>(f, q_tokens, num_tokens, q_offsets, num_queries, match_len, chosen, st); break;
-        default: e = launch_route<16>(f, q_tokens, num_tokens, q_offsets, num_queries, match_len, chosen, st); break;
+        case 1: e = launch_route<1>(f, q_tokens, num_tokens, q_offsets, num_queries, sel, match_len, chosen, st); break;
+        case 2: e = launch_route<2>(f, q_tokens, num_tokens, q_offsets, num_queries, sel, match_len, chosen, st); break;
+        case 4: e = launch_route<4>(f, q_tokens, num_tokens, q_offsets, num_queries, sel, match_len, chosen, st); break;
+        case 8: e = launch_route<8>(f, q_tokens, num_tokens, q_offsets, num_queries, sel, match_len, chosen, st); break;
+        default: e = launch_route<16>(f, q_tokens, num_tokens, q_offsets, num_queries, sel, match_len, chosen, st); break;
     }
     if (e != hipSuccess) return fail(PR_EDEVICE, std::string("route launch failed: ") + hipGetErrorString(e));
     return ok();
+}
+
+pr_status pr_route(pr_forest *f, const int32_t *q_tokens, int64_t num_tokens, const int64_t *q_offsets,
+                   int64_t num_queries, int32_t *match_len, int32_t *chosen, void *hip_stream) {
+    if (!f) return fail(PR_EINVAL, "forest is NULL");
+    if (num_queries < 0 || num_tokens < 0) return fail(PR_EINVAL, "negative count");
+    if (num_queries == 0) return ok();
+    if (!q_offsets || !match_len || !chosen) return fail(PR_EINVAL, "NULL device pointer");
+    if (num_tokens > 0 && !q_tokens) return fail(PR_EINVAL, "q_tokens is NULL");
+    const pr::Select sel{nullptr, -1, 0, nullptr};
+    return route_impl(f, q_tokens, num_tokens, q_offsets, num_queries, sel, match_len, chosen, hip_stream);
+}
+
+pr_status pr_route_select(pr_forest *f, const int32_t *q_tokens, int64_t num_tokens, const int64_t *q_offsets,
+                          int64_t num_queries, const uint64_t *eligible, int32_t local_peer, uint32_t flags,
+                          int32_t *match_len, int32_t *best, int32_t *second, void *hip_stream) {
+    if (!f) return fail(PR_EINVAL, "forest is NULL");
+    if (num_queries < 0 || num_tokens < 0) return fail(PR_EINVAL, "negative count");
+    if (local_peer < -1 || local_peer >= f->P) return fail(PR_EINVAL, "local_peer out of range");
+    if (flags & ~(uint32_t)PR_SELECT_PREFER_LOCAL) return fail(PR_EINVAL, "unknown flags");
+    if (num_queries == 0) return ok();
+    if (!q_offsets || !best) return fail(PR_EINVAL, "NULL device pointer");
+    if (num_tokens > 0 && !q_tokens) return fail(PR_EINVAL, "q_tokens is NULL");
+    const pr::Select sel{eligible, local_peer, (flags & PR_SELECT_PREFER_LOCAL) ? 1 : 0, second};
+    return route_impl(f, q_tokens, num_tokens, q_offsets, num_queries, sel, match_len, best, hip_stream);
 }
 
 pr_status pr_forest_check(pr_forest *f) {

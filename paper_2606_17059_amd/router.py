@@ -20,8 +20,10 @@ PR_OK, PR_EINVAL, PR_ENOMEM, PR_EDEVICE, PR_ESTATE = 0, -1, -2, -3, -4
 PR_MAX_PEERS = 1024
 
 EXPORTED = ("pr_abi_version", "pr_last_error", "pr_forest_create", "pr_forest_destroy",
-            "pr_load_snapshot", "pr_merge", "pr_route", "pr_forest_check", "pr_forest_info_get",
-            "pr_forest_host_image")
+            "pr_load_snapshot", "pr_merge", "pr_route", "pr_route_select", "pr_forest_check",
+            "pr_forest_info_get", "pr_forest_host_image")
+
+PR_SELECT_PREFER_LOCAL = 1
 
 
 class RouterError(RuntimeError):
@@ -75,13 +77,16 @@ def lib() -> ctypes.CDLL:
     L.pr_merge.restype = ctypes.c_int32
     L.pr_route.argtypes = [_vp, _vp, ctypes.c_int64, _vp, ctypes.c_int64, _vp, _vp, _vp]
     L.pr_route.restype = ctypes.c_int32
+    L.pr_route_select.argtypes = [_vp, _vp, ctypes.c_int64, _vp, ctypes.c_int64, _vp, ctypes.c_int32,
+                                  ctypes.c_uint32, _vp, _vp, _vp, _vp]
+    L.pr_route_select.restype = ctypes.c_int32
     L.pr_forest_check.argtypes = [_vp]
     L.pr_forest_check.restype = ctypes.c_int32
     L.pr_forest_info_get.argtypes = [_vp, ctypes.POINTER(ForestInfo)]
     L.pr_forest_info_get.restype = ctypes.c_int32
     L.pr_forest_host_image.argtypes = [_vp, ctypes.POINTER(ImageView)]
     L.pr_forest_host_image.restype = ctypes.c_int32
-    if L.pr_abi_version() != 2:
+    if L.pr_abi_version() != 3:
         raise RuntimeError("libprefix_router ABI version mismatch")
     _lib_handle = L
     return L
@@ -159,6 +164,47 @@ def pr_route(f: int, q_tokens, q_offsets, match_len, chosen, num_peers: int, str
     _check(lib().pr_route(f, q_tokens.data_ptr() or None, q_tokens.numel(), q_offsets.data_ptr(), nq,
                           match_len.data_ptr() or None, chosen.data_ptr() or None,
                           _stream_ptr(stream, q_offsets.device)))
+
+
+def pr_route_select(f: int, q_tokens, q_offsets, eligible, local_peer: int, flags: int, match_len, best, second,
+                    num_peers: int, stream=None) -> None:
+    """eligible: CUDA uint64 tensor of ceil(num_peers / 64) words (torch.int64
+    holding the bits) or None; match_len and second may be None."""
+    import torch
+    _dev(q_tokens, torch.int32, "q_tokens")
+    _dev(q_offsets, torch.int64, "q_offsets")
+    _dev(best, torch.int32, "best")
+    nq = q_offsets.numel() - 1
+    if nq < 0:
+        raise ValueError("q_offsets must have at least one entry")
+    if best.numel() != nq:
+        raise ValueError("best must hold [num_queries]")
+    if match_len is not None:
+        _dev(match_len, torch.int32, "match_len")
+        if match_len.numel() != nq * num_peers:
+            raise ValueError("match_len must hold [num_queries][num_peers]")
+    if second is not None:
+        _dev(second, torch.int32, "second")
+        if second.numel() != nq:
+            raise ValueError("second must hold [num_queries]")
+    if eligible is not None:
+        _dev(eligible, torch.int64, "eligible")
+        if eligible.numel() != (num_peers + 63) // 64:
+            raise ValueError("eligible must hold ceil(num_peers / 64) words")
+    _check(lib().pr_route_select(f, q_tokens.data_ptr() or None, q_tokens.numel(), q_offsets.data_ptr(), nq,
+                                 eligible.data_ptr() if eligible is not None else None, int(local_peer),
+                                 int(flags), match_len.data_ptr() if match_len is not None else None,
+                                 best.data_ptr() or None, second.data_ptr() if second is not None else None,
+                                 _stream_ptr(stream, q_offsets.device)))
+
+
+def eligible_words(flags) -> np.ndarray:
+    """Pack per-peer 0/1 flags into the int64 words pr_route_select reads."""
+    b = np.asarray(flags).astype(bool)
+    words = np.zeros((b.shape[0] + 63) // 64, dtype=np.uint64)
+    for p in np.nonzero(b)[0]:
+        words[p // 64] |= np.uint64(1) << np.uint64(p % 64)
+    return words.view(np.int64)
 
 
 def pr_forest_check(f: int) -> None:
@@ -246,6 +292,25 @@ class Forest:
             chosen = torch.empty(nq, dtype=torch.int32, device=dev)
         pr_route(self.handle, q_tokens, q_offsets, match_len, chosen, self.num_peers, stream)
         return match_len, chosen
+
+    def route_select(self, q_tokens, q_offsets, eligible=None, local_peer: int = -1, prefer_local: bool = False,
+                     match_len=None, best=None, second=None, want_match_len: bool = True,
+                     want_second: bool = True, stream=None) -> Tuple:
+        """Best and second-best eligible peer (pr_route_select).  eligible: a
+        CUDA int64 tensor of packed words (see eligible_words) or None."""
+        import torch
+        nq = q_offsets.numel() - 1
+        dev = q_offsets.device
+        if match_len is None and want_match_len:
+            match_len = torch.empty((nq, self.num_peers), dtype=torch.int32, device=dev)
+        if best is None:
+            best = torch.empty(nq, dtype=torch.int32, device=dev)
+        if second is None and want_second:
+            second = torch.empty(nq, dtype=torch.int32, device=dev)
+        pr_route_select(self.handle, q_tokens, q_offsets, eligible, local_peer,
+                        PR_SELECT_PREFER_LOCAL if prefer_local else 0, match_len, best, second,
+                        self.num_peers, stream)
+        return match_len, best, second
 
     def check(self) -> None:
         pr_forest_check(self.handle)

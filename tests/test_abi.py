@@ -37,3 +37,18 @@ def test_binding_refuses_missing_library(monkeypatch, tmp_path):
         raise AssertionError("loading a missing library must raise")
     except RuntimeError as e:
         assert "not built" in str(e)
+
+
+def test_route_select_argument_errors_without_gpu():
+    """Host-side checks of pr_route_select run before any device work."""
+    from paper_2606_17059_amd import router as R
+    L = R.lib()
+    f = R.pr_forest_create(3)
+    try:
+        for local, flags in [(3, 0), (-2, 0), (0, 2)]:
+            st = L.pr_route_select(f, None, 0, None, 0, None, local, flags, None, None, None, None)
+            assert st == R.PR_EINVAL, (local, flags)
+        assert L.pr_route_select(f, None, 0, None, 0, None, 2, 1, None, None, None, None) == R.PR_OK
+        assert L.pr_route_select(f, None, -1, None, 0, None, -1, 0, None, None, None, None) == R.PR_EINVAL
+    finally:
+        R.pr_forest_destroy(f)

@@ -1,0 +1,155 @@
+"""Peer selection under push-back and failover on the GPU (pr_route_select)
+versus the CPU oracle's route_select.
+
+Integer outputs, so the bar is bit-exact: match lengths, best and second-best
+peer.  Small cases compare every row; the full medium batch compares a
+sampled set of rows exactly and checks properties on every row.
+"""
+import numpy as np
+import pytest
+
+import pins
+import workloads as W
+from gpu_util import announce, device, nthreads, oracle_for, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def _forest(snapshot, P):
+    from paper_2606_17059_amd import Forest
+    f = Forest(P)
+    f.load_seqset(snapshot)
+    return f
+
+
+def _gpu_select(f, ss, eligible, local, prefer, label, want_match_len=True, want_second=True):
+    import torch
+    from paper_2606_17059_amd import eligible_words
+    announce(f"select {label}: {len(ss)} queries, {f.num_peers} peers, local={local} prefer={prefer}")
+    t, o = to_dev(ss)
+    el = None
+    if eligible is not None:
+        el = torch.from_numpy(eligible_words(eligible)).to(device())
+    m, b1, b2 = f.route_select(t, o, el, local, prefer, want_match_len=want_match_len, want_second=want_second)
+    torch.cuda.synchronize()
+    return (m.cpu().numpy() if m is not None else None, b1.cpu().numpy(),
+            b2.cpu().numpy() if b2 is not None else None)
+
+
+def test_select_golden_examples_on_gpu():
+    from paper_2606_17059_amd import Forest, eligible_words
+    import torch
+    dev = device()
+    for name, P, loads, cases in pins.parse_select_golden():
+        f = Forest(P)
+        for p, seqs in loads.items():
+            t, o = pins._csr(seqs)
+            f.load_snapshot(p, t, o)
+        for el, local, prefer, q, b1, b2 in cases:
+            t, o = pins._csr([q])
+            announce(f"select golden {name} q={q} eligible={el.tolist()} local={local} prefer={prefer}")
+            _, g1, g2 = f.route_select(torch.from_numpy(t).to(dev), torch.from_numpy(o).to(dev),
+                                       torch.from_numpy(eligible_words(el)).to(dev), local, prefer)
+            assert (int(g1.cpu()[0]), int(g2.cpu()[0])) == (b1, b2), (name, q, el.tolist(), local, prefer)
+        f.close()
+
+
+@pytest.mark.parametrize("P", [1, 3, 64, 65, 130, 1024])
+def test_select_tiny_random_all_rows(P):
+    rng = np.random.default_rng(77 + P)
+    for sd in range(4):
+        w = W.tiny_random(sd, num_peers=P, vocab=3, max_seqs=4 if P > 100 else 10, n_queries=67)
+        f = _forest(w.snapshot, P)
+        o = oracle_for(w.snapshot, P)
+        for trial in range(3):
+            el = (rng.random(P) < [0.0, 0.5, 0.9][trial]).astype(np.uint8)
+            local = int(rng.integers(-1, P))
+            prefer = bool(trial % 2)
+            m, b1, b2 = _gpu_select(f, w.queries, el, local, prefer, f"tiny P={P} seed={sd} trial={trial}")
+            m_or, b1_or, b2_or = o.route_select(w.queries.tokens, w.queries.offsets, el, local, prefer, 2)
+            assert np.array_equal(m, m_or), f"P={P} seed={sd}: match lengths differ"
+            assert np.array_equal(b1, b1_or), f"P={P} seed={sd} trial={trial}: best differs"
+            assert np.array_equal(b2, b2_or), f"P={P} seed={sd} trial={trial}: second differs"
+        f.close()
+
+
+def test_select_config1_all_rows():
+    w = W.make_config(1)
+    P = w.num_peers
+    f = _forest(w.snapshot, P)
+    o = oracle_for(w.snapshot, P)
+    for el, local, prefer in [(None, -1, False), (np.array([0, 1, 1, 1], np.uint8), 0, True),
+                              (np.array([1, 0, 0, 1], np.uint8), 2, False)]:
+        m, b1, b2 = _gpu_select(f, w.queries, el, local, prefer, f"config1 eligible={el} local={local}")
+        m_or, b1_or, b2_or = o.route_select(w.queries.tokens, w.queries.offsets, el, local, prefer, nthreads())
+        assert np.array_equal(m, m_or) and np.array_equal(b1, b1_or) and np.array_equal(b2, b2_or)
+    f.close()
+
+
+def _check_select_properties(m, b1, b2, el, local, prefer, what):
+    P = m.shape[1]
+    ok = np.ones(P, bool) if el is None else el.astype(bool).copy()
+    if local >= 0:
+        ok[local] = True
+    key = np.where(ok[None, :], m.astype(np.int64) * 4096 + (4095 - np.arange(P)[None, :] - 1), -1)
+    if prefer and local >= 0:
+        key[:, local] = np.where(ok[local], m[:, local].astype(np.int64) * 4096 + 4095, -1)
+    order = np.argsort(-key, axis=1, kind="stable")
+    want1 = np.where(key[np.arange(len(m)), order[:, 0]] >= 0, order[:, 0], -1)
+    want2 = np.where(key[np.arange(len(m)), order[:, 1]] >= 0, order[:, 1], -1) if P > 1 else -np.ones(len(m), int)
+    assert np.array_equal(b1, want1), f"{what}: best is not the first eligible candidate"
+    assert np.array_equal(b2, want2), f"{what}: second is not the next eligible candidate"
+
+
+def test_select_config2_full_batch_sampled_and_properties():
+    w = W.make_config(2)
+    P = w.num_peers
+    f = _forest(w.snapshot, P)
+    rng = np.random.default_rng(5)
+    el = (rng.random(P) < 0.75).astype(np.uint8)
+    local = 3
+    m, b1, b2 = _gpu_select(f, w.queries, el, local, True, "config2 full")
+    # every row: the match matrix equals pr_route's, the picks follow the order
+    import torch
+    t, o = to_dev(w.queries)
+    m_route, c_route = f.route(t, o)
+    torch.cuda.synchronize()
+    assert np.array_equal(m, m_route.cpu().numpy())
+    _check_select_properties(m, b1, b2, el, local, True, "config2")
+    # sampled rows exactly against the oracle
+    idx = np.sort(rng.choice(len(w.queries), size=2048, replace=False))
+    sub = w.queries.subset(idx)
+    oo = oracle_for(w.snapshot, P)
+    m_or, b1_or, b2_or = oo.route_select(sub.tokens, sub.offsets, el, local, True, nthreads())
+    assert np.array_equal(m[idx], m_or) and np.array_equal(b1[idx], b1_or) and np.array_equal(b2[idx], b2_or)
+    # without outputs that are not wanted the picks do not change
+    _, b1n, b2n = _gpu_select(f, w.queries, el, local, True, "config2 no match_len, no second",
+                              want_match_len=False, want_second=False)
+    assert b2n is None and np.array_equal(b1n, b1)
+    # every peer eligible, no local peer: best is pr_route's chosen
+    _, b1a, _ = _gpu_select(f, w.queries, None, -1, False, "config2 unrestricted")
+    assert np.array_equal(b1a, c_route.cpu().numpy())
+    f.close()
+
+
+def test_select_invalid_offsets_and_arguments():
+    import torch
+    from paper_2606_17059_amd import RouterError
+    w = W.tiny_random(3, num_peers=4, vocab=3, n_queries=8)
+    f = _forest(w.snapshot, 4)
+    dev = device()
+    t = torch.from_numpy(w.queries.tokens).to(dev)
+    bad = w.queries.offsets.copy()
+    bad[3] = bad[4] + 1  # query 3 decreasing, query 2 past query 3's start
+    bad[6] = len(w.queries.tokens) + 5
+    o = torch.from_numpy(bad).to(dev)
+    announce("select invalid offsets")
+    m, b1, b2 = f.route_select(t, o, None, 1, True)
+    torch.cuda.synchronize()
+    m, b1, b2 = m.cpu().numpy(), b1.cpu().numpy(), b2.cpu().numpy()
+    for q in range(len(bad) - 1):
+        if bad[q] < 0 or bad[q + 1] < bad[q] or bad[q + 1] > len(w.queries.tokens):
+            assert (m[q] == -1).all() and b1[q] == -1 and b2[q] == -1, q
+    with pytest.raises(RouterError):
+        f.route_select(t, torch.from_numpy(w.queries.offsets).to(dev), None, 4, False)
+    f.close()

@@ -59,6 +59,9 @@ def _load(path: str) -> ctypes.CDLL:
     lib.or_route_select.restype = ctypes.c_int
     lib.or_route_select.argtypes = [ctypes.c_void_p, _i32p, _i64p, ctypes.c_int64, ctypes.c_void_p, ctypes.c_int32,
                                     ctypes.c_int32, _i32p, _i32p, _i32p, ctypes.c_int32]
+    lib.or_export.restype = ctypes.c_int
+    lib.or_export.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
+                              ctypes.c_int64, _i64p, _i64p]
     lib.or_lcp.restype = ctypes.c_int64
     lib.or_lcp.argtypes = [_i32p, ctypes.c_int64, _i32p, ctypes.c_int64]
     lib.or_prefix_match.restype = ctypes.c_int64
@@ -180,6 +183,21 @@ class Oracle:
             return self.route(qs.tokens, qs.offsets, nthreads)
         sub = qs.subset(np.asarray(idx))
         return self.route(sub.tokens, sub.offsets, nthreads)
+
+    def export(self, peer: int) -> Tuple[np.ndarray, np.ndarray]:
+        """sendTrie: the members of S_p that are no proper prefix of another
+        (each once, empty ones left out), in lexicographic order, as CSR."""
+        ns, nt = ctypes.c_int64(0), ctypes.c_int64(0)
+        r = self._lib.or_export(self._h, int(peer), None, 0, None, 0, ctypes.byref(ns), ctypes.byref(nt))
+        if r:
+            raise ValueError(f"or_export failed ({r})")
+        t = np.zeros(max(nt.value, 1), np.int32)
+        o = np.zeros(ns.value + 1, np.int64)
+        r = self._lib.or_export(self._h, int(peer), t.ctypes.data, t.shape[0], o.ctypes.data, o.shape[0],
+                                ctypes.byref(ns), ctypes.byref(nt))
+        if r:
+            raise ValueError(f"or_export failed ({r})")
+        return t[:nt.value], o
 
     def prefix_match(self, peer: int, q) -> int:
         qa = np.ascontiguousarray(q, dtype=np.int32)

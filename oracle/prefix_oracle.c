@@ -324,3 +324,76 @@ int or_route_select(const or_forest *f, const int32_t *q_tokens, const int64_t *
     free(th);
     return 0;
 }
+
+/* ---- snapshot export (sendTrie) ------------------------------------------
+ *
+ * System Design: each node periodically broadcasts its own tree to every peer
+ * (sendTrie), and a receiver replaces its estimate with it (Section
+ * "Trie-broadcast loss": a broadcast is a complete snapshot).  A tree over S_p
+ * is fixed by its root paths, the prefixes of S_p's members; the members that
+ * are no proper prefix of another member (each once) have exactly the same
+ * prefixes, so they are the smallest set of sequences that rebuilds the tree.
+ * Empty sequences add no root path and are left out.
+ *
+ * In lexicographic order every member that has s as a proper prefix comes
+ * after s, and so does every member between s and it (they all start with s),
+ * so s is kept exactly when the member right after it does not start with s.
+ * Output: the kept sequences in that order, as CSR.
+ */
+static const or_set *cmp_set;
+
+static int cmp_seq(const void *pa, const void *pb) {
+    const int64_t a = *(const int64_t *)pa, b = *(const int64_t *)pb;
+    const int32_t *sa = cmp_set->seq[a], *sb = cmp_set->seq[b];
+    const int64_t la = cmp_set->len[a], lb = cmp_set->len[b];
+    const int64_t n = la < lb ? la : lb;
+    for (int64_t i = 0; i < n; i++)
+        if (sa[i] != sb[i]) return sa[i] < sb[i] ? -1 : 1;
+    return la < lb ? -1 : (la > lb ? 1 : 0);
+}
+
+static int starts_with(const or_set *s, int64_t t, int64_t pre) {
+    if (s->len[t] < s->len[pre]) return 0;
+    return or_lcp(s->seq[t], s->len[t], s->seq[pre], s->len[pre]) == s->len[pre];
+}
+
+/* Returns 0, or -3 if the buffers are too small (the sizes are set either way;
+   tokens / offsets may be NULL to ask for the sizes). */
+int or_export(const or_forest *f, int32_t peer, int32_t *tokens, int64_t tok_cap, int64_t *offsets,
+              int64_t seq_cap, int64_t *num_seqs, int64_t *num_tokens) {
+    if (!f || peer < 0 || peer >= f->num_peers || !num_seqs || !num_tokens) return -1;
+    const or_set *s = &f->sets[peer];
+    int64_t *ord = (int64_t *)malloc((size_t)(s->n > 0 ? s->n : 1) * sizeof(int64_t));
+    if (!ord) return -2;
+    int64_t k = 0;
+    for (int64_t i = 0; i < s->n; i++)
+        if (s->len[i] > 0) ord[k++] = i;
+    cmp_set = s;  /* the oracle is not reentrant across threads here */
+    qsort(ord, (size_t)k, sizeof(int64_t), cmp_seq);
+    int64_t ns = 0, nt = 0;
+    for (int64_t i = 0; i < k; i++) {
+#ifndef PLANT_EXPORT_KEEPS_PREFIXES
+        if (i + 1 < k && starts_with(s, ord[i + 1], ord[i])) continue;
+#endif
+        ns++;
+        nt += s->len[ord[i]];
+    }
+    *num_seqs = ns;
+    *num_tokens = nt;
+    if (!tokens || !offsets || tok_cap < nt || seq_cap < ns + 1) {
+        free(ord);
+        return (tokens || offsets) ? -3 : 0;
+    }
+    int64_t j = 0, pos = 0;
+    offsets[0] = 0;
+    for (int64_t i = 0; i < k; i++) {
+#ifndef PLANT_EXPORT_KEEPS_PREFIXES
+        if (i + 1 < k && starts_with(s, ord[i + 1], ord[i])) continue;
+#endif
+        memcpy(tokens + pos, s->seq[ord[i]], (size_t)s->len[ord[i]] * sizeof(int32_t));
+        pos += s->len[ord[i]];
+        offsets[++j] = pos;
+    }
+    free(ord);
+    return 0;
+}

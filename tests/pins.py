@@ -364,3 +364,104 @@ def check_select_random(make: Callable, seeds: Sequence[int]) -> List[str]:
         if not np.array_equal(b1, c0):
             fails.append(f"seed={sd}: unrestricted best differs from chosen")
     return fails
+
+
+# ---- snapshot export (sendTrie) -----------------------------------------------
+EXPORT_GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "export_examples.txt")
+
+
+def _seqs(body: str) -> List[List[int]]:
+    body = body.strip()
+    return [] if not body else [_toks(x) for x in body.split(";")]
+
+
+def parse_export_golden(path: str = EXPORT_GOLDEN):
+    """[(name, P, [("load", p, seqs) | ("merge", [(p, seq)]) | ("export", p, seqs)])]."""
+    out, cur = [], None
+    for raw in open(path):
+        line = raw.split("#", 1)[0].strip()
+        if not line:
+            continue
+        kw, _, rest = line.partition(" ")
+        if kw == "example":
+            cur = [rest.strip(), 0, []]
+            out.append(cur)
+        elif kw == "peers":
+            cur[1] = int(rest)
+        elif kw == "load":
+            p, _, body = rest.partition("|")
+            cur[2].append(("load", int(p), _seqs(body)))
+        elif kw == "merge":
+            items = []
+            for part in rest.split(";"):
+                p, _, seq = part.partition(":")
+                items.append((int(p), _toks(seq)))
+            cur[2].append(("merge", items))
+        elif kw == "export":
+            p, _, body = rest.partition("->")
+            cur[2].append(("export", int(p), _seqs(body)))
+        else:
+            raise ValueError(f"bad directive {kw!r}")
+    return out
+
+
+def csr_to_list(t: np.ndarray, o: np.ndarray) -> List[List[int]]:
+    return [t[o[i]:o[i + 1]].tolist() for i in range(len(o) - 1)]
+
+
+def maximal_members(seqs) -> List[tuple]:
+    """Brute force: non-empty members that are no proper prefix of another
+    member, each once, sorted."""
+    S = {tuple(int(x) for x in s) for s in seqs}
+    keep = [s for s in S if s and not any(len(t) > len(s) and t[:len(s)] == s for t in S)]
+    return sorted(keep)
+
+
+def check_export_golden(make: Callable) -> List[str]:
+    fails = []
+    for name, P, ops in parse_export_golden():
+        o = make(P)
+        for op in ops:
+            if op[0] == "load":
+                t, off = _csr(op[2])
+                o.load(op[1], t, off)
+            elif op[0] == "merge":
+                t, off = _csr([s for _, s in op[1]])
+                o.merge(np.array([p for p, _ in op[1]], np.int32), t, off)
+            else:
+                got = csr_to_list(*o.export(op[1]))
+                if got != op[2]:
+                    fails.append(f"{name}: export {op[1]} got {got} want {op[2]}")
+    return fails
+
+
+def check_export_random(make: Callable, seeds: Sequence[int]) -> List[str]:
+    """Tiny random forests with merges: the export equals the brute-force
+    maximal members (as a sorted list), and loading it into a fresh peer gives
+    the same match for every query (the same tree)."""
+    import workloads as W
+    fails = []
+    for sd in seeds:
+        w = W.tiny_random(sd, num_peers=3, vocab=2 + sd % 3, n_queries=60)
+        P = w.num_peers
+        o = make(P)
+        load_all(o, w.snapshot, P)
+        ins = W.tiny_random(sd + 500, num_peers=P, vocab=2 + sd % 3, n_queries=1)
+        o.merge(ins.snapshot.peer, ins.snapshot.tokens, ins.snapshot.offsets)
+        sets = [list(x) for x in _peer_lists(w)]
+        for i in range(len(ins.snapshot)):
+            sets[int(ins.snapshot.peer[i])].append(ins.snapshot.seq(i))
+        for p in range(P):
+            t, off = o.export(p)
+            got = [tuple(x) for x in csr_to_list(t, off)]
+            if sorted(got) != maximal_members(sets[p]) or len(set(got)) != len(got):
+                fails.append(f"seed={sd} peer={p}: export differs from the maximal members")
+                continue
+            o2 = make(1)
+            o2.load(0, t, off)
+            for i in range(len(w.queries)):
+                q = w.queries.seq(i)
+                if o2.prefix_match(0, q) != o.prefix_match(p, q):
+                    fails.append(f"seed={sd} peer={p} q={i}: the exported set matches differently")
+                    break
+    return fails

@@ -114,9 +114,17 @@ def test_select_rejects_bad_local():
         o.route_select(t, off, np.ones(2, np.uint8), -1, False)
 
 
+def test_export_golden_hand_examples():
+    assert pins.check_export_golden(make) == []
+
+
+def test_export_random_vs_bruteforce_and_round_trip():
+    assert pins.check_export_random(make, seeds=range(12)) == []
+
+
 PLANTS = ["PLANT_LCP_OFF_BY_ONE", "PLANT_MIN_NOT_MAX", "PLANT_TIE_HIGHEST",
           "PLANT_LOAD_APPENDS", "PLANT_MERGE_WRONG_PEER", "PLANT_IGNORE_ELIGIBLE",
-          "PLANT_LOCAL_ALWAYS_FIRST"]
+          "PLANT_LOCAL_ALWAYS_FIRST", "PLANT_EXPORT_KEEPS_PREFIXES"]
 
 
 @pytest.mark.parametrize("plant", PLANTS)
@@ -129,5 +137,6 @@ def test_planted_mistake_is_caught(plant, tmp_path):
 
     fails = pins.check_golden(mk) + pins.check_tiny_random(mk, seeds=range(3), vocabs=(3,)) \
         + pins.check_merge_semantics(mk, seeds=range(2)) + pins.check_select_golden(mk) \
-        + pins.check_select_random(mk, seeds=range(2))
+        + pins.check_select_random(mk, seeds=range(2)) + pins.check_export_golden(mk) \
+        + pins.check_export_random(mk, seeds=range(3))
     assert fails, f"{plant} slipped through every pin"

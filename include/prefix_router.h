@@ -134,6 +134,50 @@ pr_status pr_route(pr_forest *f, const int32_t *q_tokens, int64_t num_tokens,
                    int32_t *chosen, void *hip_stream);
 
 /*
+ * sendTrie, receive side, for a snapshot already in DEVICE memory (for
+ * example received by a GPU-direct transfer).  Same semantics as
+ * pr_load_snapshot: REPLACES peer's tree by the set of num_seqs sequences
+ * tokens[offsets[i] .. offsets[i+1]), offsets within [0, num_tokens].  The
+ * replacement runs on the device: the peer is removed from every node, then
+ * the sequences are inserted as by pr_merge (a sequence with invalid offsets
+ * is skipped and counted for pr_forest_check).  Host-synchronous like
+ * pr_merge; the inputs may be reused when the call returns.  Afterwards the
+ * forest has no host copy of this peer's snapshot.
+ * Errors: PR_EINVAL (peer out of range, negative counts, NULL offsets with
+ * num_seqs > 0, NULL tokens with num_tokens > 0), PR_ENOMEM, PR_ESTATE,
+ * PR_EDEVICE; after PR_ENOMEM or PR_EDEVICE the forest refuses every call but
+ * destroy.
+ */
+pr_status pr_load_snapshot_device(pr_forest *f, int32_t peer, const int32_t *tokens,
+                                  int64_t num_tokens, const int64_t *offsets, int64_t num_seqs,
+                                  void *hip_stream);
+
+/*
+ * sendTrie, send side (paper, System Design: each node periodically
+ * broadcasts its own tree; Section "Trie-broadcast loss": as a complete
+ * snapshot).  Writes peer's tree as the set of sequences that rebuilds it:
+ * the root paths that end at a node holding the peer none of whose children
+ * holds it, i.e. the members of the peer's set that are no proper prefix of
+ * another member, each once (empty sequences add nothing and are left out).
+ * Loading the result with pr_load_snapshot(_device) gives the same tree.
+ * Order: by node id in the device layout (deterministic for a given forest).
+ * Outputs:
+ *   *num_seqs, *num_tokens   HOST: the export's size, always written;
+ *   offsets  DEVICE int64 [num_seqs + 1] (CSR, offsets[0] = 0), capacity
+ *            seqs_cap entries;
+ *   tokens   DEVICE int32 [num_tokens], capacity tokens_cap.
+ * With tokens and offsets both NULL the call only reports the size; with
+ * buffers that are too small it returns PR_EINVAL (sizes still written) and
+ * writes nothing.  Host-synchronous; reads the forest only.  The size query
+ * and the fill each walk the tree.
+ * Errors: PR_EINVAL (peer out of range, NULL size outputs, negative or too
+ * small capacities), PR_ENOMEM, PR_ESTATE, PR_EDEVICE.
+ */
+pr_status pr_export_snapshot(pr_forest *f, int32_t peer, int32_t *tokens, int64_t tokens_cap,
+                             int64_t *offsets, int64_t seqs_cap, int64_t *num_seqs,
+                             int64_t *num_tokens, void *hip_stream);
+
+/*
  * Peer selection under push-back and failover (paper, Section "Hot specialist
  * push-back": originating nodes stop routing to a node that advertised
  * back-pressure, and such a request runs locally or on a slightly inferior

@@ -1,0 +1,111 @@
+// export_kernels.h -- snapshot export (sendTrie) from the device forest.
+//
+// A peer's tree is fixed by its root paths, so the export is the set of paths
+// that end at a node holding the peer none of whose children holds it: the
+// members of the peer's set that are no proper prefix of another (System
+// Design, sendTrie; Section "Trie-broadcast loss": a broadcast is a complete
+// snapshot).
+//
+//   1. export_level_kernel walks the forest level by level from the root,
+//      only through nodes whose mask holds p (merges leave unreachable blocks
+//      behind, which a walk from the root never visits).  Every visited node
+//      gets its depth (tokens from the root through its label) and its
+//      parent; a visited node none of whose children holds p is a leaf.
+//   2. The host sorts the leaves by node id (a deterministic order) and scans
+//      their depths into CSR offsets.
+//   3. export_write_kernel: one wave per leaf climbs the parent chain and
+//      writes every label on the path at its depth, lanes over tokens.
+#ifndef PR_EXPORT_KERNELS_H
+#define PR_EXPORT_KERNELS_H
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "forest_layout.h"
+#include "merge_kernels.h"
+
+namespace pr {
+
+constexpr int kExportWavesPerBlock = 4;
+
+__device__ __forceinline__ bool node_holds(const DevForest &F, int64_t x, int32_t p) {
+    const int32_t w = p >> 6;
+    const uint64_t word = w == 0 ? F.nodes[x].mask0 : F.mext[x * (F.W - 1) + (w - 1)];
+    return (word >> (p & 63)) & 1ull;
+}
+
+__global__ void export_init_kernel(int32_t *front, int64_t *depth, int32_t *counts) {
+    front[0] = 0;
+    depth[0] = 0;
+    counts[0] = 0;  // next frontier size
+    counts[1] = 0;  // leaves so far
+}
+
+__global__ void export_reset_kernel(int32_t *counts) { counts[0] = 0; }
+
+// One wave per frontier node x: children holding p join the next frontier
+// with their depth and parent; x becomes a leaf if none holds p.
+// The frontier, the leaf list, depth and parent hold n_nodes entries; a walk
+// of a well-formed forest never exceeds them, and the host reports counts
+// above n_nodes as a broken forest (the writes past the end are dropped).
+__global__ __launch_bounds__(64 * kExportWavesPerBlock) void export_level_kernel(
+    DevForest F, int64_t n_nodes, int32_t p, const int32_t *__restrict__ front, int32_t n_front,
+    int32_t *__restrict__ next, int32_t *__restrict__ leaves, int64_t *__restrict__ depth,
+    int32_t *__restrict__ parent, int32_t *__restrict__ counts) {
+    const int lane = (int)(threadIdx.x & 63);
+    const int64_t i = (int64_t)blockIdx.x * kExportWavesPerBlock + (threadIdx.x >> 6);
+    if (i >= n_front) return;
+    const int32_t x = front[i];
+    const int32_t beg = F.nodes[x].ct_beg, cnt = F.nodes[x].ct_cnt;
+    const int64_t dx = depth[x];
+    bool found = false;
+    for (int32_t j = lane; j < cnt; j += 64) {
+        const int32_t c = beg + j;
+        if (c < 0 || c >= n_nodes) continue;
+        if (node_holds(F, c, p)) {
+            depth[c] = dx + F.nodes[c].lab_len;
+            parent[c] = x;
+            const int32_t slot = atomicAdd(&counts[0], 1);
+            if (slot < n_nodes) next[slot] = c;
+            found = true;
+        }
+    }
+    if (__ballot(found) == 0 && x != 0 && lane == 0) {
+        const int32_t slot = atomicAdd(&counts[1], 1);
+        if (slot < n_nodes) leaves[slot] = x;
+    }
+}
+
+// Sequence lengths of the sorted leaves, written one slot to the right so
+// that an inclusive scan over [1, n] gives the CSR offsets.
+__global__ void export_lengths_kernel(const int32_t *__restrict__ leaves, int32_t n, const int64_t *__restrict__ depth,
+                                      int64_t *__restrict__ len1) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i == 0) len1[0] = 0;
+    if (i < n) len1[i + 1] = depth[leaves[i]];
+}
+
+// One wave per leaf: climb to the root, writing each label at its depth.
+__global__ __launch_bounds__(64 * kExportWavesPerBlock) void export_write_kernel(
+    DevForest F, const int32_t *__restrict__ leaves, int32_t n, const int64_t *__restrict__ depth,
+    const int32_t *__restrict__ parent, const int64_t *__restrict__ offsets, int32_t *__restrict__ out) {
+    const int lane = (int)(threadIdx.x & 63);
+    const int64_t i = (int64_t)blockIdx.x * kExportWavesPerBlock + (threadIdx.x >> 6);
+    if (i >= n) return;
+    const int64_t base = offsets[i];
+    int32_t c = leaves[i];
+    // depth falls by at least one token per step, so the climb ends at the root
+    while (c != 0) {
+        const Node r = F.nodes[c];
+        const int64_t d = depth[c];
+        if (r.lab_len <= 0 || d < r.lab_len) break;  // not a well-formed path: stop
+        const int64_t start = base + d - r.lab_len;
+        const int32_t *lab = F.pool + r.lab_off;
+        for (int32_t k = lane; k < r.lab_len; k += 64) out[start + k] = lab[k];
+        c = parent[c];
+    }
+}
+
+}  // namespace pr
+
+#endif

@@ -11,11 +11,13 @@
 #include <cstring>
 #include <new>
 #include <rocprim/device/device_radix_sort.hpp>
+#include <rocprim/device/device_scan.hpp>
 #include <string>
 #include <vector>
 
 #include "forest_host.h"
 #include "forest_layout.h"
+#include "export_kernels.h"
 #include "merge_kernels.h"
 #include "prefix_router.h"
 #include "route_kernels.h"
@@ -480,6 +482,105 @@ pr_status device_load(pr_forest *f, int32_t peer, const pr::PeerSeqs &S) {
     return run_merge(f, m.load_peer, m.load_tok, nt, m.load_off, ns, s);
 }
 
+// Device buffers of one export call, released on every return path.
+struct ExportScratch {
+    int64_t *depth = nullptr, *len1 = nullptr, *offs = nullptr;
+    int32_t *parent = nullptr, *front = nullptr, *next = nullptr, *leaves = nullptr, *sorted = nullptr;
+    int32_t *counts = nullptr;
+    void *tmp = nullptr;
+    ~ExportScratch() {
+        for (void *p : {(void *)depth, (void *)len1, (void *)offs, (void *)parent, (void *)front, (void *)next,
+                        (void *)leaves, (void *)sorted, (void *)counts, tmp})
+            if (p) (void)hipFree(p);
+    }
+};
+
+template <typename T>
+bool talloc(T **p, int64_t count) {
+    if (hipMalloc((void **)p, (size_t)std::max<int64_t>(count, 1) * sizeof(T)) != hipSuccess) {
+        (void)hipGetLastError();
+        *p = nullptr;
+        return false;
+    }
+    return true;
+}
+
+// sendTrie for one peer (see export_kernels.h).  Host-synchronous.  Writes the
+// sizes always; the data only if both buffers are given and large enough.
+pr_status export_impl(pr_forest *f, int32_t peer, int32_t *tokens, int64_t tokens_cap, int64_t *offsets,
+                      int64_t seqs_cap, int64_t *num_seqs, int64_t *num_tokens, hipStream_t s) {
+    const int64_t nn = f->dev.n_nodes;
+    ExportScratch X;
+    if (!talloc(&X.depth, nn) || !talloc(&X.parent, nn) || !talloc(&X.front, nn) || !talloc(&X.next, nn) ||
+        !talloc(&X.leaves, nn) || !talloc(&X.sorted, nn) || !talloc(&X.counts, 2) || !talloc(&X.len1, nn + 1) ||
+        !talloc(&X.offs, nn + 1))
+        return fail(PR_ENOMEM, "hipMalloc failed for the export");
+    const pr::DevForest F = dev_view(f);
+    const int wb = 64 * pr::kExportWavesPerBlock;
+    hipLaunchKernelGGL(pr::export_init_kernel, dim3(1), dim3(1), 0, s, X.front, X.depth, X.counts);
+    int32_t n_front = 1, counts[2] = {0, 0};
+    while (n_front > 0) {
+        hipLaunchKernelGGL(pr::export_reset_kernel, dim3(1), dim3(1), 0, s, X.counts);
+        hipLaunchKernelGGL(pr::export_level_kernel,
+                           dim3((unsigned)((n_front + pr::kExportWavesPerBlock - 1) / pr::kExportWavesPerBlock)),
+                           dim3(wb), 0, s, F, nn, peer, X.front, n_front, X.next, X.leaves, X.depth, X.parent,
+                           X.counts);
+        if (hipGetLastError() != hipSuccess) return fail(PR_EDEVICE, "export launch failed");
+        if (hipMemcpyAsync(counts, X.counts, sizeof(counts), hipMemcpyDeviceToHost, s) != hipSuccess ||
+            hipStreamSynchronize(s) != hipSuccess)
+            return fail(PR_EDEVICE, "export readback failed");
+        if (counts[0] > nn || counts[1] > nn) return fail(PR_EDEVICE, "export walk visited more nodes than exist");
+        n_front = counts[0];
+        std::swap(X.front, X.next);
+    }
+    const int32_t n_leaves = counts[1];
+    int64_t total = 0;
+    if (n_leaves > 0) {
+        size_t need = 0, need2 = 0;
+        if (rocprim::radix_sort_keys(nullptr, need, X.leaves, X.sorted, (size_t)n_leaves, 0, 32, s) != hipSuccess ||
+            rocprim::inclusive_scan(nullptr, need2, X.len1 + 1, X.offs + 1, (size_t)n_leaves,
+                                    rocprim::plus<int64_t>(), s) != hipSuccess)
+            return fail(PR_EDEVICE, "export sort / scan sizing failed");
+        need = std::max(need, need2);
+        if (hipMalloc(&X.tmp, std::max<size_t>(need, 1)) != hipSuccess) {
+            (void)hipGetLastError();
+            return fail(PR_ENOMEM, "hipMalloc failed for the export");
+        }
+        size_t t1 = need;
+        if (rocprim::radix_sort_keys(X.tmp, t1, X.leaves, X.sorted, (size_t)n_leaves, 0, 32, s) != hipSuccess)
+            return fail(PR_EDEVICE, "export sort failed");
+        hipLaunchKernelGGL(pr::export_lengths_kernel, dim3(grid_threads(n_leaves, 256)), dim3(256), 0, s, X.sorted,
+                           n_leaves, X.depth, X.len1);
+        size_t t2 = need;
+        if (rocprim::inclusive_scan(X.tmp, t2, X.len1 + 1, X.offs + 1, (size_t)n_leaves, rocprim::plus<int64_t>(),
+                                    s) != hipSuccess)
+            return fail(PR_EDEVICE, "export scan failed");
+        if (hipMemcpyAsync(&total, X.offs + n_leaves, sizeof(total), hipMemcpyDeviceToHost, s) != hipSuccess ||
+            hipStreamSynchronize(s) != hipSuccess)
+            return fail(PR_EDEVICE, "export readback failed");
+    }
+    *num_seqs = n_leaves;
+    *num_tokens = total;
+    if (!tokens && !offsets) return ok();
+    if (!offsets || (total > 0 && !tokens) || tokens_cap < total || seqs_cap < (int64_t)n_leaves + 1)
+        return fail(PR_EINVAL, "export buffers too small: need " + std::to_string(n_leaves + 1) + " offsets and " +
+                                   std::to_string(total) + " tokens");
+    const int64_t zero = 0;
+    if (hipMemcpyAsync(offsets, &zero, sizeof(zero), hipMemcpyHostToDevice, s) != hipSuccess)
+        return fail(PR_EDEVICE, "export copy failed");
+    if (n_leaves > 0) {
+        if (hipMemcpyAsync(offsets + 1, X.offs + 1, (size_t)n_leaves * sizeof(int64_t), hipMemcpyDeviceToDevice,
+                           s) != hipSuccess)
+            return fail(PR_EDEVICE, "export copy failed");
+        hipLaunchKernelGGL(pr::export_write_kernel,
+                           dim3((unsigned)((n_leaves + pr::kExportWavesPerBlock - 1) / pr::kExportWavesPerBlock)),
+                           dim3(wb), 0, s, F, X.sorted, n_leaves, X.depth, X.parent, offsets, tokens);
+        if (hipGetLastError() != hipSuccess) return fail(PR_EDEVICE, "export launch failed");
+    }
+    if (hipStreamSynchronize(s) != hipSuccess) return fail(PR_EDEVICE, "export failed");
+    return ok();
+}
+
 }  // namespace
 
 extern "C" {
@@ -576,6 +677,68 @@ pr_status pr_merge(pr_forest *f, const int32_t *peer_of, const int32_t *tokens, 
         return s;
     }
     return ok();
+}
+
+pr_status pr_load_snapshot_device(pr_forest *f, int32_t peer, const int32_t *tokens, int64_t num_tokens,
+                                  const int64_t *offsets, int64_t num_seqs, void *hip_stream) {
+    if (!f) return fail(PR_EINVAL, "forest is NULL");
+    if (peer < 0 || peer >= f->P) return fail(PR_EINVAL, "peer out of range");
+    if (num_seqs < 0 || num_tokens < 0) return fail(PR_EINVAL, "negative count");
+    if (num_seqs > 0 && !offsets) return fail(PR_EINVAL, "offsets is NULL");
+    if (num_tokens > 0 && !tokens) return fail(PR_EINVAL, "tokens is NULL");
+    if (num_seqs > (int64_t)INT32_MAX) return fail(PR_EINVAL, "too many sequences");
+    if (f->broken) return fail(PR_ESTATE, "an earlier device update failed; destroy the forest");
+    DeviceScope ds(f);
+    if (!ds.ok()) return fail(PR_EDEVICE, "cannot select the forest's device");
+    pr_status r = commit(f);
+    if (r) return r;
+    hipStream_t s = (hipStream_t)hip_stream;
+    MergeScratch &m = f->ms;
+    hipLaunchKernelGGL(pr::clear_peer_kernel, dim3(grid_threads(f->dev.n_nodes, 256)), dim3(256), 0, s,
+                       dev_view(f), f->dev.n_nodes, peer);
+    if (hipGetLastError() != hipSuccess) {
+        f->broken = true;
+        return fail(PR_EDEVICE, "snapshot kernels failed to launch");
+    }
+    if (num_seqs > 0) {
+        if (num_seqs > m.load_seq_cap) {
+            dfree(f, &m.load_peer, m.load_seq_cap);
+            dfree(f, &m.load_off, m.load_seq_cap + 1);
+            m.load_seq_cap = 0;
+            if (!dalloc(f, &m.load_peer, num_seqs) || !dalloc(f, &m.load_off, num_seqs + 1)) {
+                f->broken = true;
+                return fail(PR_ENOMEM, "hipMalloc failed for the snapshot");
+            }
+            m.load_seq_cap = num_seqs;
+        }
+        hipLaunchKernelGGL(pr::fill_peer_kernel, dim3(grid_threads(num_seqs, 256)), dim3(256), 0, s, m.load_peer,
+                           num_seqs, peer);
+        r = run_merge(f, m.load_peer, tokens, num_tokens, offsets, num_seqs, s);
+    } else {
+        r = hipStreamSynchronize(s) == hipSuccess ? PR_OK : fail(PR_EDEVICE, "sync failed");
+        f->merged = true;
+    }
+    if (r) {
+        f->broken = true;
+        return r;
+    }
+    f->sets[(size_t)peer] = pr::PeerSeqs();  // the host copy no longer describes the peer
+    return ok();
+}
+
+pr_status pr_export_snapshot(pr_forest *f, int32_t peer, int32_t *tokens, int64_t tokens_cap, int64_t *offsets,
+                             int64_t seqs_cap, int64_t *num_seqs, int64_t *num_tokens, void *hip_stream) {
+    if (!f) return fail(PR_EINVAL, "forest is NULL");
+    if (peer < 0 || peer >= f->P) return fail(PR_EINVAL, "peer out of range");
+    if (!num_seqs || !num_tokens) return fail(PR_EINVAL, "size outputs are NULL");
+    if (tokens_cap < 0 || seqs_cap < 0) return fail(PR_EINVAL, "negative capacity");
+    if (f->broken) return fail(PR_ESTATE, "an earlier device update failed; destroy the forest");
+    DeviceScope ds(f);
+    if (!ds.ok()) return fail(PR_EDEVICE, "cannot select the forest's device");
+    pr_status r = commit(f);
+    if (r) return r;
+    return export_impl(f, peer, tokens, tokens_cap, offsets, seqs_cap, num_seqs, num_tokens,
+                       (hipStream_t)hip_stream);
 }
 
 static pr_status route_impl(pr_forest *f, const int32_t *q_tokens, int64_t num_tokens, const int64_t *q_offsets,

@@ -20,7 +20,8 @@ PR_OK, PR_EINVAL, PR_ENOMEM, PR_EDEVICE, PR_ESTATE = 0, -1, -2, -3, -4
 PR_MAX_PEERS = 1024
 
 EXPORTED = ("pr_abi_version", "pr_last_error", "pr_forest_create", "pr_forest_destroy",
-            "pr_load_snapshot", "pr_merge", "pr_route", "pr_route_select", "pr_forest_check",
+            "pr_load_snapshot", "pr_load_snapshot_device", "pr_export_snapshot", "pr_merge", "pr_route",
+            "pr_route_select", "pr_forest_check",
             "pr_forest_info_get", "pr_forest_host_image")
 
 PR_SELECT_PREFER_LOCAL = 1
@@ -73,6 +74,11 @@ def lib() -> ctypes.CDLL:
     L.pr_forest_destroy.restype = None
     L.pr_load_snapshot.argtypes = [_vp, ctypes.c_int32, _vp, _vp, ctypes.c_int64]
     L.pr_load_snapshot.restype = ctypes.c_int32
+    L.pr_load_snapshot_device.argtypes = [_vp, ctypes.c_int32, _vp, ctypes.c_int64, _vp, ctypes.c_int64, _vp]
+    L.pr_load_snapshot_device.restype = ctypes.c_int32
+    L.pr_export_snapshot.argtypes = [_vp, ctypes.c_int32, _vp, ctypes.c_int64, _vp, ctypes.c_int64, _i64p, _i64p,
+                                     _vp]
+    L.pr_export_snapshot.restype = ctypes.c_int32
     L.pr_merge.argtypes = [_vp, _vp, _vp, ctypes.c_int64, _vp, ctypes.c_int64, _vp]
     L.pr_merge.restype = ctypes.c_int32
     L.pr_route.argtypes = [_vp, _vp, ctypes.c_int64, _vp, ctypes.c_int64, _vp, _vp, _vp]
@@ -136,6 +142,31 @@ def _stream_ptr(stream, device) -> int:
     import torch
     s = stream if stream is not None else torch.cuda.current_stream(device)
     return int(s.cuda_stream)
+
+
+def pr_load_snapshot_device(f: int, peer: int, tokens, offsets, stream=None) -> None:
+    import torch
+    _dev(tokens, torch.int32, "tokens")
+    _dev(offsets, torch.int64, "offsets")
+    n = offsets.numel() - 1
+    if n < 0:
+        raise ValueError("offsets must have at least one entry")
+    _check(lib().pr_load_snapshot_device(f, int(peer), tokens.data_ptr() or None, tokens.numel(),
+                                         offsets.data_ptr(), n, _stream_ptr(stream, offsets.device)))
+
+
+def pr_export_snapshot(f: int, peer: int, device=None, stream=None):
+    """Export peer's tree: (tokens, offsets) as CUDA tensors (int32, int64)."""
+    import torch
+    dev = device if device is not None else torch.device("cuda", torch.cuda.current_device())
+    ns, nt = ctypes.c_int64(0), ctypes.c_int64(0)
+    st = _stream_ptr(stream, dev)
+    _check(lib().pr_export_snapshot(f, int(peer), None, 0, None, 0, ctypes.byref(ns), ctypes.byref(nt), st))
+    toks = torch.empty(max(nt.value, 1), dtype=torch.int32, device=dev)
+    offs = torch.empty(ns.value + 1, dtype=torch.int64, device=dev)
+    _check(lib().pr_export_snapshot(f, int(peer), toks.data_ptr(), toks.numel(), offs.data_ptr(), offs.numel(),
+                                    ctypes.byref(ns), ctypes.byref(nt), st))
+    return toks[:nt.value], offs
 
 
 def pr_merge(f: int, peer_of, tokens, offsets, stream=None) -> None:
@@ -281,6 +312,12 @@ class Forest:
 
     def merge(self, peer_of, tokens, offsets, stream=None) -> None:
         pr_merge(self.handle, peer_of, tokens, offsets, stream)
+
+    def load_snapshot_device(self, peer: int, tokens, offsets, stream=None) -> None:
+        pr_load_snapshot_device(self.handle, peer, tokens, offsets, stream)
+
+    def export_snapshot(self, peer: int, device=None, stream=None):
+        return pr_export_snapshot(self.handle, peer, device, stream)
 
     def route(self, q_tokens, q_offsets, match_len=None, chosen=None, stream=None) -> Tuple:
         import torch

@@ -227,6 +227,29 @@ def bench_select(f, w, qt, qo, needed, K, warmup, dev) -> dict:
     return out
 
 
+def bench_snapshot(f, w, dev, peers: int = 4) -> dict:
+    """Anti-entropy on the device: export peers 0..peers-1 (sendTrie) and load
+    each export back into the same peer (receive side, device input).  The
+    exported set rebuilds the same tree, so routing does not change.  Both
+    calls are host-synchronous; wall time per call."""
+    import torch
+    out = {"peers": peers, "export": [], "load": []}
+    for p in range(min(peers, w.num_peers)):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        toks, offs = f.export_snapshot(p)
+        t1 = time.perf_counter()
+        ns, nt = offs.numel() - 1, toks.numel()
+        f.load_snapshot_device(p, toks.contiguous(), offs)
+        t2 = time.perf_counter()
+        out["export"].append({"peer": p, "ms": (t1 - t0) * 1e3, "seqs": ns, "tokens": nt,
+                              "tokens_per_s": nt / (t1 - t0)})
+        out["load"].append({"peer": p, "ms": (t2 - t1) * 1e3, "seqs": ns, "tokens": nt,
+                            "inserts_per_s": ns / (t2 - t1), "tokens_per_s": nt / (t2 - t1)})
+    f.check()
+    return out
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -235,6 +258,8 @@ def main() -> int:
     ap.add_argument("--config", type=int, default=2, choices=sorted(WORKLOADS))
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU time of the oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--snapshot", action="store_true",
+                    help="also time snapshot export and device-input load of a few peers")
     ap.add_argument("--no-select", action="store_true",
                     help="skip timing pr_route_select (push-back / failover selection)")
     ap.add_argument("--copies", type=int, default=2, help="device copies of the query batch to rotate")
@@ -357,6 +382,10 @@ def main() -> int:
     if not args.no_select:
         extra["select"] = bench_select(f, w, qt, qo, needed, K, args.warmup, dev)
         log(f"[bench] select: {extra['select']}")
+    if args.snapshot:
+        # after the timed routes: the device loads switch the forest to its device path
+        extra["snapshot"] = bench_snapshot(f, w, dev)
+        log(f"[bench] snapshot: {extra['snapshot']}")
 
     cpu = None
     if not args.no_cpu_baseline:

@@ -66,6 +66,16 @@ struct MergeScratch {
     int64_t load_tok_cap = 0, load_seq_cap = 0;
 };
 
+// Scratch of snapshot exports, kept between calls and grown on demand.
+struct ExportScratch {
+    int64_t *depth = nullptr, *len1 = nullptr, *offs = nullptr;
+    int32_t *parent = nullptr, *front = nullptr, *next = nullptr, *leaves = nullptr, *sorted = nullptr;
+    int32_t *counts = nullptr;
+    void *tmp = nullptr;
+    size_t tmp_bytes = 0;
+    int64_t cap = 0;  // node capacity of the per-node arrays
+};
+
 }  // namespace
 
 struct pr_forest {
@@ -82,6 +92,7 @@ struct pr_forest {
     pr::MergeCounters *d_ctr = nullptr;
     unsigned long long *d_skipped = nullptr;  // inputs skipped by device calls
     MergeScratch ms;
+    ExportScratch xs;
     long long stamp = 0;          // add-round counter (stamps of moved records)
     int64_t device_bytes = 0;
     bool broken = false;          // a device update failed; only destroy is valid
@@ -145,6 +156,22 @@ void free_image(pr_forest *f) {
     f->has_dev = false;
 }
 
+void free_export_scratch(pr_forest *f) {
+    ExportScratch &X = f->xs;
+    dfree(f, &X.depth, X.cap);
+    dfree(f, &X.len1, X.cap + 1);
+    dfree(f, &X.offs, X.cap + 1);
+    dfree(f, &X.parent, X.cap);
+    dfree(f, &X.front, X.cap);
+    dfree(f, &X.next, X.cap);
+    dfree(f, &X.leaves, X.cap);
+    dfree(f, &X.sorted, X.cap);
+    dfree(f, &X.counts, 2);
+    if (X.tmp) (void)hipFree(X.tmp);
+    f->device_bytes -= (int64_t)X.tmp_bytes;
+    X = ExportScratch();
+}
+
 void free_scratch(pr_forest *f) {
     MergeScratch &m = f->ms;
     dfree(f, &m.st, m.cap);
@@ -162,6 +189,7 @@ void free_scratch(pr_forest *f) {
     dfree(f, &m.load_peer, m.load_seq_cap);
     dfree(f, &m.load_off, m.load_seq_cap + 1);
     m = MergeScratch();
+    free_export_scratch(f);
 }
 
 pr_status ensure_host_image(pr_forest *f) {
@@ -482,27 +510,19 @@ pr_status device_load(pr_forest *f, int32_t peer, const pr::PeerSeqs &S) {
     return run_merge(f, m.load_peer, m.load_tok, nt, m.load_off, ns, s);
 }
 
-// Device buffers of one export call, released on every return path.
-struct ExportScratch {
-    int64_t *depth = nullptr, *len1 = nullptr, *offs = nullptr;
-    int32_t *parent = nullptr, *front = nullptr, *next = nullptr, *leaves = nullptr, *sorted = nullptr;
-    int32_t *counts = nullptr;
-    void *tmp = nullptr;
-    ~ExportScratch() {
-        for (void *p : {(void *)depth, (void *)len1, (void *)offs, (void *)parent, (void *)front, (void *)next,
-                        (void *)leaves, (void *)sorted, (void *)counts, tmp})
-            if (p) (void)hipFree(p);
+pr_status ensure_export_scratch(pr_forest *f, int64_t nn) {
+    ExportScratch &X = f->xs;
+    if (nn <= X.cap && X.counts) return PR_OK;
+    const int64_t cap = std::max<int64_t>(nn, X.cap + X.cap / 2);
+    free_export_scratch(f);
+    if (!dalloc(f, &X.depth, cap) || !dalloc(f, &X.len1, cap + 1) || !dalloc(f, &X.offs, cap + 1) ||
+        !dalloc(f, &X.parent, cap) || !dalloc(f, &X.front, cap) || !dalloc(f, &X.next, cap) ||
+        !dalloc(f, &X.leaves, cap) || !dalloc(f, &X.sorted, cap) || !dalloc(f, &X.counts, 2)) {
+        free_export_scratch(f);
+        return fail(PR_ENOMEM, "hipMalloc failed for the export");
     }
-};
-
-template <typename T>
-bool talloc(T **p, int64_t count) {
-    if (hipMalloc((void **)p, (size_t)std::max<int64_t>(count, 1) * sizeof(T)) != hipSuccess) {
-        (void)hipGetLastError();
-        *p = nullptr;
-        return false;
-    }
-    return true;
+    X.cap = cap;
+    return PR_OK;
 }
 
 // sendTrie for one peer (see export_kernels.h).  Host-synchronous.  Writes the
@@ -510,11 +530,9 @@ bool talloc(T **p, int64_t count) {
 pr_status export_impl(pr_forest *f, int32_t peer, int32_t *tokens, int64_t tokens_cap, int64_t *offsets,
                       int64_t seqs_cap, int64_t *num_seqs, int64_t *num_tokens, hipStream_t s) {
     const int64_t nn = f->dev.n_nodes;
-    ExportScratch X;
-    if (!talloc(&X.depth, nn) || !talloc(&X.parent, nn) || !talloc(&X.front, nn) || !talloc(&X.next, nn) ||
-        !talloc(&X.leaves, nn) || !talloc(&X.sorted, nn) || !talloc(&X.counts, 2) || !talloc(&X.len1, nn + 1) ||
-        !talloc(&X.offs, nn + 1))
-        return fail(PR_ENOMEM, "hipMalloc failed for the export");
+    pr_status r = ensure_export_scratch(f, nn);
+    if (r) return r;
+    ExportScratch &X = f->xs;
     const pr::DevForest F = dev_view(f);
     const int wb = 64 * pr::kExportWavesPerBlock;
     hipLaunchKernelGGL(pr::export_init_kernel, dim3(1), dim3(1), 0, s, X.front, X.depth, X.counts);
@@ -542,9 +560,17 @@ pr_status export_impl(pr_forest *f, int32_t peer, int32_t *tokens, int64_t token
                                     rocprim::plus<int64_t>(), s) != hipSuccess)
             return fail(PR_EDEVICE, "export sort / scan sizing failed");
         need = std::max(need, need2);
-        if (hipMalloc(&X.tmp, std::max<size_t>(need, 1)) != hipSuccess) {
-            (void)hipGetLastError();
-            return fail(PR_ENOMEM, "hipMalloc failed for the export");
+        if (need > X.tmp_bytes) {
+            if (X.tmp) (void)hipFree(X.tmp);
+            f->device_bytes -= (int64_t)X.tmp_bytes;
+            X.tmp = nullptr;
+            X.tmp_bytes = 0;
+            if (hipMalloc(&X.tmp, need) != hipSuccess) {
+                (void)hipGetLastError();
+                return fail(PR_ENOMEM, "hipMalloc failed for the export");
+            }
+            X.tmp_bytes = need;
+            f->device_bytes += (int64_t)need;
         }
         size_t t1 = need;
         if (rocprim::radix_sort_keys(X.tmp, t1, X.leaves, X.sorted, (size_t)n_leaves, 0, 32, s) != hipSuccess)

@@ -62,6 +62,14 @@ def _load(path: str) -> ctypes.CDLL:
     lib.or_export.restype = ctypes.c_int
     lib.or_export.argtypes = [ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
                               ctypes.c_int64, _i64p, _i64p]
+    lib.or_set_local.restype = ctypes.c_int
+    lib.or_set_local.argtypes = [ctypes.c_void_p, ctypes.c_int32]
+    lib.or_set_time.restype = ctypes.c_int
+    lib.or_set_time.argtypes = [ctypes.c_void_p, ctypes.c_int64]
+    lib.or_touch.restype = ctypes.c_int
+    lib.or_touch.argtypes = [ctypes.c_void_p, _i32p, _i64p, ctypes.c_int64]
+    lib.or_evict.restype = ctypes.c_int64
+    lib.or_evict.argtypes = [ctypes.c_void_p, ctypes.c_int64]
     lib.or_lcp.restype = ctypes.c_int64
     lib.or_lcp.argtypes = [_i32p, ctypes.c_int64, _i32p, ctypes.c_int64]
     lib.or_prefix_match.restype = ctypes.c_int64
@@ -198,6 +206,28 @@ class Oracle:
         if r:
             raise ValueError(f"or_export failed ({r})")
         return t[:nt.value], o
+
+    # ---- local LRU tree (Algorithm 1's EvictLRUTrie) ----
+    def set_local(self, peer: int) -> None:
+        """Make peer the local one: its tree keeps access times (-1: none)."""
+        if self._lib.or_set_local(self._h, int(peer)):
+            raise ValueError("or_set_local failed")
+
+    def set_time(self, t: int) -> None:
+        """Current time for loads, merges and touches of the local peer."""
+        if self._lib.or_set_time(self._h, int(t)):
+            raise ValueError("or_set_time failed (time went backwards)")
+
+    def touch(self, tokens, offsets) -> None:
+        t, o = _csr(tokens, offsets)
+        if self._lib.or_touch(self._h, _p32(t), _p64(o), o.shape[0] - 1):
+            raise ValueError("or_touch failed")
+
+    def evict(self, n: int) -> int:
+        r = int(self._lib.or_evict(self._h, int(n)))
+        if r < 0:
+            raise ValueError("or_evict failed")
+        return r
 
     def prefix_match(self, peer: int, q) -> int:
         qa = np.ascontiguousarray(q, dtype=np.int32)

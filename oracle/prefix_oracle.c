@@ -36,9 +36,25 @@ typedef struct {
     int64_t *len;
 } or_set;
 
+/* The local peer's tree with access times (see "local LRU tree" below). */
+typedef struct {
+    int32_t tok, parent, depth, alive;
+    int64_t tau;
+    int32_t nch, cap;
+    int32_t *ch; /* children, sorted by token */
+} lru_node;
+
+typedef struct {
+    lru_node *v;
+    int64_t n, cap;
+} lru_trie;
+
 typedef struct {
     int32_t num_peers;
     or_set *sets;
+    int32_t local; /* -1: no peer keeps access times */
+    int64_t now;   /* current time, set by the caller, never decreasing */
+    lru_trie lt;   /* the local peer's tree when local >= 0 */
 } or_forest;
 
 /* ---- the definition ---------------------------------------------------- */
@@ -56,8 +72,11 @@ int64_t or_lcp(const int32_t *a, int64_t na, const int32_t *b, int64_t nb) {
 #endif
 }
 
+static int64_t lru_match(const lru_trie *t, const int32_t *q, int64_t qlen);
+
 /* PrefixMatch(q, T_p): the longest prefix of q shared with any s in S_p. */
 int64_t or_prefix_match(const or_forest *f, int32_t peer, const int32_t *q, int64_t qlen) {
+    if (peer == f->local) return lru_match(&f->lt, q, qlen);
     const or_set *s = &f->sets[peer];
     int64_t best = 0;
     for (int64_t i = 0; i < s->n; i++) {
@@ -91,6 +110,7 @@ or_forest *or_create(int32_t num_peers) {
     or_forest *f = (or_forest *)calloc(1, sizeof(or_forest));
     if (!f) return NULL;
     f->num_peers = num_peers;
+    f->local = -1;
     f->sets = (or_set *)calloc((size_t)num_peers, sizeof(or_set));
     if (!f->sets) { free(f); return NULL; }
     return f;
@@ -103,8 +123,11 @@ static void set_clear(or_set *s) {
     memset(s, 0, sizeof(*s));
 }
 
+static void lru_free(lru_trie *t);
+
 void or_destroy(or_forest *f) {
     if (!f) return;
+    lru_free(&f->lt);
     for (int32_t p = 0; p < f->num_peers; p++) set_clear(&f->sets[p]);
     free(f->sets);
     free(f);
@@ -138,8 +161,16 @@ static int check_csr(const int64_t *offsets, int64_t n) {
 }
 
 /* sendTrie receive: the snapshot REPLACES peer's set. */
+static int lru_reset(lru_trie *t);
+static int lru_insert(lru_trie *t, const int32_t *s, int64_t len, int64_t now);
+
 int or_load(or_forest *f, int32_t peer, const int32_t *tokens, const int64_t *offsets, int64_t n) {
     if (!f || peer < 0 || peer >= f->num_peers || check_csr(offsets, n)) return -1;
+    if (peer == f->local) {
+        if (lru_reset(&f->lt)) return -2;
+        for (int64_t i = 0; i < n; i++)
+            if (lru_insert(&f->lt, tokens + offsets[i], offsets[i + 1] - offsets[i], f->now)) return -2;
+    }
 #ifndef PLANT_LOAD_APPENDS
     set_clear(&f->sets[peer]);
 #endif
@@ -162,6 +193,7 @@ int or_merge(or_forest *f, const int32_t *peer_of, const int32_t *tokens, const 
 #endif
         int r = set_add(&f->sets[p], tokens + offsets[i], offsets[i + 1] - offsets[i]);
         if (r) return r;
+        if (p == f->local && lru_insert(&f->lt, tokens + offsets[i], offsets[i + 1] - offsets[i], f->now)) return -2;
     }
     return 0;
 }
@@ -359,9 +391,13 @@ static int starts_with(const or_set *s, int64_t t, int64_t pre) {
 
 /* Returns 0, or -3 if the buffers are too small (the sizes are set either way;
    tokens / offsets may be NULL to ask for the sizes). */
+static int lru_export(const lru_trie *t, int32_t *tokens, int64_t tok_cap, int64_t *offsets, int64_t seq_cap,
+                      int64_t *num_seqs, int64_t *num_tokens);
+
 int or_export(const or_forest *f, int32_t peer, int32_t *tokens, int64_t tok_cap, int64_t *offsets,
               int64_t seq_cap, int64_t *num_seqs, int64_t *num_tokens) {
     if (!f || peer < 0 || peer >= f->num_peers || !num_seqs || !num_tokens) return -1;
+    if (peer == f->local) return lru_export(&f->lt, tokens, tok_cap, offsets, seq_cap, num_seqs, num_tokens);
     const or_set *s = &f->sets[peer];
     int64_t *ord = (int64_t *)malloc((size_t)(s->n > 0 ? s->n : 1) * sizeof(int64_t));
     if (!ord) return -2;
@@ -396,4 +432,254 @@ int or_export(const or_forest *f, int32_t peer, int32_t *tokens, int64_t tok_cap
     }
     free(ord);
     return 0;
+}
+
+/* ---- local LRU tree --------------------------------------------------------
+ *
+ * Algorithm 1: when a node runs a request itself and its GPU memory is short,
+ * it calls EvictLRUTrie() -- which removes one least-recently-used leaf token
+ * from the local tree and returns it -- and frees that token's KV cache, until
+ * the request fits.  The local peer's tree is kept here as a plain token trie
+ * (one node per token; the root is the empty path) whose every path pi has an
+ * access time tau(pi):
+ *   - a load or merge of s into the local peer at time t sets tau = max(tau, t)
+ *     on every non-empty prefix of s (a load first empties the tree);
+ *   - or_touch(q) at time t does the same on the prefixes of q up to its match
+ *     in the tree (the cached prefix that serving q reuses);
+ *   - EvictLRUTrie removes the leaf with the smallest tau; among equal tau the
+ *     deepest; among equal depth the lexicographically smallest path (the
+ *     paper leaves ties open).
+ * Times come from the caller (or_set_time), never decreasing, so tau never
+ * grows along a path.  or_evict(n) calls EvictLRUTrie up to n times.
+ */
+static void lru_free(lru_trie *t) {
+    for (int64_t i = 0; i < t->n; i++) free(t->v[i].ch);
+    free(t->v);
+    memset(t, 0, sizeof(*t));
+}
+
+static int64_t lru_new(lru_trie *t, int32_t tok, int32_t parent, int32_t depth, int64_t tau) {
+    if (t->n == t->cap) {
+        int64_t nc = t->cap ? 2 * t->cap : 64;
+        lru_node *nv = (lru_node *)realloc(t->v, (size_t)nc * sizeof(lru_node));
+        if (!nv) return -1;
+        t->v = nv;
+        t->cap = nc;
+    }
+    lru_node *x = &t->v[t->n];
+    memset(x, 0, sizeof(*x));
+    x->tok = tok;
+    x->parent = parent;
+    x->depth = depth;
+    x->alive = 1;
+    x->tau = tau;
+    return t->n++;
+}
+
+static int lru_reset(lru_trie *t) {
+    lru_free(t);
+    return lru_new(t, 0, -1, 0, 0) < 0 ? -1 : 0;
+}
+
+/* child of x with token tok, or -1 */
+static int32_t lru_child(const lru_trie *t, int32_t x, int32_t tok) {
+    const lru_node *n = &t->v[x];
+    for (int32_t i = 0; i < n->nch; i++)
+        if (t->v[n->ch[i]].tok == tok) return n->ch[i];
+    return -1;
+}
+
+static int lru_insert(lru_trie *t, const int32_t *s, int64_t len, int64_t now) {
+    if (t->n == 0 && lru_reset(t)) return -1;
+    int32_t x = 0;
+    for (int64_t i = 0; i < len; i++) {
+        int32_t c = lru_child(t, x, s[i]);
+        if (c < 0) {
+            int64_t id = lru_new(t, s[i], x, t->v[x].depth + 1, now);
+            if (id < 0) return -1;
+            lru_node *p = &t->v[x];
+            if (p->nch == p->cap) {
+                int32_t nc = p->cap ? 2 * p->cap : 4;
+                int32_t *nch = (int32_t *)realloc(p->ch, (size_t)nc * sizeof(int32_t));
+                if (!nch) return -1;
+                p->ch = nch;
+                p->cap = nc;
+            }
+            int32_t k = p->nch++;
+            while (k > 0 && t->v[p->ch[k - 1]].tok > s[i]) {  /* keep children sorted */
+                p->ch[k] = p->ch[k - 1];
+                k--;
+            }
+            p->ch[k] = (int32_t)id;
+            c = (int32_t)id;
+        }
+        if (t->v[c].tau < now) t->v[c].tau = now;
+        x = c;
+    }
+    return 0;
+}
+
+static int64_t lru_match(const lru_trie *t, const int32_t *q, int64_t qlen) {
+    if (t->n == 0) return 0;
+    int32_t x = 0;
+    int64_t m = 0;
+    while (m < qlen) {
+        int32_t c = lru_child(t, x, q[m]);
+        if (c < 0) break;
+        x = c;
+        m++;
+    }
+    return m;
+}
+
+/* fills path[0 .. depth) with the tokens from the root to x */
+static void lru_path(const lru_trie *t, int32_t x, int32_t *path) {
+    for (int32_t d = t->v[x].depth; d > 0; d--) {
+        path[d - 1] = t->v[x].tok;
+        x = t->v[x].parent;
+    }
+}
+
+/* does leaf a come before leaf b in the eviction order? */
+static int lru_before(const lru_trie *t, int32_t a, int32_t b, int32_t *pa, int32_t *pb) {
+    const lru_node *x = &t->v[a], *y = &t->v[b];
+#ifdef PLANT_EVICT_MRU
+    if (x->tau != y->tau) return x->tau > y->tau;
+#else
+    if (x->tau != y->tau) return x->tau < y->tau;
+#endif
+    if (x->depth != y->depth) return x->depth > y->depth;
+    lru_path(t, a, pa);
+    lru_path(t, b, pb);
+    for (int32_t i = 0; i < x->depth; i++)
+        if (pa[i] != pb[i]) return pa[i] < pb[i];
+    return a < b;
+}
+
+static int32_t lru_max_depth(const lru_trie *t) {
+    int32_t d = 0;
+    for (int64_t i = 0; i < t->n; i++)
+        if (t->v[i].alive && t->v[i].depth > d) d = t->v[i].depth;
+    return d;
+}
+
+/* EvictLRUTrie, n times (or until the tree is empty). */
+static int64_t lru_evict(lru_trie *t, int64_t n) {
+    if (t->n == 0) return 0;
+    int32_t D = lru_max_depth(t);
+    int32_t *pa = (int32_t *)malloc((size_t)(D > 0 ? D : 1) * sizeof(int32_t));
+    int32_t *pb = (int32_t *)malloc((size_t)(D > 0 ? D : 1) * sizeof(int32_t));
+    if (!pa || !pb) { free(pa); free(pb); return -1; }
+    int64_t done = 0;
+    for (; done < n; done++) {
+        int32_t best = -1;
+        for (int64_t i = 1; i < t->n; i++) {
+            const lru_node *x = &t->v[i];
+            if (!x->alive || x->nch > 0) continue;  /* leaves only */
+            if (best < 0 || lru_before(t, (int32_t)i, best, pa, pb)) best = (int32_t)i;
+        }
+        if (best < 0) break;
+        lru_node *x = &t->v[best], *p = &t->v[x->parent];
+        x->alive = 0;
+        int32_t k = 0;
+        while (p->ch[k] != best) k++;
+        for (; k + 1 < p->nch; k++) p->ch[k] = p->ch[k + 1];
+        p->nch--;
+    }
+    free(pa);
+    free(pb);
+    return done;
+}
+
+/* leaves in lexicographic order (depth-first over sorted children) */
+static void lru_collect(const lru_trie *t, int32_t x, int32_t *path, int32_t *tokens, int64_t *offsets,
+                        int64_t *ns, int64_t *nt, int fill) {
+    const lru_node *n = &t->v[x];
+    if (x != 0) path[n->depth - 1] = n->tok;
+    if (n->nch == 0) {
+        if (x == 0) return;
+        if (fill) {
+            memcpy(tokens + *nt, path, (size_t)n->depth * sizeof(int32_t));
+            offsets[*ns + 1] = *nt + n->depth;
+        }
+        (*ns)++;
+        *nt += n->depth;
+        return;
+    }
+    for (int32_t i = 0; i < n->nch; i++) lru_collect(t, n->ch[i], path, tokens, offsets, ns, nt, fill);
+}
+
+static int lru_export(const lru_trie *t, int32_t *tokens, int64_t tok_cap, int64_t *offsets, int64_t seq_cap,
+                      int64_t *num_seqs, int64_t *num_tokens) {
+    *num_seqs = 0;
+    *num_tokens = 0;
+    if (t->n == 0) {
+        if (offsets && seq_cap >= 1) offsets[0] = 0;
+        return 0;
+    }
+    int32_t D = lru_max_depth(t);
+    int32_t *path = (int32_t *)malloc((size_t)(D > 0 ? D : 1) * sizeof(int32_t));
+    if (!path) return -2;
+    int64_t ns = 0, nt = 0;
+    lru_collect(t, 0, path, NULL, NULL, &ns, &nt, 0);
+    *num_seqs = ns;
+    *num_tokens = nt;
+    if (!tokens || !offsets || tok_cap < nt || seq_cap < ns + 1) {
+        free(path);
+        return (tokens || offsets) ? -3 : 0;
+    }
+    offsets[0] = 0;
+    ns = 0;
+    nt = 0;
+    lru_collect(t, 0, path, tokens, offsets, &ns, &nt, 1);
+    free(path);
+    return 0;
+}
+
+/* Make peer the local one (its tree keeps access times; -1: none).  Its
+   current sequences get the current time. */
+int or_set_local(or_forest *f, int32_t peer) {
+    if (!f || peer < -1 || peer >= f->num_peers) return -1;
+    lru_free(&f->lt);
+    f->local = peer;
+    if (peer < 0) return 0;
+    if (lru_reset(&f->lt)) return -2;
+    const or_set *s = &f->sets[peer];
+    for (int64_t i = 0; i < s->n; i++)
+        if (lru_insert(&f->lt, s->seq[i], s->len[i], f->now)) return -2;
+    return 0;
+}
+
+int or_set_time(or_forest *f, int64_t t) {
+    if (!f || t < f->now) return -1;
+    f->now = t;
+    return 0;
+}
+
+/* Serving the queries at the current time: their matched prefixes in the
+   local tree become the most recently used. */
+int or_touch(or_forest *f, const int32_t *q_tokens, const int64_t *q_offsets, int64_t nq) {
+    if (!f || f->local < 0 || check_csr(q_offsets, nq)) return -1;
+    lru_trie *t = &f->lt;
+    if (t->n == 0) return 0;
+    for (int64_t q = 0; q < nq; q++) {
+        const int32_t *s = q_tokens + q_offsets[q];
+        const int64_t len = q_offsets[q + 1] - q_offsets[q];
+        int32_t x = 0;
+        for (int64_t i = 0; i < len; i++) {
+            int32_t c = lru_child(t, x, s[i]);
+            if (c < 0) break;
+#ifndef PLANT_TOUCH_NOTHING
+            if (t->v[c].tau < f->now) t->v[c].tau = f->now;
+#endif
+            x = c;
+        }
+    }
+    return 0;
+}
+
+/* Evict up to n tokens from the local tree; returns the number evicted. */
+int64_t or_evict(or_forest *f, int64_t n) {
+    if (!f || f->local < 0 || n < 0) return -1;
+    return lru_evict(&f->lt, n);
 }

@@ -465,3 +465,166 @@ def check_export_random(make: Callable, seeds: Sequence[int]) -> List[str]:
                     fails.append(f"seed={sd} peer={p} q={i}: the exported set matches differently")
                     break
     return fails
+
+
+# ---- local LRU tree ------------------------------------------------------------
+LRU_GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "lru_examples.txt")
+
+
+def parse_lru_golden(path: str = LRU_GOLDEN):
+    out, cur = [], None
+    for raw in open(path):
+        line = raw.split("#", 1)[0].strip()
+        if not line:
+            continue
+        kw, _, rest = line.partition(" ")
+        if kw == "example":
+            cur = [rest.strip(), []]
+            out.append(cur)
+        elif kw == "time":
+            cur[1].append(("time", int(rest)))
+        elif kw == "load":
+            cur[1].append(("load", _seqs(rest.partition("|")[2])))
+        elif kw in ("merge", "touch"):
+            cur[1].append((kw, _seqs(rest)))
+        elif kw == "evict":
+            n, _, c = rest.partition("->")
+            cur[1].append(("evict", int(n), int(c)))
+        elif kw == "export":
+            cur[1].append(("export", _seqs(rest.partition("->")[2])))
+        elif kw == "match":
+            q, _, m = rest.partition("->")
+            cur[1].append(("match", _toks(q), int(m)))
+        else:
+            raise ValueError(f"bad directive {kw!r}")
+    return out
+
+
+def run_lru_ops(make: Callable, ops, check: bool = True) -> List[str]:
+    """Apply golden LRU operations to an oracle-like object (local peer 0 of 2)."""
+    fails = []
+    o = make(2)
+    o.set_local(0)
+    for op in ops:
+        if op[0] == "time":
+            o.set_time(op[1])
+        elif op[0] == "load":
+            t, off = _csr(op[1])
+            o.load(0, t, off)
+        elif op[0] == "merge":
+            t, off = _csr(op[1])
+            o.merge(np.zeros(len(op[1]), np.int32), t, off)
+        elif op[0] == "touch":
+            t, off = _csr(op[1])
+            o.touch(t, off)
+        elif op[0] == "evict":
+            got = o.evict(op[1])
+            if got != op[2]:
+                fails.append(f"evict {op[1]}: got {got} want {op[2]}")
+        elif op[0] == "export":
+            got = csr_to_list(*o.export(0))
+            if got != op[1]:
+                fails.append(f"export: got {got} want {op[1]}")
+        elif op[0] == "match":
+            got = o.prefix_match(0, np.array(op[1], np.int32))
+            if got != op[2]:
+                fails.append(f"match {op[1]}: got {got} want {op[2]}")
+    return fails
+
+
+def check_lru_golden(make: Callable) -> List[str]:
+    fails = []
+    for name, ops in parse_lru_golden():
+        fails += [f"{name}: {x}" for x in run_lru_ops(make, ops)]
+    return fails
+
+
+class LruModel:
+    """Independent formulation: a dict from every path to its access time;
+    n evictions remove the first n paths in the order (time, -length, path)."""
+
+    def __init__(self):
+        self.tau = {}
+
+    def load(self, seqs, t):
+        self.tau = {}
+        self.merge(seqs, t)
+
+    def merge(self, seqs, t):
+        for s in seqs:
+            s = tuple(int(x) for x in s)
+            for k in range(1, len(s) + 1):
+                self.tau[s[:k]] = max(self.tau.get(s[:k], t), t)
+
+    def match(self, q) -> int:
+        q = tuple(int(x) for x in q)
+        m = 0
+        while m < len(q) and q[:m + 1] in self.tau:
+            m += 1
+        return m
+
+    def touch(self, qs, t):
+        for q in qs:
+            q = tuple(int(x) for x in q)
+            for k in range(1, self.match(q) + 1):
+                self.tau[q[:k]] = max(self.tau[q[:k]], t)
+
+    def evict(self, n) -> int:
+        order = sorted(self.tau, key=lambda p: (self.tau[p], -len(p), p))[:n]
+        for p in order:
+            del self.tau[p]
+        return len(order)
+
+    def export(self):
+        return sorted(p for p in self.tau if not any(q[:len(p)] == p and len(q) > len(p) for q in self.tau))
+
+
+def check_lru_random(make: Callable, seeds: Sequence[int]) -> List[str]:
+    """Random loads, merges, touches and evictions on tiny tries: the oracle's
+    tree (export and matches) equals the sort-based model's after every step."""
+    fails = []
+    for sd in seeds:
+        rng = np.random.default_rng(4000 + sd)
+        vocab = 2 + sd % 3
+
+        def seqs(k, lo=0, hi=7):
+            return [rng.integers(0, vocab, size=int(rng.integers(lo, hi))).tolist() for _ in range(k)]
+
+        o = make(2)
+        o.set_local(0)
+        mdl = LruModel()
+        t = 0
+        first = seqs(8)
+        o.set_time(t)
+        tt, off = _csr(first)
+        o.load(0, tt, off)
+        mdl.load(first, t)
+        queries = seqs(12, 0, 9)
+        for step in range(14):
+            t += int(rng.integers(0, 2))
+            o.set_time(t)
+            kind = step % 3
+            if kind == 0:
+                batch = seqs(3)
+                tt, off = _csr(batch)
+                o.merge(np.zeros(len(batch), np.int32), tt, off)
+                mdl.merge(batch, t)
+            elif kind == 1:
+                batch = [queries[i] for i in rng.integers(0, len(queries), size=4)]
+                tt, off = _csr(batch)
+                o.touch(tt, off)
+                mdl.touch(batch, t)
+            else:
+                n = int(rng.integers(0, 6))
+                got, want = o.evict(n), mdl.evict(n)
+                if got != want:
+                    fails.append(f"seed={sd} step={step}: evicted {got}, model {want}")
+            exp = [tuple(x) for x in csr_to_list(*o.export(0))]
+            if exp != mdl.export():
+                fails.append(f"seed={sd} step={step}: tree differs from the model")
+                break
+            for q in queries:
+                if o.prefix_match(0, np.array(q, np.int32)) != mdl.match(q):
+                    fails.append(f"seed={sd} step={step}: match of {q} differs")
+                    break
+    return fails

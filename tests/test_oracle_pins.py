@@ -122,9 +122,32 @@ def test_export_random_vs_bruteforce_and_round_trip():
     assert pins.check_export_random(make, seeds=range(12)) == []
 
 
+def test_lru_golden_hand_examples():
+    assert pins.check_lru_golden(make) == []
+
+
+def test_lru_random_vs_sort_model():
+    assert pins.check_lru_random(make, seeds=range(16)) == []
+
+
+def test_lru_evicting_everything_empties_and_time_is_monotone():
+    o = oracle.Oracle(2)
+    o.set_local(1)
+    o.set_time(5)
+    o.load(1, np.array([1, 2, 3, 4], np.int32), np.array([0, 2, 4], np.int64))
+    assert o.evict(100) == 4
+    assert o.export(1)[1].tolist() == [0]
+    with pytest.raises(ValueError):
+        o.set_time(4)
+    # other peers are unaffected by the local peer's evictions
+    o.load(0, np.array([1, 2], np.int32), np.array([0, 2], np.int64))
+    assert o.prefix_match(0, np.array([1, 2], np.int32)) == 2
+
+
 PLANTS = ["PLANT_LCP_OFF_BY_ONE", "PLANT_MIN_NOT_MAX", "PLANT_TIE_HIGHEST",
           "PLANT_LOAD_APPENDS", "PLANT_MERGE_WRONG_PEER", "PLANT_IGNORE_ELIGIBLE",
-          "PLANT_LOCAL_ALWAYS_FIRST", "PLANT_EXPORT_KEEPS_PREFIXES"]
+          "PLANT_LOCAL_ALWAYS_FIRST", "PLANT_EXPORT_KEEPS_PREFIXES", "PLANT_EVICT_MRU",
+          "PLANT_TOUCH_NOTHING"]
 
 
 @pytest.mark.parametrize("plant", PLANTS)
@@ -138,5 +161,6 @@ def test_planted_mistake_is_caught(plant, tmp_path):
     fails = pins.check_golden(mk) + pins.check_tiny_random(mk, seeds=range(3), vocabs=(3,)) \
         + pins.check_merge_semantics(mk, seeds=range(2)) + pins.check_select_golden(mk) \
         + pins.check_select_random(mk, seeds=range(2)) + pins.check_export_golden(mk) \
-        + pins.check_export_random(mk, seeds=range(3))
+        + pins.check_export_random(mk, seeds=range(3)) + pins.check_lru_golden(mk) \
+        + pins.check_lru_random(mk, seeds=range(3))
     assert fails, f"{plant} slipped through every pin"

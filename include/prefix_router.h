@@ -178,6 +178,55 @@ pr_status pr_export_snapshot(pr_forest *f, int32_t peer, int32_t *tokens, int64_
                              int64_t *num_tokens, void *hip_stream);
 
 /*
+ * The local tree's LRU state (paper, Algorithm 1: a node that runs a request
+ * itself and lacks GPU memory calls EvictLRUTrie -- which removes one
+ * least-recently-used leaf token of its local tree -- and frees that token's
+ * KV cache, until the request fits).  One peer of the forest, the local one,
+ * keeps an access time on every path (prefix) of its tree:
+ *   - a snapshot load, device load or merge into the local peer stamps the
+ *     inserted sequences' prefixes with the current time;
+ *   - pr_touch stamps each query's matched prefix (serving a query reuses the
+ *     cached prefix it matches);
+ *   - pr_evict_lru removes least-recently-used leaf tokens: one eviction
+ *     removes the leaf with the smallest time, ties to the deepest leaf, then
+ *     to the lexicographically smallest path (signed tokens).
+ * Times come from the caller and never decrease (pr_set_time).
+ */
+
+/* Make peer the local one (-1: none).  Its current tree gets the current
+ * time.  Errors: PR_EINVAL (peer outside [-1, num_peers)), PR_ESTATE,
+ * PR_ENOMEM, PR_EDEVICE. */
+pr_status pr_set_local_peer(pr_forest *f, int32_t peer);
+
+/* Set the current time (>= the previous one; 0 at creation).  Host only.
+ * Errors: PR_EINVAL (NULL forest, time going backwards). */
+pr_status pr_set_time(pr_forest *f, int64_t t);
+
+/*
+ * Serve num_queries queries at the current time: the prefix of each query
+ * that the local tree matches is stamped (DEVICE CSR input as in pr_route; a
+ * query with invalid offsets is ignored).  Where a matched prefix ends inside
+ * an edge label the edge is split, so the stamp covers exactly the matched
+ * tokens.  Match lengths are unchanged.  Host-synchronous.
+ * Errors: PR_EINVAL (NULL pointers with num_queries > 0, negative counts),
+ * PR_ESTATE (no local peer), PR_ENOMEM, PR_EDEVICE.
+ */
+pr_status pr_touch(pr_forest *f, const int32_t *q_tokens, int64_t num_tokens,
+                   const int64_t *q_offsets, int64_t num_queries, void *hip_stream);
+
+/*
+ * EvictLRUTrie, max_tokens times (or until the local tree is empty): removes
+ * the first max_tokens paths of the local tree in the order (time ascending,
+ * depth descending, path ascending), which is what max_tokens successive
+ * single evictions remove since times never grow along a path.  *evicted
+ * (HOST) gets the number removed.  Other peers' trees are unchanged.
+ * Host-synchronous.
+ * Errors: PR_EINVAL (evicted NULL, max_tokens < 0), PR_ESTATE (no local
+ * peer), PR_ENOMEM, PR_EDEVICE.
+ */
+pr_status pr_evict_lru(pr_forest *f, int64_t max_tokens, int64_t *evicted, void *hip_stream);
+
+/*
  * Peer selection under push-back and failover (paper, Section "Hot specialist
  * push-back": originating nodes stop routing to a node that advertised
  * back-pressure, and such a request runs locally or on a slightly inferior

@@ -11,6 +11,7 @@
 //      behind, which a walk from the root never visits).  Every visited node
 //      gets its depth (tokens from the root through its label) and its
 //      parent; a visited node none of whose children holds p is a leaf.
+//      The LRU eviction uses the same walk and also lists every visited node.
 //   2. The host sorts the leaves by node id (a deterministic order) and scans
 //      their depths into CSR offsets.
 //   3. export_write_kernel: one wave per leaf climbs the parent chain and
@@ -39,6 +40,7 @@ __global__ void export_init_kernel(int32_t *front, int64_t *depth, int32_t *coun
     depth[0] = 0;
     counts[0] = 0;  // next frontier size
     counts[1] = 0;  // leaves so far
+    counts[2] = 0;  // visited nodes so far (root excluded)
 }
 
 __global__ void export_reset_kernel(int32_t *counts) { counts[0] = 0; }
@@ -51,7 +53,7 @@ __global__ void export_reset_kernel(int32_t *counts) { counts[0] = 0; }
 __global__ __launch_bounds__(64 * kExportWavesPerBlock) void export_level_kernel(
     DevForest F, int64_t n_nodes, int32_t p, const int32_t *__restrict__ front, int32_t n_front,
     int32_t *__restrict__ next, int32_t *__restrict__ leaves, int64_t *__restrict__ depth,
-    int32_t *__restrict__ parent, int32_t *__restrict__ counts) {
+    int32_t *__restrict__ parent, int32_t *__restrict__ counts, int32_t *__restrict__ all) {
     const int lane = (int)(threadIdx.x & 63);
     const int64_t i = (int64_t)blockIdx.x * kExportWavesPerBlock + (threadIdx.x >> 6);
     if (i >= n_front) return;
@@ -67,6 +69,10 @@ __global__ __launch_bounds__(64 * kExportWavesPerBlock) void export_level_kernel
             parent[c] = x;
             const int32_t slot = atomicAdd(&counts[0], 1);
             if (slot < n_nodes) next[slot] = c;
+            if (all) {
+                const int32_t k = atomicAdd(&counts[2], 1);
+                if (k < n_nodes) all[k] = c;
+            }
             found = true;
         }
     }

@@ -66,6 +66,12 @@ struct DevForest {
     long long *moved;  // (stamp << 32) | new position, per node id
     int64_t cap_nodes, cap_pool;
     int32_t W;
+    // access times of the local peer's nodes (nullptr: no local peer); a node's
+    // time covers every token of its label, so records carry it when they
+    // move or split
+    unsigned long long *ltime;
+    int32_t local;
+    unsigned long long now;
 };
 
 struct Batch {
@@ -75,6 +81,7 @@ struct Batch {
     int64_t num_tokens;
     int64_t n;
     int32_t P;
+    int32_t stamp;  // 1: inserts into the local peer stamp their path with F.now
 };
 
 constexpr int kMergeWavesPerBlock = 4;
@@ -246,6 +253,10 @@ __global__ __launch_bounds__(64 *kMergeWavesPerBlock) void split_apply_kernel(De
     if (lane == 0) {
         F.nodes[pos_lower] = lower;
         F.ntok[pos_lower] = lower.tok;
+        if (F.ltime) {
+            F.ltime[pos_lower] = F.ltime[r.c];  // both parts of the edge keep its time
+            if (rest > 0) F.ltime[pos_leaf] = 0ull;
+        }
         if (rest > 0) {
             Node leaf;
             leaf.tok = s[r.d + r.l];
@@ -356,6 +367,7 @@ __global__ __launch_bounds__(64 *kMergeWavesPerBlock) void add_build_kernel(
         const int64_t dst = nb + j + lower_count(win_tok + k, nw, F.ntok[src]);
         F.nodes[dst] = F.nodes[src];
         F.ntok[dst] = F.ntok[src];
+        if (F.ltime) F.ltime[dst] = F.ltime[src];
         F.moved[src] = (stamp << 32) | (long long)(uint32_t)dst;
     }
     if (F.W > 1)
@@ -386,6 +398,7 @@ __global__ __launch_bounds__(64 *kMergeWavesPerBlock) void add_build_kernel(
             leaf.mask0 = 0ull;
             F.nodes[dst] = leaf;
             F.ntok[dst] = leaf.tok;
+            if (F.ltime) F.ltime[dst] = 0ull;
         }
         pb += rest;
     }
@@ -424,7 +437,8 @@ __global__ void add_fix_kernel(DevForest F, const unsigned long long *keys, int6
     F.nodes[pos].ct_beg = grp_nb[k];
 }
 
-// OR each insert's peer bit into every node on its path (the root included).
+// OR each insert's peer bit into every node on its path (the root included);
+// inserts into the local peer also stamp the path with the current time.
 __global__ __launch_bounds__(64 *kMergeWavesPerBlock) void merge_mask_kernel(DevForest F, Batch B,
                                                                             const InsState *st,
                                                                             MergeCounters *ctr) {
@@ -436,6 +450,7 @@ __global__ __launch_bounds__(64 *kMergeWavesPerBlock) void merge_mask_kernel(Dev
     const unsigned long long bit = 1ull << (p & 63);
     const int32_t *s = B.tokens + B.offsets[i];
     const int64_t len = B.offsets[i + 1] - B.offsets[i];
+    const bool stamp = F.ltime && B.stamp && p == F.local;
     int32_t x = 0;
     int64_t d = 0;
     while (true) {
@@ -444,6 +459,7 @@ __global__ __launch_bounds__(64 *kMergeWavesPerBlock) void merge_mask_kernel(Dev
                 atomicOr((unsigned long long *)&F.nodes[x].mask0, bit);
             else
                 atomicOr((unsigned long long *)&F.mext[(int64_t)x * (F.W - 1) + (w - 1)], bit);
+            if (stamp) atomicMax(&F.ltime[x], F.now);
         }
         if (d == len) break;
         const Node nx = F.nodes[x];

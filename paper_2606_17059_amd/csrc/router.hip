@@ -18,6 +18,7 @@
 #include "forest_host.h"
 #include "forest_layout.h"
 #include "export_kernels.h"
+#include "lru_kernels.h"
 #include "merge_kernels.h"
 #include "prefix_router.h"
 #include "route_kernels.h"
@@ -47,6 +48,7 @@ struct DevImage {
     uint64_t *mext = nullptr;
     int32_t *pool = nullptr;
     long long *moved = nullptr;
+    unsigned long long *ltime = nullptr;  // local peer's access times (allocated while a local peer is set)
     int64_t cap_nodes = 0, cap_pool = 0;
     int64_t n_nodes = 0, n_pool = 0;  // host mirror of the device counters
 };
@@ -70,6 +72,7 @@ struct MergeScratch {
 struct ExportScratch {
     int64_t *depth = nullptr, *len1 = nullptr, *offs = nullptr;
     int32_t *parent = nullptr, *front = nullptr, *next = nullptr, *leaves = nullptr, *sorted = nullptr;
+    int32_t *all = nullptr;  // every visited node (LRU eviction)
     int32_t *counts = nullptr;
     void *tmp = nullptr;
     size_t tmp_bytes = 0;
@@ -94,6 +97,9 @@ struct pr_forest {
     MergeScratch ms;
     ExportScratch xs;
     long long stamp = 0;          // add-round counter (stamps of moved records)
+    int32_t local = -1;           // peer whose tree keeps access times (-1: none)
+    int64_t now = 0;              // current time, set by the caller, never decreasing
+    int64_t local_load_time = 0;  // time of the local peer's last host snapshot
     int64_t device_bytes = 0;
     bool broken = false;          // a device update failed; only destroy is valid
 };
@@ -122,6 +128,9 @@ class DeviceScope {
     bool ok_ = true;
     bool switched_ = false;
 };
+
+unsigned grid_threads(int64_t n, int bs) { return (unsigned)((n + bs - 1) / bs); }
+unsigned grid_waves(int64_t n) { return (unsigned)((n + pr::kMergeWavesPerBlock - 1) / pr::kMergeWavesPerBlock); }
 
 template <typename T>
 bool dalloc(pr_forest *f, T **p, int64_t count) {
@@ -154,6 +163,7 @@ void free_image(pr_forest *f) {
     dfree(f, &d.pool, d.cap_pool);
     d = DevImage();
     f->has_dev = false;
+    dfree(f, &d.ltime, d.cap_nodes);
 }
 
 void free_export_scratch(pr_forest *f) {
@@ -166,7 +176,8 @@ void free_export_scratch(pr_forest *f) {
     dfree(f, &X.next, X.cap);
     dfree(f, &X.leaves, X.cap);
     dfree(f, &X.sorted, X.cap);
-    dfree(f, &X.counts, 2);
+    dfree(f, &X.all, X.cap);
+    dfree(f, &X.counts, 3);
     if (X.tmp) (void)hipFree(X.tmp);
     f->device_bytes -= (int64_t)X.tmp_bytes;
     X = ExportScratch();
@@ -233,6 +244,23 @@ pr_status ensure_capacity(pr_forest *f, int64_t need_nodes, int64_t need_pool, h
             hipMemsetAsync(mv + d.cap_nodes, 0, (cap - d.cap_nodes) * sizeof(long long), s) != hipSuccess ||
             hipStreamSynchronize(s) != hipSuccess)
             return fail(PR_EDEVICE, "device copy failed while growing the forest");
+        if (d.ltime) {
+            unsigned long long *lt = nullptr;
+            if (!dalloc(f, &lt, cap) ||
+                hipMemcpyAsync(lt, d.ltime, n * sizeof(unsigned long long), hipMemcpyDeviceToDevice, s) !=
+                    hipSuccess ||
+                hipStreamSynchronize(s) != hipSuccess) {
+                dfree(f, &lt, cap);
+                dfree(f, &nn, cap);
+                dfree(f, &nt, cap);
+                dfree(f, &ns, cap);
+                dfree(f, &nm, cap * (f->W - 1));
+                dfree(f, &mv, cap);
+                return fail(PR_ENOMEM, "growing the access times failed");
+            }
+            dfree(f, &d.ltime, d.cap_nodes);
+            d.ltime = lt;
+        }
         dfree(f, &d.nodes, d.cap_nodes);
         dfree(f, &d.ntok, d.cap_nodes);
         dfree(f, &d.nsep, d.cap_nodes);
@@ -257,6 +285,19 @@ pr_status ensure_capacity(pr_forest *f, int64_t need_nodes, int64_t need_pool, h
         d.pool = np;
         d.cap_pool = cap;
     }
+    return PR_OK;
+}
+
+pr::DevForest dev_view(const pr_forest *f);
+
+// Access times of the local peer: every node it holds gets time t, others 0.
+pr_status init_local_times(pr_forest *f, int64_t t) {
+    DevImage &d = f->dev;
+    if (!d.ltime && !dalloc(f, &d.ltime, d.cap_nodes)) return fail(PR_ENOMEM, "hipMalloc failed for access times");
+    hipLaunchKernelGGL(pr::lru_init_kernel, dim3(grid_threads(std::max<int64_t>(d.n_nodes, 1), 256)), dim3(256), 0,
+                       nullptr, dev_view(f), d.n_nodes, (unsigned long long)t);
+    if (hipGetLastError() != hipSuccess || hipStreamSynchronize(nullptr) != hipSuccess)
+        return fail(PR_EDEVICE, "access-time initialisation failed");
     return PR_OK;
 }
 
@@ -305,6 +346,10 @@ pr_status commit(pr_forest *f) {
     f->has_dev = true;
     f->dirty = false;
     f->merged = false;
+    if (f->local >= 0) {
+        pr_status r = init_local_times(f, f->local_load_time);
+        if (r) return r;
+    }
     // the device image is the state of record now; drop the host copy of it
     f->host_img = pr::HostImage();
     f->host_img_valid = false;
@@ -402,22 +447,23 @@ pr::DevForest dev_view(const pr_forest *f) {
     F.mext = f->dev.mext;
     F.pool = f->dev.pool;
     F.moved = f->dev.moved;
+    F.ltime = f->local >= 0 ? f->dev.ltime : nullptr;
+    F.local = f->local;
+    F.now = (unsigned long long)f->now;
     F.cap_nodes = f->dev.cap_nodes;
     F.cap_pool = f->dev.cap_pool;
     F.W = f->W;
     return F;
 }
 
-unsigned grid_threads(int64_t n, int bs) { return (unsigned)((n + bs - 1) / bs); }
-unsigned grid_waves(int64_t n) { return (unsigned)((n + pr::kMergeWavesPerBlock - 1) / pr::kMergeWavesPerBlock); }
 
 // Insert a device batch into the device forest (see merge_kernels.h).
 pr_status run_merge(pr_forest *f, const int32_t *peer_of, const int32_t *tokens, int64_t num_tokens,
-                    const int64_t *offsets, int64_t n, hipStream_t s) {
+                    const int64_t *offsets, int64_t n, hipStream_t s, int32_t stamp = 1) {
     pr_status r = ensure_merge_scratch(f, n, s);
     if (r) return r;
     MergeScratch &m = f->ms;
-    pr::Batch B{peer_of, tokens, offsets, num_tokens, n, f->P};
+    pr::Batch B{peer_of, tokens, offsets, num_tokens, n, f->P, stamp};
     const int bs = 256, wb = 64 * pr::kMergeWavesPerBlock;
     hipLaunchKernelGGL(reset_call_kernel, dim3(1), dim3(1), 0, s, f->d_ctr);
     hipLaunchKernelGGL(pr::merge_validate_kernel, dim3(grid_threads(n, bs)), dim3(bs), 0, s, B, m.st, f->d_ctr);
@@ -517,11 +563,43 @@ pr_status ensure_export_scratch(pr_forest *f, int64_t nn) {
     free_export_scratch(f);
     if (!dalloc(f, &X.depth, cap) || !dalloc(f, &X.len1, cap + 1) || !dalloc(f, &X.offs, cap + 1) ||
         !dalloc(f, &X.parent, cap) || !dalloc(f, &X.front, cap) || !dalloc(f, &X.next, cap) ||
-        !dalloc(f, &X.leaves, cap) || !dalloc(f, &X.sorted, cap) || !dalloc(f, &X.counts, 2)) {
+        !dalloc(f, &X.leaves, cap) || !dalloc(f, &X.sorted, cap) || !dalloc(f, &X.all, cap) ||
+        !dalloc(f, &X.counts, 3)) {
         free_export_scratch(f);
         return fail(PR_ENOMEM, "hipMalloc failed for the export");
     }
     X.cap = cap;
+    return PR_OK;
+}
+
+// Walk peer's nodes level by level from the root (export_kernels.h) into the
+// forest's export scratch: depth and parent of every visited node, the leaves
+// (counts[1]) and, if want_all, every visited node (counts[2]).
+pr_status walk_peer(pr_forest *f, int32_t peer, bool want_all, hipStream_t s, int32_t counts[3]) {
+    const int64_t nn = f->dev.n_nodes;
+    pr_status r = ensure_export_scratch(f, nn);
+    if (r) return r;
+    ExportScratch &X = f->xs;
+    const pr::DevForest F = dev_view(f);
+    const int wb = 64 * pr::kExportWavesPerBlock;
+    hipLaunchKernelGGL(pr::export_init_kernel, dim3(1), dim3(1), 0, s, X.front, X.depth, X.counts);
+    int32_t n_front = 1;
+    counts[0] = counts[1] = counts[2] = 0;
+    while (n_front > 0) {
+        hipLaunchKernelGGL(pr::export_reset_kernel, dim3(1), dim3(1), 0, s, X.counts);
+        hipLaunchKernelGGL(pr::export_level_kernel,
+                           dim3((unsigned)((n_front + pr::kExportWavesPerBlock - 1) / pr::kExportWavesPerBlock)),
+                           dim3(wb), 0, s, F, nn, peer, X.front, n_front, X.next, X.leaves, X.depth, X.parent,
+                           X.counts, want_all ? X.all : nullptr);
+        if (hipGetLastError() != hipSuccess) return fail(PR_EDEVICE, "tree walk launch failed");
+        if (hipMemcpyAsync(counts, X.counts, 3 * sizeof(int32_t), hipMemcpyDeviceToHost, s) != hipSuccess ||
+            hipStreamSynchronize(s) != hipSuccess)
+            return fail(PR_EDEVICE, "tree walk readback failed");
+        if (counts[0] > nn || counts[1] > nn || counts[2] > nn)
+            return fail(PR_EDEVICE, "tree walk visited more nodes than exist");
+        n_front = counts[0];
+        std::swap(X.front, X.next);
+    }
     return PR_OK;
 }
 
@@ -535,22 +613,9 @@ pr_status export_impl(pr_forest *f, int32_t peer, int32_t *tokens, int64_t token
     ExportScratch &X = f->xs;
     const pr::DevForest F = dev_view(f);
     const int wb = 64 * pr::kExportWavesPerBlock;
-    hipLaunchKernelGGL(pr::export_init_kernel, dim3(1), dim3(1), 0, s, X.front, X.depth, X.counts);
-    int32_t n_front = 1, counts[2] = {0, 0};
-    while (n_front > 0) {
-        hipLaunchKernelGGL(pr::export_reset_kernel, dim3(1), dim3(1), 0, s, X.counts);
-        hipLaunchKernelGGL(pr::export_level_kernel,
-                           dim3((unsigned)((n_front + pr::kExportWavesPerBlock - 1) / pr::kExportWavesPerBlock)),
-                           dim3(wb), 0, s, F, nn, peer, X.front, n_front, X.next, X.leaves, X.depth, X.parent,
-                           X.counts);
-        if (hipGetLastError() != hipSuccess) return fail(PR_EDEVICE, "export launch failed");
-        if (hipMemcpyAsync(counts, X.counts, sizeof(counts), hipMemcpyDeviceToHost, s) != hipSuccess ||
-            hipStreamSynchronize(s) != hipSuccess)
-            return fail(PR_EDEVICE, "export readback failed");
-        if (counts[0] > nn || counts[1] > nn) return fail(PR_EDEVICE, "export walk visited more nodes than exist");
-        n_front = counts[0];
-        std::swap(X.front, X.next);
-    }
+    int32_t counts[3] = {0, 0, 0};
+    r = walk_peer(f, peer, false, s, counts);
+    if (r) return r;
     const int32_t n_leaves = counts[1];
     int64_t total = 0;
     if (n_leaves > 0) {
@@ -606,6 +671,25 @@ pr_status export_impl(pr_forest *f, int32_t peer, int32_t *tokens, int64_t token
     if (hipStreamSynchronize(s) != hipSuccess) return fail(PR_EDEVICE, "export failed");
     return ok();
 }
+
+// Device buffers of one touch or eviction call, released on every return path.
+struct CallScratch {
+    std::vector<void *> bufs;
+    template <typename T>
+    bool get(T **p, int64_t count) {
+        *p = nullptr;
+        if (hipMalloc((void **)p, (size_t)std::max<int64_t>(count, 1) * sizeof(T)) != hipSuccess) {
+            (void)hipGetLastError();
+            *p = nullptr;
+            return false;
+        }
+        bufs.push_back((void *)*p);
+        return true;
+    }
+    ~CallScratch() {
+        for (void *b : bufs) (void)hipFree(b);
+    }
+};
 
 }  // namespace
 
@@ -681,6 +765,7 @@ pr_status pr_load_snapshot(pr_forest *f, int32_t peer, const int32_t *tokens, co
     f->sets[(size_t)peer] = std::move(S);
     f->dirty = true;
     f->host_img_valid = false;
+    if (peer == f->local) f->local_load_time = f->now;
     return ok();
 }
 
@@ -765,6 +850,252 @@ pr_status pr_export_snapshot(pr_forest *f, int32_t peer, int32_t *tokens, int64_
     if (r) return r;
     return export_impl(f, peer, tokens, tokens_cap, offsets, seqs_cap, num_seqs, num_tokens,
                        (hipStream_t)hip_stream);
+}
+
+pr_status pr_set_local_peer(pr_forest *f, int32_t peer) {
+    if (!f) return fail(PR_EINVAL, "forest is NULL");
+    if (peer < -1 || peer >= f->P) return fail(PR_EINVAL, "peer out of range");
+    if (f->broken) return fail(PR_ESTATE, "an earlier device update failed; destroy the forest");
+    f->local = peer;
+    f->local_load_time = f->now;
+    if (!f->has_dev) return ok();
+    DeviceScope ds(f);
+    if (!ds.ok()) return fail(PR_EDEVICE, "cannot select the forest's device");
+    if (hipDeviceSynchronize() != hipSuccess) return fail(PR_EDEVICE, "hipDeviceSynchronize failed");
+    if (peer < 0) {
+        dfree(f, &f->dev.ltime, f->dev.cap_nodes);
+        return ok();
+    }
+    if (f->dirty) return ok();  // the next rebuild initialises the times
+    pr_status r = init_local_times(f, f->now);
+    if (r) {
+        f->broken = true;
+        return r;
+    }
+    return ok();
+}
+
+pr_status pr_set_time(pr_forest *f, int64_t t) {
+    if (!f) return fail(PR_EINVAL, "forest is NULL");
+    if (t < f->now) return fail(PR_EINVAL, "time must not decrease");
+    f->now = t;
+    return ok();
+}
+
+static pr_status route_impl(pr_forest *f, const int32_t *q_tokens, int64_t num_tokens, const int64_t *q_offsets,
+                            int64_t num_queries, const pr::Select &sel, int32_t *match_len, int32_t *chosen,
+                            void *hip_stream);
+
+pr_status pr_touch(pr_forest *f, const int32_t *q_tokens, int64_t num_tokens, const int64_t *q_offsets,
+                   int64_t num_queries, void *hip_stream) {
+    if (!f) return fail(PR_EINVAL, "forest is NULL");
+    if (num_queries < 0 || num_tokens < 0) return fail(PR_EINVAL, "negative count");
+    if (f->local < 0) return fail(PR_ESTATE, "no local peer is set");
+    if (num_queries == 0) return ok();
+    if (!q_offsets) return fail(PR_EINVAL, "NULL device pointer");
+    if (num_tokens > 0 && !q_tokens) return fail(PR_EINVAL, "q_tokens is NULL");
+    if (num_queries > (int64_t)INT32_MAX) return fail(PR_EINVAL, "too many queries");
+    if (f->broken) return fail(PR_ESTATE, "an earlier device update failed; destroy the forest");
+    DeviceScope ds(f);
+    if (!ds.ok()) return fail(PR_EDEVICE, "cannot select the forest's device");
+    hipStream_t s = (hipStream_t)hip_stream;
+    CallScratch X;
+    int32_t *ml = nullptr, *ch = nullptr, *peer_of = nullptr, *ttok = nullptr;
+    int64_t *len1 = nullptr, *toff = nullptr;
+    if (!X.get(&ml, num_queries * (int64_t)f->P) || !X.get(&ch, num_queries) || !X.get(&len1, num_queries + 1) ||
+        !X.get(&toff, num_queries + 1) || !X.get(&peer_of, num_queries))
+        return fail(PR_ENOMEM, "hipMalloc failed for the touch");
+    // 1. the matched prefix of every query in the local tree
+    const pr::Select sel{nullptr, -1, 0, nullptr};
+    pr_status r = route_impl(f, q_tokens, num_tokens, q_offsets, num_queries, sel, ml, ch, hip_stream);
+    if (r) return r;
+    // 2. gather the prefixes into one batch
+    hipLaunchKernelGGL(pr::touch_lengths_kernel, dim3(grid_threads(num_queries, 256)), dim3(256), 0, s, ml, f->P,
+                       f->local, num_queries, len1);
+    size_t need = 0;
+    if (rocprim::inclusive_scan(nullptr, need, len1, toff, (size_t)num_queries + 1, rocprim::plus<int64_t>(), s) !=
+        hipSuccess)
+        return fail(PR_EDEVICE, "touch scan sizing failed");
+    void *tmp = nullptr;
+    if (!X.get((char **)&tmp, (int64_t)need)) return fail(PR_ENOMEM, "hipMalloc failed for the touch");
+    if (rocprim::inclusive_scan(tmp, need, len1, toff, (size_t)num_queries + 1, rocprim::plus<int64_t>(), s) !=
+        hipSuccess)
+        return fail(PR_EDEVICE, "touch scan failed");
+    int64_t total = 0;
+    if (hipMemcpyAsync(&total, toff + num_queries, sizeof(total), hipMemcpyDeviceToHost, s) != hipSuccess ||
+        hipStreamSynchronize(s) != hipSuccess)
+        return fail(PR_EDEVICE, "touch readback failed");
+    if (!X.get(&ttok, total)) return fail(PR_ENOMEM, "hipMalloc failed for the touch");
+    hipLaunchKernelGGL(pr::touch_gather_kernel, dim3((unsigned)((num_queries + 3) / 4)), dim3(256), 0, s, q_tokens,
+                       q_offsets, toff, num_queries, ttok);
+    hipLaunchKernelGGL(pr::fill_peer_kernel, dim3(grid_threads(num_queries, 256)), dim3(256), 0, s, peer_of,
+                       num_queries, f->local);
+    if (hipGetLastError() != hipSuccess) return fail(PR_EDEVICE, "touch launch failed");
+    // 3. inserting the prefixes into the local peer adds nothing but node
+    //    boundaries where a prefix ends inside a label, and stamps the paths
+    r = run_merge(f, peer_of, ttok, total, toff, num_queries, s, 1);
+    if (r) {
+        f->broken = true;
+        return r;
+    }
+    return ok();
+}
+
+pr_status pr_evict_lru(pr_forest *f, int64_t max_tokens, int64_t *evicted, void *hip_stream) {
+    if (!f) return fail(PR_EINVAL, "forest is NULL");
+    if (!evicted) return fail(PR_EINVAL, "evicted is NULL");
+    *evicted = 0;
+    if (max_tokens < 0) return fail(PR_EINVAL, "max_tokens < 0");
+    if (f->local < 0) return fail(PR_ESTATE, "no local peer is set");
+    if (f->broken) return fail(PR_ESTATE, "an earlier device update failed; destroy the forest");
+    if (max_tokens == 0) return ok();
+    DeviceScope ds(f);
+    if (!ds.ok()) return fail(PR_EDEVICE, "cannot select the forest's device");
+    pr_status r = commit(f);
+    if (r) return r;
+    if (!f->dev.ltime && (r = init_local_times(f, f->local_load_time))) return r;
+    hipStream_t s = (hipStream_t)hip_stream;
+    int32_t counts[3];
+    if ((r = walk_peer(f, f->local, true, s, counts))) return r;
+    const int64_t V = counts[2];
+    if (V == 0) return ok();
+    ExportScratch &W = f->xs;
+    CallScratch X;
+    unsigned long long *keys = nullptr, *keys_s = nullptr;
+    int32_t *vals = nullptr, *vals_s = nullptr;
+    int64_t *cnt1 = nullptr, *cum = nullptr;
+    pr::EvictPlan *d_plan = nullptr;
+    if (!X.get(&keys, V) || !X.get(&keys_s, V) || !X.get(&vals, V) || !X.get(&vals_s, V) || !X.get(&cnt1, V + 1) ||
+        !X.get(&cum, V + 1) || !X.get(&d_plan, 1))
+        return fail(PR_ENOMEM, "hipMalloc failed for the eviction");
+    auto fail_dev = [&](const char *m) {
+        f->broken = true;
+        return fail(PR_EDEVICE, m);
+    };
+    const pr::DevForest F = dev_view(f);
+    hipLaunchKernelGGL(pr::lru_keys_kernel, dim3(grid_threads(V, 256)), dim3(256), 0, s, F, W.all, V, keys, vals);
+    size_t need = 0, need2 = 0;
+    if (rocprim::radix_sort_pairs(nullptr, need, keys, keys_s, vals, vals_s, (size_t)V, 0, 64, s) != hipSuccess ||
+        rocprim::inclusive_scan(nullptr, need2, cnt1, cum, (size_t)V + 1, rocprim::plus<int64_t>(), s) != hipSuccess)
+        return fail_dev("eviction sort sizing failed");
+    char *tmp = nullptr;
+    const size_t tmp_bytes = std::max(need, need2);
+    if (!X.get(&tmp, (int64_t)tmp_bytes)) return fail(PR_ENOMEM, "hipMalloc failed for the eviction");
+    size_t t1 = tmp_bytes;
+    if (rocprim::radix_sort_pairs(tmp, t1, keys, keys_s, vals, vals_s, (size_t)V, 0, 64, s) != hipSuccess)
+        return fail_dev("eviction sort failed");
+    hipLaunchKernelGGL(pr::lru_counts_kernel, dim3(grid_threads(V, 256)), dim3(256), 0, s, F, vals_s, V, cnt1);
+    size_t t2 = tmp_bytes;
+    if (rocprim::inclusive_scan(tmp, t2, cnt1, cum, (size_t)V + 1, rocprim::plus<int64_t>(), s) != hipSuccess)
+        return fail_dev("eviction scan failed");
+    hipLaunchKernelGGL(pr::lru_plan_kernel, dim3(1), dim3(1), 0, s, keys_s, cum, V, max_tokens, d_plan);
+    pr::EvictPlan plan;
+    if (hipMemcpyAsync(&plan, d_plan, sizeof(plan), hipMemcpyDeviceToHost, s) != hipSuccess ||
+        hipStreamSynchronize(s) != hipSuccess)
+        return fail_dev("eviction readback failed");
+    const int64_t n_evict = std::min<int64_t>(max_tokens, plan.total);
+    if (plan.a > 0)
+        hipLaunchKernelGGL(pr::lru_clear_sorted_kernel, dim3(grid_threads(plan.a, 256)), dim3(256), 0, s, F, vals_s,
+                           plan.a);
+    if (plan.r > 0) {
+        const int64_t a = plan.a, b = plan.b, nc = b - a;
+        hipLaunchKernelGGL(pr::lru_maxdepth_kernel, dim3(grid_threads(nc, 256)), dim3(256), 0, s, vals_s, a, b,
+                           W.depth, d_plan);
+        if (hipMemcpyAsync(&plan, d_plan, sizeof(plan), hipMemcpyDeviceToHost, s) != hipSuccess ||
+            hipStreamSynchronize(s) != hipSuccess)
+            return fail_dev("eviction readback failed");
+        const int32_t maxd = plan.maxd;
+        long long *hist = nullptr, *cnt = nullptr, *rev = nullptr, *S = nullptr;
+        int32_t *level = nullptr, *n_level = nullptr, *rank_of = nullptr, *cut_node = nullptr, *n_cut = nullptr;
+        int64_t *cut_len1 = nullptr;
+        if (!X.get(&hist, maxd + 2) || !X.get(&cnt, maxd + 2) || !X.get(&rev, maxd) || !X.get(&S, maxd) ||
+            !X.get(&level, nc) || !X.get(&n_level, 1) || !X.get(&rank_of, f->dev.n_nodes) ||
+            !X.get(&cut_node, nc) || !X.get(&n_cut, 1) || !X.get(&cut_len1, nc + 1))
+            return fail(PR_ENOMEM, "hipMalloc failed for the eviction");
+        if (hipMemsetAsync(hist, 0, (maxd + 2) * sizeof(long long), s) != hipSuccess ||
+            hipMemsetAsync(n_level, 0, sizeof(int32_t), s) != hipSuccess ||
+            hipMemsetAsync(n_cut, 0, sizeof(int32_t), s) != hipSuccess ||
+            hipMemsetAsync(cut_len1, 0, (nc + 1) * sizeof(int64_t), s) != hipSuccess)
+            return fail_dev("eviction memset failed");
+        hipLaunchKernelGGL(pr::lru_hist_kernel, dim3(grid_threads(nc, 256)), dim3(256), 0, s, F, vals_s, a, b,
+                           W.depth, hist);
+        size_t n3 = 0, n4 = 0;
+        if (rocprim::inclusive_scan(nullptr, n3, hist, cnt, (size_t)maxd + 2, rocprim::plus<long long>(), s) !=
+                hipSuccess ||
+            rocprim::inclusive_scan(nullptr, n4, rev, S, (size_t)maxd, rocprim::plus<long long>(), s) != hipSuccess)
+            return fail_dev("eviction scan sizing failed");
+        char *tmp2 = nullptr;
+        const size_t tb2 = std::max(n3, n4);
+        if (!X.get(&tmp2, (int64_t)tb2)) return fail(PR_ENOMEM, "hipMalloc failed for the eviction");
+        size_t u3 = tb2, u4 = tb2;
+        if (rocprim::inclusive_scan(tmp2, u3, hist, cnt, (size_t)maxd + 2, rocprim::plus<long long>(), s) !=
+            hipSuccess)
+            return fail_dev("eviction scan failed");
+        hipLaunchKernelGGL(pr::lru_reverse_kernel, dim3(grid_threads(maxd, 256)), dim3(256), 0, s, cnt, maxd, rev);
+        if (rocprim::inclusive_scan(tmp2, u4, rev, S, (size_t)maxd, rocprim::plus<long long>(), s) != hipSuccess)
+            return fail_dev("eviction scan failed");
+        hipLaunchKernelGGL(pr::lru_depth_plan_kernel, dim3(1), dim3(1), 0, s, S, d_plan);
+        hipLaunchKernelGGL(pr::lru_level_nodes_kernel, dim3(grid_threads(nc, 256)), dim3(256), 0, s, F, vals_s, a, b,
+                           W.depth, d_plan, level, n_level);
+        int32_t h_level = 0;
+        if (hipMemcpyAsync(&h_level, n_level, sizeof(h_level), hipMemcpyDeviceToHost, s) != hipSuccess ||
+            hipStreamSynchronize(s) != hipSuccess)
+            return fail_dev("eviction readback failed");
+        if (h_level > nc) return fail_dev("eviction level list overflow");
+        hipLaunchKernelGGL(pr::lru_rank_kernel, dim3(grid_threads(h_level, 256)), dim3(256), 0, s, F, level, h_level,
+                           W.parent, W.depth, rank_of);
+        hipLaunchKernelGGL(pr::lru_apply_kernel, dim3(grid_threads(nc, 256)), dim3(256), 0, s, F, vals_s, a, b,
+                           W.depth, rank_of, d_plan, cut_node, cut_len1, n_cut);
+        int32_t h_cut = 0;
+        if (hipGetLastError() != hipSuccess ||
+            hipMemcpyAsync(&h_cut, n_cut, sizeof(h_cut), hipMemcpyDeviceToHost, s) != hipSuccess ||
+            hipStreamSynchronize(s) != hipSuccess)
+            return fail_dev("eviction failed");
+        if (h_cut > 0) {
+            int64_t *offs = nullptr, *old_len = nullptr;
+            int32_t *peer_of = nullptr, *ctok = nullptr;
+            if (!X.get(&offs, h_cut + 1) || !X.get(&old_len, h_cut) || !X.get(&peer_of, h_cut))
+                return fail(PR_ENOMEM, "hipMalloc failed for the eviction");
+            size_t n5 = 0;
+            if (rocprim::inclusive_scan(nullptr, n5, cut_len1, offs, (size_t)h_cut + 1, rocprim::plus<int64_t>(),
+                                        s) != hipSuccess)
+                return fail_dev("eviction scan sizing failed");
+            char *tmp3 = nullptr;
+            if (!X.get(&tmp3, (int64_t)n5)) return fail(PR_ENOMEM, "hipMalloc failed for the eviction");
+            if (rocprim::inclusive_scan(tmp3, n5, cut_len1, offs, (size_t)h_cut + 1, rocprim::plus<int64_t>(), s) !=
+                hipSuccess)
+                return fail_dev("eviction scan failed");
+            int64_t total_cut = 0;
+            if (hipMemcpyAsync(&total_cut, offs + h_cut, sizeof(total_cut), hipMemcpyDeviceToHost, s) !=
+                    hipSuccess ||
+                hipStreamSynchronize(s) != hipSuccess)
+                return fail_dev("eviction readback failed");
+            if (!X.get(&ctok, total_cut)) return fail(PR_ENOMEM, "hipMalloc failed for the eviction");
+            hipLaunchKernelGGL(pr::lru_cut_paths_kernel, dim3((unsigned)((h_cut + 3) / 4)), dim3(256), 0, s, F,
+                               cut_node, h_cut, offs, W.parent, W.depth, ctok);
+            hipLaunchKernelGGL(pr::lru_old_len_kernel, dim3(grid_threads(h_cut, 256)), dim3(256), 0, s, F, cut_node,
+                               h_cut, old_len);
+            hipLaunchKernelGGL(pr::fill_peer_kernel, dim3(grid_threads(h_cut, 256)), dim3(256), 0, s, peer_of,
+                               (int64_t)h_cut, f->local);
+            if (hipGetLastError() != hipSuccess) return fail_dev("eviction launch failed");
+            // the kept paths are held already: inserting them only splits the cut nodes
+            if ((r = run_merge(f, peer_of, ctok, total_cut, offs, h_cut, s, 0))) {
+                f->broken = true;
+                return r;
+            }
+            hipLaunchKernelGGL(pr::lru_clear_lower_kernel, dim3(grid_threads(h_cut, 256)), dim3(256), 0, s,
+                               dev_view(f), cut_node, h_cut, offs, W.depth, old_len, d_plan);
+            if (hipMemcpyAsync(&plan, d_plan, sizeof(plan), hipMemcpyDeviceToHost, s) != hipSuccess ||
+                hipStreamSynchronize(s) != hipSuccess)
+                return fail_dev("eviction readback failed");
+            if (plan.bad) return fail_dev("eviction split left an unexpected structure; destroy the forest");
+        }
+    }
+    if (hipGetLastError() != hipSuccess || hipStreamSynchronize(s) != hipSuccess) return fail_dev("eviction failed");
+    f->merged = true;
+    f->sets[(size_t)f->local] = pr::PeerSeqs();  // the host copy no longer describes the local peer
+    *evicted = n_evict;
+    return ok();
 }
 
 static pr_status route_impl(pr_forest *f, const int32_t *q_tokens, int64_t num_tokens, const int64_t *q_offsets,

@@ -21,7 +21,8 @@ PR_MAX_PEERS = 1024
 
 EXPORTED = ("pr_abi_version", "pr_last_error", "pr_forest_create", "pr_forest_destroy",
             "pr_load_snapshot", "pr_load_snapshot_device", "pr_export_snapshot", "pr_merge", "pr_route",
-            "pr_route_select", "pr_forest_check",
+            "pr_route_select", "pr_set_local_peer", "pr_set_time", "pr_touch", "pr_evict_lru",
+            "pr_forest_check",
             "pr_forest_info_get", "pr_forest_host_image")
 
 PR_SELECT_PREFER_LOCAL = 1
@@ -79,6 +80,14 @@ def lib() -> ctypes.CDLL:
     L.pr_export_snapshot.argtypes = [_vp, ctypes.c_int32, _vp, ctypes.c_int64, _vp, ctypes.c_int64, _i64p, _i64p,
                                      _vp]
     L.pr_export_snapshot.restype = ctypes.c_int32
+    L.pr_set_local_peer.argtypes = [_vp, ctypes.c_int32]
+    L.pr_set_local_peer.restype = ctypes.c_int32
+    L.pr_set_time.argtypes = [_vp, ctypes.c_int64]
+    L.pr_set_time.restype = ctypes.c_int32
+    L.pr_touch.argtypes = [_vp, _vp, ctypes.c_int64, _vp, ctypes.c_int64, _vp]
+    L.pr_touch.restype = ctypes.c_int32
+    L.pr_evict_lru.argtypes = [_vp, ctypes.c_int64, _i64p, _vp]
+    L.pr_evict_lru.restype = ctypes.c_int32
     L.pr_merge.argtypes = [_vp, _vp, _vp, ctypes.c_int64, _vp, ctypes.c_int64, _vp]
     L.pr_merge.restype = ctypes.c_int32
     L.pr_route.argtypes = [_vp, _vp, ctypes.c_int64, _vp, ctypes.c_int64, _vp, _vp, _vp]
@@ -167,6 +176,33 @@ def pr_export_snapshot(f: int, peer: int, device=None, stream=None):
     _check(lib().pr_export_snapshot(f, int(peer), toks.data_ptr(), toks.numel(), offs.data_ptr(), offs.numel(),
                                     ctypes.byref(ns), ctypes.byref(nt), st))
     return toks[:nt.value], offs
+
+
+def pr_set_local_peer(f: int, peer: int) -> None:
+    _check(lib().pr_set_local_peer(f, int(peer)))
+
+
+def pr_set_time(f: int, t: int) -> None:
+    _check(lib().pr_set_time(f, int(t)))
+
+
+def pr_touch(f: int, q_tokens, q_offsets, stream=None) -> None:
+    import torch
+    _dev(q_tokens, torch.int32, "q_tokens")
+    _dev(q_offsets, torch.int64, "q_offsets")
+    n = q_offsets.numel() - 1
+    if n < 0:
+        raise ValueError("q_offsets must have at least one entry")
+    _check(lib().pr_touch(f, q_tokens.data_ptr() or None, q_tokens.numel(), q_offsets.data_ptr(), n,
+                          _stream_ptr(stream, q_offsets.device)))
+
+
+def pr_evict_lru(f: int, max_tokens: int, stream=None) -> int:
+    import torch
+    ev = ctypes.c_int64(0)
+    st = _stream_ptr(stream, torch.device("cuda", torch.cuda.current_device()))
+    _check(lib().pr_evict_lru(f, int(max_tokens), ctypes.byref(ev), st))
+    return ev.value
 
 
 def pr_merge(f: int, peer_of, tokens, offsets, stream=None) -> None:
@@ -318,6 +354,18 @@ class Forest:
 
     def export_snapshot(self, peer: int, device=None, stream=None):
         return pr_export_snapshot(self.handle, peer, device, stream)
+
+    def set_local_peer(self, peer: int) -> None:
+        pr_set_local_peer(self.handle, peer)
+
+    def set_time(self, t: int) -> None:
+        pr_set_time(self.handle, t)
+
+    def touch(self, q_tokens, q_offsets, stream=None) -> None:
+        pr_touch(self.handle, q_tokens, q_offsets, stream)
+
+    def evict_lru(self, max_tokens: int, stream=None) -> int:
+        return pr_evict_lru(self.handle, max_tokens, stream)
 
     def route(self, q_tokens, q_offsets, match_len=None, chosen=None, stream=None) -> Tuple:
         import torch

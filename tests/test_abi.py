@@ -52,3 +52,26 @@ def test_route_select_argument_errors_without_gpu():
         assert L.pr_route_select(f, None, -1, None, 0, None, -1, 0, None, None, None, None) == R.PR_EINVAL
     finally:
         R.pr_forest_destroy(f)
+
+
+def test_lru_argument_errors_without_gpu():
+    """Host-side checks of the LRU calls run before any device work."""
+    import ctypes
+    from paper_2606_17059_amd import router as R
+    L = R.lib()
+    f = R.pr_forest_create(3)
+    try:
+        ev = ctypes.c_int64(-1)
+        assert L.pr_evict_lru(f, 5, ctypes.byref(ev), None) == R.PR_ESTATE  # no local peer yet
+        assert L.pr_touch(f, None, 0, None, 0, None) == R.PR_ESTATE
+        assert L.pr_set_local_peer(f, 3) == R.PR_EINVAL
+        assert L.pr_set_local_peer(f, -2) == R.PR_EINVAL
+        assert L.pr_set_local_peer(f, 1) == R.PR_OK  # no device image yet: no GPU work
+        assert L.pr_set_time(f, 10) == R.PR_OK
+        assert L.pr_set_time(f, 9) == R.PR_EINVAL
+        assert L.pr_evict_lru(f, -1, ctypes.byref(ev), None) == R.PR_EINVAL
+        assert L.pr_evict_lru(f, 0, ctypes.byref(ev), None) == R.PR_OK and ev.value == 0
+        assert L.pr_evict_lru(f, 1, None, None) == R.PR_EINVAL
+        assert L.pr_touch(f, None, -1, None, 0, None) == R.PR_EINVAL
+    finally:
+        R.pr_forest_destroy(f)

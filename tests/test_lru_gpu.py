@@ -1,0 +1,178 @@
+"""The local tree's access times and LRU eviction on the GPU versus the CPU
+oracle (bit-exact: the local tree's paths, every peer's match lengths and the
+number of evicted tokens)."""
+import numpy as np
+import pytest
+
+import pins
+import workloads as W
+from gpu_util import announce, assert_rows_equal, device, gpu_route, oracle_for, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def _gpu_export(f, p, label=""):
+    import torch
+    announce(f"lru export {label}")
+    t, o = f.export_snapshot(p)
+    torch.cuda.synchronize()
+    return sorted(tuple(x) for x in pins.csr_to_list(t.cpu().numpy(), o.cpu().numpy()))
+
+
+def _oracle_export(o, p):
+    return sorted(tuple(x) for x in pins.csr_to_list(*o.export(p)))
+
+
+def _dev_csr(seqs):
+    import torch
+    t, o = pins._csr(seqs)
+    dev = device()
+    return torch.from_numpy(t).to(dev), torch.from_numpy(o).to(dev)
+
+
+class Both:
+    """Apply every operation to the GPU forest and to the oracle."""
+
+    def __init__(self, P, local):
+        import oracle
+        from paper_2606_17059_amd import Forest
+        self.f, self.o, self.P, self.L = Forest(P), oracle.Oracle(P), P, local
+        self.f.set_local_peer(local)
+        self.o.set_local(local)
+
+    def time(self, t):
+        self.f.set_time(t)
+        self.o.set_time(t)
+
+    def load(self, p, seqs):
+        t, off = pins._csr(seqs)
+        self.f.load_snapshot(p, t, off)
+        self.o.load(p, t, off)
+
+    def merge(self, items):
+        import torch
+        t, off = _dev_csr([s for _, s in items])
+        peers = np.array([p for p, _ in items], np.int32)
+        self.f.merge(torch.from_numpy(peers).to(device()), t, off)
+        th, oh = pins._csr([s for _, s in items])
+        self.o.merge(peers, th, oh)
+
+    def touch(self, seqs):
+        t, off = _dev_csr(seqs)
+        self.f.touch(t, off)
+        th, oh = pins._csr(seqs)
+        self.o.touch(th, oh)
+
+    def evict(self, n):
+        announce(f"lru evict {n}")
+        return self.f.evict_lru(n), self.o.evict(n)
+
+    def check(self, queries, what):
+        for p in range(self.P):
+            assert _gpu_export(self.f, p, what) == _oracle_export(self.o, p), (what, p)
+        t, off = pins._csr(queries)
+        ss = W.SeqSet(t, off, np.zeros(len(queries), np.int32))
+        m, c = gpu_route(self.f, ss, what)
+        m_or, c_or = self.o.route(t, off, 2)
+        assert_rows_equal(m, c, m_or, c_or, what=what)
+
+
+def test_lru_golden_examples_on_gpu():
+    for name, ops in pins.parse_lru_golden():
+        b = Both(2, 0)
+        for op in ops:
+            if op[0] == "time":
+                b.time(op[1])
+            elif op[0] == "load":
+                b.load(0, op[1])
+            elif op[0] == "merge":
+                b.merge([(0, s) for s in op[1]])
+            elif op[0] == "touch":
+                b.touch(op[1])
+            elif op[0] == "evict":
+                g, o = b.evict(op[1])
+                assert g == op[2] and o == op[2], (name, op, g)
+            elif op[0] == "export":
+                assert _gpu_export(b.f, 0, name) == sorted(tuple(s) for s in op[1]), (name, op)
+        b.f.close()
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_lru_random_operations_shared_with_other_peers(seed):
+    """Local peer 1 of 3; the other peers share prefixes with it, so splits and
+    evictions cut edges that other peers keep whole."""
+    rng = np.random.default_rng(9000 + seed)
+    vocab = 2 + seed % 3
+
+    def seqs(k, lo=1, hi=9):
+        return [rng.integers(0, vocab, size=int(rng.integers(lo, hi))).tolist() for _ in range(k)]
+
+    b = Both(3, 1)
+    t = 0
+    b.time(t)
+    for p in range(3):
+        b.load(p, seqs(6))
+    queries = seqs(20, 0, 10)
+    b.check(queries, f"seed={seed} start")
+    for step in range(12):
+        t += int(rng.integers(0, 3))
+        b.time(t)
+        kind = step % 4
+        if kind == 0:
+            b.merge([(int(rng.integers(0, 3)), s) for s in seqs(4)])
+        elif kind == 1:
+            b.touch([queries[i] for i in rng.integers(0, len(queries), size=5)])
+        elif kind == 2:
+            g, o = b.evict(int(rng.integers(1, 8)))
+            assert g == o, (seed, step, g, o)
+        else:
+            b.load(int(rng.integers(0, 3)), seqs(5))
+        b.check(queries, f"seed={seed} step={step}")
+    b.f.close()
+
+
+def test_lru_config1_local_peer():
+    """Config 1 with peer 2 local: touches of a query sample, then evictions of
+    a few hundred tokens at a time, checked against the oracle."""
+    w = W.make_config(1)
+    P = w.num_peers
+    b = Both(P, 2)
+    b.time(1)
+    for p in range(P):
+        lo, hi = w.snapshot.peer_range(p)
+        b.load(p, [w.snapshot.seq(i) for i in range(lo, hi)])
+    rng = np.random.default_rng(3)
+    qi = rng.choice(len(w.queries), size=200, replace=False)
+    queries = [w.queries.seq(int(i)) for i in qi]
+    b.time(2)
+    b.touch(queries[:100])
+    for n in (50, 400, 1500):
+        g, o = b.evict(n)
+        assert g == o == n
+        b.check(queries, f"config1 evict {n}")
+    b.time(3)
+    b.touch(queries[100:])
+    g, o = b.evict(2000)
+    assert g == o
+    b.check(queries, "config1 after second touch")
+    b.f.close()
+
+
+def test_touch_keeps_matches_and_evicting_all_empties():
+    w = W.tiny_random(2, num_peers=2, vocab=3, n_queries=40)
+    b = Both(2, 0)
+    b.time(1)
+    for p in range(2):
+        lo, hi = w.snapshot.peer_range(p)
+        b.load(p, [w.snapshot.seq(i) for i in range(lo, hi)])
+    queries = [w.queries.seq(i) for i in range(len(w.queries))]
+    b.check(queries, "before touch")
+    b.time(2)
+    b.touch(queries)
+    b.check(queries, "after touch")
+    g, o = b.evict(10 ** 9)
+    assert g == o
+    assert _gpu_export(b.f, 0, "emptied") == []
+    b.check(queries, "after evicting everything")
+    b.f.check()
+    b.f.close()

@@ -250,6 +250,34 @@ def bench_snapshot(f, w, dev, peers: int = 4) -> dict:
     return out
 
 
+def bench_lru(f, w, qt, qo, dev) -> dict:
+    """Local tree LRU on the device: peer 0 is local; the whole query batch is
+    touched at time 2 (its matched prefixes refreshed), then 1%, 5% and 20% of
+    the local tree's tokens are evicted in turn.  Host-synchronous calls; wall
+    time each."""
+    import torch
+    out = {"local_peer": 0}
+    f.set_time(1)
+    f.set_local_peer(0)
+    toks0, _ = f.export_snapshot(0)
+    f.set_time(2)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    f.touch(qt[0], qo[0])
+    out["touch"] = {"queries": len(w.queries), "ms": (time.perf_counter() - t0) * 1e3}
+    out["touch"]["queries_per_s"] = len(w.queries) / (out["touch"]["ms"] / 1e3)
+    total = int(toks0.numel())  # tokens of the local tree's maximal paths (an upper bound of its size)
+    out["evict"] = []
+    for frac in (0.01, 0.05, 0.20):
+        n = max(1, int(total * frac))
+        t0 = time.perf_counter()
+        got = f.evict_lru(n)
+        ms = (time.perf_counter() - t0) * 1e3
+        out["evict"].append({"requested": n, "evicted": got, "ms": ms, "tokens_per_s": got / (ms / 1e3)})
+    f.check()
+    return out
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -258,6 +286,8 @@ def main() -> int:
     ap.add_argument("--config", type=int, default=2, choices=sorted(WORKLOADS))
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU time of the oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--lru", action="store_true",
+                    help="also time touching the batch in the local tree and LRU evictions")
     ap.add_argument("--snapshot", action="store_true",
                     help="also time snapshot export and device-input load of a few peers")
     ap.add_argument("--no-select", action="store_true",
@@ -382,6 +412,10 @@ def main() -> int:
     if not args.no_select:
         extra["select"] = bench_select(f, w, qt, qo, needed, K, args.warmup, dev)
         log(f"[bench] select: {extra['select']}")
+    if args.lru:
+        # after the timed routes: touches and evictions change the forest
+        extra["lru"] = bench_lru(f, w, qt, qo, dev)
+        log(f"[bench] lru: {extra['lru']}")
     if args.snapshot:
         # after the timed routes: the device loads switch the forest to its device path
         extra["snapshot"] = bench_snapshot(f, w, dev)

@@ -178,6 +178,15 @@ pr_status pr_export_snapshot(pr_forest *f, int32_t peer, int32_t *tokens, int64_
                              int64_t *num_tokens, void *hip_stream);
 
 /*
+ * Tokens peer's tree holds: the number of distinct non-empty prefixes of its
+ * set (one KV-cache entry each for the local peer).  *tokens is HOST.  Walks
+ * the tree on the device; host-synchronous.
+ * Errors: PR_EINVAL (peer out of range, tokens NULL), PR_ESTATE, PR_ENOMEM,
+ * PR_EDEVICE.
+ */
+pr_status pr_tree_tokens(pr_forest *f, int32_t peer, int64_t *tokens, void *hip_stream);
+
+/*
  * The local tree's LRU state (paper, Algorithm 1: a node that runs a request
  * itself and lacks GPU memory calls EvictLRUTrie -- which removes one
  * least-recently-used leaf token of its local tree -- and frees that token's

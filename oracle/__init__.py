@@ -70,6 +70,8 @@ def _load(path: str) -> ctypes.CDLL:
     lib.or_touch.argtypes = [ctypes.c_void_p, _i32p, _i64p, ctypes.c_int64]
     lib.or_evict.restype = ctypes.c_int64
     lib.or_evict.argtypes = [ctypes.c_void_p, ctypes.c_int64]
+    lib.or_tree_tokens.restype = ctypes.c_int64
+    lib.or_tree_tokens.argtypes = [ctypes.c_void_p, ctypes.c_int32]
     lib.or_lcp.restype = ctypes.c_int64
     lib.or_lcp.argtypes = [_i32p, ctypes.c_int64, _i32p, ctypes.c_int64]
     lib.or_prefix_match.restype = ctypes.c_int64
@@ -227,6 +229,13 @@ class Oracle:
         r = int(self._lib.or_evict(self._h, int(n)))
         if r < 0:
             raise ValueError("or_evict failed")
+        return r
+
+    def tree_tokens(self, peer: int) -> int:
+        """Distinct non-empty prefixes of peer's set (tokens its tree holds)."""
+        r = int(self._lib.or_tree_tokens(self._h, int(peer)))
+        if r < 0:
+            raise ValueError("or_tree_tokens failed")
         return r
 
     def prefix_match(self, peer: int, q) -> int:

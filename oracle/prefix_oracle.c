@@ -683,3 +683,31 @@ int64_t or_evict(or_forest *f, int64_t n) {
     if (!f || f->local < 0 || n < 0) return -1;
     return lru_evict(&f->lt, n);
 }
+
+/* ---- tree size -------------------------------------------------------------
+ * Tokens a peer's tree holds: the number of distinct non-empty prefixes of
+ * its set (one KV-cache entry each).  For the local peer, the live nodes of
+ * its token trie; otherwise, in lexicographic order every member adds the
+ * tokens it does not share with the member before it.
+ */
+int64_t or_tree_tokens(const or_forest *f, int32_t peer) {
+    if (!f || peer < 0 || peer >= f->num_peers) return -1;
+    if (peer == f->local) {
+        int64_t n = 0;
+        for (int64_t i = 1; i < f->lt.n; i++) n += f->lt.v[i].alive;
+        return n;
+    }
+    const or_set *s = &f->sets[peer];
+    int64_t *ord = (int64_t *)malloc((size_t)(s->n > 0 ? s->n : 1) * sizeof(int64_t));
+    if (!ord) return -2;
+    for (int64_t i = 0; i < s->n; i++) ord[i] = i;
+    cmp_set = s;
+    qsort(ord, (size_t)s->n, sizeof(int64_t), cmp_seq);
+    int64_t total = 0;
+    for (int64_t i = 0; i < s->n; i++) {
+        int64_t shared = i == 0 ? 0 : or_lcp(s->seq[ord[i]], s->len[ord[i]], s->seq[ord[i - 1]], s->len[ord[i - 1]]);
+        total += s->len[ord[i]] - shared;
+    }
+    free(ord);
+    return total;
+}

@@ -112,6 +112,13 @@ __global__ __launch_bounds__(64 * kExportWavesPerBlock) void export_write_kernel
     }
 }
 
+// Tokens a peer's tree holds: the label lengths of the nodes the walk visited.
+__global__ void tree_tokens_kernel(DevForest F, const int32_t *__restrict__ all, int32_t V,
+                                   unsigned long long *__restrict__ out) {
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < V) atomicAdd(out, (unsigned long long)F.nodes[all[i]].lab_len);
+}
+
 }  // namespace pr
 
 #endif

@@ -852,6 +852,34 @@ pr_status pr_export_snapshot(pr_forest *f, int32_t peer, int32_t *tokens, int64_
                        (hipStream_t)hip_stream);
 }
 
+pr_status pr_tree_tokens(pr_forest *f, int32_t peer, int64_t *tokens, void *hip_stream) {
+    if (!f) return fail(PR_EINVAL, "forest is NULL");
+    if (peer < 0 || peer >= f->P) return fail(PR_EINVAL, "peer out of range");
+    if (!tokens) return fail(PR_EINVAL, "tokens is NULL");
+    *tokens = 0;
+    if (f->broken) return fail(PR_ESTATE, "an earlier device update failed; destroy the forest");
+    DeviceScope ds(f);
+    if (!ds.ok()) return fail(PR_EDEVICE, "cannot select the forest's device");
+    pr_status r = commit(f);
+    if (r) return r;
+    hipStream_t s = (hipStream_t)hip_stream;
+    int32_t counts[3];
+    if ((r = walk_peer(f, peer, true, s, counts))) return r;
+    if (counts[2] == 0) return ok();
+    CallScratch X;
+    unsigned long long *d = nullptr;
+    if (!X.get(&d, 1)) return fail(PR_ENOMEM, "hipMalloc failed");
+    unsigned long long h = 0;
+    if (hipMemsetAsync(d, 0, sizeof(h), s) != hipSuccess) return fail(PR_EDEVICE, "hipMemsetAsync failed");
+    hipLaunchKernelGGL(pr::tree_tokens_kernel, dim3(grid_threads(counts[2], 256)), dim3(256), 0, s, dev_view(f),
+                       f->xs.all, counts[2], d);
+    if (hipGetLastError() != hipSuccess || hipMemcpyAsync(&h, d, sizeof(h), hipMemcpyDeviceToHost, s) != hipSuccess ||
+        hipStreamSynchronize(s) != hipSuccess)
+        return fail(PR_EDEVICE, "tree size failed");
+    *tokens = (int64_t)h;
+    return ok();
+}
+
 pr_status pr_set_local_peer(pr_forest *f, int32_t peer) {
     if (!f) return fail(PR_EINVAL, "forest is NULL");
     if (peer < -1 || peer >= f->P) return fail(PR_EINVAL, "peer out of range");

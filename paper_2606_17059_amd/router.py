@@ -21,7 +21,7 @@ PR_MAX_PEERS = 1024
 
 EXPORTED = ("pr_abi_version", "pr_last_error", "pr_forest_create", "pr_forest_destroy",
             "pr_load_snapshot", "pr_load_snapshot_device", "pr_export_snapshot", "pr_merge", "pr_route",
-            "pr_route_select", "pr_set_local_peer", "pr_set_time", "pr_touch", "pr_evict_lru",
+            "pr_route_select", "pr_tree_tokens", "pr_set_local_peer", "pr_set_time", "pr_touch", "pr_evict_lru",
             "pr_forest_check",
             "pr_forest_info_get", "pr_forest_host_image")
 
@@ -80,6 +80,8 @@ def lib() -> ctypes.CDLL:
     L.pr_export_snapshot.argtypes = [_vp, ctypes.c_int32, _vp, ctypes.c_int64, _vp, ctypes.c_int64, _i64p, _i64p,
                                      _vp]
     L.pr_export_snapshot.restype = ctypes.c_int32
+    L.pr_tree_tokens.argtypes = [_vp, ctypes.c_int32, _i64p, _vp]
+    L.pr_tree_tokens.restype = ctypes.c_int32
     L.pr_set_local_peer.argtypes = [_vp, ctypes.c_int32]
     L.pr_set_local_peer.restype = ctypes.c_int32
     L.pr_set_time.argtypes = [_vp, ctypes.c_int64]
@@ -176,6 +178,14 @@ def pr_export_snapshot(f: int, peer: int, device=None, stream=None):
     _check(lib().pr_export_snapshot(f, int(peer), toks.data_ptr(), toks.numel(), offs.data_ptr(), offs.numel(),
                                     ctypes.byref(ns), ctypes.byref(nt), st))
     return toks[:nt.value], offs
+
+
+def pr_tree_tokens(f: int, peer: int, stream=None) -> int:
+    import torch
+    n = ctypes.c_int64(0)
+    st = _stream_ptr(stream, torch.device("cuda", torch.cuda.current_device()))
+    _check(lib().pr_tree_tokens(f, int(peer), ctypes.byref(n), st))
+    return n.value
 
 
 def pr_set_local_peer(f: int, peer: int) -> None:
@@ -354,6 +364,9 @@ class Forest:
 
     def export_snapshot(self, peer: int, device=None, stream=None):
         return pr_export_snapshot(self.handle, peer, device, stream)
+
+    def tree_tokens(self, peer: int, stream=None) -> int:
+        return pr_tree_tokens(self.handle, peer, stream)
 
     def set_local_peer(self, peer: int) -> None:
         pr_set_local_peer(self.handle, peer)

@@ -70,6 +70,7 @@ class Both:
     def check(self, queries, what):
         for p in range(self.P):
             assert _gpu_export(self.f, p, what) == _oracle_export(self.o, p), (what, p)
+            assert self.f.tree_tokens(p) == self.o.tree_tokens(p), (what, p, "tree tokens")
         t, off = pins._csr(queries)
         ss = W.SeqSet(t, off, np.zeros(len(queries), np.int32))
         m, c = gpu_route(self.f, ss, what)

@@ -144,6 +144,19 @@ def test_lru_evicting_everything_empties_and_time_is_monotone():
     assert o.prefix_match(0, np.array([1, 2], np.int32)) == 2
 
 
+def test_tree_tokens_vs_prefix_set():
+    """Tokens a tree holds = the number of distinct non-empty prefixes."""
+    for sd in range(8):
+        w = W.tiny_random(sd, num_peers=3, vocab=2 + sd % 3, n_queries=1)
+        o = make(3)
+        pins.load_all(o, w.snapshot, 3)
+        if sd % 2:
+            o.set_local(sd % 3)
+        for p, S in enumerate(pins._peer_lists(w)):
+            prefixes = {tuple(int(x) for x in s[:k]) for s in S for k in range(1, len(s) + 1)}
+            assert o.tree_tokens(p) == len(prefixes), (sd, p)
+
+
 PLANTS = ["PLANT_LCP_OFF_BY_ONE", "PLANT_MIN_NOT_MAX", "PLANT_TIE_HIGHEST",
           "PLANT_LOAD_APPENDS", "PLANT_MERGE_WRONG_PEER", "PLANT_IGNORE_ELIGIBLE",
           "PLANT_LOCAL_ALWAYS_FIRST", "PLANT_EXPORT_KEEPS_PREFIXES", "PLANT_EVICT_MRU",

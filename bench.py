@@ -101,6 +101,7 @@ def bench_stream(args, w, dev):
     phases_out = []
     tot_ins = tot_merge_s = tot_q = tot_route_s = tot_bytes = 0.0
     kern_all = []
+    compact_out = []
     cpu = None
     for dist in ("uniform", "zipf"):
         f = Forest(P)
@@ -179,6 +180,9 @@ def bench_stream(args, w, dev):
                                  f"oracle merge of that round's {len(ins)} inserts: "
                                  f"{len(ins) / o_merge_s:.0f} inserts/s (1 thread)"}
                 log(f"[bench] cpu baseline: {cpu}")
+            if args.compact and rnd == w.meta["rounds"] - 1:
+                compact_out.append(bench_compact(f, qt, qo, ml, ch, qs, args.steps, dist, float(km.mean())))
+                log(f"[bench] compact: {compact_out[-1]}")
             del qt, qo, ml, ch
         f.close()
     kern = np.array(kern_all)
@@ -188,7 +192,31 @@ def bench_stream(args, w, dev):
         "achieved": achieved, "bytes_per_launch": tot_bytes / len(kern),
         "merge": {"inserts_per_s": tot_ins / tot_merge_s, "inserts": tot_ins, "seconds": tot_merge_s,
                   "note": "wall time of pr_merge calls (host-synchronous), 8 rounds x 10,000 inserts"},
-        "phases": phases_out, "cpu": cpu}
+        "phases": phases_out, "cpu": cpu, "compact": compact_out or None}
+
+
+def bench_compact(f, qt, qo, ml, ch, qs, steps, dist, route_ms_before) -> dict:
+    """Compaction after the last merge round: records and label tokens before
+    and after, wall time of the (host-synchronous) call, and the lookup kernel
+    time on the same batch before and after."""
+    import torch
+    i0 = f.info()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    before, after = f.compact()
+    ms = (time.perf_counter() - t0) * 1e3
+    i1 = f.info()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for a, b in ev:
+        a.record()
+        f.route(qt, qo, ml, ch)
+        b.record()
+    torch.cuda.synchronize()
+    f.check()
+    km = np.array([a.elapsed_time(b) for a, b in ev])
+    return {"dist": dist, "nodes_before": before, "nodes_after": after, "pool_before": i0["pool_tokens"],
+            "pool_after": i1["pool_tokens"], "compact_ms": ms, "nodes_per_s": before / (ms / 1e3),
+            "route_ms_before": route_ms_before, "route_ms_after": float(km.mean())}
 
 
 def bench_select(f, w, qt, qo, needed, K, warmup, dev) -> dict:
@@ -290,6 +318,8 @@ def main() -> int:
                     help="also time touching the batch in the local tree and LRU evictions")
     ap.add_argument("--snapshot", action="store_true",
                     help="also time snapshot export and device-input load of a few peers")
+    ap.add_argument("--compact", action="store_true",
+                    help="config 5: compact the forest after the last merge round and time it")
     ap.add_argument("--no-select", action="store_true",
                     help="skip timing pr_route_select (push-back / failover selection)")
     ap.add_argument("--copies", type=int, default=2, help="device copies of the query batch to rotate")
@@ -339,6 +369,8 @@ def main() -> int:
                          "kernel": "route_kernel",
                          "kernel_ms": r["kernel_ms"], "algorithmic_bytes_per_launch": r["bytes_per_launch"]},
             "cpu_baseline": r["cpu"], "merge": r["merge"], "phases": r["phases"]}
+        if r["compact"]:
+            out["compact"] = r["compact"]
         print(json.dumps(out), flush=True)
         return 0
     queries = w.queries

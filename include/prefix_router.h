@@ -187,6 +187,24 @@ pr_status pr_export_snapshot(pr_forest *f, int32_t peer, int32_t *tokens, int64_
 pr_status pr_tree_tokens(pr_forest *f, int32_t peer, int64_t *tokens, void *hip_stream);
 
 /*
+ * Rebuild the device forest from the nodes some peer still holds.  Device
+ * merges (Sec. 3.3's delta updates) rebuild a parent's child block elsewhere
+ * and leave the old one behind, and cleared snapshots or evictions leave
+ * nodes no peer holds; routing never reaches either, but they take HBM.  The
+ * rebuild copies the live nodes level by level into fresh arrays with
+ * contiguous child blocks and a fresh label pool.  Routing, exports, token
+ * counts and local access times are unchanged; node ids are not kept.
+ * Outputs: *nodes_before, *nodes_after HOST, may be NULL (node records in
+ * use).  Host-synchronous; waits for the whole device before it frees the old
+ * image, so no launch on any stream may still read it.  Holds the old and new
+ * image at once while it runs.
+ * Errors: PR_EINVAL (f NULL), PR_ESTATE, PR_ENOMEM, PR_EDEVICE.  After an
+ * error before the install the old image stays in use; a failed install
+ * leaves the forest broken (PR_ESTATE from then on).
+ */
+pr_status pr_forest_compact(pr_forest *f, int64_t *nodes_before, int64_t *nodes_after, void *hip_stream);
+
+/*
  * The local tree's LRU state (paper, Algorithm 1: a node that runs a request
  * itself and lacks GPU memory calls EvictLRUTrie -- which removes one
  * least-recently-used leaf token of its local tree -- and frees that token's

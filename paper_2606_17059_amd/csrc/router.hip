@@ -17,6 +17,7 @@
 
 #include "forest_host.h"
 #include "forest_layout.h"
+#include "compact_kernels.h"
 #include "export_kernels.h"
 #include "lru_kernels.h"
 #include "merge_kernels.h"
@@ -161,9 +162,9 @@ void free_image(pr_forest *f) {
     dfree(f, &d.mext, d.cap_nodes * (f->W - 1));
     dfree(f, &d.moved, d.cap_nodes);
     dfree(f, &d.pool, d.cap_pool);
+    dfree(f, &d.ltime, d.cap_nodes);
     d = DevImage();
     f->has_dev = false;
-    dfree(f, &d.ltime, d.cap_nodes);
 }
 
 void free_export_scratch(pr_forest *f) {
@@ -850,6 +851,149 @@ pr_status pr_export_snapshot(pr_forest *f, int32_t peer, int32_t *tokens, int64_
     if (r) return r;
     return export_impl(f, peer, tokens, tokens_cap, offsets, seqs_cap, num_seqs, num_tokens,
                        (hipStream_t)hip_stream);
+}
+
+pr_status pr_forest_compact(pr_forest *f, int64_t *nodes_before, int64_t *nodes_after, void *hip_stream) {
+    if (!f) return fail(PR_EINVAL, "forest is NULL");
+    if (f->broken) return fail(PR_ESTATE, "an earlier device update failed; destroy the forest");
+    DeviceScope ds(f);
+    if (!ds.ok()) return fail(PR_EDEVICE, "cannot select the forest's device");
+    pr_status r = commit(f);
+    if (r) return r;
+    hipStream_t s = (hipStream_t)hip_stream;
+    DevImage &d = f->dev;
+    const int64_t n_old = d.n_nodes;
+    if (nodes_before) *nodes_before = n_old;
+    // the new image (capacity: the old node count plus spare; labels sized below)
+    DevImage nw;
+    nw.cap_nodes = std::max<int64_t>(n_old + n_old / 8, 1024);
+    auto free_new = [&]() {
+        dfree(f, &nw.nodes, nw.cap_nodes);
+        dfree(f, &nw.ntok, nw.cap_nodes);
+        dfree(f, &nw.nsep, nw.cap_nodes);
+        dfree(f, &nw.mext, nw.cap_nodes * (f->W - 1));
+        dfree(f, &nw.moved, nw.cap_nodes);
+        dfree(f, &nw.ltime, nw.cap_nodes);
+        dfree(f, &nw.pool, nw.cap_pool);
+    };
+    if (!dalloc(f, &nw.nodes, nw.cap_nodes) || !dalloc(f, &nw.ntok, nw.cap_nodes) ||
+        !dalloc(f, &nw.nsep, nw.cap_nodes) || !dalloc(f, &nw.mext, nw.cap_nodes * (f->W - 1)) ||
+        !dalloc(f, &nw.moved, nw.cap_nodes) || (d.ltime && !dalloc(f, &nw.ltime, nw.cap_nodes))) {
+        free_new();
+        return fail(PR_ENOMEM, "hipMalloc failed for the compacted forest");
+    }
+    CallScratch X;
+    int32_t *fo = nullptr, *fn = nullptr, *go = nullptr, *gn = nullptr;
+    int64_t *kept1 = nullptr, *start1 = nullptr;
+    if (!X.get(&fo, n_old) || !X.get(&fn, n_old) || !X.get(&go, n_old) || !X.get(&gn, n_old) ||
+        !X.get(&kept1, n_old + 1) || !X.get(&start1, n_old + 1)) {
+        free_new();
+        return fail(PR_ENOMEM, "hipMalloc failed for the compaction");
+    }
+    const pr::DevForest O = dev_view(f);
+    pr::DevForest N = O;
+    N.nodes = nw.nodes;
+    N.ntok = nw.ntok;
+    N.nsep = nw.nsep;
+    N.mext = nw.mext;
+    N.moved = nw.moved;
+    N.ltime = nw.ltime;
+    N.pool = nullptr;
+    N.cap_nodes = nw.cap_nodes;
+    auto fail_dev = [&](const char *m) {
+        free_new();
+        return fail(PR_EDEVICE, m);
+    };
+    hipLaunchKernelGGL(pr::compact_init_kernel, dim3(1), dim3(1), 0, s, O, N, fo, fn);
+    size_t need = 0;
+    if (rocprim::inclusive_scan(nullptr, need, kept1, start1, (size_t)n_old + 1, rocprim::plus<int64_t>(), s) !=
+        hipSuccess)
+        return fail_dev("compaction scan sizing failed");
+    char *tmp = nullptr;
+    if (!X.get(&tmp, (int64_t)need)) {
+        free_new();
+        return fail(PR_ENOMEM, "hipMalloc failed for the compaction");
+    }
+    const int wb = 64 * pr::kCompactWavesPerBlock;
+    int64_t n_front = 1, first_new = 1;
+    while (n_front > 0) {
+        const unsigned g = (unsigned)((n_front + pr::kCompactWavesPerBlock - 1) / pr::kCompactWavesPerBlock);
+        if (hipMemsetAsync(kept1, 0, sizeof(int64_t), s) != hipSuccess) return fail_dev("compaction memset failed");
+        hipLaunchKernelGGL(pr::compact_count_kernel, dim3(g), dim3(wb), 0, s, O, fo, (int32_t)n_front, kept1 + 1);
+        size_t t = need;
+        if (rocprim::inclusive_scan(tmp, t, kept1, start1, (size_t)n_front + 1, rocprim::plus<int64_t>(), s) !=
+            hipSuccess)
+            return fail_dev("compaction scan failed");
+        int64_t total = 0;
+        if (hipMemcpyAsync(&total, start1 + n_front, sizeof(total), hipMemcpyDeviceToHost, s) != hipSuccess ||
+            hipStreamSynchronize(s) != hipSuccess)
+            return fail_dev("compaction readback failed");
+        // live nodes are distinct old records: more than n_old means a malformed forest
+        if (total < 0 || first_new + total > n_old) return fail_dev("compaction found more live nodes than exist");
+        hipLaunchKernelGGL(pr::compact_copy_kernel, dim3(g), dim3(wb), 0, s, O, N, fo, fn, (int32_t)n_front, start1,
+                           first_new, go, gn, (int64_t)0);
+        if (hipGetLastError() != hipSuccess) return fail_dev("compaction launch failed");
+        first_new += total;
+        n_front = total;
+        std::swap(fo, go);
+        std::swap(fn, gn);
+    }
+    const int64_t n_new = first_new;
+    // labels into a fresh pool, then separators
+    int64_t *len1 = nullptr, *off = nullptr;
+    if (!X.get(&len1, n_new + 1) || !X.get(&off, n_new + 1)) {
+        free_new();
+        return fail(PR_ENOMEM, "hipMalloc failed for the compaction");
+    }
+    hipLaunchKernelGGL(pr::compact_lab_len_kernel, dim3(grid_threads(n_new, 256)), dim3(256), 0, s, N, n_new, len1);
+    size_t need2 = 0;
+    if (rocprim::inclusive_scan(nullptr, need2, len1, off, (size_t)n_new + 1, rocprim::plus<int64_t>(), s) !=
+        hipSuccess)
+        return fail_dev("compaction scan sizing failed");
+    char *tmp2 = nullptr;
+    if (!X.get(&tmp2, (int64_t)need2)) {
+        free_new();
+        return fail(PR_ENOMEM, "hipMalloc failed for the compaction");
+    }
+    if (rocprim::inclusive_scan(tmp2, need2, len1, off, (size_t)n_new + 1, rocprim::plus<int64_t>(), s) != hipSuccess)
+        return fail_dev("compaction scan failed");
+    int64_t n_pool = 0;
+    if (hipMemcpyAsync(&n_pool, off + n_new, sizeof(n_pool), hipMemcpyDeviceToHost, s) != hipSuccess ||
+        hipStreamSynchronize(s) != hipSuccess)
+        return fail_dev("compaction readback failed");
+    if (n_pool > (int64_t)UINT32_MAX) return fail_dev("compacted label pool exceeds 2^32 tokens");
+    nw.cap_pool = std::min<int64_t>(std::max<int64_t>(n_pool + n_pool / 8, 4096), (int64_t)UINT32_MAX);
+    if (!dalloc(f, &nw.pool, nw.cap_pool)) {
+        free_new();
+        return fail(PR_ENOMEM, "hipMalloc failed for the compacted label pool");
+    }
+    N.pool = nw.pool;
+    N.cap_pool = nw.cap_pool;
+    const unsigned gn_all = (unsigned)((n_new + pr::kCompactWavesPerBlock - 1) / pr::kCompactWavesPerBlock);
+    hipLaunchKernelGGL(pr::compact_labels_kernel, dim3(gn_all), dim3(wb), 0, s, d.pool, N, n_new, off);
+    hipLaunchKernelGGL(pr::compact_sep_kernel, dim3(gn_all), dim3(wb), 0, s, N, n_new);
+    if (hipGetLastError() != hipSuccess ||
+        hipMemsetAsync(nw.moved, 0, nw.cap_nodes * sizeof(long long), s) != hipSuccess ||
+        hipStreamSynchronize(s) != hipSuccess)
+        return fail_dev("compaction failed");
+    // install the new image once no launch on another stream still reads the old one
+    if (hipDeviceSynchronize() != hipSuccess) return fail_dev("hipDeviceSynchronize failed");
+    free_image(f);
+    nw.n_nodes = n_new;
+    nw.n_pool = n_pool;
+    f->dev = nw;
+    f->has_dev = true;
+    pr::MergeCounters c;
+    std::memset(&c, 0, sizeof(c));
+    c.n_nodes = (unsigned long long)n_new;
+    c.n_pool = (unsigned long long)n_pool;
+    if (hipMemcpy(f->d_ctr, &c, sizeof(c), hipMemcpyHostToDevice) != hipSuccess) {
+        f->broken = true;
+        return fail(PR_EDEVICE, "counter upload failed");
+    }
+    f->host_img_valid = false;  // the host image no longer mirrors the device layout
+    if (nodes_after) *nodes_after = n_new;
+    return ok();
 }
 
 pr_status pr_tree_tokens(pr_forest *f, int32_t peer, int64_t *tokens, void *hip_stream) {

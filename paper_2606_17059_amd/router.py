@@ -21,7 +21,7 @@ PR_MAX_PEERS = 1024
 
 EXPORTED = ("pr_abi_version", "pr_last_error", "pr_forest_create", "pr_forest_destroy",
             "pr_load_snapshot", "pr_load_snapshot_device", "pr_export_snapshot", "pr_merge", "pr_route",
-            "pr_route_select", "pr_tree_tokens", "pr_set_local_peer", "pr_set_time", "pr_touch", "pr_evict_lru",
+            "pr_route_select", "pr_tree_tokens", "pr_forest_compact", "pr_set_local_peer", "pr_set_time", "pr_touch", "pr_evict_lru",
             "pr_forest_check",
             "pr_forest_info_get", "pr_forest_host_image")
 
@@ -82,6 +82,8 @@ def lib() -> ctypes.CDLL:
     L.pr_export_snapshot.restype = ctypes.c_int32
     L.pr_tree_tokens.argtypes = [_vp, ctypes.c_int32, _i64p, _vp]
     L.pr_tree_tokens.restype = ctypes.c_int32
+    L.pr_forest_compact.argtypes = [_vp, _i64p, _i64p, _vp]
+    L.pr_forest_compact.restype = ctypes.c_int32
     L.pr_set_local_peer.argtypes = [_vp, ctypes.c_int32]
     L.pr_set_local_peer.restype = ctypes.c_int32
     L.pr_set_time.argtypes = [_vp, ctypes.c_int64]
@@ -186,6 +188,15 @@ def pr_tree_tokens(f: int, peer: int, stream=None) -> int:
     st = _stream_ptr(stream, torch.device("cuda", torch.cuda.current_device()))
     _check(lib().pr_tree_tokens(f, int(peer), ctypes.byref(n), st))
     return n.value
+
+
+def pr_forest_compact(f: int, stream=None) -> tuple:
+    """Drop unreachable and unheld node records; returns (nodes_before, nodes_after)."""
+    import torch
+    a, b = ctypes.c_int64(0), ctypes.c_int64(0)
+    st = _stream_ptr(stream, torch.device("cuda", torch.cuda.current_device()))
+    _check(lib().pr_forest_compact(f, ctypes.byref(a), ctypes.byref(b), st))
+    return a.value, b.value
 
 
 def pr_set_local_peer(f: int, peer: int) -> None:
@@ -367,6 +378,9 @@ class Forest:
 
     def tree_tokens(self, peer: int, stream=None) -> int:
         return pr_tree_tokens(self.handle, peer, stream)
+
+    def compact(self, stream=None) -> tuple:
+        return pr_forest_compact(self.handle, stream)
 
     def set_local_peer(self, peer: int) -> None:
         pr_set_local_peer(self.handle, peer)

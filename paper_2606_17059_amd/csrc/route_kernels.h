@@ -40,10 +40,13 @@
 #define PR_LCP_VECTORS 16
 #endif
 #ifndef PR_LCP_FIRST_VECTORS
-#define PR_LCP_FIRST_VECTORS 8
+#define PR_LCP_FIRST_VECTORS 9
 #endif
 #ifndef PR_QUERY_NT
 #define PR_QUERY_NT 1
+#endif
+#ifndef PR_ALIGN_STEPS
+#define PR_ALIGN_STEPS 1
 #endif
 #ifndef PR_FIRST_WINDOW
 #define PR_FIRST_WINDOW 1
@@ -109,21 +112,33 @@ __device__ __forceinline__ int32_t lcp_step(__amdgpu_buffer_rsrc_t ra, __amdgpu_
 // compares up to `first` tokens (a label's first step: 64 * kLcpFirstVectors,
 // which bounds what a mismatch early in a long label reads in vain), later
 // steps up to 64 * kLcpVectors, which halves the round trips over long labels
-// that match in full.  A step of at most 128 tokens takes a two-vector form.
+// that match in full.  Every step but a label's last ends at a query line, 0 to
+// 31 tokens short of its nominal size; the nine-vector first step leaves the
+// rest of a 1024-token label to an eight-vector step.  Steps of at most 128
+// and 512 tokens take two- and eight-vector forms.
 __device__ __forceinline__ int64_t wave_lcp(const int32_t *__restrict__ a, const int32_t *__restrict__ b,
                                             int64_t n, int64_t base, int64_t first, int lane) {
-    for (int64_t step = first; base < n; base += step, step = (int64_t)kWave * kLcpVectors) {
-        const int32_t cnt = (int32_t)min(n - base, step);
+    for (int64_t step = first; base < n; step = (int64_t)kWave * kLcpVectors) {
+        int32_t cnt = (int32_t)min(n - base, step);
+#if PR_ALIGN_STEPS
+        // a step that is not the label's last ends at a 128-byte line of the
+        // query, so no line is split between two steps: its non-temporal read
+        // would not keep the line in the L2 for the next step
+        if (n - base > step) cnt -= (int32_t)(((uint32_t)((uintptr_t)(b + base) >> 2) + (uint32_t)step) & 31u);
+#endif
         const __amdgpu_buffer_rsrc_t ra = token_rsrc(a + base, cnt * 4);
         const __amdgpu_buffer_rsrc_t rb = token_rsrc(b + base, cnt * 4);
         int32_t r;
         if (cnt <= 2 * kWave)
             r = lcp_step<2>(ra, rb, lane);
-        else if (kLcpVectors > kLcpFirstVectors && cnt <= kWave * kLcpFirstVectors)
+        else if (cnt <= 8 * kWave)
+            r = lcp_step<8>(ra, rb, lane);
+        else if (kLcpFirstVectors > 8 && kLcpVectors > kLcpFirstVectors && cnt <= kWave * kLcpFirstVectors)
             r = lcp_step<kLcpFirstVectors>(ra, rb, lane);
         else
             r = lcp_step<kLcpVectors>(ra, rb, lane);
         if (r >= 0 && r < cnt) return base + r;
+        base += cnt;
     }
     return n;
 }
@@ -310,14 +325,17 @@ __device__ __forceinline__ int32_t select_peers(const int32_t (&m)[W], int32_t P
     return select_decode(k1, sel);
 }
 
-template <int W>
+// SEL = false: plain routing (every peer eligible, ties to the lowest id, no
+// second pick); the selection options are compiled out.
+template <int W, bool SEL>
 __global__ __launch_bounds__(kWave *kRouteWavesPerBlock)
 __attribute__((amdgpu_waves_per_eu(PR_ROUTE_WAVES_PER_EU))) void route_kernel(
     const Node *__restrict__ nodes, const int32_t *__restrict__ ntok, const int32_t *__restrict__ nsep,
     const uint64_t *__restrict__ mext,
     const int32_t *__restrict__ pool, const int32_t *__restrict__ qtok, int64_t num_tokens,
-    const int64_t *__restrict__ qoff, int64_t nq, int32_t P, const Select sel, int32_t *__restrict__ match_len,
+    const int64_t *__restrict__ qoff, int64_t nq, int32_t P, const Select sel_in, int32_t *__restrict__ match_len,
     int32_t *__restrict__ chosen) {
+    const Select sel = SEL ? sel_in : Select{nullptr, -1, 0, nullptr};
     const int lane = (int)(threadIdx.x & (kWave - 1));
     const int64_t q = (int64_t)blockIdx.x * kRouteWavesPerBlock + uniform((int32_t)(threadIdx.x / kWave));
     if (q >= nq) return;

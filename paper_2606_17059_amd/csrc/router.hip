@@ -361,9 +361,15 @@ template <int W>
 hipError_t launch_route(const pr_forest *f, const int32_t *qt, int64_t ntok, const int64_t *qo, int64_t nq,
                         const pr::Select &sel, int32_t *ml, int32_t *ch, hipStream_t s) {
     const int64_t blocks = (nq + pr::kRouteWavesPerBlock - 1) / pr::kRouteWavesPerBlock;
-    hipLaunchKernelGGL(pr::route_kernel<W>, dim3((unsigned)blocks), dim3(pr::kWave * pr::kRouteWavesPerBlock), 0, s,
-                       f->dev.nodes, f->dev.ntok, f->dev.nsep, f->dev.mext, f->dev.pool, qt, ntok, qo, nq, f->P,
-                       sel, ml, ch);
+    const bool plain = !sel.eligible && !sel.prefer_local && !sel.second;
+    if (plain)
+        hipLaunchKernelGGL((pr::route_kernel<W, false>), dim3((unsigned)blocks),
+                           dim3(pr::kWave * pr::kRouteWavesPerBlock), 0, s, f->dev.nodes, f->dev.ntok, f->dev.nsep,
+                           f->dev.mext, f->dev.pool, qt, ntok, qo, nq, f->P, sel, ml, ch);
+    else
+        hipLaunchKernelGGL((pr::route_kernel<W, true>), dim3((unsigned)blocks),
+                           dim3(pr::kWave * pr::kRouteWavesPerBlock), 0, s, f->dev.nodes, f->dev.ntok, f->dev.nsep,
+                           f->dev.mext, f->dev.pool, qt, ntok, qo, nq, f->P, sel, ml, ch);
     return hipGetLastError();
 }
 

@@ -405,6 +405,35 @@ class Forest:
         pr_route(self.handle, q_tokens, q_offsets, match_len, chosen, self.num_peers, stream)
         return match_len, chosen
 
+    def route_launcher(self, q_tokens, q_offsets, match_len, chosen, stream=None):
+        """Check the buffers once and return a callable that launches pr_route on
+        them with no per-call checks or conversions (tight launch loops).  The
+        callable keeps the tensors alive; it raises RouterError on a failed call."""
+        import torch
+        _dev(q_tokens, torch.int32, "q_tokens")
+        _dev(q_offsets, torch.int64, "q_offsets")
+        _dev(match_len, torch.int32, "match_len")
+        _dev(chosen, torch.int32, "chosen")
+        nq = q_offsets.numel() - 1
+        if nq < 0:
+            raise ValueError("q_offsets must have at least one entry")
+        if match_len.numel() != nq * self.num_peers or chosen.numel() != nq:
+            raise ValueError("match_len must hold [num_queries][num_peers] and chosen [num_queries]")
+        fn = lib().pr_route
+        args = (ctypes.c_void_p(self.handle), ctypes.c_void_p(q_tokens.data_ptr() or None),
+                ctypes.c_int64(q_tokens.numel()), ctypes.c_void_p(q_offsets.data_ptr()), ctypes.c_int64(nq),
+                ctypes.c_void_p(match_len.data_ptr() or None), ctypes.c_void_p(chosen.data_ptr() or None),
+                ctypes.c_void_p(_stream_ptr(stream, q_offsets.device)))
+        keep = (q_tokens, q_offsets, match_len, chosen, stream)
+
+        def launch() -> None:
+            st = fn(*args)
+            if st != PR_OK:
+                _check(st)
+
+        launch.buffers = keep
+        return launch
+
     def route_select(self, q_tokens, q_offsets, eligible=None, local_peer: int = -1, prefer_local: bool = False,
                      match_len=None, best=None, second=None, want_match_len: bool = True,
                      want_second: bool = True, stream=None) -> Tuple:

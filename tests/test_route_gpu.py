@@ -193,3 +193,35 @@ def test_config4_long_context_full_batch():
     o = oracle_for(w.snapshot, w.num_peers)
     m_or, c_or = o.route_seqset(w.queries, idx, nthreads())
     assert_rows_equal(m, c, m_or, c_or, idx, "config 4 sample")
+
+
+def test_route_launcher_matches_oracle():
+    """The pre-checked launcher (the timed loop's launch path) writes the same
+    outputs as the oracle, call after call, on two query batches."""
+    import torch
+    w = W.make_config(1)
+    P = w.num_peers
+    f = _forest(w.snapshot, P)
+    o = oracle_for(w.snapshot, P)
+    m_or, c_or = o.route(w.queries.tokens, w.queries.offsets, nthreads())
+    qt, qo = to_dev(w.queries)
+    half = w.queries.subset(np.arange(len(w.queries) // 2))
+    ht, ho = to_dev(half)
+    nq, nh = len(w.queries), len(half)
+    ml = torch.full((nq, P), -7, dtype=torch.int32, device=device())
+    ch = torch.full((nq,), -7, dtype=torch.int32, device=device())
+    mh = torch.full((nh, P), -7, dtype=torch.int32, device=device())
+    chh = torch.full((nh,), -7, dtype=torch.int32, device=device())
+    la = f.route_launcher(qt, qo, ml, ch)
+    lb = f.route_launcher(ht, ho, mh, chh)
+    announce("route launcher")
+    for _ in range(3):
+        la()
+        lb()
+    torch.cuda.synchronize()
+    assert_rows_equal(ml.cpu().numpy(), ch.cpu().numpy(), m_or, c_or, what="launcher full batch")
+    assert_rows_equal(mh.cpu().numpy(), chh.cpu().numpy(), m_or[:nh], c_or[:nh], what="launcher half batch")
+    with pytest.raises(ValueError):
+        f.route_launcher(qt, qo, mh, ch)
+    f.close()
+    o.close()

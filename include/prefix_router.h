@@ -25,7 +25,11 @@
  *     whose match length is the largest (so an all-zero row chooses peer 0).
  *   - Single writer: calls on one forest must be serialised by the caller
  *     (each tree has one writer, paper Section 1).  pr_route only reads the
- *     forest.
+ *     forest; calls that update it (merge, loads, touch, eviction, compaction)
+ *     change the device image in place, so a route still queued on another
+ *     stream must be ordered before them (the same stream, or an event).  When
+ *     they move the image (growth, rebuild) they wait for the whole device
+ *     before freeing the old arrays.
  *   - Device calls (pr_merge, pr_route) take device pointers and a HIP stream
  *     (NULL = the legacy default stream) and are ordered on that stream after
  *     the work already queued there.  pr_route returns without waiting for the

@@ -236,6 +236,13 @@ pr_status ensure_capacity(pr_forest *f, int64_t need_nodes, int64_t need_pool, h
             return fail(PR_ENOMEM, "hipMalloc failed while growing the forest");
         }
         const int64_t n = d.n_nodes;
+        auto free_new = [&]() {
+            dfree(f, &nn, cap);
+            dfree(f, &nt, cap);
+            dfree(f, &ns, cap);
+            dfree(f, &nm, cap * (f->W - 1));
+            dfree(f, &mv, cap);
+        };
         if (hipMemcpyAsync(nn, d.nodes, n * sizeof(Node), hipMemcpyDeviceToDevice, s) != hipSuccess ||
             hipMemcpyAsync(nt, d.ntok, n * sizeof(int32_t), hipMemcpyDeviceToDevice, s) != hipSuccess ||
             hipMemcpyAsync(ns, d.nsep, n * sizeof(int32_t), hipMemcpyDeviceToDevice, s) != hipSuccess ||
@@ -243,22 +250,26 @@ pr_status ensure_capacity(pr_forest *f, int64_t need_nodes, int64_t need_pool, h
                                         s) != hipSuccess) ||
             hipMemcpyAsync(mv, d.moved, d.cap_nodes * sizeof(long long), hipMemcpyDeviceToDevice, s) != hipSuccess ||
             hipMemsetAsync(mv + d.cap_nodes, 0, (cap - d.cap_nodes) * sizeof(long long), s) != hipSuccess ||
-            hipStreamSynchronize(s) != hipSuccess)
+            hipStreamSynchronize(s) != hipSuccess) {
+            free_new();
             return fail(PR_EDEVICE, "device copy failed while growing the forest");
-        if (d.ltime) {
-            unsigned long long *lt = nullptr;
-            if (!dalloc(f, &lt, cap) ||
-                hipMemcpyAsync(lt, d.ltime, n * sizeof(unsigned long long), hipMemcpyDeviceToDevice, s) !=
-                    hipSuccess ||
-                hipStreamSynchronize(s) != hipSuccess) {
-                dfree(f, &lt, cap);
-                dfree(f, &nn, cap);
-                dfree(f, &nt, cap);
-                dfree(f, &ns, cap);
-                dfree(f, &nm, cap * (f->W - 1));
-                dfree(f, &mv, cap);
-                return fail(PR_ENOMEM, "growing the access times failed");
-            }
+        }
+        unsigned long long *lt = nullptr;
+        if (d.ltime && (!dalloc(f, &lt, cap) ||
+                        hipMemcpyAsync(lt, d.ltime, n * sizeof(unsigned long long), hipMemcpyDeviceToDevice, s) !=
+                            hipSuccess ||
+                        hipStreamSynchronize(s) != hipSuccess)) {
+            dfree(f, &lt, cap);
+            free_new();
+            return fail(PR_ENOMEM, "growing the access times failed");
+        }
+        // a route launched earlier on another stream may still read the old arrays
+        if (hipDeviceSynchronize() != hipSuccess) {
+            dfree(f, &lt, cap);
+            free_new();
+            return fail(PR_EDEVICE, "hipDeviceSynchronize failed while growing the forest");
+        }
+        if (lt) {
             dfree(f, &d.ltime, d.cap_nodes);
             d.ltime = lt;
         }
@@ -280,8 +291,10 @@ pr_status ensure_capacity(pr_forest *f, int64_t need_nodes, int64_t need_pool, h
         int32_t *np = nullptr;
         if (!dalloc(f, &np, cap)) return fail(PR_ENOMEM, "hipMalloc failed while growing the label pool");
         if (hipMemcpyAsync(np, d.pool, d.n_pool * sizeof(int32_t), hipMemcpyDeviceToDevice, s) != hipSuccess ||
-            hipStreamSynchronize(s) != hipSuccess)
+            hipStreamSynchronize(s) != hipSuccess || hipDeviceSynchronize() != hipSuccess) {
+            dfree(f, &np, cap);
             return fail(PR_EDEVICE, "device copy failed while growing the label pool");
+        }
         dfree(f, &d.pool, d.cap_pool);
         d.pool = np;
         d.cap_pool = cap;

@@ -15,9 +15,13 @@
 // sequence goes on, a leaf with the winner's remaining tokens.  Otherwise the
 // round adds leaves: ADD inserts are radix-sorted by (x, next token); per slot
 // the lowest batch index wins, and one wave per node x writes a new, sorted
-// child block holding x's old children and one leaf per winning slot.  Records
-// that move are stamped with their new position so that a parent rebuilt in
-// the same round can be pointed at its new block wherever its record lives.
+// child block holding x's old children and one leaf per winning slot.  The
+// round is data-parallel however the inserts crowd on one parent: scans over
+// the sorted entries give every winner its slot and label span, one thread per
+// parent allocates its block, one wave per 64 old children moves them, and one
+// wave per winner writes its leaf.  Records that move are stamped with their
+// new position so that a parent rebuilt in the same round can be pointed at its
+// new block wherever its record lives.
 // Losers walk again in the next round and find the structure the winners
 // built.  When every insert is DONE, a last pass ORs each insert's peer bit
 // into the mask of every node on its path.  The match function afterwards is
@@ -55,6 +59,7 @@ struct MergeCounters {
     unsigned long long overflow;  // allocations refused for lack of capacity
     unsigned long long skipped;   // inserts with invalid peer or offsets
     unsigned long long bad_path;  // mask pass found a sequence not ending at a node
+    unsigned long long move_chunks;  // add round: 64-child chunks of the old blocks that move
 };
 
 struct DevForest {
@@ -291,33 +296,6 @@ __global__ void add_keys_kernel(Batch B, const InsState *st, unsigned long long 
 
 __device__ __forceinline__ int32_t key_parent(unsigned long long k) { return (int32_t)(k >> 32); }
 
-// For each group of sorted ADD entries with one parent: the records its new
-// child block needs (old children + one leaf per distinct token).
-// The group's winners (first entry of each distinct key) are compacted, in
-// token order, to win_tok / win_ins [k, k + nw) for the build kernel.
-__global__ void add_count_kernel(DevForest F, const unsigned long long *keys, const int32_t *vals, int64_t n_add,
-                                 const InsState *st, Batch B, int32_t *grp_nw, int32_t *win_tok, int32_t *win_ins,
-                                 MergeCounters *ctr) {
-    const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (k >= n_add) return;
-    if (k > 0 && key_parent(keys[k - 1]) == key_parent(keys[k])) return;  // not a group head
-    const int32_t x = key_parent(keys[k]);
-    int32_t nw = 0;
-    unsigned long long pool = 0;
-    for (int64_t e = k; e < n_add && key_parent(keys[e]) == x; e++) {
-        if (e == k || keys[e] != keys[e - 1]) {
-            const int32_t i = vals[e];
-            win_tok[k + nw] = st[i].t;
-            win_ins[k + nw] = i;
-            pool += (unsigned long long)(B.offsets[i + 1] - B.offsets[i] - st[i].d);
-            nw++;
-        }
-    }
-    grp_nw[k] = nw;
-    atomicAdd(&ctr->node_need, (unsigned long long)(F.nodes[x].ct_cnt + nw));
-    atomicAdd(&ctr->pool_need, pool);
-}
-
 // Number of entries of the sorted int32 array a[0..n) that are < v.
 __device__ __forceinline__ int32_t lower_count(const int32_t *a, int32_t n, int32_t v) {
     int32_t lo = 0, hi = n;
@@ -331,78 +309,143 @@ __device__ __forceinline__ int32_t lower_count(const int32_t *a, int32_t n, int3
     return lo;
 }
 
-// One wave per group head: write the parent's new child block.
-__global__ __launch_bounds__(64 *kMergeWavesPerBlock) void add_build_kernel(
-    DevForest F, Batch B, const unsigned long long *keys, int64_t n_add, const InsState *st,
-    const int32_t *grp_nw, const int32_t *win_tok, const int32_t *win_ins, int32_t *grp_nb, long long stamp,
-    MergeCounters *ctr) {
-    const int lane = (int)(threadIdx.x & 63);
-    const int64_t k = m_wave_index();
-    if (k >= n_add) return;
-    if (k > 0 && key_parent(keys[k - 1]) == key_parent(keys[k])) return;  // not a group head
-    const int32_t x = key_parent(keys[k]);
-    const int32_t nw = grp_nw[k];
-    const Node nx = F.nodes[x];
-    const int32_t old_cnt = nx.ct_cnt, old_beg = nx.ct_beg;
-    const int32_t cnt = old_cnt + nw;
-    // label tokens of all leaves of the group, allocated in one span
-    int64_t group_pool = 0;
-    for (int32_t w = 0; w < nw; w++) {
-        const int32_t i = win_ins[k + w];
-        group_pool += B.offsets[i + 1] - B.offsets[i] - st[i].d;
+__device__ __forceinline__ bool add_is_head(const unsigned long long *keys, int64_t e) {
+    return e == 0 || key_parent(keys[e - 1]) != key_parent(keys[e]);
+}
+
+// ADD round, step 1 (one thread per sorted ADD entry e, plus one): the slot
+// winner flag (first entry of each (parent, token) key) and the winner's label
+// tokens; the entry index if e heads its parent's group (else -1, for a max
+// scan); per group head the 64-child chunks of the parent's old block.
+__global__ void add_mark_kernel(DevForest F, Batch B, const unsigned long long *keys, const int32_t *vals,
+                                int64_t n_add, const InsState *st, int32_t *win, int64_t *rest, int32_t *headv,
+                                int32_t *nch) {
+    const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (e == n_add) nch[n_add] = 0;  // the chunk scan's total lands at n_add
+    if (e >= n_add) return;
+    const bool head = add_is_head(keys, e);
+    const bool w = e == 0 || keys[e] != keys[e - 1];
+    const int32_t i = vals[e];
+    win[e] = w ? 1 : 0;
+    rest[e] = w ? B.offsets[i + 1] - B.offsets[i] - st[i].d : 0;
+    headv[e] = head ? (int32_t)e : -1;
+    nch[e] = head ? (F.nodes[key_parent(keys[e])].ct_cnt + 63) / 64 : 0;
+}
+
+// Step 2 (one thread per entry; widx, poff: exclusive scans of win, rest; hd:
+// the entry's group head; cstart: exclusive scan of nch).  Winners go to
+// win_tok / win_ins [k + w] of their group (head k, ordinal w, token order),
+// and the last entry of each group records the group's winner count and label
+// tokens and counts the records it needs.
+__global__ void add_group_kernel(DevForest F, const unsigned long long *keys, const int32_t *vals, int64_t n_add,
+                                 const InsState *st, const int32_t *win, const int64_t *rest, const int32_t *widx,
+                                 const int64_t *poff, const int32_t *hd, const int32_t *cstart, int32_t *grp_nw,
+                                 int64_t *grp_pool, int32_t *win_tok, int32_t *win_ins, MergeCounters *ctr) {
+    const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (e >= n_add) return;
+    const int32_t k = hd[e];
+    if (win[e]) {
+        const int32_t w = widx[e] - widx[k];
+        win_tok[k + w] = st[vals[e]].t;
+        win_ins[k + w] = vals[e];
     }
-    const int64_t nb = (int64_t)wave_atomic_add(&ctr->n_nodes, (unsigned long long)cnt, lane);
-    const int64_t pb0 = (int64_t)wave_atomic_add(&ctr->n_pool, (unsigned long long)group_pool, lane);
-    if (nb + cnt > F.cap_nodes || pb0 + group_pool > F.cap_pool) {
-        // nothing written: the parent keeps its old, consistent block
-        if (lane == 0) {
-            atomicAdd(&ctr->overflow, 1ull);
-            grp_nb[k] = -1;
-        }
+    if (e + 1 < n_add && !add_is_head(keys, e + 1)) return;  // not the group's last entry
+    const int32_t nw = widx[e] + win[e] - widx[k];
+    const int64_t pool = poff[e] + rest[e] - poff[k];
+    grp_nw[k] = nw;
+    grp_pool[k] = pool;
+    atomicAdd(&ctr->node_need, (unsigned long long)(F.nodes[key_parent(keys[e])].ct_cnt + nw));
+    atomicAdd(&ctr->pool_need, (unsigned long long)pool);
+    if (e == n_add - 1) ctr->move_chunks = (unsigned long long)cstart[n_add];
+}
+
+// Step 3 (one thread per group head): records and label tokens of the new
+// block, or grp_nb = -1 (nothing is written; the parent keeps its old,
+// consistent block) when the capacity runs out.
+__global__ void add_alloc_kernel(DevForest F, const unsigned long long *keys, int64_t n_add, const int32_t *grp_nw,
+                                 const int64_t *grp_pool, int32_t *grp_nb, int64_t *grp_pb, MergeCounters *ctr) {
+    const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (k >= n_add || !add_is_head(keys, k)) return;
+    const int32_t cnt = F.nodes[key_parent(keys[k])].ct_cnt + grp_nw[k];
+    const int64_t nb = (int64_t)atomicAdd(&ctr->n_nodes, (unsigned long long)cnt);
+    const int64_t pb = (int64_t)atomicAdd(&ctr->n_pool, (unsigned long long)grp_pool[k]);
+    if (nb + cnt > F.cap_nodes || pb + grp_pool[k] > F.cap_pool) {
+        atomicAdd(&ctr->overflow, 1ull);
+        grp_nb[k] = -1;
         return;
     }
-    // old children keep their order; each moves up by the winners below it
-    for (int32_t j = lane; j < old_cnt; j += 64) {
-        const int32_t src = old_beg + j;
-        const int64_t dst = nb + j + lower_count(win_tok + k, nw, F.ntok[src]);
-        F.nodes[dst] = F.nodes[src];
-        F.ntok[dst] = F.ntok[src];
-        if (F.ltime) F.ltime[dst] = F.ltime[src];
-        F.moved[src] = (stamp << 32) | (long long)(uint32_t)dst;
+    grp_nb[k] = (int32_t)nb;
+    grp_pb[k] = pb;
+}
+
+// Step 4 (one wave per 64-child chunk of every rebuilt parent's old block):
+// old children keep their order, each moving up by the winners below it, and
+// are stamped with their new position.
+__global__ __launch_bounds__(64 *kMergeWavesPerBlock) void add_move_kernel(
+    DevForest F, const unsigned long long *keys, int64_t n_add, const int32_t *cstart, int64_t n_chunks,
+    const int32_t *grp_nw, const int32_t *grp_nb, const int32_t *win_tok, long long stamp) {
+    const int lane = (int)(threadIdx.x & 63);
+    const int64_t c = m_wave_index();
+    if (c >= n_chunks) return;
+    // the group whose chunks hold c: cstart[k] <= c < cstart[k + 1]
+    int64_t lo = 0, hi = n_add;
+    while (lo < hi) {
+        const int64_t mid = (lo + hi) >> 1;
+        if (cstart[mid] <= c)
+            lo = mid + 1;
+        else
+            hi = mid;
     }
-    if (F.W > 1)
-        for (int32_t j = 0; j < old_cnt; j++) {
-            const int32_t src = old_beg + j;
-            const int64_t dst = nb + j + lower_count(win_tok + k, nw, F.ntok[src]);
-            copy_mext(F, dst, src, lane);
-        }
-    // one leaf per winner, holding the rest of its sequence
-    int64_t pb = pb0;
-    for (int32_t w = 0; w < nw; w++) {
-        const int32_t i = win_ins[k + w];
-        const int32_t *s = B.tokens + B.offsets[i];
-        const int64_t len = B.offsets[i + 1] - B.offsets[i];
-        const int32_t d = st[i].d;
-        const int64_t rest = len - d;  // >= 1: an ADD insert has a next token
-        const int64_t dst = nb + w + lower_count(F.ntok + old_beg, old_cnt, win_tok[k + w]);
-        copy_tokens(F.pool + pb, s + d, rest, lane);
-        zero_mext(F, dst, lane);
-        if (lane == 0) {
-            Node leaf;
-            leaf.tok = s[d];
-            leaf.lab_off = (uint32_t)pb;
-            leaf.lab_len = (int32_t)rest;
-            leaf.ct_beg = 0;
-            leaf.ct_cnt = 0;
-            leaf.aux = 0;
-            leaf.mask0 = 0ull;
-            F.nodes[dst] = leaf;
-            F.ntok[dst] = leaf.tok;
-            if (F.ltime) F.ltime[dst] = 0ull;
-        }
-        pb += rest;
+    const int64_t k = lo - 1;
+    const int32_t nb = grp_nb[k];
+    if (nb < 0) return;
+    const Node nx = F.nodes[key_parent(keys[k])];
+    const int32_t j = (int32_t)(c - cstart[k]) * 64 + lane;
+    if (j >= nx.ct_cnt) return;
+    const int32_t src = nx.ct_beg + j;
+    const int64_t dst = nb + j + lower_count(win_tok + k, grp_nw[k], F.ntok[src]);
+    F.nodes[dst] = F.nodes[src];
+    F.ntok[dst] = F.ntok[src];
+    if (F.ltime) F.ltime[dst] = F.ltime[src];
+    for (int w = 0; w < F.W - 1; w++) F.mext[dst * (F.W - 1) + w] = F.mext[(int64_t)src * (F.W - 1) + w];
+    F.moved[src] = (stamp << 32) | (long long)(uint32_t)dst;
+}
+
+// Step 5 (one wave per winning entry): the leaf holding the rest of the
+// winner's sequence, in its token's slot among the parent's children.
+__global__ __launch_bounds__(64 *kMergeWavesPerBlock) void add_leaf_kernel(
+    DevForest F, Batch B, const unsigned long long *keys, const int32_t *vals, int64_t n_add, const InsState *st,
+    const int32_t *win, const int32_t *widx, const int64_t *poff, const int32_t *hd, const int32_t *grp_nb,
+    const int64_t *grp_pb) {
+    const int lane = (int)(threadIdx.x & 63);
+    const int64_t e = m_wave_index();
+    if (e >= n_add || !win[e]) return;
+    const int32_t k = hd[e];
+    const int32_t nb = grp_nb[k];
+    if (nb < 0) return;
+    const int32_t i = vals[e];
+    const Node nx = F.nodes[key_parent(keys[e])];
+    const int32_t *s = B.tokens + B.offsets[i];
+    const int64_t len = B.offsets[i + 1] - B.offsets[i];
+    const int32_t d = st[i].d;
+    const int64_t rest = len - d;  // >= 1: an ADD insert has a next token
+    const int64_t dst = nb + (widx[e] - widx[k]) + lower_count(F.ntok + nx.ct_beg, nx.ct_cnt, s[d]);
+    const int64_t pb = grp_pb[k] + (poff[e] - poff[k]);
+    copy_tokens(F.pool + pb, s + d, rest, lane);
+    zero_mext(F, dst, lane);
+    if (lane == 0) {
+        Node leaf;
+        leaf.tok = s[d];
+        leaf.lab_off = (uint32_t)pb;
+        leaf.lab_len = (int32_t)rest;
+        leaf.ct_beg = 0;
+        leaf.ct_cnt = 0;
+        leaf.aux = 0;
+        leaf.mask0 = 0ull;
+        F.nodes[dst] = leaf;
+        F.ntok[dst] = leaf.tok;
+        if (F.ltime) F.ltime[dst] = 0ull;
     }
-    if (lane == 0) grp_nb[k] = (int32_t)nb;
 }
 
 // Separators of every rebuilt wide block (runs after the build, before the

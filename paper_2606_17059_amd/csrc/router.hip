@@ -60,6 +60,9 @@ struct MergeScratch {
     unsigned long long *keys_in = nullptr, *keys_out = nullptr;
     int32_t *vals_in = nullptr, *vals_out = nullptr;
     int32_t *grp_nw = nullptr, *grp_nb = nullptr, *win_tok = nullptr, *win_ins = nullptr;
+    // add rounds: per sorted entry (cap + 1 entries)
+    int32_t *win = nullptr, *widx = nullptr, *headv = nullptr, *hd = nullptr, *nch = nullptr, *cstart = nullptr;
+    int64_t *rest = nullptr, *poff = nullptr, *grp_pool = nullptr, *grp_pb = nullptr;
     int64_t cap = 0;
     void *sort_tmp = nullptr;
     size_t sort_tmp_bytes = 0;
@@ -184,6 +187,21 @@ void free_export_scratch(pr_forest *f) {
     X = ExportScratch();
 }
 
+void free_add_scratch(pr_forest *f) {
+    MergeScratch &m = f->ms;
+    const int64_t c = m.cap + 1;
+    dfree(f, &m.win, c);
+    dfree(f, &m.widx, c);
+    dfree(f, &m.headv, c);
+    dfree(f, &m.hd, c);
+    dfree(f, &m.nch, c);
+    dfree(f, &m.cstart, c);
+    dfree(f, &m.rest, c);
+    dfree(f, &m.poff, c);
+    dfree(f, &m.grp_pool, c);
+    dfree(f, &m.grp_pb, c);
+}
+
 void free_scratch(pr_forest *f) {
     MergeScratch &m = f->ms;
     dfree(f, &m.st, m.cap);
@@ -195,6 +213,7 @@ void free_scratch(pr_forest *f) {
     dfree(f, &m.grp_nb, m.cap);
     dfree(f, &m.win_tok, m.cap);
     dfree(f, &m.win_ins, m.cap);
+    free_add_scratch(f);
     if (m.sort_tmp) (void)hipFree(m.sort_tmp);
     f->device_bytes -= (int64_t)m.sort_tmp_bytes;
     dfree(f, &m.load_tok, m.load_tok_cap);
@@ -401,19 +420,41 @@ pr_status ensure_merge_scratch(pr_forest *f, int64_t n, hipStream_t s) {
         dfree(f, &m.grp_nb, m.cap);
         dfree(f, &m.win_tok, m.cap);
         dfree(f, &m.win_ins, m.cap);
+        free_add_scratch(f);
         m.cap = 0;
+        const int64_t c1 = cap + 1;
         if (!dalloc(f, &m.st, cap) || !dalloc(f, &m.keys_in, cap) || !dalloc(f, &m.keys_out, cap) ||
             !dalloc(f, &m.vals_in, cap) || !dalloc(f, &m.vals_out, cap) || !dalloc(f, &m.grp_nw, cap) ||
-            !dalloc(f, &m.grp_nb, cap) || !dalloc(f, &m.win_tok, cap) || !dalloc(f, &m.win_ins, cap)) {
+            !dalloc(f, &m.grp_nb, cap) || !dalloc(f, &m.win_tok, cap) || !dalloc(f, &m.win_ins, cap) ||
+            !dalloc(f, &m.win, c1) || !dalloc(f, &m.widx, c1) || !dalloc(f, &m.headv, c1) ||
+            !dalloc(f, &m.hd, c1) || !dalloc(f, &m.nch, c1) || !dalloc(f, &m.cstart, c1) ||
+            !dalloc(f, &m.rest, c1) || !dalloc(f, &m.poff, c1) || !dalloc(f, &m.grp_pool, c1) ||
+            !dalloc(f, &m.grp_pb, c1)) {
+            m.cap = cap;  // so that free_scratch releases the add arrays by their size
             free_scratch(f);
             return fail(PR_ENOMEM, "hipMalloc failed for merge scratch");
         }
         m.cap = cap;
     }
-    size_t need = 0;
+    // one temporary buffer serves the sort and the add round's scans
+    size_t need = 0, q = 0;
     if (rocprim::radix_sort_pairs(nullptr, need, m.keys_in, m.keys_out, m.vals_in, m.vals_out, n, 0, 64, s) !=
         hipSuccess)
         return fail(PR_EDEVICE, "radix sort size query failed");
+    if (rocprim::exclusive_scan(nullptr, q, m.win, m.widx, 0, (size_t)n, rocprim::plus<int32_t>(), s) != hipSuccess)
+        return fail(PR_EDEVICE, "scan size query failed");
+    need = std::max(need, q);
+    if (rocprim::exclusive_scan(nullptr, q, m.rest, m.poff, (int64_t)0, (size_t)n, rocprim::plus<int64_t>(), s) !=
+        hipSuccess)
+        return fail(PR_EDEVICE, "scan size query failed");
+    need = std::max(need, q);
+    if (rocprim::inclusive_scan(nullptr, q, m.headv, m.hd, (size_t)n, rocprim::maximum<int32_t>(), s) != hipSuccess)
+        return fail(PR_EDEVICE, "scan size query failed");
+    need = std::max(need, q);
+    if (rocprim::exclusive_scan(nullptr, q, m.nch, m.cstart, 0, (size_t)n + 1, rocprim::plus<int32_t>(), s) !=
+        hipSuccess)
+        return fail(PR_EDEVICE, "scan size query failed");
+    need = std::max(need, q);
     if (need > m.sort_tmp_bytes) {
         if (m.sort_tmp) (void)hipFree(m.sort_tmp);
         f->device_bytes -= (int64_t)m.sort_tmp_bytes;
@@ -434,6 +475,7 @@ __global__ void reset_round_kernel(pr::MergeCounters *c) {
     c->n_split = 0;
     c->pool_need = 0;
     c->node_need = 0;
+    c->move_chunks = 0;
 }
 
 __global__ void reset_call_kernel(pr::MergeCounters *c) {
@@ -444,6 +486,7 @@ __global__ void reset_call_kernel(pr::MergeCounters *c) {
     c->overflow = 0;
     c->skipped = 0;
     c->bad_path = 0;
+    c->move_chunks = 0;
 }
 
 __global__ void add_skipped_kernel(unsigned long long *acc, const pr::MergeCounters *c) { *acc += c->skipped; }
@@ -511,17 +554,43 @@ pr_status run_merge(pr_forest *f, const int32_t *peer_of, const int32_t *tokens,
             if (rocprim::radix_sort_pairs(m.sort_tmp, tmp, m.keys_in, m.keys_out, m.vals_in, m.vals_out, n, 0, 64,
                                           s) != hipSuccess)
                 return fail(PR_EDEVICE, "radix sort failed");
+            // winners, group heads and chunks; their scans; per-group totals
+            hipLaunchKernelGGL(pr::add_mark_kernel, dim3(grid_threads(n_add + 1, bs)), dim3(bs), 0, s, dev_view(f),
+                               B, m.keys_out, m.vals_out, n_add, m.st, m.win, m.rest, m.headv, m.nch);
+            size_t t1 = m.sort_tmp_bytes;
+            if (rocprim::exclusive_scan(m.sort_tmp, t1, m.win, m.widx, 0, (size_t)n_add, rocprim::plus<int32_t>(),
+                                        s) != hipSuccess)
+                return fail(PR_EDEVICE, "add scan failed");
+            t1 = m.sort_tmp_bytes;
+            if (rocprim::exclusive_scan(m.sort_tmp, t1, m.rest, m.poff, (int64_t)0, (size_t)n_add,
+                                        rocprim::plus<int64_t>(), s) != hipSuccess)
+                return fail(PR_EDEVICE, "add scan failed");
+            t1 = m.sort_tmp_bytes;
+            if (rocprim::inclusive_scan(m.sort_tmp, t1, m.headv, m.hd, (size_t)n_add, rocprim::maximum<int32_t>(),
+                                        s) != hipSuccess)
+                return fail(PR_EDEVICE, "add scan failed");
+            t1 = m.sort_tmp_bytes;
+            if (rocprim::exclusive_scan(m.sort_tmp, t1, m.nch, m.cstart, 0, (size_t)n_add + 1,
+                                        rocprim::plus<int32_t>(), s) != hipSuccess)
+                return fail(PR_EDEVICE, "add scan failed");
             hipLaunchKernelGGL(reset_round_kernel, dim3(1), dim3(1), 0, s, f->d_ctr);
-            hipLaunchKernelGGL(pr::add_count_kernel, dim3(grid_threads(n_add, bs)), dim3(bs), 0, s, dev_view(f),
-                               m.keys_out, m.vals_out, n_add, m.st, B, m.grp_nw, m.win_tok, m.win_ins, f->d_ctr);
+            hipLaunchKernelGGL(pr::add_group_kernel, dim3(grid_threads(n_add, bs)), dim3(bs), 0, s, dev_view(f),
+                               m.keys_out, m.vals_out, n_add, m.st, m.win, m.rest, m.widx, m.poff, m.hd, m.cstart,
+                               m.grp_nw, m.grp_pool, m.win_tok, m.win_ins, f->d_ctr);
             if ((r = read_counters(f, &c, s))) return r;
             if ((r = ensure_capacity(f, (int64_t)c.n_nodes + (int64_t)c.node_need,
                                      (int64_t)c.n_pool + (int64_t)c.pool_need, s)))
                 return r;
             const long long stamp = ++f->stamp;
             const pr::DevForest F = dev_view(f);
-            hipLaunchKernelGGL(pr::add_build_kernel, dim3(grid_waves(n_add)), dim3(wb), 0, s, F, B, m.keys_out,
-                               n_add, m.st, m.grp_nw, m.win_tok, m.win_ins, m.grp_nb, stamp, f->d_ctr);
+            const int64_t chunks = (int64_t)c.move_chunks;
+            hipLaunchKernelGGL(pr::add_alloc_kernel, dim3(grid_threads(n_add, bs)), dim3(bs), 0, s, F, m.keys_out,
+                               n_add, m.grp_nw, m.grp_pool, m.grp_nb, m.grp_pb, f->d_ctr);
+            if (chunks > 0)
+                hipLaunchKernelGGL(pr::add_move_kernel, dim3(grid_waves(chunks)), dim3(wb), 0, s, F, m.keys_out,
+                                   n_add, m.cstart, chunks, m.grp_nw, m.grp_nb, m.win_tok, stamp);
+            hipLaunchKernelGGL(pr::add_leaf_kernel, dim3(grid_waves(n_add)), dim3(wb), 0, s, F, B, m.keys_out,
+                               m.vals_out, n_add, m.st, m.win, m.widx, m.poff, m.hd, m.grp_nb, m.grp_pb);
             hipLaunchKernelGGL(pr::add_sep_kernel, dim3(grid_waves(n_add)), dim3(wb), 0, s, F, m.keys_out, n_add,
                                m.grp_nw, m.grp_nb);
             hipLaunchKernelGGL(pr::add_fix_kernel, dim3(grid_threads(n_add, bs)), dim3(bs), 0, s, F, m.keys_out,

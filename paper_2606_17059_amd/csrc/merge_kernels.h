@@ -120,16 +120,32 @@ __device__ __forceinline__ int64_t m_lcp(const int32_t *a, const int32_t *b, int
     return n;
 }
 
-// Child of node x whose first token is t, or -1 (wave-cooperative scan).
+// Child of node x whose first token is t, or -1 (wave-cooperative).  Blocks
+// of up to 64 children take one ballot over their first tokens; wider blocks
+// first pick their sub-range through the block's 64 separators.
 __device__ __forceinline__ int32_t m_find_child(const DevForest &F, const Node &x, int32_t t, int lane) {
-    for (int32_t base = 0; base < x.ct_cnt; base += 64) {
-        const int32_t j = base + lane;
-        bool eq = false;
-        if (j < x.ct_cnt) eq = F.ntok[x.ct_beg + j] == t;
-        const uint64_t b = __ballot(eq);
-        if (b) return x.ct_beg + base + (int32_t)(__ffsll((unsigned long long)b) - 1);
+    const int32_t beg = x.ct_beg, cnt = x.ct_cnt;
+    if (cnt <= kSepCount) {
+        const uint64_t b = __ballot(lane < cnt && F.ntok[beg + lane] == t);
+        return b ? beg + (int32_t)(__ffsll((unsigned long long)b) - 1) : -1;
     }
-    return -1;
+    // separators ascend, so the lanes with sep <= t form a prefix
+    const uint64_t b = __ballot(F.nsep[beg + lane] <= t);
+    if (!b) return -1;  // t is below every first token
+    const int32_t k = (int32_t)__popcll(b) - 1;
+    int32_t lo = PR_SEP_INDEX(k, cnt);
+    int32_t hi = k == kSepCount - 1 ? cnt : PR_SEP_INDEX(k + 1, cnt);
+    while (hi - lo > 64) {  // sub-ranges of more than 64 children: 64-ary search
+        const int32_t stride = (hi - lo + 63) / 64;
+        const int32_t j = lo + lane * stride;
+        const uint64_t bl = __ballot(j < hi && F.ntok[beg + j] <= t);
+        if (!bl) return -1;
+        lo = lo + (__popcll(bl) - 1) * stride;
+        hi = min(lo + stride, hi);
+    }
+    const int32_t j = lo + lane;
+    const uint64_t be = __ballot(j < hi && F.ntok[beg + j] == t);
+    return be ? beg + lo + (int32_t)(__ffsll((unsigned long long)be) - 1) : -1;
 }
 
 __global__ void merge_validate_kernel(Batch B, InsState *st, MergeCounters *ctr) {
@@ -187,15 +203,47 @@ __global__ __launch_bounds__(64 *kMergeWavesPerBlock) void merge_walk_kernel(Dev
     }
     r.x = x;
     r.d = (int32_t)d;
-    if (lane == 0) {
-        st[i] = r;
-        if (r.kind == kInsAdd) {
-            atomicAdd(&ctr->n_add, 1ull);
-            atomicAdd(&ctr->pool_need, (unsigned long long)(len - d));
-        } else if (r.kind == kInsSplit) {
-            atomicAdd(&ctr->n_split, 1ull);
-            atomicAdd(&ctr->pool_need, (unsigned long long)(len - d));
+    if (lane == 0) st[i] = r;  // merge_tally_kernel counts the kinds
+}
+
+// Counts of the walk's ADD and SPLIT inserts and the pool tokens they may
+// need, reduced per block before one atomic each: per-insert atomics on the
+// same counters would serialise.
+constexpr int kTallyThreads = 256;
+__global__ __launch_bounds__(kTallyThreads) void merge_tally_kernel(Batch B, const InsState *st,
+                                                                    MergeCounters *ctr) {
+    __shared__ unsigned long long part[3][kTallyThreads / 64];
+    unsigned long long n_add = 0, n_split = 0, pool = 0;
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < B.n; i += (int64_t)gridDim.x * blockDim.x) {
+        const int32_t kind = st[i].kind;
+        if (kind == kInsAdd || kind == kInsSplit) {
+            n_add += kind == kInsAdd;
+            n_split += kind == kInsSplit;
+            pool += (unsigned long long)(B.offsets[i + 1] - B.offsets[i] - st[i].d);
         }
+    }
+    for (int off = 32; off >= 1; off >>= 1) {
+        n_add += __shfl_xor(n_add, off);
+        n_split += __shfl_xor(n_split, off);
+        pool += __shfl_xor(pool, off);
+    }
+    const int wv = (int)(threadIdx.x / 64);
+    if ((threadIdx.x & 63) == 0) {
+        part[0][wv] = n_add;
+        part[1][wv] = n_split;
+        part[2][wv] = pool;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        unsigned long long a = 0, b = 0, c = 0;
+        for (int k = 0; k < kTallyThreads / 64; k++) {
+            a += part[0][k];
+            b += part[1][k];
+            c += part[2][k];
+        }
+        if (a) atomicAdd(&ctr->n_add, a);
+        if (b) atomicAdd(&ctr->n_split, b);
+        if (c) atomicAdd(&ctr->pool_need, c);
     }
 }
 
@@ -498,11 +546,13 @@ __global__ __launch_bounds__(64 *kMergeWavesPerBlock) void merge_mask_kernel(Dev
     int64_t d = 0;
     while (true) {
         if (lane == 0) {
-            if (w == 0)
-                atomicOr((unsigned long long *)&F.nodes[x].mask0, bit);
-            else
-                atomicOr((unsigned long long *)&F.mext[(int64_t)x * (F.W - 1) + (w - 1)], bit);
-            if (stamp) atomicMax(&F.ltime[x], F.now);
+            // bits only get set during the pass, so a bit already seen set
+            // needs no atomic (nodes near the root are on almost every path)
+            unsigned long long *mw =
+                w == 0 ? (unsigned long long *)&F.nodes[x].mask0 : (unsigned long long *)&F.mext[(int64_t)x * (F.W - 1) + (w - 1)];
+            if (!(__hip_atomic_load(mw, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & bit)) atomicOr(mw, bit);
+            if (stamp && __hip_atomic_load(&F.ltime[x], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < F.now)
+                atomicMax(&F.ltime[x], F.now);
         }
         if (d == len) break;
         const Node nx = F.nodes[x];

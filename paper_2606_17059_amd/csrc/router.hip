@@ -537,6 +537,9 @@ pr_status run_merge(pr_forest *f, const int32_t *peer_of, const int32_t *tokens,
         hipLaunchKernelGGL(reset_round_kernel, dim3(1), dim3(1), 0, s, f->d_ctr);
         hipLaunchKernelGGL(pr::merge_walk_kernel, dim3(grid_waves(n)), dim3(wb), 0, s, dev_view(f), B, m.st,
                            f->d_ctr);
+        hipLaunchKernelGGL(pr::merge_tally_kernel,
+                           dim3((unsigned)std::min<int64_t>(256, (n + pr::kTallyThreads - 1) / pr::kTallyThreads)),
+                           dim3(pr::kTallyThreads), 0, s, B, m.st, f->d_ctr);
         if ((r = read_counters(f, &c, s))) return r;
         if (c.overflow) break;  // reported below; the forest stays consistent
         if (c.n_split > 0) {

@@ -239,8 +239,7 @@ pr_status ensure_capacity(pr_forest *f, int64_t need_nodes, int64_t need_pool, h
     if (need_pool > (int64_t)UINT32_MAX) return fail(PR_ENOMEM, "label pool would exceed 2^32 tokens");
     if (need_nodes > (int64_t)INT32_MAX) return fail(PR_ENOMEM, "node count would exceed 2^31");
     if (need_nodes > d.cap_nodes) {
-        const int64_t cap = std::min<int64_t>(std::max<int64_t>(need_nodes, d.cap_nodes + d.cap_nodes / 2),
-                                              (int64_t)INT32_MAX);
+        const int64_t cap = std::min<int64_t>(std::max<int64_t>(need_nodes, 2 * d.cap_nodes), (int64_t)INT32_MAX);
         Node *nn = nullptr;
         int32_t *nt = nullptr, *ns = nullptr;
         uint64_t *nm = nullptr;
@@ -350,8 +349,10 @@ pr_status commit(pr_forest *f) {
     const pr::HostImage &h = f->host_img;
     DevImage &d = f->dev;
     const int64_t n = (int64_t)h.nodes.size(), np = (int64_t)h.pool.size();
-    d.cap_nodes = std::max<int64_t>(n + n / 8, 1024);
-    d.cap_pool = std::max<int64_t>(np + np / 8, 4096);
+    // merges append records (rebuilt blocks move), so node capacity starts at
+    // twice the image; labels grow only by new leaves
+    d.cap_nodes = std::max<int64_t>(2 * n, 1024);
+    d.cap_pool = std::max<int64_t>(np + np / 4, 4096);
     if (!dalloc(f, &d.nodes, d.cap_nodes) || !dalloc(f, &d.ntok, d.cap_nodes) || !dalloc(f, &d.nsep, d.cap_nodes) ||
         !dalloc(f, &d.mext, d.cap_nodes * (f->W - 1)) || !dalloc(f, &d.moved, d.cap_nodes) ||
         !dalloc(f, &d.pool, d.cap_pool)) {

@@ -61,22 +61,32 @@ __global__ __launch_bounds__(64 * kExportWavesPerBlock) void export_level_kernel
     const int32_t beg = F.nodes[x].ct_beg, cnt = F.nodes[x].ct_cnt;
     const int64_t dx = depth[x];
     bool found = false;
-    for (int32_t j = lane; j < cnt; j += 64) {
-        const int32_t c = beg + j;
-        if (c < 0 || c >= n_nodes) continue;
-        if (node_holds(F, c, p)) {
+    // slots are taken with one atomic per wave and 64 children: atomics on
+    // one counter serialise
+    const uint64_t below = (1ull << lane) - 1ull;
+    for (int32_t base = 0; base < cnt; base += 64) {
+        const int32_t c = beg + base + lane;
+        const bool h = base + lane < cnt && c >= 0 && c < n_nodes && node_holds(F, c, p);
+        const uint64_t b = __ballot(h);
+        if (!b) continue;
+        found = true;
+        const int32_t n = (int32_t)__popcll(b);
+        int32_t s0 = 0, k0 = 0;
+        if (lane == 0) {
+            s0 = atomicAdd(&counts[0], n);
+            if (all) k0 = atomicAdd(&counts[2], n);
+        }
+        s0 = __shfl(s0, 0);
+        k0 = __shfl(k0, 0);
+        if (h) {
+            const int32_t r = (int32_t)__popcll(b & below);
             depth[c] = dx + F.nodes[c].lab_len;
             parent[c] = x;
-            const int32_t slot = atomicAdd(&counts[0], 1);
-            if (slot < n_nodes) next[slot] = c;
-            if (all) {
-                const int32_t k = atomicAdd(&counts[2], 1);
-                if (k < n_nodes) all[k] = c;
-            }
-            found = true;
+            if (s0 + r < n_nodes) next[s0 + r] = c;
+            if (all && k0 + r < n_nodes) all[k0 + r] = c;
         }
     }
-    if (__ballot(found) == 0 && x != 0 && lane == 0) {
+    if (!found && x != 0 && lane == 0) {
         const int32_t slot = atomicAdd(&counts[1], 1);
         if (slot < n_nodes) leaves[slot] = x;
     }
@@ -112,11 +122,14 @@ __global__ __launch_bounds__(64 * kExportWavesPerBlock) void export_write_kernel
     }
 }
 
-// Tokens a peer's tree holds: the label lengths of the nodes the walk visited.
+// Tokens a peer's tree holds: the label lengths of the nodes the walk visited
+// (a wave sum, then one atomic per wave).
 __global__ void tree_tokens_kernel(DevForest F, const int32_t *__restrict__ all, int32_t V,
                                    unsigned long long *__restrict__ out) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < V) atomicAdd(out, (unsigned long long)F.nodes[all[i]].lab_len);
+    unsigned long long v = i < V ? (unsigned long long)F.nodes[all[i]].lab_len : 0ull;
+    for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
+    if ((threadIdx.x & 63) == 0 && v) atomicAdd(out, v);
 }
 
 }  // namespace pr

@@ -143,6 +143,20 @@ __global__ void lru_plan_kernel(const unsigned long long *__restrict__ keys, con
     *plan = p;
 }
 
+// Slot in a list shared by every wave: one atomic per wave (atomics on one
+// counter serialise), ranks by ballot.  Called by every active lane; returns
+// -1 for lanes that take no slot.
+__device__ __forceinline__ int32_t lru_wave_slot(int32_t *ctr, bool want) {
+    const uint64_t b = __ballot(want);
+    if (!b) return -1;
+    const int lane = (int)(threadIdx.x & 63);
+    const int leader = __ffsll((unsigned long long)b) - 1;
+    int32_t base = 0;
+    if (lane == leader) base = atomicAdd(ctr, (int32_t)__popcll(b));
+    base = __shfl(base, leader);
+    return want ? base + (int32_t)__popcll(b & ((1ull << lane) - 1ull)) : -1;
+}
+
 // The local peer leaves the first a nodes in time order.
 __global__ void lru_clear_sorted_kernel(DevForest F, const int32_t *__restrict__ vals, int64_t a) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -153,7 +167,9 @@ __global__ void lru_clear_sorted_kernel(DevForest F, const int32_t *__restrict__
 __global__ void lru_maxdepth_kernel(const int32_t *__restrict__ vals, int64_t a, int64_t b,
                                     const int64_t *__restrict__ depth, EvictPlan *plan) {
     const int64_t i = a + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < b) atomicMax(&plan->maxd, (int32_t)depth[vals[i]]);
+    int32_t m = i < b ? (int32_t)depth[vals[i]] : 0;
+    for (int off = 32; off >= 1; off >>= 1) m = max(m, __shfl_xor(m, off));
+    if ((threadIdx.x & 63) == 0 && m > 0) atomicMax(&plan->maxd, m);
 }
 
 // Difference array of the class's token depths: a node covers depths
@@ -196,7 +212,8 @@ __global__ void lru_level_nodes_kernel(DevForest F, const int32_t *__restrict__ 
     if (i >= b) return;
     const int32_t v = vals[i];
     const int64_t e = depth[v], s = e - F.nodes[v].lab_len + 1;
-    if (s <= plan->depth && plan->depth <= e) level[atomicAdd(n_level, 1)] = v;
+    const int32_t k = lru_wave_slot(n_level, s <= plan->depth && plan->depth <= e);
+    if (k >= 0) level[k] = v;
 }
 
 // Is the path through u lexicographically before the path through v?  u and
@@ -243,10 +260,9 @@ __global__ void lru_apply_kernel(DevForest F, const int32_t *__restrict__ vals, 
         keep = rank_of[v] < plan->r_at ? D - 1 : D;
     else
         keep = s > D ? s - 1 : e;
-    if (keep < s) {
-        lru_clear(F, v, F.local);
-    } else if (keep < e) {
-        const int32_t k = atomicAdd(n_cut, 1);
+    if (keep < s) lru_clear(F, v, F.local);
+    const int32_t k = lru_wave_slot(n_cut, keep >= s && keep < e);
+    if (k >= 0) {
         cut_node[k] = v;
         cut_len1[k + 1] = keep;
     }

@@ -97,6 +97,7 @@ struct pr_forest {
     DevImage dev;
     bool has_dev = false;
     pr::MergeCounters *d_ctr = nullptr;
+    void *h_stage = nullptr;      // pinned host staging for the small readbacks between device rounds
     unsigned long long *d_skipped = nullptr;  // inputs skipped by device calls
     MergeScratch ms;
     ExportScratch xs;
@@ -132,6 +133,8 @@ class DeviceScope {
     bool ok_ = true;
     bool switched_ = false;
 };
+
+constexpr size_t kStageBytes = 256;  // pinned readback staging per forest
 
 unsigned grid_threads(int64_t n, int bs) { return (unsigned)((n + bs - 1) / bs); }
 unsigned grid_waves(int64_t n) { return (unsigned)((n + pr::kMergeWavesPerBlock - 1) / pr::kMergeWavesPerBlock); }
@@ -239,7 +242,10 @@ pr_status ensure_capacity(pr_forest *f, int64_t need_nodes, int64_t need_pool, h
     if (need_pool > (int64_t)UINT32_MAX) return fail(PR_ENOMEM, "label pool would exceed 2^32 tokens");
     if (need_nodes > (int64_t)INT32_MAX) return fail(PR_ENOMEM, "node count would exceed 2^31");
     if (need_nodes > d.cap_nodes) {
-        const int64_t cap = std::min<int64_t>(std::max<int64_t>(need_nodes, 2 * d.cap_nodes), (int64_t)INT32_MAX);
+        // rebuilt child blocks append records with every add round, so node
+        // arrays grow fourfold: each growth (allocate, copy, wait for the
+        // device, free) costs milliseconds of host time
+        const int64_t cap = std::min<int64_t>(std::max<int64_t>(need_nodes, 4 * d.cap_nodes), (int64_t)INT32_MAX);
         Node *nn = nullptr;
         int32_t *nt = nullptr, *ns = nullptr;
         uint64_t *nm = nullptr;
@@ -340,6 +346,10 @@ pr_status commit(pr_forest *f) {
     if (s) return s;
     if (!f->d_skipped) {
         if (!dalloc(f, &f->d_skipped, 1) || !dalloc(f, &f->d_ctr, 1)) return fail(PR_ENOMEM, "hipMalloc failed");
+        if (!f->h_stage && hipHostMalloc(&f->h_stage, kStageBytes, hipHostMallocDefault) != hipSuccess) {
+            f->h_stage = nullptr;
+            return fail(PR_ENOMEM, "hipHostMalloc failed for the readback staging");
+        }
         if (hipMemset(f->d_skipped, 0, sizeof(unsigned long long)) != hipSuccess)
             return fail(PR_EDEVICE, "hipMemset failed");
     }
@@ -350,8 +360,9 @@ pr_status commit(pr_forest *f) {
     DevImage &d = f->dev;
     const int64_t n = (int64_t)h.nodes.size(), np = (int64_t)h.pool.size();
     // merges append records (rebuilt blocks move), so node capacity starts at
-    // twice the image; labels grow only by new leaves
-    d.cap_nodes = std::max<int64_t>(2 * n, 1024);
+    // four times the image (a few merge batches before the first growth);
+    // labels grow only by new leaves
+    d.cap_nodes = std::max<int64_t>(4 * n, 1024);
     d.cap_pool = std::max<int64_t>(np + np / 4, 4096);
     if (!dalloc(f, &d.nodes, d.cap_nodes) || !dalloc(f, &d.ntok, d.cap_nodes) || !dalloc(f, &d.nsep, d.cap_nodes) ||
         !dalloc(f, &d.mext, d.cap_nodes * (f->W - 1)) || !dalloc(f, &d.moved, d.cap_nodes) ||
@@ -494,10 +505,22 @@ __global__ void add_skipped_kernel(unsigned long long *acc, const pr::MergeCount
 
 // Read the device counters and refresh the host mirror of the used sizes
 // (growing the arrays copies exactly the used part).
-pr_status read_counters(pr_forest *f, pr::MergeCounters *c, hipStream_t s) {
-    if (hipMemcpyAsync(c, f->d_ctr, sizeof(*c), hipMemcpyDeviceToHost, s) != hipSuccess ||
+// Copy `bytes` (<= kStageBytes) of device memory to the host through the
+// forest's pinned staging buffer (a direct DMA, no pageable bounce) and wait.
+bool read_small(pr_forest *f, void *out, const void *dsrc, size_t bytes, hipStream_t s) {
+    if (bytes > kStageBytes || !f->h_stage) return false;
+    if (hipMemcpyAsync(f->h_stage, dsrc, bytes, hipMemcpyDeviceToHost, s) != hipSuccess ||
         hipStreamSynchronize(s) != hipSuccess)
-        return fail(PR_EDEVICE, "reading merge counters failed");
+        return false;
+    std::memcpy(out, f->h_stage, bytes);
+    return true;
+}
+
+static_assert(sizeof(pr::MergeCounters) <= kStageBytes && sizeof(pr::EvictPlan) <= kStageBytes,
+              "readbacks fit the staging buffer");
+
+pr_status read_counters(pr_forest *f, pr::MergeCounters *c, hipStream_t s) {
+    if (!read_small(f, c, f->d_ctr, sizeof(*c), s)) return fail(PR_EDEVICE, "reading merge counters failed");
     f->dev.n_nodes = (int64_t)c->n_nodes;
     f->dev.n_pool = (int64_t)c->n_pool;
     return PR_OK;
@@ -685,8 +708,7 @@ pr_status walk_peer(pr_forest *f, int32_t peer, bool want_all, hipStream_t s, in
                            dim3(wb), 0, s, F, nn, peer, X.front, n_front, X.next, X.leaves, X.depth, X.parent,
                            X.counts, want_all ? X.all : nullptr);
         if (hipGetLastError() != hipSuccess) return fail(PR_EDEVICE, "tree walk launch failed");
-        if (hipMemcpyAsync(counts, X.counts, 3 * sizeof(int32_t), hipMemcpyDeviceToHost, s) != hipSuccess ||
-            hipStreamSynchronize(s) != hipSuccess)
+        if (!read_small(f, counts, X.counts, 3 * sizeof(int32_t), s))
             return fail(PR_EDEVICE, "tree walk readback failed");
         if (counts[0] > nn || counts[1] > nn || counts[2] > nn)
             return fail(PR_EDEVICE, "tree walk visited more nodes than exist");
@@ -739,8 +761,7 @@ pr_status export_impl(pr_forest *f, int32_t peer, int32_t *tokens, int64_t token
         if (rocprim::inclusive_scan(X.tmp, t2, X.len1 + 1, X.offs + 1, (size_t)n_leaves, rocprim::plus<int64_t>(),
                                     s) != hipSuccess)
             return fail(PR_EDEVICE, "export scan failed");
-        if (hipMemcpyAsync(&total, X.offs + n_leaves, sizeof(total), hipMemcpyDeviceToHost, s) != hipSuccess ||
-            hipStreamSynchronize(s) != hipSuccess)
+        if (!read_small(f, &total, X.offs + n_leaves, sizeof(total), s))
             return fail(PR_EDEVICE, "export readback failed");
     }
     *num_seqs = n_leaves;
@@ -820,6 +841,7 @@ void pr_forest_destroy(pr_forest *f) {
         free_scratch(f);
         dfree(f, &f->d_skipped, 1);
         dfree(f, &f->d_ctr, 1);
+        if (f->h_stage) (void)hipHostFree(f->h_stage);
     }
     delete f;
 }
@@ -1017,8 +1039,7 @@ pr_status pr_forest_compact(pr_forest *f, int64_t *nodes_before, int64_t *nodes_
             hipSuccess)
             return fail_dev("compaction scan failed");
         int64_t total = 0;
-        if (hipMemcpyAsync(&total, start1 + n_front, sizeof(total), hipMemcpyDeviceToHost, s) != hipSuccess ||
-            hipStreamSynchronize(s) != hipSuccess)
+        if (!read_small(f, &total, start1 + n_front, sizeof(total), s))
             return fail_dev("compaction readback failed");
         // live nodes are distinct old records: more than n_old means a malformed forest
         if (total < 0 || first_new + total > n_old) return fail_dev("compaction found more live nodes than exist");
@@ -1050,8 +1071,7 @@ pr_status pr_forest_compact(pr_forest *f, int64_t *nodes_before, int64_t *nodes_
     if (rocprim::inclusive_scan(tmp2, need2, len1, off, (size_t)n_new + 1, rocprim::plus<int64_t>(), s) != hipSuccess)
         return fail_dev("compaction scan failed");
     int64_t n_pool = 0;
-    if (hipMemcpyAsync(&n_pool, off + n_new, sizeof(n_pool), hipMemcpyDeviceToHost, s) != hipSuccess ||
-        hipStreamSynchronize(s) != hipSuccess)
+    if (!read_small(f, &n_pool, off + n_new, sizeof(n_pool), s))
         return fail_dev("compaction readback failed");
     if (n_pool > (int64_t)UINT32_MAX) return fail_dev("compacted label pool exceeds 2^32 tokens");
     nw.cap_pool = std::min<int64_t>(std::max<int64_t>(n_pool + n_pool / 8, 4096), (int64_t)UINT32_MAX);
@@ -1109,8 +1129,7 @@ pr_status pr_tree_tokens(pr_forest *f, int32_t peer, int64_t *tokens, void *hip_
     if (hipMemsetAsync(d, 0, sizeof(h), s) != hipSuccess) return fail(PR_EDEVICE, "hipMemsetAsync failed");
     hipLaunchKernelGGL(pr::tree_tokens_kernel, dim3(grid_threads(counts[2], 256)), dim3(256), 0, s, dev_view(f),
                        f->xs.all, counts[2], d);
-    if (hipGetLastError() != hipSuccess || hipMemcpyAsync(&h, d, sizeof(h), hipMemcpyDeviceToHost, s) != hipSuccess ||
-        hipStreamSynchronize(s) != hipSuccess)
+    if (hipGetLastError() != hipSuccess || !read_small(f, &h, d, sizeof(h), s))
         return fail(PR_EDEVICE, "tree size failed");
     *tokens = (int64_t)h;
     return ok();
@@ -1186,8 +1205,7 @@ pr_status pr_touch(pr_forest *f, const int32_t *q_tokens, int64_t num_tokens, co
         hipSuccess)
         return fail(PR_EDEVICE, "touch scan failed");
     int64_t total = 0;
-    if (hipMemcpyAsync(&total, toff + num_queries, sizeof(total), hipMemcpyDeviceToHost, s) != hipSuccess ||
-        hipStreamSynchronize(s) != hipSuccess)
+    if (!read_small(f, &total, toff + num_queries, sizeof(total), s))
         return fail(PR_EDEVICE, "touch readback failed");
     if (!X.get(&ttok, total)) return fail(PR_ENOMEM, "hipMalloc failed for the touch");
     hipLaunchKernelGGL(pr::touch_gather_kernel, dim3((unsigned)((num_queries + 3) / 4)), dim3(256), 0, s, q_tokens,
@@ -1254,8 +1272,7 @@ pr_status pr_evict_lru(pr_forest *f, int64_t max_tokens, int64_t *evicted, void 
         return fail_dev("eviction scan failed");
     hipLaunchKernelGGL(pr::lru_plan_kernel, dim3(1), dim3(1), 0, s, keys_s, cum, V, max_tokens, d_plan);
     pr::EvictPlan plan;
-    if (hipMemcpyAsync(&plan, d_plan, sizeof(plan), hipMemcpyDeviceToHost, s) != hipSuccess ||
-        hipStreamSynchronize(s) != hipSuccess)
+    if (!read_small(f, &plan, d_plan, sizeof(plan), s))
         return fail_dev("eviction readback failed");
     const int64_t n_evict = std::min<int64_t>(max_tokens, plan.total);
     if (plan.a > 0)
@@ -1265,8 +1282,7 @@ pr_status pr_evict_lru(pr_forest *f, int64_t max_tokens, int64_t *evicted, void 
         const int64_t a = plan.a, b = plan.b, nc = b - a;
         hipLaunchKernelGGL(pr::lru_maxdepth_kernel, dim3(grid_threads(nc, 256)), dim3(256), 0, s, vals_s, a, b,
                            W.depth, d_plan);
-        if (hipMemcpyAsync(&plan, d_plan, sizeof(plan), hipMemcpyDeviceToHost, s) != hipSuccess ||
-            hipStreamSynchronize(s) != hipSuccess)
+        if (!read_small(f, &plan, d_plan, sizeof(plan), s))
             return fail_dev("eviction readback failed");
         const int32_t maxd = plan.maxd;
         long long *hist = nullptr, *cnt = nullptr, *rev = nullptr, *S = nullptr;
@@ -1302,8 +1318,7 @@ pr_status pr_evict_lru(pr_forest *f, int64_t max_tokens, int64_t *evicted, void 
         hipLaunchKernelGGL(pr::lru_level_nodes_kernel, dim3(grid_threads(nc, 256)), dim3(256), 0, s, F, vals_s, a, b,
                            W.depth, d_plan, level, n_level);
         int32_t h_level = 0;
-        if (hipMemcpyAsync(&h_level, n_level, sizeof(h_level), hipMemcpyDeviceToHost, s) != hipSuccess ||
-            hipStreamSynchronize(s) != hipSuccess)
+        if (!read_small(f, &h_level, n_level, sizeof(h_level), s))
             return fail_dev("eviction readback failed");
         if (h_level > nc) return fail_dev("eviction level list overflow");
         hipLaunchKernelGGL(pr::lru_rank_kernel, dim3(grid_threads(h_level, 256)), dim3(256), 0, s, F, level, h_level,
@@ -1312,8 +1327,7 @@ pr_status pr_evict_lru(pr_forest *f, int64_t max_tokens, int64_t *evicted, void 
                            W.depth, rank_of, d_plan, cut_node, cut_len1, n_cut);
         int32_t h_cut = 0;
         if (hipGetLastError() != hipSuccess ||
-            hipMemcpyAsync(&h_cut, n_cut, sizeof(h_cut), hipMemcpyDeviceToHost, s) != hipSuccess ||
-            hipStreamSynchronize(s) != hipSuccess)
+            !read_small(f, &h_cut, n_cut, sizeof(h_cut), s))
             return fail_dev("eviction failed");
         if (h_cut > 0) {
             int64_t *offs = nullptr, *old_len = nullptr;
@@ -1330,9 +1344,7 @@ pr_status pr_evict_lru(pr_forest *f, int64_t max_tokens, int64_t *evicted, void 
                 hipSuccess)
                 return fail_dev("eviction scan failed");
             int64_t total_cut = 0;
-            if (hipMemcpyAsync(&total_cut, offs + h_cut, sizeof(total_cut), hipMemcpyDeviceToHost, s) !=
-                    hipSuccess ||
-                hipStreamSynchronize(s) != hipSuccess)
+            if (!read_small(f, &total_cut, offs + h_cut, sizeof(total_cut), s))
                 return fail_dev("eviction readback failed");
             if (!X.get(&ctok, total_cut)) return fail(PR_ENOMEM, "hipMalloc failed for the eviction");
             hipLaunchKernelGGL(pr::lru_cut_paths_kernel, dim3((unsigned)((h_cut + 3) / 4)), dim3(256), 0, s, F,
@@ -1349,8 +1361,7 @@ pr_status pr_evict_lru(pr_forest *f, int64_t max_tokens, int64_t *evicted, void 
             }
             hipLaunchKernelGGL(pr::lru_clear_lower_kernel, dim3(grid_threads(h_cut, 256)), dim3(256), 0, s,
                                dev_view(f), cut_node, h_cut, offs, W.depth, old_len, d_plan);
-            if (hipMemcpyAsync(&plan, d_plan, sizeof(plan), hipMemcpyDeviceToHost, s) != hipSuccess ||
-                hipStreamSynchronize(s) != hipSuccess)
+            if (!read_small(f, &plan, d_plan, sizeof(plan), s))
                 return fail_dev("eviction readback failed");
             if (plan.bad) return fail_dev("eviction split left an unexpected structure; destroy the forest");
         }

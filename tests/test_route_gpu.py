@@ -225,3 +225,52 @@ def test_route_launcher_matches_oracle():
         f.route_launcher(qt, qo, mh, ch)
     f.close()
     o.close()
+
+
+def test_deep_paths():
+    """Every prefix of a 300-token sequence ends a stored sequence of some peer,
+    so a walk passes 300 one-token edges whose peer sets change along the way;
+    queries stop at every kind of point along it."""
+    rng = np.random.default_rng(7)
+    s = rng.integers(0, 5, 300).astype(np.int32)
+    P = 4
+    seqs, owners = [], []
+    for L in range(1, 301):
+        seqs.append(s[:L].tolist())
+        owners.append(L % P if L % 7 else 0)
+    snap = W.from_lists(seqs, owners)
+    qs = [s.tolist(), s[:150].tolist(), s[:8].tolist(), s[:9].tolist(), []]
+    for cut in (1, 7, 8, 9, 16, 17, 64, 65, 299):
+        q = s.copy()
+        q[cut] = (q[cut] + 1) % 5  # mismatch inside the walk
+        qs.append(q.tolist())
+    qs.append(s.tolist() + [1, 2, 3])  # longer than every stored sequence
+    queries = W.from_lists(qs)
+    f = _forest(snap, P)
+    o = oracle_for(snap, P)
+    m_or, c_or = o.route(queries.tokens, queries.offsets, 2)
+    m, c = gpu_route(f, queries, "deep path")
+    assert_rows_equal(m, c, m_or, c_or, what="deep path")
+    f.close()
+
+
+def test_invalid_offsets_between_valid_queries():
+    """Queries with bad offsets get rows of -1 wherever they sit in a batch;
+    their neighbours are routed normally."""
+    import torch
+    from paper_2606_17059_amd import Forest
+    dev = device()
+    f = Forest(3)
+    f.load_snapshot(0, np.array([1, 2, 3, 4, 5], np.int32), np.array([0, 5]))
+    f.load_snapshot(2, np.array([1, 2, 9], np.int32), np.array([0, 3]))
+    toks = torch.tensor([1, 2, 3, 4, 1, 2, 9, 9], dtype=torch.int32, device=dev)
+    # offsets 0,4,2,7,99 and 99,-1,3,8 give the queries [0,4) ok, [4,2) bad,
+    # [2,7) ok, [7,99) bad, then [99,-1) bad, [-1,3) bad, [3,8) ok
+    offs = [0, 4, 2, 7, 99, -1, 3, 8]
+    exp_m = [[4, 0, 2], [-1] * 3, [0, 0, 0], [-1] * 3, [-1] * 3, [-1] * 3, [0, 0, 0]]
+    exp_c = [0, -1, 0, -1, -1, -1, 0]
+    o = torch.tensor(offs, dtype=torch.int64, device=dev)
+    announce("invalid offsets between valid queries")
+    m, c = f.route(toks, o)
+    assert m.cpu().numpy().tolist() == exp_m and c.cpu().numpy().tolist() == exp_c
+    f.close()

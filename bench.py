@@ -68,6 +68,16 @@ def cpu_threads() -> int:
     return max(1, min(16, n))
 
 
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(w, queries, target_s: float):
     """Time the CPU oracle, as it stands, on a bounded sample of the same batch."""
     import oracle
@@ -88,9 +98,17 @@ def cpu_baseline(w, queries, target_s: float):
         if dt >= 0.25 * target_s or n >= len(queries):
             break
         n = int(min(len(queries), max(2 * n, n * target_s / max(dt, 1e-3))))
+    # the same oracle on one thread, over a sample sized to about a fifth of the target time
+    n1 = max(1, min(n, int(n * 0.2 * target_s / max(dt * T, 1e-3))))
+    sub1 = queries.subset(np.sort(rng.choice(len(queries), n1, replace=False)))
+    t0 = time.perf_counter()
+    o.route(sub1.tokens, sub1.offsets, 1)
+    dt1 = time.perf_counter() - t0
     o.close()
     return {"value": n / dt, "unit": "queries/s", "cores": T, "kind": "oracle",
-            "sample": f"{n} of {len(queries)} queries drawn uniformly (seed 12345), {dt:.1f} s with {T} threads"}
+            "sample": f"{n} of {len(queries)} queries drawn uniformly (seed 12345), {dt:.1f} s with {T} threads",
+            "one_thread": {"value": n1 / dt1, "unit": "queries/s", "sample": f"{n1} queries, {dt1:.1f} s"},
+            "cpu_model": cpu_model()}
 
 
 def bench_stream(args, w, dev):
@@ -179,7 +197,8 @@ def bench_stream(args, w, dev):
                 cpu = {"value": n / dt, "unit": "queries/s", "cores": T, "kind": "oracle",
                        "sample": f"{n} of {nq} lookups of the first uniform round, {dt:.1f} s with {T} threads; "
                                  f"oracle merge of that round's {len(ins)} inserts: "
-                                 f"{len(ins) / o_merge_s:.0f} inserts/s (1 thread)"}
+                                 f"{len(ins) / o_merge_s:.0f} inserts/s (1 thread)",
+                       "cpu_model": cpu_model()}
                 log(f"[bench] cpu baseline: {cpu}")
             if args.compact and rnd == w.meta["rounds"] - 1:
                 compact_out.append(bench_compact(f, qt, qo, ml, ch, qs, args.steps, dist, float(km.mean())))

@@ -43,6 +43,9 @@ pr_status ok() {
 // Device arrays of the forest.  Node ids and pool offsets never move: growing
 // a capacity copies the arrays into larger ones.
 struct DevImage {
+    // nodes, ntok, nsep, mext and moved share one allocation (node_block)
+    void *node_block = nullptr;
+    size_t node_block_bytes = 0;
     Node *nodes = nullptr;
     int32_t *ntok = nullptr;
     int32_t *nsep = nullptr;
@@ -160,13 +163,53 @@ void dfree(pr_forest *f, T **p, int64_t count) {
     *p = nullptr;
 }
 
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// The per-node arrays of one capacity (records, first tokens, separators,
+// extra mask words, move stamps) in one device allocation, each 256-byte
+// aligned: growing the forest costs one hipMalloc and one hipFree instead of
+// one per array.  Sets d's array pointers and d.cap_nodes.
+bool alloc_node_arrays(pr_forest *f, DevImage &d, int64_t cap) {
+    const size_t c = (size_t)std::max<int64_t>(cap, 1);
+    const size_t o_ntok = align256(c * sizeof(Node));
+    const size_t o_nsep = o_ntok + align256(c * sizeof(int32_t));
+    const size_t o_mext = o_nsep + align256(c * sizeof(int32_t));
+    const size_t o_moved = o_mext + align256(std::max<size_t>(c * (size_t)(f->W - 1), 1) * sizeof(uint64_t));
+    const size_t bytes = o_moved + c * sizeof(long long);
+    void *b = nullptr;
+    if (hipMalloc(&b, bytes) != hipSuccess) {
+        (void)hipGetLastError();
+        return false;
+    }
+    f->device_bytes += (int64_t)bytes;
+    char *p = static_cast<char *>(b);
+    d.node_block = b;
+    d.node_block_bytes = bytes;
+    d.nodes = reinterpret_cast<Node *>(p);
+    d.ntok = reinterpret_cast<int32_t *>(p + o_ntok);
+    d.nsep = reinterpret_cast<int32_t *>(p + o_nsep);
+    d.mext = reinterpret_cast<uint64_t *>(p + o_mext);
+    d.moved = reinterpret_cast<long long *>(p + o_moved);
+    d.cap_nodes = (int64_t)c;
+    return true;
+}
+
+void free_node_arrays(pr_forest *f, DevImage &d) {
+    if (d.node_block) {
+        (void)hipFree(d.node_block);
+        f->device_bytes -= (int64_t)d.node_block_bytes;
+    }
+    d.node_block = nullptr;
+    d.node_block_bytes = 0;
+    d.nodes = nullptr;
+    d.ntok = d.nsep = nullptr;
+    d.mext = nullptr;
+    d.moved = nullptr;
+}
+
 void free_image(pr_forest *f) {
     DevImage &d = f->dev;
-    dfree(f, &d.nodes, d.cap_nodes);
-    dfree(f, &d.ntok, d.cap_nodes);
-    dfree(f, &d.nsep, d.cap_nodes);
-    dfree(f, &d.mext, d.cap_nodes * (f->W - 1));
-    dfree(f, &d.moved, d.cap_nodes);
+    free_node_arrays(f, d);
     dfree(f, &d.pool, d.cap_pool);
     dfree(f, &d.ltime, d.cap_nodes);
     d = DevImage();
@@ -246,68 +289,50 @@ pr_status ensure_capacity(pr_forest *f, int64_t need_nodes, int64_t need_pool, h
         // arrays grow fourfold: each growth (allocate, copy, wait for the
         // device, free) costs milliseconds of host time
         const int64_t cap = std::min<int64_t>(std::max<int64_t>(need_nodes, 4 * d.cap_nodes), (int64_t)INT32_MAX);
-        Node *nn = nullptr;
-        int32_t *nt = nullptr, *ns = nullptr;
-        uint64_t *nm = nullptr;
-        long long *mv = nullptr;
-        if (!dalloc(f, &nn, cap) || !dalloc(f, &nt, cap) || !dalloc(f, &ns, cap) ||
-            !dalloc(f, &nm, cap * (f->W - 1)) || !dalloc(f, &mv, cap)) {
-            dfree(f, &nn, cap);
-            dfree(f, &nt, cap);
-            dfree(f, &ns, cap);
-            dfree(f, &nm, cap * (f->W - 1));
-            dfree(f, &mv, cap);
-            return fail(PR_ENOMEM, "hipMalloc failed while growing the forest");
-        }
+        DevImage nd;
+        if (!alloc_node_arrays(f, nd, cap)) return fail(PR_ENOMEM, "hipMalloc failed while growing the forest");
         const int64_t n = d.n_nodes;
-        auto free_new = [&]() {
-            dfree(f, &nn, cap);
-            dfree(f, &nt, cap);
-            dfree(f, &ns, cap);
-            dfree(f, &nm, cap * (f->W - 1));
-            dfree(f, &mv, cap);
-        };
-        if (hipMemcpyAsync(nn, d.nodes, n * sizeof(Node), hipMemcpyDeviceToDevice, s) != hipSuccess ||
-            hipMemcpyAsync(nt, d.ntok, n * sizeof(int32_t), hipMemcpyDeviceToDevice, s) != hipSuccess ||
-            hipMemcpyAsync(ns, d.nsep, n * sizeof(int32_t), hipMemcpyDeviceToDevice, s) != hipSuccess ||
-            (f->W > 1 && hipMemcpyAsync(nm, d.mext, n * (f->W - 1) * sizeof(uint64_t), hipMemcpyDeviceToDevice,
+        if (hipMemcpyAsync(nd.nodes, d.nodes, n * sizeof(Node), hipMemcpyDeviceToDevice, s) != hipSuccess ||
+            hipMemcpyAsync(nd.ntok, d.ntok, n * sizeof(int32_t), hipMemcpyDeviceToDevice, s) != hipSuccess ||
+            hipMemcpyAsync(nd.nsep, d.nsep, n * sizeof(int32_t), hipMemcpyDeviceToDevice, s) != hipSuccess ||
+            (f->W > 1 && hipMemcpyAsync(nd.mext, d.mext, n * (f->W - 1) * sizeof(uint64_t), hipMemcpyDeviceToDevice,
                                         s) != hipSuccess) ||
-            hipMemcpyAsync(mv, d.moved, d.cap_nodes * sizeof(long long), hipMemcpyDeviceToDevice, s) != hipSuccess ||
-            hipMemsetAsync(mv + d.cap_nodes, 0, (cap - d.cap_nodes) * sizeof(long long), s) != hipSuccess ||
+            hipMemcpyAsync(nd.moved, d.moved, d.cap_nodes * sizeof(long long), hipMemcpyDeviceToDevice, s) !=
+                hipSuccess ||
+            hipMemsetAsync(nd.moved + d.cap_nodes, 0, (nd.cap_nodes - d.cap_nodes) * sizeof(long long), s) !=
+                hipSuccess ||
             hipStreamSynchronize(s) != hipSuccess) {
-            free_new();
+            free_node_arrays(f, nd);
             return fail(PR_EDEVICE, "device copy failed while growing the forest");
         }
         unsigned long long *lt = nullptr;
-        if (d.ltime && (!dalloc(f, &lt, cap) ||
+        if (d.ltime && (!dalloc(f, &lt, nd.cap_nodes) ||
                         hipMemcpyAsync(lt, d.ltime, n * sizeof(unsigned long long), hipMemcpyDeviceToDevice, s) !=
                             hipSuccess ||
                         hipStreamSynchronize(s) != hipSuccess)) {
-            dfree(f, &lt, cap);
-            free_new();
+            dfree(f, &lt, nd.cap_nodes);
+            free_node_arrays(f, nd);
             return fail(PR_ENOMEM, "growing the access times failed");
         }
         // a route launched earlier on another stream may still read the old arrays
         if (hipDeviceSynchronize() != hipSuccess) {
-            dfree(f, &lt, cap);
-            free_new();
+            dfree(f, &lt, nd.cap_nodes);
+            free_node_arrays(f, nd);
             return fail(PR_EDEVICE, "hipDeviceSynchronize failed while growing the forest");
         }
         if (lt) {
             dfree(f, &d.ltime, d.cap_nodes);
             d.ltime = lt;
         }
-        dfree(f, &d.nodes, d.cap_nodes);
-        dfree(f, &d.ntok, d.cap_nodes);
-        dfree(f, &d.nsep, d.cap_nodes);
-        dfree(f, &d.mext, d.cap_nodes * (f->W - 1));
-        dfree(f, &d.moved, d.cap_nodes);
-        d.nodes = nn;
-        d.ntok = nt;
-        d.nsep = ns;
-        d.mext = nm;
-        d.moved = mv;
-        d.cap_nodes = cap;
+        free_node_arrays(f, d);
+        d.node_block = nd.node_block;
+        d.node_block_bytes = nd.node_block_bytes;
+        d.nodes = nd.nodes;
+        d.ntok = nd.ntok;
+        d.nsep = nd.nsep;
+        d.mext = nd.mext;
+        d.moved = nd.moved;
+        d.cap_nodes = nd.cap_nodes;
     }
     if (need_pool > d.cap_pool) {
         const int64_t cap = std::min<int64_t>(std::max<int64_t>(need_pool, d.cap_pool + d.cap_pool / 2),
@@ -362,11 +387,8 @@ pr_status commit(pr_forest *f) {
     // merges append records (rebuilt blocks move), so node capacity starts at
     // four times the image (a few merge batches before the first growth);
     // labels grow only by new leaves
-    d.cap_nodes = std::max<int64_t>(4 * n, 1024);
     d.cap_pool = std::max<int64_t>(np + np / 4, 4096);
-    if (!dalloc(f, &d.nodes, d.cap_nodes) || !dalloc(f, &d.ntok, d.cap_nodes) || !dalloc(f, &d.nsep, d.cap_nodes) ||
-        !dalloc(f, &d.mext, d.cap_nodes * (f->W - 1)) || !dalloc(f, &d.moved, d.cap_nodes) ||
-        !dalloc(f, &d.pool, d.cap_pool)) {
+    if (!alloc_node_arrays(f, d, std::max<int64_t>(4 * n, 1024)) || !dalloc(f, &d.pool, d.cap_pool)) {
         free_image(f);
         return fail(PR_ENOMEM, "hipMalloc failed for the forest image");
     }
@@ -982,17 +1004,11 @@ pr_status pr_forest_compact(pr_forest *f, int64_t *nodes_before, int64_t *nodes_
     DevImage nw;
     nw.cap_nodes = std::max<int64_t>(n_old + n_old / 8, 1024);
     auto free_new = [&]() {
-        dfree(f, &nw.nodes, nw.cap_nodes);
-        dfree(f, &nw.ntok, nw.cap_nodes);
-        dfree(f, &nw.nsep, nw.cap_nodes);
-        dfree(f, &nw.mext, nw.cap_nodes * (f->W - 1));
-        dfree(f, &nw.moved, nw.cap_nodes);
         dfree(f, &nw.ltime, nw.cap_nodes);
         dfree(f, &nw.pool, nw.cap_pool);
+        free_node_arrays(f, nw);
     };
-    if (!dalloc(f, &nw.nodes, nw.cap_nodes) || !dalloc(f, &nw.ntok, nw.cap_nodes) ||
-        !dalloc(f, &nw.nsep, nw.cap_nodes) || !dalloc(f, &nw.mext, nw.cap_nodes * (f->W - 1)) ||
-        !dalloc(f, &nw.moved, nw.cap_nodes) || (d.ltime && !dalloc(f, &nw.ltime, nw.cap_nodes))) {
+    if (!alloc_node_arrays(f, nw, nw.cap_nodes) || (d.ltime && !dalloc(f, &nw.ltime, nw.cap_nodes))) {
         free_new();
         return fail(PR_ENOMEM, "hipMalloc failed for the compacted forest");
     }

@@ -55,6 +55,16 @@ def measured_traffic(workload: str):
     return rec["traffic_bytes_per_launch"] if rec.get("kernel_source_sha256_16") == sha else None
 
 
+def step_kernels(nq: int, ntok: int) -> list:
+    """Kernels one pr_route call launches (the library's rule: batches of more
+    than 8,192 and at most 65,536 queries averaging at least 4,096 tokens are
+    walked longest first, after two order launches).  kernel_ms is the time of
+    the whole call, so there it includes the order launches."""
+    if 8192 < nq <= 65536 and ntok >= 4096 * nq:
+        return ["route_order_count_kernel", "route_order_scatter_kernel", "route_kernel<W, false>"]
+    return ["route_kernel<W, false>"]
+
+
 def log(msg: str) -> None:
     sys.stderr.write(msg + "\n")
     sys.stderr.flush()
@@ -525,6 +535,7 @@ def main() -> int:
                      "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
                      "kernel": "route_kernel<W, false>", "kernel_ms": total_ms / K,
                      "kernel_ms_own_events": {"mean": float(kern_ms.mean()), "median": float(np.median(kern_ms))},
+                     "kernels_per_step": step_kernels(nq, int(qlen.sum())),
                      "algorithmic_bytes_per_launch": total_bytes},
         "cpu_baseline": cpu,
     }

@@ -129,9 +129,15 @@ pr_status pr_merge(pr_forest *f, const int32_t *peer_of, const int32_t *tokens,
  * A query whose offsets are outside [0, num_tokens], decreasing, or span more
  * than INT32_MAX tokens gets match_len -1 in every column and chosen -1.
  * num_queries == 0 is a no-op.  Reads the forest only.
+ * Batches of more than 8,192 and at most 65,536 queries averaging at least
+ * 4,096 tokens are walked longest first (a length bucketing on the stream
+ * before the walk; results are unchanged).  The order lives in a buffer the
+ * forest keeps: the first such call, or a larger batch, allocates it (after
+ * waiting for the previous user), and such calls on one forest are ordered on
+ * the device through an event even when issued on different streams.
  * Errors (host side, nothing enqueued): PR_EINVAL (NULL pointers with
  * num_queries > 0, negative counts), PR_ENOMEM / PR_EDEVICE (rebuild after a
- * snapshot load failed).
+ * snapshot load failed, or the order buffer could not be allocated).
  */
 pr_status pr_route(pr_forest *f, const int32_t *q_tokens, int64_t num_tokens,
                    const int64_t *q_offsets, int64_t num_queries, int32_t *match_len,

@@ -334,11 +334,14 @@ __attribute__((amdgpu_waves_per_eu(PR_ROUTE_WAVES_PER_EU))) void route_kernel(
     const uint64_t *__restrict__ mext,
     const int32_t *__restrict__ pool, const int32_t *__restrict__ qtok, int64_t num_tokens,
     const int64_t *__restrict__ qoff, int64_t nq, int32_t P, const Select sel_in, int32_t *__restrict__ match_len,
-    int32_t *__restrict__ chosen) {
+    int32_t *__restrict__ chosen, const int32_t *__restrict__ order) {
     const Select sel = SEL ? sel_in : Select{nullptr, -1, 0, nullptr};
     const int lane = (int)(threadIdx.x & (kWave - 1));
-    const int64_t q = (int64_t)blockIdx.x * kRouteWavesPerBlock + uniform((int32_t)(threadIdx.x / kWave));
-    if (q >= nq) return;
+    const int64_t slot = (int64_t)blockIdx.x * kRouteWavesPerBlock + uniform((int32_t)(threadIdx.x / kWave));
+    if (slot >= nq) return;
+    // order (optional) is a permutation of the queries: the dispatcher starts
+    // slots in index order, so slot i serves query order[i]
+    const int64_t q = order ? (int64_t)order[slot] : slot;
     int32_t *row = match_len + q * (int64_t)P;
     const int64_t qb = qoff[q], qe = qoff[q + 1];
     if (qb < 0 || qe < qb || qe > num_tokens || qe - qb > (int64_t)INT32_MAX) {
@@ -432,6 +435,137 @@ __attribute__((amdgpu_waves_per_eu(PR_ROUTE_WAVES_PER_EU))) void route_kernel(
     if (lane == 0) {
         chosen[q] = best;
         if (sel.second) sel.second[q] = second;
+    }
+}
+
+// Longest-first order of a batch, a counting sort in two launches of a few
+// workgroups: every query gets a length bucket (unit tokens wide, the last
+// one open-ended), and order lists the queries by bucket, longest bucket
+// first.  Within a bucket the order is fixed by the layout below, so it is
+// deterministic.  Offsets are not checked here (a bad pair lands in some
+// bucket); the route kernel checks every query's offsets itself.
+constexpr int kOrderThreads = 1024;
+constexpr int kOrderWaves = kOrderThreads / kWave;
+constexpr int kOrderPerThread = 4;
+constexpr int kOrderChunk = kOrderThreads * kOrderPerThread;  // queries per workgroup
+constexpr int kOrderBuckets = 16;
+constexpr int kOrderMaxBlocks = 16;
+constexpr int32_t kOrderMaxQueries = kOrderChunk * kOrderMaxBlocks;  // 65,536
+
+// Query i of thread t in workgroup b: base + i * kOrderThreads + t.
+__device__ __forceinline__ int32_t order_query(int b, int i, int t) {
+    return b * kOrderChunk + i * kOrderThreads + t;
+}
+
+// Launch 1: each query's bucket, and each workgroup's bucket counts.
+__global__ __launch_bounds__(kOrderThreads) void route_order_count_kernel(const int64_t *__restrict__ qoff,
+                                                                          int32_t nq, uint32_t unit,
+                                                                          uint8_t *__restrict__ bkt,
+                                                                          int32_t *__restrict__ blockcnt) {
+    __shared__ int32_t cnt[kOrderWaves][kOrderBuckets];
+    const int t = (int)threadIdx.x, lane = t & (kWave - 1), wv = t / kWave, b = (int)blockIdx.x;
+    int64_t lo[kOrderPerThread], hi[kOrderPerThread];
+#pragma unroll
+    for (int i = 0; i < kOrderPerThread; i++) {
+        const int32_t q = min(order_query(b, i, t), nq - 1);
+        lo[i] = qoff[q];
+        hi[i] = qoff[q + 1];
+    }
+    int32_t c[kOrderBuckets];
+#pragma unroll
+    for (int k = 0; k < kOrderBuckets; k++) c[k] = 0;
+#pragma unroll
+    for (int i = 0; i < kOrderPerThread; i++) {
+        const int32_t q = order_query(b, i, t);
+        int bk = -1;
+        if (q < nq) {
+            const int64_t len = hi[i] - lo[i];
+            const uint32_t l32 = len <= 0 ? 0u : (len > (int64_t)INT32_MAX ? (uint32_t)INT32_MAX : (uint32_t)len);
+            const uint32_t x = l32 / unit;
+            bk = (int)(x < kOrderBuckets - 1 ? x : kOrderBuckets - 1);
+            bkt[q] = (uint8_t)bk;
+        }
+#pragma unroll
+        for (int k = 0; k < kOrderBuckets; k++) c[k] += __popcll(__ballot(bk == k));
+    }
+    if (lane == 0)
+#pragma unroll
+        for (int k = 0; k < kOrderBuckets; k++) cnt[wv][k] = c[k];
+    __syncthreads();
+    if (t < kOrderBuckets) {
+        int32_t sum = 0;
+        for (int w = 0; w < kOrderWaves; w++) sum += cnt[w][t];
+        blockcnt[b * kOrderBuckets + t] = sum;
+    }
+}
+
+// Launch 2: position of every query.  Bucket k of workgroup b starts after
+// every longer bucket and after bucket k of the earlier workgroups; inside
+// the workgroup, wave by wave, each wave in query order i then lane.
+__global__ __launch_bounds__(kOrderThreads) void route_order_scatter_kernel(const uint8_t *__restrict__ bkt,
+                                                                            int32_t nq,
+                                                                            const int32_t *__restrict__ blockcnt,
+                                                                            int32_t *__restrict__ order) {
+    __shared__ int32_t cnt[kOrderWaves][kOrderBuckets];
+    __shared__ int32_t bc[kOrderMaxBlocks * kOrderBuckets];
+    const int t = (int)threadIdx.x, lane = t & (kWave - 1), wv = t / kWave, b = (int)blockIdx.x;
+    const int nb = (int)gridDim.x;
+    if (t < nb * kOrderBuckets) bc[t] = blockcnt[t];  // every workgroup's counts, one load per thread
+    int bk[kOrderPerThread];
+#pragma unroll
+    for (int i = 0; i < kOrderPerThread; i++) {
+        const int32_t q = order_query(b, i, t);
+        bk[i] = q < nq ? (int)bkt[q] : -1;
+    }
+    int32_t c[kOrderBuckets];
+#pragma unroll
+    for (int k = 0; k < kOrderBuckets; k++) c[k] = 0;
+#pragma unroll
+    for (int i = 0; i < kOrderPerThread; i++)
+#pragma unroll
+        for (int k = 0; k < kOrderBuckets; k++) c[k] += __popcll(__ballot(bk[i] == k));
+    if (lane == 0)
+#pragma unroll
+        for (int k = 0; k < kOrderBuckets; k++) cnt[wv][k] = c[k];
+    __syncthreads();
+    // bucket totals over all workgroups, and bucket t's count in earlier ones
+    __shared__ int32_t tot[kOrderBuckets], pre[kOrderBuckets];
+    if (t < kOrderBuckets) {
+        int32_t all = 0, earlier = 0;
+        for (int j = 0; j < nb; j++) {
+            const int32_t v = bc[j * kOrderBuckets + t];
+            all += v;
+            earlier += j < b ? v : 0;
+        }
+        tot[t] = all;
+        pre[t] = earlier;
+    }
+    __syncthreads();
+    if (t < kOrderBuckets) {
+        // this workgroup's start in bucket t, then the waves' starts inside it
+        int32_t before = pre[t];
+        for (int k = t + 1; k < kOrderBuckets; k++) before += tot[k];  // longer buckets come first
+        int32_t run = before;
+        for (int w = 0; w < kOrderWaves; w++) {
+            const int32_t v = cnt[w][t];
+            cnt[w][t] = run;
+            run += v;
+        }
+    }
+    __syncthreads();
+    int32_t start[kOrderBuckets];
+#pragma unroll
+    for (int k = 0; k < kOrderBuckets; k++) start[k] = cnt[wv][k];
+    const uint64_t below = (1ull << lane) - 1ull;
+#pragma unroll
+    for (int i = 0; i < kOrderPerThread; i++) {
+        const int32_t q = order_query(b, i, t);
+#pragma unroll
+        for (int k = 0; k < kOrderBuckets; k++) {
+            const uint64_t m = __ballot(bk[i] == k);
+            if (bk[i] == k) order[start[k] + __popcll(m & below)] = q;
+            start[k] += __popcll(m);
+        }
     }
 }
 

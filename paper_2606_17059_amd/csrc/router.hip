@@ -86,6 +86,19 @@ struct ExportScratch {
     int64_t cap = 0;  // node capacity of the per-node arrays
 };
 
+// Longest-first order of one route call: sort keys and values, their sorted
+// copies (the order) and rocPRIM's temporary storage.  One set per forest,
+// grown on demand; `done` is recorded on the stream of the last route that
+// used it, and a route on any stream waits for it before reusing the set.
+struct RouteScratch {
+    int32_t *order = nullptr;
+    uint8_t *bkt = nullptr;
+    int32_t *blockcnt = nullptr;
+    int64_t cap = 0;
+    hipEvent_t done = nullptr;
+    bool pending = false;
+};
+
 }  // namespace
 
 struct pr_forest {
@@ -104,6 +117,7 @@ struct pr_forest {
     unsigned long long *d_skipped = nullptr;  // inputs skipped by device calls
     MergeScratch ms;
     ExportScratch xs;
+    RouteScratch rs;
     long long stamp = 0;          // add-round counter (stamps of moved records)
     int32_t local = -1;           // peer whose tree keeps access times (-1: none)
     int64_t now = 0;              // current time, set by the caller, never decreasing
@@ -113,6 +127,10 @@ struct pr_forest {
 };
 
 namespace {
+
+#ifndef PR_ROUTE_LONGEST_FIRST
+#define PR_ROUTE_LONGEST_FIRST 1
+#endif
 
 // Makes the forest's device current for the duration of a call.
 class DeviceScope {
@@ -269,6 +287,15 @@ void free_scratch(pr_forest *f) {
     free_export_scratch(f);
 }
 
+// Buffers only (the event stays); callers make sure no route still uses them.
+void free_route_buffers(pr_forest *f) {
+    RouteScratch &R = f->rs;
+    dfree(f, &R.order, R.cap);
+    dfree(f, &R.bkt, R.cap);
+    dfree(f, &R.blockcnt, (int64_t)pr::kOrderMaxBlocks * pr::kOrderBuckets);
+    R.cap = 0;
+}
+
 pr_status ensure_host_image(pr_forest *f) {
     if (f->host_img_valid) return PR_OK;
     std::string err;
@@ -423,19 +450,68 @@ pr_status commit(pr_forest *f) {
     return PR_OK;
 }
 
+// Longest-first order: the dispatcher starts one wave per query in index
+// order and refills a slot when its query ends, so with only a few long
+// queries per slot the last long ones to start leave most slots idle at the
+// end of the launch.  Taking the batch longest first removes that tail.  It
+// pays where a wave slot of the chip (256 CUs x 32 waves) gets between one
+// and eight queries of at least 4,096 tokens on average; elsewhere the order
+// kernel (a few microseconds) costs more than the tail.
+bool use_longest_first(int64_t nq, int64_t ntok) {
+    const int64_t slots = 256 * 32;
+    return PR_ROUTE_LONGEST_FIRST && nq > slots && nq <= 8 * slots && nq <= pr::kOrderMaxQueries &&
+           ntok >= 4096 * nq;
+}
+
+// Fill f->rs.order with the queries longest first (two launches of at most 16
+// workgroups) on stream s; length buckets are a quarter of the mean query wide.
+pr_status route_order(pr_forest *f, const int64_t *q_offsets, int64_t nq, int64_t ntok, hipStream_t s,
+                      const int32_t **order) {
+    RouteScratch &R = f->rs;
+    if (!R.done && hipEventCreateWithFlags(&R.done, hipEventDisableTiming) != hipSuccess) {
+        R.done = nullptr;
+        return fail(PR_EDEVICE, "hipEventCreate failed");
+    }
+    if (nq > R.cap) {
+        // an earlier route, on any stream, may still read the old buffer
+        if (R.pending && hipEventSynchronize(R.done) != hipSuccess)
+            return fail(PR_EDEVICE, "waiting for an earlier route failed");
+        R.pending = false;
+        free_route_buffers(f);
+        const int64_t cap = std::max<int64_t>(nq, std::min<int64_t>(2 * R.cap, pr::kOrderMaxQueries));
+        R.cap = cap;  // sizes for free_route_buffers, also after a partial allocation
+        if (!dalloc(f, &R.order, cap) || !dalloc(f, &R.bkt, cap) ||
+            !dalloc(f, &R.blockcnt, (int64_t)pr::kOrderMaxBlocks * pr::kOrderBuckets)) {
+            free_route_buffers(f);
+            return fail(PR_ENOMEM, "hipMalloc failed for the route order");
+        }
+    }
+    if (R.pending && hipStreamWaitEvent(s, R.done, 0) != hipSuccess)
+        return fail(PR_EDEVICE, "hipStreamWaitEvent failed");
+    const uint32_t unit = (uint32_t)std::min<int64_t>(std::max<int64_t>(1, ntok / nq / 4), INT32_MAX);
+    const unsigned blocks = (unsigned)((nq + pr::kOrderChunk - 1) / pr::kOrderChunk);
+    hipLaunchKernelGGL(pr::route_order_count_kernel, dim3(blocks), dim3(pr::kOrderThreads), 0, s, q_offsets,
+                       (int32_t)nq, unit, R.bkt, R.blockcnt);
+    hipLaunchKernelGGL(pr::route_order_scatter_kernel, dim3(blocks), dim3(pr::kOrderThreads), 0, s, R.bkt,
+                       (int32_t)nq, R.blockcnt, R.order);
+    if (hipGetLastError() != hipSuccess) return fail(PR_EDEVICE, "route order launch failed");
+    *order = R.order;
+    return PR_OK;
+}
+
 template <int W>
 hipError_t launch_route(const pr_forest *f, const int32_t *qt, int64_t ntok, const int64_t *qo, int64_t nq,
-                        const pr::Select &sel, int32_t *ml, int32_t *ch, hipStream_t s) {
+                        const pr::Select &sel, int32_t *ml, int32_t *ch, const int32_t *order, hipStream_t s) {
     const int64_t blocks = (nq + pr::kRouteWavesPerBlock - 1) / pr::kRouteWavesPerBlock;
     const bool plain = !sel.eligible && !sel.prefer_local && !sel.second;
     if (plain)
         hipLaunchKernelGGL((pr::route_kernel<W, false>), dim3((unsigned)blocks),
                            dim3(pr::kWave * pr::kRouteWavesPerBlock), 0, s, f->dev.nodes, f->dev.ntok, f->dev.nsep,
-                           f->dev.mext, f->dev.pool, qt, ntok, qo, nq, f->P, sel, ml, ch);
+                           f->dev.mext, f->dev.pool, qt, ntok, qo, nq, f->P, sel, ml, ch, order);
     else
         hipLaunchKernelGGL((pr::route_kernel<W, true>), dim3((unsigned)blocks),
                            dim3(pr::kWave * pr::kRouteWavesPerBlock), 0, s, f->dev.nodes, f->dev.ntok, f->dev.nsep,
-                           f->dev.mext, f->dev.pool, qt, ntok, qo, nq, f->P, sel, ml, ch);
+                           f->dev.mext, f->dev.pool, qt, ntok, qo, nq, f->P, sel, ml, ch, order);
     return hipGetLastError();
 }
 
@@ -864,6 +940,8 @@ void pr_forest_destroy(pr_forest *f) {
         dfree(f, &f->d_skipped, 1);
         dfree(f, &f->d_ctr, 1);
         if (f->h_stage) (void)hipHostFree(f->h_stage);
+        free_route_buffers(f);
+        if (f->rs.done) (void)hipEventDestroy(f->rs.done);
     }
     delete f;
 }
@@ -1399,15 +1477,34 @@ static pr_status route_impl(pr_forest *f, const int32_t *q_tokens, int64_t num_t
     pr_status s = commit(f);
     if (s) return s;
     hipStream_t st = (hipStream_t)hip_stream;
+    const int32_t *order = nullptr;
+    if (use_longest_first(num_queries, num_tokens) &&
+        (s = route_order(f, q_offsets, num_queries, num_tokens, st, &order)))
+        return s;
     hipError_t e;
     switch (f->W) {
-        case 1: e = launch_route<1>(f, q_tokens, num_tokens, q_offsets, num_queries, sel, match_len, chosen, st); break;
-        case 2: e = launch_route<2>(f, q_tokens, num_tokens, q_offsets, num_queries, sel, match_len, chosen, st); break;
-        case 4: e = launch_route<4>(f, q_tokens, num_tokens, q_offsets, num_queries, sel, match_len, chosen, st); break;
-        case 8: e = launch_route<8>(f, q_tokens, num_tokens, q_offsets, num_queries, sel, match_len, chosen, st); break;
-        default: e = launch_route<16>(f, q_tokens, num_tokens, q_offsets, num_queries, sel, match_len, chosen, st); break;
+        case 1:
+            e = launch_route<1>(f, q_tokens, num_tokens, q_offsets, num_queries, sel, match_len, chosen, order, st);
+            break;
+        case 2:
+            e = launch_route<2>(f, q_tokens, num_tokens, q_offsets, num_queries, sel, match_len, chosen, order, st);
+            break;
+        case 4:
+            e = launch_route<4>(f, q_tokens, num_tokens, q_offsets, num_queries, sel, match_len, chosen, order, st);
+            break;
+        case 8:
+            e = launch_route<8>(f, q_tokens, num_tokens, q_offsets, num_queries, sel, match_len, chosen, order, st);
+            break;
+        default:
+            e = launch_route<16>(f, q_tokens, num_tokens, q_offsets, num_queries, sel, match_len, chosen, order, st);
+            break;
     }
     if (e != hipSuccess) return fail(PR_EDEVICE, std::string("route launch failed: ") + hipGetErrorString(e));
+    if (order) {
+        // the order buffers are in use until the stream passes this launch
+        if (hipEventRecord(f->rs.done, st) != hipSuccess) return fail(PR_EDEVICE, "hipEventRecord failed");
+        f->rs.pending = true;
+    }
     return ok();
 }
 

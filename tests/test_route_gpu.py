@@ -274,3 +274,48 @@ def test_invalid_offsets_between_valid_queries():
     m, c = f.route(toks, o)
     assert m.cpu().numpy().tolist() == exp_m and c.cpu().numpy().tolist() == exp_c
     f.close()
+
+
+@pytest.mark.timeout(600)
+def test_longest_first_order_batches():
+    """Batches with more queries than wave slots (8,192) and at least 4,096
+    tokens per query on average are taken longest first through a permutation;
+    every row must still land at its own index.  The same queries routed in
+    batches of at most 8,192 (index order) give the reference rows, and a
+    sample is checked against the oracle."""
+    rng = np.random.default_rng(41)
+    P, V = 8, 50000
+    prefixes = [rng.integers(0, V, int(rng.integers(3000, 7000))).astype(np.int32) for _ in range(6)]
+    seqs, owners = [], []
+    for p in range(P):
+        for j in range(12):
+            k = int(rng.integers(0, len(prefixes)))
+            seqs.append(np.concatenate([prefixes[k], rng.integers(0, V, int(rng.integers(1, 400))).astype(np.int32)]))
+            owners.append(p)
+    snap = W.from_lists([s.tolist() for s in seqs], owners)
+    nq = 8192 + 77
+    qs = []
+    for i in range(nq):
+        k = int(rng.integers(0, len(prefixes)))
+        L = int(rng.integers(2048, 10240))
+        body = prefixes[k][:min(L, len(prefixes[k]))]
+        qs.append(np.concatenate([body, rng.integers(0, V, max(0, L - len(body))).astype(np.int32)]))
+    lens = np.array([len(q) for q in qs], dtype=np.int64)
+    assert lens.sum() >= 4096 * nq
+    offs = np.zeros(nq + 1, dtype=np.int64)
+    offs[1:] = np.cumsum(lens)
+    toks = np.concatenate(qs).astype(np.int32)
+    queries = W.SeqSet(toks, offs, None)
+    f = _forest(snap, P)
+    m, c = gpu_route(f, queries, "longest-first batch")
+    assert_properties(m, c, queries, "longest-first batch")
+    for lo, hi in ((0, 8192), (8192, nq)):
+        sub = queries.subset(np.arange(lo, hi))
+        m_ref, c_ref = gpu_route(f, sub, f"index-order batch [{lo}, {hi})")
+        assert_rows_equal(m[lo:hi], c[lo:hi], m_ref, c_ref, what=f"longest-first vs index order [{lo}, {hi})")
+    o = oracle_for(snap, P)
+    idx = np.unique(np.concatenate([rng.choice(nq, 200, replace=False), np.arange(nq - 5, nq)]))
+    m_or, c_or = o.route_seqset(queries, idx, nthreads())
+    assert_rows_equal(m, c, m_or, c_or, idx, "longest-first batch sample")
+    o.close()
+    f.close()

@@ -300,15 +300,15 @@ __device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
     return v;
 }
 
+// elig: the eligibility words, loaded by the caller (all ones for every peer).
 template <int W>
 __device__ __forceinline__ int32_t select_peers(const int32_t (&m)[W], int32_t P, int lane, const Select &sel,
-                                                bool want_second, int32_t &second) {
+                                                const uint64_t (&elig)[W], bool want_second, int32_t &second) {
     uint64_t key[W];
 #pragma unroll
     for (int w = 0; w < W; w++) {
         const int p = lane + 64 * w;
-        bool ok = p < P;
-        if (ok && sel.eligible) ok = ((sel.eligible[w] >> lane) & 1ull) || p == sel.local;
+        const bool ok = p < P && (((elig[w] >> lane) & 1ull) || p == sel.local);
         key[w] = ok ? select_key(m[w], p, sel) : 0ull;
     }
     uint64_t k1 = 0;
@@ -355,6 +355,11 @@ __attribute__((amdgpu_waves_per_eu(PR_ROUTE_WAVES_PER_EU))) void route_kernel(
     }
     const int32_t *qs = qtok + qb;
     const int64_t qlen = qe - qb;
+    // the eligibility words are read now and used after the walk, so their
+    // load is not one more round trip at the end
+    uint64_t elig[W];
+#pragma unroll
+    for (int w = 0; w < W; w++) elig[w] = (SEL && sel.eligible) ? sel.eligible[w] : ~0ull;
 
     int32_t m[W];
     uint64_t alive[W];
@@ -431,7 +436,7 @@ __attribute__((amdgpu_waves_per_eu(PR_ROUTE_WAVES_PER_EU))) void route_kernel(
         }
     }
     int32_t second;
-    const int32_t best = select_peers<W>(m, P, lane, sel, sel.second != nullptr, second);
+    const int32_t best = select_peers<W>(m, P, lane, sel, elig, sel.second != nullptr, second);
     if (lane == 0) {
         chosen[q] = best;
         if (sel.second) sel.second[q] = second;

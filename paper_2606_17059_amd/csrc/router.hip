@@ -601,8 +601,6 @@ __global__ void reset_call_kernel(pr::MergeCounters *c) {
 
 __global__ void add_skipped_kernel(unsigned long long *acc, const pr::MergeCounters *c) { *acc += c->skipped; }
 
-// Read the device counters and refresh the host mirror of the used sizes
-// (growing the arrays copies exactly the used part).
 // Copy `bytes` (<= kStageBytes) of device memory to the host through the
 // forest's pinned staging buffer (a direct DMA, no pageable bounce) and wait.
 bool read_small(pr_forest *f, void *out, const void *dsrc, size_t bytes, hipStream_t s) {
@@ -617,6 +615,8 @@ bool read_small(pr_forest *f, void *out, const void *dsrc, size_t bytes, hipStre
 static_assert(sizeof(pr::MergeCounters) <= kStageBytes && sizeof(pr::EvictPlan) <= kStageBytes,
               "readbacks fit the staging buffer");
 
+// Read the device counters and refresh the host mirror of the used sizes
+// (growing the arrays copies exactly the used part).
 pr_status read_counters(pr_forest *f, pr::MergeCounters *c, hipStream_t s) {
     if (!read_small(f, c, f->d_ctr, sizeof(*c), s)) return fail(PR_EDEVICE, "reading merge counters failed");
     f->dev.n_nodes = (int64_t)c->n_nodes;

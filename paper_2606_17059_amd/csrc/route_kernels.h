@@ -343,18 +343,20 @@ __attribute__((amdgpu_waves_per_eu(PR_ROUTE_WAVES_PER_EU))) void route_kernel(
     // slots in index order, so slot i serves query order[i]
     const int64_t q = order ? (int64_t)order[slot] : slot;
     int32_t *row = match_len + q * (int64_t)P;
-    const int64_t qb = qoff[q], qe = qoff[q + 1];
-    if (qb < 0 || qe < qb || qe > num_tokens || qe - qb > (int64_t)INT32_MAX) {
-        if (match_len)
-            for (int p = lane; p < P; p += kWave) row[p] = -1;
-        if (lane == 0) {
-            chosen[q] = -1;
-            if (sel.second) sel.second[q] = -1;
-        }
-        return;
-    }
+    // The offsets and the root's record are loaded together, and a query with
+    // bad offsets runs as an empty one (its row is written as -1 at the end),
+    // so that no branch on the offsets sits between those loads and the
+    // walk's first loads.
+    int64_t qb0 = qoff[q], qe0 = qoff[q + 1];
+    const Node root = nodes[0];
+    int32_t root_beg = root.ct_beg, root_cnt = root.ct_cnt;
+    // both loads are issued before anything waits on either (the compiler
+    // would otherwise sink the offsets' load below the root's branches)
+    asm volatile("" : "+s"(qb0), "+s"(qe0), "+s"(root_beg), "+s"(root_cnt));
+    const bool bad = qb0 < 0 || qe0 < qb0 || qe0 > num_tokens || qe0 - qb0 > (int64_t)INT32_MAX;
+    const int64_t qb = bad ? 0 : qb0;
+    const int64_t qlen = bad ? 0 : qe0 - qb0;
     const int32_t *qs = qtok + qb;
-    const int64_t qlen = qe - qb;
     // the eligibility words are read now and used after the walk, so their
     // load is not one more round trip at the end
     uint64_t elig[W];
@@ -371,18 +373,39 @@ __attribute__((amdgpu_waves_per_eu(PR_ROUTE_WAVES_PER_EU))) void route_kernel(
     }
 
     int64_t d = 0;
+    // The root's child block and, when the root has a single child (every
+    // stored sequence starts with the same token, as behind a shared system
+    // prompt), that child's record: the first level then issues its batch of
+    // loads without waiting for the query's first token or a record load.
     ChildBlock cb;
-    {
-        const Node root = nodes[0];
-        load_block(cb, ntok, nsep, root.ct_beg, root.ct_cnt, lane);
-    }
+    load_block(cb, ntok, nsep, root_beg, root_cnt, lane);
+    const bool single = root_cnt == 1;
+    const int32_t c0_id = single ? root_beg : 0;  // node 0 always exists
+    const Node r0 = nodes[c0_id];
+    const Child c0{c0_id, (int32_t)r0.lab_off, r0.lab_len, r0.ct_beg, r0.ct_cnt, r0.mask0};
+    const int32_t c0_tok = r0.tok;
+#if PR_FIRST_WINDOW
+    // the query's first token comes with the window (lane 0 of its first
+    // vector), read where the first level needs it
+    int32_t t = 0;
+#else
     int32_t t = qlen > 0 ? qs[0] : 0;
+#endif
     // One tree level; returns whether the walk goes on.  The first level is a
     // separate instance (FIRST), so that the window's registers die after it.
-    auto level = [&](auto first_tag, const auto &win) __attribute__((always_inline)) -> bool {
+    // With `known` the level's child is the root's single child c0, taken on
+    // the assumption that the query starts with its first token; the check
+    // waits until the level's loads are issued.
+    auto level = [&](auto first_tag, const auto &win, auto known_tag) __attribute__((always_inline)) -> bool {
         constexpr bool FIRST = decltype(first_tag)::value;
+        constexpr bool KNOWN = FIRST && decltype(known_tag)::value;
         Child c;
-        if (!locate(cb, t, nodes, ntok, lane, c)) return false;
+        if constexpr (KNOWN) {
+            c = c0;
+        } else {
+            if constexpr (FIRST && PR_FIRST_WINDOW) t = uniform(win[0]);
+            if (!locate(cb, t, nodes, ntok, lane, c)) return false;
+        }
         if (c.lab_len <= 0) return false;  // only the root has an empty label
         // one batch of loads per level: next token, ext mask words, the next
         // child block (used if the label matches in full) and the label compare
@@ -399,6 +422,10 @@ __attribute__((amdgpu_waves_per_eu(PR_ROUTE_WAVES_PER_EU))) void route_kernel(
             l = wave_lcp_first(pool + (uint32_t)c.lab_off, qs, n, win, lane);
         else
             l = wave_lcp(pool + (uint32_t)c.lab_off, qs + d, n, 0, (int64_t)kWave * kLcpFirstVectors, lane);
+        if constexpr (KNOWN) {
+            if constexpr (PR_FIRST_WINDOW) t = uniform(win[0]);
+            if (t != c0_tok) return false;  // no child starts with the query's first token
+        }
         bool any = false;
 #pragma unroll
         for (int w = 0; w < W; w++) {
@@ -417,12 +444,23 @@ __attribute__((amdgpu_waves_per_eu(PR_ROUTE_WAVES_PER_EU))) void route_kernel(
 #if PR_FIRST_WINDOW
     int32_t win[kWinVectors];
     load_window(win, qs, (int32_t)min(qlen, (int64_t)kWinTokens), lane);
-    bool more = qlen > 0 && level(std::true_type{}, win);
+    bool more = false;
+    if (qlen > 0) more = single ? level(std::true_type{}, win, std::true_type{})
+                                : level(std::true_type{}, win, std::false_type{});
 #else
-    bool more = qlen > 0 && level(std::false_type{}, NoWindow{});
+    bool more = qlen > 0 && level(std::false_type{}, NoWindow{}, std::false_type{});
 #endif
-    while (more) more = level(std::false_type{}, NoWindow{});
+    while (more) more = level(std::false_type{}, NoWindow{}, std::false_type{});
 
+    if (bad) {
+        if (match_len)
+            for (int p = lane; p < P; p += kWave) row[p] = -1;
+        if (lane == 0) {
+            chosen[q] = -1;
+            if (sel.second) sel.second[q] = -1;
+        }
+        return;
+    }
     // peers still holding the walked path matched all of it
 #pragma unroll
     for (int w = 0; w < W; w++)

@@ -277,13 +277,15 @@ def test_invalid_offsets_between_valid_queries():
 
 
 @pytest.mark.timeout(600)
-def test_longest_first_order_batches():
+@pytest.mark.parametrize("nq,lo,hi", [(8192 + 77, 2048, 10240), (65536, 4096, 4400)])
+def test_longest_first_order_batches(nq, lo, hi):
     """Batches with more queries than wave slots (8,192) and at least 4,096
     tokens per query on average are taken longest first through a permutation;
     every row must still land at its own index.  The same queries routed in
     batches of at most 8,192 (index order) give the reference rows, and a
-    sample is checked against the oracle."""
-    rng = np.random.default_rng(41)
+    sample is checked against the oracle.  65,536 queries is the largest batch
+    the order takes (sixteen workgroups of the counting sort)."""
+    rng = np.random.default_rng(41 + nq)
     P, V = 8, 50000
     prefixes = [rng.integers(0, V, int(rng.integers(3000, 7000))).astype(np.int32) for _ in range(6)]
     seqs, owners = [], []
@@ -293,11 +295,10 @@ def test_longest_first_order_batches():
             seqs.append(np.concatenate([prefixes[k], rng.integers(0, V, int(rng.integers(1, 400))).astype(np.int32)]))
             owners.append(p)
     snap = W.from_lists([s.tolist() for s in seqs], owners)
-    nq = 8192 + 77
     qs = []
     for i in range(nq):
         k = int(rng.integers(0, len(prefixes)))
-        L = int(rng.integers(2048, 10240))
+        L = int(rng.integers(lo, hi))
         body = prefixes[k][:min(L, len(prefixes[k]))]
         qs.append(np.concatenate([body, rng.integers(0, V, max(0, L - len(body))).astype(np.int32)]))
     lens = np.array([len(q) for q in qs], dtype=np.int64)
@@ -309,10 +310,11 @@ def test_longest_first_order_batches():
     f = _forest(snap, P)
     m, c = gpu_route(f, queries, "longest-first batch")
     assert_properties(m, c, queries, "longest-first batch")
-    for lo, hi in ((0, 8192), (8192, nq)):
-        sub = queries.subset(np.arange(lo, hi))
-        m_ref, c_ref = gpu_route(f, sub, f"index-order batch [{lo}, {hi})")
-        assert_rows_equal(m[lo:hi], c[lo:hi], m_ref, c_ref, what=f"longest-first vs index order [{lo}, {hi})")
+    for a in range(0, nq, 8192):
+        b = min(a + 8192, nq)
+        sub = queries.subset(np.arange(a, b))
+        m_ref, c_ref = gpu_route(f, sub, f"index-order batch [{a}, {b})")
+        assert_rows_equal(m[a:b], c[a:b], m_ref, c_ref, what=f"longest-first vs index order [{a}, {b})")
     o = oracle_for(snap, P)
     idx = np.unique(np.concatenate([rng.choice(nq, 200, replace=False), np.arange(nq - 5, nq)]))
     m_or, c_or = o.route_seqset(queries, idx, nthreads())

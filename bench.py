@@ -41,18 +41,27 @@ WORKLOADS = {
 }
 
 
+def kernel_code_sha(path: str) -> str:
+    """sha256 prefix of a kernel source with comments and whitespace removed:
+    it changes when the code does, not when a comment does."""
+    import hashlib
+    import re
+    src = open(path).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    src = re.sub(r"//[^\n]*", "", src)
+    return hashlib.sha256(re.sub(r"\s+", " ", src).strip().encode()).hexdigest()[:16]
+
+
 def measured_traffic(workload: str):
     """HBM bytes per launch of the route kernel from the committed rocprofv3
     FETCH_SIZE / WRITE_SIZE summary, or None if it does not cover this workload
-    or the kernel source changed since it was taken."""
-    import hashlib
+    or the kernel code changed since it was taken."""
     try:
         rec = json.load(open(os.path.join(ROOT, "profiles", "route_kernel_traffic.json")))[workload]
-        src = os.path.join(ROOT, "paper_2606_17059_amd", "csrc", "route_kernels.h")
-        sha = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+        sha = kernel_code_sha(os.path.join(ROOT, "paper_2606_17059_amd", "csrc", "route_kernels.h"))
     except (OSError, KeyError, ValueError):
         return None
-    return rec["traffic_bytes_per_launch"] if rec.get("kernel_source_sha256_16") == sha else None
+    return rec["traffic_bytes_per_launch"] if rec.get("kernel_code_sha256_16") == sha else None
 
 
 def step_kernels(nq: int, ntok: int) -> list:

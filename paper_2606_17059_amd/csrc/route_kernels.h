@@ -22,6 +22,11 @@
 // Peers still in the set at the end matched the whole walked depth.  A wave
 // reduction then takes the largest match and the lowest peer id holding it
 // (the argmax of Algorithm 1, ties to the lowest id).
+// When the root has a single child (a prompt prefix every stored sequence
+// shares), its record is loaded before the walk and the first level's batch
+// goes out without waiting for the query's first token.  Batches of long
+// queries can be served in an order computed on the device (longest first,
+// route_order_count_kernel and route_order_scatter_kernel below).
 #ifndef PR_ROUTE_KERNELS_H
 #define PR_ROUTE_KERNELS_H
 

@@ -307,6 +307,56 @@ def bench_select(f, w, qt, qo, needed, K, warmup, dev) -> dict:
     return out
 
 
+def bench_latency(f, w, dev, reps: int = 200) -> dict:
+    """Small batches, as a router serving requests as they arrive would send
+    them: the first b queries of the batch, per call the host wall time of
+    pr_route plus a stream synchronisation, and of pr_route plus the copy of
+    the chosen peers into pinned host memory (medians over `reps` calls), and
+    the GPU time per launch of back-to-back launches."""
+    import torch
+    q = w.queries
+    P = w.num_peers
+    out = {}
+    for b in (1, 8, 64, 512, 4096, 32768):
+        if b > len(q):
+            break
+        end = int(q.offsets[b])
+        qt = torch.from_numpy(q.tokens[:end].copy()).to(dev)
+        qo = torch.from_numpy(q.offsets[:b + 1].copy()).to(dev)
+        ml = torch.empty((b, P), dtype=torch.int32, device=dev)
+        ch = torch.empty(b, dtype=torch.int32, device=dev)
+        host = torch.empty(b, dtype=torch.int32, pin_memory=True)
+        launch = f.route_launcher(qt, qo, ml, ch)
+        for _ in range(20):
+            launch()
+        torch.cuda.synchronize()
+        sync_us, copy_us = np.empty(reps), np.empty(reps)
+        for i in range(reps):
+            t0 = time.perf_counter()
+            launch()
+            torch.cuda.synchronize()
+            sync_us[i] = (time.perf_counter() - t0) * 1e6
+        for i in range(reps):
+            t0 = time.perf_counter()
+            launch()
+            host.copy_(ch, non_blocking=True)
+            torch.cuda.synchronize()
+            copy_us[i] = (time.perf_counter() - t0) * 1e6
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            launch()
+        e1.record()
+        torch.cuda.synchronize()
+        out[str(b)] = {"query_tokens": end, "route_sync_us": float(np.median(sync_us)),
+                       "route_sync_p99_us": float(np.percentile(sync_us, 99)),
+                       "route_chosen_to_host_us": float(np.median(copy_us)),
+                       "gpu_us_per_launch_back_to_back": e0.elapsed_time(e1) * 1e3 / reps}
+        log(f"[bench] latency b={b}: {out[str(b)]}")
+    f.check()
+    return out
+
+
 def bench_snapshot(f, w, dev, peers: int = 4) -> dict:
     """Anti-entropy on the device: export peers 0..peers-1 (sendTrie) and load
     each export back into the same peer (receive side, device input).  The
@@ -372,6 +422,8 @@ def main() -> int:
                     help="also time snapshot export and device-input load of a few peers")
     ap.add_argument("--compact", action="store_true",
                     help="config 5: compact the forest after the last merge round and time it")
+    ap.add_argument("--latency", action="store_true",
+                    help="also time small batches (1 to 32,768 queries) per call, host wall time included")
     ap.add_argument("--no-select", action="store_true",
                     help="skip timing pr_route_select (push-back / failover selection)")
     ap.add_argument("--copies", type=int, default=4, help="device copies of the query batch to rotate")
@@ -509,6 +561,8 @@ def main() -> int:
     if not args.no_select:
         extra["select"] = bench_select(f, w, qt, qo, needed, K, args.warmup, dev)
         log(f"[bench] select: {extra['select']}")
+    if args.latency:
+        extra["latency"] = bench_latency(f, w, dev)
     if args.lru:
         # after the timed routes: touches and evictions change the forest
         extra["lru"] = bench_lru(f, w, qt, qo, dev)

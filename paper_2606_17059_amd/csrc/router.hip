@@ -86,8 +86,8 @@ struct ExportScratch {
     int64_t cap = 0;  // node capacity of the per-node arrays
 };
 
-// Longest-first order of one route call: sort keys and values, their sorted
-// copies (the order) and rocPRIM's temporary storage.  One set per forest,
+// Longest-first order of one route call: each query's length bucket, the
+// per-workgroup bucket counts and the order itself.  One set per forest,
 // grown on demand; `done` is recorded on the stream of the last route that
 // used it, and a route on any stream waits for it before reusing the set.
 struct RouteScratch {

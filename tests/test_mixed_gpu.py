@@ -6,7 +6,8 @@ selection with random eligibility.
 Half of the seeds draw first tokens from 150 values, so merges grow the root's
 child block past 64 children (the width at which it needs separators) while
 routing runs between them; the others use a vocabulary of 2-4 tokens, so edges
-split at every depth.  130 peers take three mask words, 5 peers one.
+split at every depth.  5, 65, 130 and 1,024 peers run the route kernel's
+one-, two-, four- and sixteen-word peer-mask forms.
 """
 import numpy as np
 import pytest
@@ -54,10 +55,10 @@ def _device_load(b, p, seqs):
     b.o.load(p, t, off)
 
 
-@pytest.mark.parametrize("seed", range(6))
+@pytest.mark.parametrize("seed", range(8))
 def test_mixed_operations(seed):
     rng = np.random.default_rng(9300 + seed)
-    P = 130 if seed % 3 == 2 else 5
+    P = {6: 65, 7: 1024}.get(seed, 130 if seed % 3 == 2 else 5)
     wide = seed % 2 == 0
     vocab = 2 + seed % 3
 
@@ -76,7 +77,7 @@ def test_mixed_operations(seed):
     t = 1
     b.time(t)
     for p in range(P):  # the root starts with fewer than 64 children
-        if rng.random() < (0.5 if P < 64 else 0.2):
+        if rng.random() < (0.5 if P < 64 else 0.2 if P < 1000 else 0.03):
             b.load(p, seqs(int(rng.integers(0, 5))))
     queries = seqs(40, 0, 11)
     widths = []

@@ -276,6 +276,84 @@ def test_invalid_offsets_between_valid_queries():
     f.close()
 
 
+_LONG_VOCAB = 50000
+
+
+def _long_forest(rng, P):
+    """Six shared prefixes of 3,000-7,000 tokens; every peer holds twelve
+    prompts, each one prefix plus a short suffix."""
+    V = _LONG_VOCAB
+    prefixes = [rng.integers(0, V, int(rng.integers(3000, 7000))).astype(np.int32) for _ in range(6)]
+    seqs, owners = [], []
+    for p in range(P):
+        for j in range(12):
+            k = int(rng.integers(0, len(prefixes)))
+            seqs.append(np.concatenate([prefixes[k], rng.integers(0, V, int(rng.integers(1, 400))).astype(np.int32)]))
+            owners.append(p)
+    return W.from_lists([s.tolist() for s in seqs], owners), prefixes
+
+
+def _long_batch(rng, prefixes, nq, lo, hi):
+    """nq queries of lo..hi tokens, each a stored prefix (cut to the length)
+    and fresh tokens; at least 4,096 tokens per query on average."""
+    qs = []
+    for i in range(nq):
+        k = int(rng.integers(0, len(prefixes)))
+        L = int(rng.integers(lo, hi))
+        body = prefixes[k][:min(L, len(prefixes[k]))]
+        qs.append(np.concatenate([body, rng.integers(0, _LONG_VOCAB, max(0, L - len(body))).astype(np.int32)]))
+    lens = np.array([len(q) for q in qs], dtype=np.int64)
+    assert lens.sum() >= 4096 * nq
+    offs = np.zeros(nq + 1, dtype=np.int64)
+    offs[1:] = np.cumsum(lens)
+    return W.SeqSet(np.concatenate(qs).astype(np.int32), offs, None)
+
+
+def _index_order_rows(f, queries, what):
+    """Reference rows: the batch routed in pieces of at most 8,192 queries,
+    which are taken in index order."""
+    ms, cs = [], []
+    for a in range(0, len(queries), 8192):
+        sub = queries.subset(np.arange(a, min(a + 8192, len(queries))))
+        m, c = gpu_route(f, sub, f"{what} index-order piece at {a}")
+        ms.append(m)
+        cs.append(c)
+    return np.concatenate(ms), np.concatenate(cs)
+
+
+@pytest.mark.timeout(600)
+def test_longest_first_batches_on_two_streams():
+    """The forest keeps one order buffer.  Three long batches routed back to
+    back without a host wait, on two streams: the second, larger than the
+    first, on another stream (the buffer grows once the first route is done
+    with it), the third on the first stream again (it waits for the second
+    route before reusing the buffer).  Each result equals its index-order
+    reference."""
+    import torch
+    rng = np.random.default_rng(4242)
+    P = 8
+    snap, prefixes = _long_forest(rng, P)
+    batches = [_long_batch(rng, prefixes, n, 4096, 6000) for n in (8192 + 8, 9000, 8192 + 300)]
+    f = _forest(snap, P)
+    dev = device()
+    ins = [to_dev(b) for b in batches]
+    outs = [(torch.empty((len(b), P), dtype=torch.int32, device=dev), torch.empty(len(b), dtype=torch.int32, device=dev))
+            for b in batches]
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    announce("longest-first: three long batches on two streams, no host wait between them")
+    for i, st in enumerate((s1, s2, s1)):
+        with torch.cuda.stream(st):
+            f.route(ins[i][0], ins[i][1], outs[i][0], outs[i][1], stream=st)
+    torch.cuda.synchronize()
+    for i, b in enumerate(batches):
+        m, c = outs[i][0].cpu().numpy(), outs[i][1].cpu().numpy()
+        assert_properties(m, c, b, f"two streams, batch {i}")
+        m_ref, c_ref = _index_order_rows(f, b, f"two streams, batch {i}")
+        assert_rows_equal(m, c, m_ref, c_ref, what=f"two streams, batch {i}")
+    f.close()
+
+
 @pytest.mark.timeout(600)
 @pytest.mark.parametrize("nq,lo,hi", [(8192 + 77, 2048, 10240), (65536, 4096, 4400)])
 def test_longest_first_order_batches(nq, lo, hi):
@@ -286,35 +364,14 @@ def test_longest_first_order_batches(nq, lo, hi):
     sample is checked against the oracle.  65,536 queries is the largest batch
     the order takes (sixteen workgroups of the counting sort)."""
     rng = np.random.default_rng(41 + nq)
-    P, V = 8, 50000
-    prefixes = [rng.integers(0, V, int(rng.integers(3000, 7000))).astype(np.int32) for _ in range(6)]
-    seqs, owners = [], []
-    for p in range(P):
-        for j in range(12):
-            k = int(rng.integers(0, len(prefixes)))
-            seqs.append(np.concatenate([prefixes[k], rng.integers(0, V, int(rng.integers(1, 400))).astype(np.int32)]))
-            owners.append(p)
-    snap = W.from_lists([s.tolist() for s in seqs], owners)
-    qs = []
-    for i in range(nq):
-        k = int(rng.integers(0, len(prefixes)))
-        L = int(rng.integers(lo, hi))
-        body = prefixes[k][:min(L, len(prefixes[k]))]
-        qs.append(np.concatenate([body, rng.integers(0, V, max(0, L - len(body))).astype(np.int32)]))
-    lens = np.array([len(q) for q in qs], dtype=np.int64)
-    assert lens.sum() >= 4096 * nq
-    offs = np.zeros(nq + 1, dtype=np.int64)
-    offs[1:] = np.cumsum(lens)
-    toks = np.concatenate(qs).astype(np.int32)
-    queries = W.SeqSet(toks, offs, None)
+    P = 8
+    snap, prefixes = _long_forest(rng, P)
+    queries = _long_batch(rng, prefixes, nq, lo, hi)
     f = _forest(snap, P)
     m, c = gpu_route(f, queries, "longest-first batch")
     assert_properties(m, c, queries, "longest-first batch")
-    for a in range(0, nq, 8192):
-        b = min(a + 8192, nq)
-        sub = queries.subset(np.arange(a, b))
-        m_ref, c_ref = gpu_route(f, sub, f"index-order batch [{a}, {b})")
-        assert_rows_equal(m[a:b], c[a:b], m_ref, c_ref, what=f"longest-first vs index order [{a}, {b})")
+    m_ref, c_ref = _index_order_rows(f, queries, "longest-first batch")
+    assert_rows_equal(m, c, m_ref, c_ref, what="longest-first vs index order")
     o = oracle_for(snap, P)
     idx = np.unique(np.concatenate([rng.choice(nq, 200, replace=False), np.arange(nq - 5, nq)]))
     m_or, c_or = o.route_seqset(queries, idx, nthreads())

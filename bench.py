@@ -324,8 +324,9 @@ def bench_latency(f, w, dev, reps: int = 200) -> dict:
     """Small batches, as a router serving requests as they arrive would send
     them: the first b queries of the batch, per call the host wall time of
     pr_route plus a stream synchronisation, and of pr_route plus the copy of
-    the chosen peers into pinned host memory (medians over `reps` calls), and
-    the GPU time per launch of back-to-back launches."""
+    the chosen peers into pinned host memory, and of one replay of a HIP graph
+    holding the launch (medians over `reps` calls), and the GPU time per
+    launch of back-to-back launches."""
     import torch
     q = w.queries
     P = w.num_peers
@@ -361,9 +362,28 @@ def bench_latency(f, w, dev, reps: int = 200) -> dict:
             launch()
         e1.record()
         torch.cuda.synchronize()
+        # the same launch captured into a HIP graph and replayed
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            f.route_launcher(qt, qo, ml, ch, stream=side)()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            f.route_launcher(qt, qo, ml, ch, stream=torch.cuda.current_stream())()
+        torch.cuda.synchronize()
+        graph_us = np.empty(reps)
+        for i in range(reps):
+            t0 = time.perf_counter()
+            g.replay()
+            torch.cuda.synchronize()
+            graph_us[i] = (time.perf_counter() - t0) * 1e6
+        del g
         out[str(b)] = {"query_tokens": end, "route_sync_us": float(np.median(sync_us)),
                        "route_sync_p99_us": float(np.percentile(sync_us, 99)),
                        "route_chosen_to_host_us": float(np.median(copy_us)),
+                       "graph_replay_sync_us": float(np.median(graph_us)),
                        "gpu_us_per_launch_back_to_back": e0.elapsed_time(e1) * 1e3 / reps}
         log(f"[bench] latency b={b}: {out[str(b)]}")
     f.check()

@@ -135,9 +135,16 @@ pr_status pr_merge(pr_forest *f, const int32_t *peer_of, const int32_t *tokens,
  * forest keeps: the first such call, or a larger batch, allocates it (after
  * waiting for the previous user), and such calls on one forest are ordered on
  * the device through an event even when issued on different streams.
+ * HIP graph capture: on a capturing stream the call enqueues the route kernel
+ * only (no allocation, copy, wait or event), walking the batch in index order
+ * (same results); a replay routes what the captured buffers hold at replay
+ * time.  Under capture, a forest whose snapshots changed since its last
+ * upload (pr_load_snapshot without a route, merge or device call after it)
+ * returns PR_ESTATE: route once outside capture first.
  * Errors (host side, nothing enqueued): PR_EINVAL (NULL pointers with
- * num_queries > 0, negative counts), PR_ENOMEM / PR_EDEVICE (rebuild after a
- * snapshot load failed, or the order buffer could not be allocated).
+ * num_queries > 0, negative counts), PR_ESTATE (see capture above),
+ * PR_ENOMEM / PR_EDEVICE (rebuild after a snapshot load failed, or the order
+ * buffer could not be allocated).
  */
 pr_status pr_route(pr_forest *f, const int32_t *q_tokens, int64_t num_tokens,
                    const int64_t *q_offsets, int64_t num_queries, int32_t *match_len,
@@ -288,9 +295,10 @@ pr_status pr_evict_lru(pr_forest *f, int64_t max_tokens, int64_t *evicted, void 
  *   second      DEVICE int32 [num_queries], or NULL.
  * With eligible NULL, local_peer -1 and flags 0, best equals pr_route's chosen.
  * A query with invalid offsets gets match_len -1, best -1 and second -1.
+ * Longest-first order and graph capture as in pr_route.
  * Errors (host side, nothing enqueued): PR_EINVAL (local_peer outside
  * [-1, num_peers), unknown flags, NULL q_offsets or best with num_queries > 0,
- * negative counts), PR_ENOMEM / PR_EDEVICE as in pr_route.
+ * negative counts), PR_ESTATE / PR_ENOMEM / PR_EDEVICE as in pr_route.
  */
 #define PR_SELECT_PREFER_LOCAL 1u
 

@@ -1474,11 +1474,20 @@ static pr_status route_impl(pr_forest *f, const int32_t *q_tokens, int64_t num_t
     if (f->broken) return fail(PR_ESTATE, "an earlier device update failed; destroy the forest");
     DeviceScope ds(f);
     if (!ds.ok()) return fail(PR_EDEVICE, "cannot select the forest's device");
+    hipStream_t st = (hipStream_t)hip_stream;
+    // Under graph capture only the launch may be enqueued: no upload of a
+    // changed forest (allocations, copies, waits) and no longest-first order
+    // (its buffer, events and cross-stream wait); the batch goes in index
+    // order, with the same results.
+    hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(st, &cap) != hipSuccess) return fail(PR_EDEVICE, "hipStreamIsCapturing failed");
+    const bool capturing = cap != hipStreamCaptureStatusNone;
+    if (capturing && (f->dirty || !f->has_dev))
+        return fail(PR_ESTATE, "snapshots changed since the forest's last upload; route once outside graph capture");
     pr_status s = commit(f);
     if (s) return s;
-    hipStream_t st = (hipStream_t)hip_stream;
     const int32_t *order = nullptr;
-    if (use_longest_first(num_queries, num_tokens) &&
+    if (!capturing && use_longest_first(num_queries, num_tokens) &&
         (s = route_order(f, q_offsets, num_queries, num_tokens, st, &order)))
         return s;
     hipError_t e;

@@ -61,6 +61,10 @@ typedef int32_t pr_status;
 typedef struct pr_forest pr_forest;
 
 /* ABI version of this header (incremented on incompatible changes). */
+#define PR_ABI_VERSION 4
+
+/* PR_ABI_VERSION of the header the library was built with; a client built
+ * against another version must not call the library. */
 int32_t pr_abi_version(void);
 
 /* Message describing the calling thread's last failed call ("" if none). */
@@ -140,7 +144,10 @@ pr_status pr_merge(pr_forest *f, const int32_t *peer_of, const int32_t *tokens,
  * (same results); a replay routes what the captured buffers hold at replay
  * time.  Under capture, a forest whose snapshots changed since its last
  * upload (pr_load_snapshot without a route, merge or device call after it)
- * returns PR_ESTATE: route once outside capture first.
+ * returns PR_ESTATE: route once outside capture first.  The graph holds the
+ * addresses of the forest's device arrays: replay it only while the forest
+ * lives and pr_forest_info's layout_epoch still has its value at capture
+ * (after the arrays move, a replay would read freed memory; capture again).
  * Errors (host side, nothing enqueued): PR_EINVAL (NULL pointers with
  * num_queries > 0, negative counts), PR_ESTATE (see capture above),
  * PR_ENOMEM / PR_EDEVICE (rebuild after a snapshot load failed, or the order
@@ -323,6 +330,10 @@ typedef struct {
     int64_t pool_tokens;     /* edge-label tokens in use */
     int64_t device_bytes;    /* device memory held by the forest */
     int64_t host_seq_tokens; /* tokens of the host-side snapshot copies */
+    int64_t layout_epoch;    /* advances whenever the device arrays that routes
+                                read move: an upload after host snapshot loads,
+                                growth inside a merge, device load, touch or
+                                eviction, and compaction */
 } pr_forest_info;
 
 pr_status pr_forest_info_get(pr_forest *f, pr_forest_info *out);

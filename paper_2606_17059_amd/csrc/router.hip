@@ -123,6 +123,7 @@ struct pr_forest {
     int64_t now = 0;              // current time, set by the caller, never decreasing
     int64_t local_load_time = 0;  // time of the local peer's last host snapshot
     int64_t device_bytes = 0;
+    int64_t layout_epoch = 0;     // advances whenever the device arrays the route reads move
     bool broken = false;          // a device update failed; only destroy is valid
 };
 
@@ -360,6 +361,7 @@ pr_status ensure_capacity(pr_forest *f, int64_t need_nodes, int64_t need_pool, h
         d.mext = nd.mext;
         d.moved = nd.moved;
         d.cap_nodes = nd.cap_nodes;
+        f->layout_epoch++;
     }
     if (need_pool > d.cap_pool) {
         const int64_t cap = std::min<int64_t>(std::max<int64_t>(need_pool, d.cap_pool + d.cap_pool / 2),
@@ -374,6 +376,7 @@ pr_status ensure_capacity(pr_forest *f, int64_t need_nodes, int64_t need_pool, h
         dfree(f, &d.pool, d.cap_pool);
         d.pool = np;
         d.cap_pool = cap;
+        f->layout_epoch++;
     }
     return PR_OK;
 }
@@ -440,6 +443,7 @@ pr_status commit(pr_forest *f) {
     f->has_dev = true;
     f->dirty = false;
     f->merged = false;
+    f->layout_epoch++;
     if (f->local >= 0) {
         pr_status r = init_local_times(f, f->local_load_time);
         if (r) return r;
@@ -907,7 +911,7 @@ struct CallScratch {
 
 extern "C" {
 
-int32_t pr_abi_version(void) { return 3; }
+int32_t pr_abi_version(void) { return PR_ABI_VERSION; }
 
 const char *pr_last_error(void) { return g_err.c_str(); }
 
@@ -1189,6 +1193,7 @@ pr_status pr_forest_compact(pr_forest *f, int64_t *nodes_before, int64_t *nodes_
     nw.n_pool = n_pool;
     f->dev = nw;
     f->has_dev = true;
+    f->layout_epoch++;
     pr::MergeCounters c;
     std::memset(&c, 0, sizeof(c));
     c.n_nodes = (unsigned long long)n_new;
@@ -1568,6 +1573,7 @@ pr_status pr_forest_info_get(pr_forest *f, pr_forest_info *out) {
         out->pool_tokens = (int64_t)f->host_img.pool.size();
     }
     out->device_bytes = f->device_bytes;
+    out->layout_epoch = f->layout_epoch;
     int64_t t = 0;
     for (const auto &S : f->sets) t += (int64_t)S.tokens.size();
     out->host_seq_tokens = t;

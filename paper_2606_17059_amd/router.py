@@ -38,7 +38,7 @@ class ForestInfo(ctypes.Structure):
     _fields_ = [("num_peers", ctypes.c_int32), ("mask_words", ctypes.c_int32),
                 ("num_nodes", ctypes.c_int64),
                 ("pool_tokens", ctypes.c_int64), ("device_bytes", ctypes.c_int64),
-                ("host_seq_tokens", ctypes.c_int64)]
+                ("host_seq_tokens", ctypes.c_int64), ("layout_epoch", ctypes.c_int64)]
 
 
 class ImageView(ctypes.Structure):
@@ -105,7 +105,7 @@ def lib() -> ctypes.CDLL:
     L.pr_forest_info_get.restype = ctypes.c_int32
     L.pr_forest_host_image.argtypes = [_vp, ctypes.POINTER(ImageView)]
     L.pr_forest_host_image.restype = ctypes.c_int32
-    if L.pr_abi_version() != 3:
+    if L.pr_abi_version() != 4:
         raise RuntimeError("libprefix_router ABI version mismatch")
     _lib_handle = L
     return L
@@ -424,9 +424,12 @@ class Forest:
                 ctypes.c_int64(q_tokens.numel()), ctypes.c_void_p(q_offsets.data_ptr()), ctypes.c_int64(nq),
                 ctypes.c_void_p(match_len.data_ptr() or None), ctypes.c_void_p(chosen.data_ptr() or None),
                 ctypes.c_void_p(_stream_ptr(stream, q_offsets.device)))
-        keep = (q_tokens, q_offsets, match_len, chosen, stream)
+        # the launcher holds the forest too, so that the forest outlives it
+        keep = (self, q_tokens, q_offsets, match_len, chosen, stream)
 
         def launch() -> None:
+            if not self._h:
+                raise RuntimeError("forest is closed")
             st = fn(*args)
             if st != PR_OK:
                 _check(st)

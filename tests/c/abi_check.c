@@ -31,7 +31,7 @@ static int failures = 0;
 
 static int host_checks(void) {
     pr_forest *f = NULL;
-    CHECK(pr_abi_version() >= 1);
+    CHECK(pr_abi_version() == PR_ABI_VERSION);
     CHECK(pr_forest_create(0, &f) == PR_EINVAL);
     CHECK(pr_forest_create(PR_MAX_PEERS + 1, &f) == PR_EINVAL);
     CHECK(pr_forest_create(3, NULL) == PR_EINVAL);

@@ -164,3 +164,49 @@ def test_capture_refuses_a_forest_that_changed():
     m, c = gpu_route(f, x, "eager route after the refused capture")
     assert (m[:, 0] == 0).all()
     f.close()
+
+
+def test_layout_epoch_marks_moved_arrays():
+    """Routes leave layout_epoch alone and a small merge that fits the spare
+    capacity does too, so a graph captured before it replays on the merged
+    forest; an upload after host loads and a compaction move the arrays and
+    advance it."""
+    import torch
+    from paper_2606_17059_amd import Forest
+    w = W.make_config(1)
+    P = w.num_peers
+    f = Forest(P)
+    f.load_seqset(w.snapshot)
+    assert f.info()["layout_epoch"] == 0  # nothing uploaded yet
+    x = w.queries.subset(np.arange(100))
+    qt, qo = to_dev(x)
+    ml = torch.empty((len(x), P), dtype=torch.int32, device=device())
+    ch = torch.empty(len(x), dtype=torch.int32, device=device())
+    f.route(qt, qo, ml, ch)
+    torch.cuda.synchronize()
+    e1 = f.info()["layout_epoch"]
+    assert e1 >= 1
+    announce("graph: capture before a small merge")
+    g = _capture(lambda st: f.route_launcher(qt, qo, ml, ch, stream=st)())
+    assert f.info()["layout_epoch"] == e1
+    # insert a few of the queries themselves into peer 2: their rows change
+    ins = x.subset(np.arange(5))
+    it, io = to_dev(ins)
+    f.merge(torch.full((len(ins),), 2, dtype=torch.int32, device=device()), it, io)
+    torch.cuda.synchronize()
+    assert f.info()["layout_epoch"] == e1, "a merge within the spare capacity moved the arrays"
+    ml.fill_(-7)
+    g.replay()
+    torch.cuda.synchronize()
+    m, c = ml.cpu().numpy().copy(), ch.cpu().numpy().copy()
+    m_ref, c_ref = gpu_route(f, x, "eager route after the merge")
+    assert_rows_equal(m, c, m_ref, c_ref, what="replay after a merge in place")
+    assert (m[:5, 2] == x.lengths()[:5]).all()
+    del g
+    f.compact()
+    e2 = f.info()["layout_epoch"]
+    assert e2 > e1
+    f.load_snapshot(1, np.zeros(0, np.int32), np.zeros(1, np.int64))
+    gpu_route(f, x, "route after a device load")
+    assert f.info()["layout_epoch"] >= e2
+    f.close()

@@ -378,3 +378,34 @@ def test_longest_first_order_batches(nq, lo, hi):
     assert_rows_equal(m, c, m_or, c_or, idx, "longest-first batch sample")
     o.close()
     f.close()
+
+
+def test_launcher_keeps_its_forest():
+    """A route launcher holds its forest: dropping every other reference does
+    not free the forest under it; after an explicit close the launcher
+    refuses to run instead of passing a freed handle to the library."""
+    import gc
+
+    import torch
+    from paper_2606_17059_amd import Forest
+    w = W.make_config(1)
+    P = w.num_peers
+    f = Forest(P)
+    f.load_seqset(w.snapshot)
+    x = w.queries.subset(np.arange(64))
+    qt, qo = to_dev(x)
+    ml = torch.empty((len(x), P), dtype=torch.int32, device=device())
+    ch = torch.empty(len(x), dtype=torch.int32, device=device())
+    launch = f.route_launcher(qt, qo, ml, ch)
+    del f
+    gc.collect()
+    announce("launcher after its forest's last other reference went")
+    launch()
+    torch.cuda.synchronize()
+    o = oracle_for(w.snapshot, P)
+    m_or, c_or = o.route(x.tokens, x.offsets, 2)
+    o.close()
+    assert_rows_equal(ml.cpu().numpy(), ch.cpu().numpy(), m_or, c_or, what="launcher keeps its forest")
+    launch.buffers[0].close()
+    with pytest.raises(RuntimeError, match="closed"):
+        launch()

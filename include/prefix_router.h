@@ -61,7 +61,7 @@ typedef int32_t pr_status;
 typedef struct pr_forest pr_forest;
 
 /* ABI version of this header (incremented on incompatible changes). */
-#define PR_ABI_VERSION 4
+#define PR_ABI_VERSION 5
 
 /* PR_ABI_VERSION of the header the library was built with; a client built
  * against another version must not call the library. */
@@ -333,7 +333,10 @@ typedef struct {
     int64_t layout_epoch;    /* advances whenever the device arrays that routes
                                 read move: an upload after host snapshot loads,
                                 growth inside a merge, device load, touch or
-                                eviction, and compaction */
+                                eviction, compaction, and the switch from 16-bit
+                                to int32 labels */
+    int64_t label_token_bytes; /* 2 while routes read a 16-bit copy of the label
+                                  pool (every label token in [0, 65535]), else 4 */
 } pr_forest_info;
 
 pr_status pr_forest_info_get(pr_forest *f, pr_forest_info *out);

@@ -60,6 +60,7 @@ struct MergeCounters {
     unsigned long long skipped;   // inserts with invalid peer or offsets
     unsigned long long bad_path;  // mask pass found a sequence not ending at a node
     unsigned long long move_chunks;  // add round: 64-child chunks of the old blocks that move
+    unsigned long long wide_tokens;  // appended label tokens outside [0, 65535] (16-bit copy)
 };
 
 struct DevForest {

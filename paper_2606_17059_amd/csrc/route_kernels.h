@@ -27,6 +27,9 @@
 // goes out without waiting for the query's first token.  Batches of long
 // queries can be served in an order computed on the device (longest first,
 // route_order_count_kernel and route_order_scatter_kernel below).
+// Labels are read from the int32 pool, or, while every label token lies in
+// [0, 65535], from a 16-bit copy of it (half the label bytes and requests; a
+// query token outside that range equals no label token either way).
 #ifndef PR_ROUTE_KERNELS_H
 #define PR_ROUTE_KERNELS_H
 
@@ -79,10 +82,26 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t token_rsrc(const int32_t *p, i
 // Cache policy of the query loads: non-temporal (read once).
 constexpr int kQueryPolicy = PR_QUERY_NT ? 2 : 0;
 
-// One compare step over cnt <= 64 * NV tokens: ra holds the label tokens,
-// rb the query tokens, both ranged to cnt tokens so that lanes past the end
-// read 0 on both sides and compare equal.  Returns the first mismatch, or -1.
-template <int NV>
+// Label tokens: int32, or uint16 (the 16-bit copy of the pool).  Raw buffer
+// resources over the label bytes and loads of one token per lane.
+template <typename LT>
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t label_rsrc(const LT *p, int32_t cnt) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<LT *>(p), (short)0, cnt * (int32_t)sizeof(LT), 0x00020000);
+}
+
+template <typename LT>
+__device__ __forceinline__ int32_t load_label(__amdgpu_buffer_rsrc_t r, int32_t off) {
+    if constexpr (sizeof(LT) == 2)
+        return (int32_t)(uint16_t)__builtin_amdgcn_raw_buffer_load_b16(r, off, 0, 0);
+    else
+        return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
+}
+
+// One compare step over cnt <= 64 * NV tokens: ra holds the label tokens
+// (LT wide), rb the query tokens, both ranged to cnt tokens so that lanes past
+// the end read 0 on both sides and compare equal.  Returns the first
+// mismatch, or -1.
+template <int NV, typename LT>
 __device__ __forceinline__ int32_t lcp_step(__amdgpu_buffer_rsrc_t ra, __amdgpu_buffer_rsrc_t rb, int lane) {
     int32_t va[NV], vb[NV];
     // opaque lane offset: with its range unknown the per-vector constant stays
@@ -92,9 +111,15 @@ __device__ __forceinline__ int32_t lcp_step(__amdgpu_buffer_rsrc_t ra, __amdgpu_
     // step issues the rest
     int32_t off = lane * 4;
     asm volatile("" : "+v"(off));
+    // 16-bit labels take their own (opaque) lane offset
+    int32_t offa = off;
+    if constexpr (sizeof(LT) != 4) {
+        offa = lane * (int32_t)sizeof(LT);
+        asm volatile("" : "+v"(offa));
+    }
 #pragma unroll
     for (int j = 0; j < NV; j++) {
-        va[j] = __builtin_amdgcn_raw_buffer_load_b32(ra, off + j * kWave * 4, 0, 0);
+        va[j] = load_label<LT>(ra, offa + j * kWave * (int32_t)sizeof(LT));
         vb[j] = __builtin_amdgcn_raw_buffer_load_b32(rb, off + j * kWave * 4, 0, kQueryPolicy);
     }
     // fold every vector's mismatches into a lane mask before branching, so
@@ -121,7 +146,8 @@ __device__ __forceinline__ int32_t lcp_step(__amdgpu_buffer_rsrc_t ra, __amdgpu_
 // 31 tokens short of its nominal size; the nine-vector first step leaves the
 // rest of a 1024-token label to an eight-vector step.  Steps of at most 128
 // and 512 tokens take two- and eight-vector forms.
-__device__ __forceinline__ int64_t wave_lcp(const int32_t *__restrict__ a, const int32_t *__restrict__ b,
+template <typename LT>
+__device__ __forceinline__ int64_t wave_lcp(const LT *__restrict__ a, const int32_t *__restrict__ b,
                                             int64_t n, int64_t base, int64_t first, int lane) {
     for (int64_t step = first; base < n; step = (int64_t)kWave * kLcpVectors) {
         int32_t cnt = (int32_t)min(n - base, step);
@@ -131,17 +157,17 @@ __device__ __forceinline__ int64_t wave_lcp(const int32_t *__restrict__ a, const
         // would not keep the line in the L2 for the next step
         if (n - base > step) cnt -= (int32_t)(((uint32_t)((uintptr_t)(b + base) >> 2) + (uint32_t)step) & 31u);
 #endif
-        const __amdgpu_buffer_rsrc_t ra = token_rsrc(a + base, cnt * 4);
+        const __amdgpu_buffer_rsrc_t ra = label_rsrc(a + base, cnt);
         const __amdgpu_buffer_rsrc_t rb = token_rsrc(b + base, cnt * 4);
         int32_t r;
         if (cnt <= 2 * kWave)
-            r = lcp_step<2>(ra, rb, lane);
+            r = lcp_step<2, LT>(ra, rb, lane);
         else if (cnt <= 8 * kWave)
-            r = lcp_step<8>(ra, rb, lane);
+            r = lcp_step<8, LT>(ra, rb, lane);
         else if (kLcpFirstVectors > 8 && kLcpVectors > kLcpFirstVectors && cnt <= kWave * kLcpFirstVectors)
-            r = lcp_step<kLcpFirstVectors>(ra, rb, lane);
+            r = lcp_step<kLcpFirstVectors, LT>(ra, rb, lane);
         else
-            r = lcp_step<kLcpVectors>(ra, rb, lane);
+            r = lcp_step<kLcpVectors, LT>(ra, rb, lane);
         if (r >= 0 && r < cnt) return base + r;
         base += cnt;
     }
@@ -169,17 +195,17 @@ __device__ __forceinline__ void load_window(int32_t (&win)[kWinVectors], const i
         win[j] = __builtin_amdgcn_raw_buffer_load_b32(r, off + j * kWave * 4, 0, 0);
 }
 
-// Label tokens [0, cnt) (ra, cnt <= 64 * NL) against the window, which
-// may hold query tokens past cnt: only lanes below cnt count.  Returns the
-// first mismatch, or -1.
-template <int NL>
+// Label tokens [0, cnt) (ra, LT wide, cnt <= 64 * NL) against the window,
+// which may hold query tokens past cnt: only lanes below cnt count.  Returns
+// the first mismatch, or -1.
+template <int NL, typename LT>
 __device__ __forceinline__ int32_t lcp_step_win(__amdgpu_buffer_rsrc_t ra, const int32_t (&win)[kWinVectors],
                                                 int32_t cnt, int lane) {
     int32_t va[NL];
-    int32_t off = lane * 4;  // opaque, as in lcp_step
+    int32_t off = lane * (int32_t)sizeof(LT);  // opaque, as in lcp_step
     asm volatile("" : "+v"(off));
 #pragma unroll
-    for (int j = 0; j < NL; j++) va[j] = __builtin_amdgcn_raw_buffer_load_b32(ra, off + j * kWave * 4, 0, 0);
+    for (int j = 0; j < NL; j++) va[j] = load_label<LT>(ra, off + j * kWave * (int32_t)sizeof(LT));
     uint32_t mm = 0;
 #pragma unroll
     for (int j = 0; j < NL; j++) mm |= (uint32_t)(j * kWave + lane < cnt && va[j] != win[j]) << j;
@@ -193,14 +219,15 @@ __device__ __forceinline__ int32_t lcp_step_win(__amdgpu_buffer_rsrc_t ra, const
 }
 
 // wave_lcp for the first level, whose first query tokens are in win.
-__device__ __forceinline__ int64_t wave_lcp_first(const int32_t *__restrict__ a, const int32_t *__restrict__ b,
+template <typename LT>
+__device__ __forceinline__ int64_t wave_lcp_first(const LT *__restrict__ a, const int32_t *__restrict__ b,
                                                   int64_t n, const int32_t (&win)[kWinVectors], int lane) {
     const int32_t cnt = (int32_t)min(n, (int64_t)kWinTokens);
-    const __amdgpu_buffer_rsrc_t ra = token_rsrc(a, cnt * 4);
-    const int32_t r =
-        cnt <= 2 * kWave ? lcp_step_win<2>(ra, win, cnt, lane) : lcp_step_win<kWinVectors>(ra, win, cnt, lane);
+    const __amdgpu_buffer_rsrc_t ra = label_rsrc(a, cnt);
+    const int32_t r = cnt <= 2 * kWave ? lcp_step_win<2, LT>(ra, win, cnt, lane)
+                                       : lcp_step_win<kWinVectors, LT>(ra, win, cnt, lane);
     if (r >= 0 && r < cnt) return r;
-    return wave_lcp(a, b, n, kWinTokens, (int64_t)kWave * kLcpVectors, lane);
+    return wave_lcp<LT>(a, b, n, kWinTokens, (int64_t)kWave * kLcpVectors, lane);
 }
 #endif
 
@@ -331,13 +358,14 @@ __device__ __forceinline__ int32_t select_peers(const int32_t (&m)[W], int32_t P
 }
 
 // SEL = false: plain routing (every peer eligible, ties to the lowest id, no
-// second pick); the selection options are compiled out.
-template <int W, bool SEL>
+// second pick); the selection options are compiled out.  LT: the label
+// pool's token type (int32_t, or uint16_t for the 16-bit copy).
+template <int W, bool SEL, typename LT>
 __global__ __launch_bounds__(kWave *kRouteWavesPerBlock)
 __attribute__((amdgpu_waves_per_eu(PR_ROUTE_WAVES_PER_EU))) void route_kernel(
     const Node *__restrict__ nodes, const int32_t *__restrict__ ntok, const int32_t *__restrict__ nsep,
     const uint64_t *__restrict__ mext,
-    const int32_t *__restrict__ pool, const int32_t *__restrict__ qtok, int64_t num_tokens,
+    const LT *__restrict__ pool, const int32_t *__restrict__ qtok, int64_t num_tokens,
     const int64_t *__restrict__ qoff, int64_t nq, int32_t P, const Select sel_in, int32_t *__restrict__ match_len,
     int32_t *__restrict__ chosen, const int32_t *__restrict__ order) {
     const Select sel = SEL ? sel_in : Select{nullptr, -1, 0, nullptr};
@@ -424,9 +452,9 @@ __attribute__((amdgpu_waves_per_eu(PR_ROUTE_WAVES_PER_EU))) void route_kernel(
         const int64_t n = min((int64_t)c.lab_len, qlen - d);
         int64_t l;
         if constexpr (FIRST)
-            l = wave_lcp_first(pool + (uint32_t)c.lab_off, qs, n, win, lane);
+            l = wave_lcp_first<LT>(pool + (uint32_t)c.lab_off, qs, n, win, lane);
         else
-            l = wave_lcp(pool + (uint32_t)c.lab_off, qs + d, n, 0, (int64_t)kWave * kLcpFirstVectors, lane);
+            l = wave_lcp<LT>(pool + (uint32_t)c.lab_off, qs + d, n, 0, (int64_t)kWave * kLcpFirstVectors, lane);
         if constexpr (KNOWN) {
             if constexpr (PR_FIRST_WINDOW) t = uniform(win[0]);
             if (t != c0_tok) return false;  // no child starts with the query's first token
@@ -484,6 +512,22 @@ __attribute__((amdgpu_waves_per_eu(PR_ROUTE_WAVES_PER_EU))) void route_kernel(
         chosen[q] = best;
         if (sel.second) sel.second[q] = second;
     }
+}
+
+// The 16-bit copy of the label pool: p16[i] = pool[i] for i in [from, to);
+// tokens outside [0, 65535] (which make the copy unusable) are counted.
+__global__ void pool16_copy_kernel(const int32_t *__restrict__ pool, uint16_t *__restrict__ p16, int64_t from,
+                                   int64_t to, unsigned long long *__restrict__ wide) {
+    const int64_t i = from + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    bool out = false;
+    if (i < to) {
+        const int32_t t = pool[i];
+        out = (uint32_t)t > 0xFFFFu;
+        p16[i] = (uint16_t)t;
+    }
+    const uint64_t b = __ballot(out);
+    if (b && (int)(threadIdx.x & (kWave - 1)) == __ffsll((unsigned long long)b) - 1)
+        atomicAdd(wide, (unsigned long long)__popcll(b));
 }
 
 // Longest-first order of a batch, a counting sort in two launches of a few

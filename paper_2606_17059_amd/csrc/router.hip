@@ -53,6 +53,8 @@ struct DevImage {
     int32_t *pool = nullptr;
     long long *moved = nullptr;
     unsigned long long *ltime = nullptr;  // local peer's access times (allocated while a local peer is set)
+    uint16_t *pool16 = nullptr;  // 16-bit copy of pool, which routes read while every label token fits
+    int64_t cap_pool16 = 0;
     int64_t cap_nodes = 0, cap_pool = 0;
     int64_t n_nodes = 0, n_pool = 0;  // host mirror of the device counters
 };
@@ -124,6 +126,7 @@ struct pr_forest {
     int64_t local_load_time = 0;  // time of the local peer's last host snapshot
     int64_t device_bytes = 0;
     int64_t layout_epoch = 0;     // advances whenever the device arrays the route reads move
+    bool narrow = false;          // dev.pool16 mirrors dev.pool[0, n_pool) (every label token in [0, 65535])
     bool broken = false;          // a device update failed; only destroy is valid
 };
 
@@ -231,8 +234,10 @@ void free_image(pr_forest *f) {
     free_node_arrays(f, d);
     dfree(f, &d.pool, d.cap_pool);
     dfree(f, &d.ltime, d.cap_nodes);
+    dfree(f, &d.pool16, d.cap_pool16);
     d = DevImage();
     f->has_dev = false;
+    f->narrow = false;
 }
 
 void free_export_scratch(pr_forest *f) {
@@ -383,6 +388,56 @@ pr_status ensure_capacity(pr_forest *f, int64_t need_nodes, int64_t need_pool, h
 
 pr::DevForest dev_view(const pr_forest *f);
 
+// The 16-bit label copy.  Routes read labels from it while every label token
+// lies in [0, 65535] (half the label bytes); otherwise from the int32 pool.
+// Labels are only ever appended to the pool (a split reuses a span of its
+// label), so the copy follows merges by converting the appended range.
+void drop_pool16(pr_forest *f) {
+    DevImage &d = f->dev;
+    if (d.pool16) {
+        // a route launched earlier on another stream may still read it
+        (void)hipDeviceSynchronize();
+        dfree(f, &d.pool16, d.cap_pool16);
+        f->layout_epoch++;
+    }
+    d.cap_pool16 = 0;
+    f->narrow = false;
+}
+
+// Enqueue the copy of pool[from, n_pool) on s, first growing the copy to the
+// pool's capacity (then it is rebuilt from 0).  Tokens out of range are
+// counted in the merge counters' wide_tokens; the caller reads them with its
+// next counter readback and drops the copy if there are any.  Without memory
+// for a larger copy, routes fall back to the int32 pool.
+pr_status pool16_extend(pr_forest *f, int64_t from, hipStream_t s) {
+    DevImage &d = f->dev;
+    if (!f->narrow) return PR_OK;
+    if (d.cap_pool16 < d.cap_pool) {
+        uint16_t *np = nullptr;
+        if (!dalloc(f, &np, d.cap_pool)) {
+            drop_pool16(f);
+            return PR_OK;
+        }
+        if (d.pool16) {
+            if (hipDeviceSynchronize() != hipSuccess) {
+                dfree(f, &np, d.cap_pool);
+                return fail(PR_EDEVICE, "hipDeviceSynchronize failed while growing the 16-bit labels");
+            }
+            dfree(f, &d.pool16, d.cap_pool16);
+        }
+        d.pool16 = np;
+        d.cap_pool16 = d.cap_pool;
+        from = 0;
+        f->layout_epoch++;
+    }
+    if (d.n_pool > from) {
+        hipLaunchKernelGGL(pr::pool16_copy_kernel, dim3(grid_threads(d.n_pool - from, 256)), dim3(256), 0, s, d.pool,
+                           d.pool16, from, d.n_pool, &f->d_ctr->wide_tokens);
+        if (hipGetLastError() != hipSuccess) return fail(PR_EDEVICE, "16-bit label copy failed to launch");
+    }
+    return PR_OK;
+}
+
 // Access times of the local peer: every node it holds gets time t, others 0.
 pr_status init_local_times(pr_forest *f, int64_t t) {
     DevImage &d = f->dev;
@@ -440,6 +495,25 @@ pr_status commit(pr_forest *f) {
     c.n_pool = (unsigned long long)np;
     if (hipMemcpy(f->d_ctr, &c, sizeof(c), hipMemcpyHostToDevice) != hipSuccess)
         return fail(PR_EDEVICE, "counter upload failed");
+    // 16-bit labels when every token fits (else, or without the memory, int32)
+    f->narrow = std::all_of(h.pool.begin(), h.pool.end(), [](int32_t t) { return (uint32_t)t <= 0xFFFFu; });
+    if (f->narrow) {
+        std::vector<uint16_t> p16;
+        try {
+            p16.assign(h.pool.begin(), h.pool.end());
+        } catch (const std::bad_alloc &) {
+            f->narrow = false;
+        }
+        if (f->narrow && dalloc(f, &d.pool16, d.cap_pool)) {
+            d.cap_pool16 = d.cap_pool;
+            if (np > 0 && hipMemcpy(d.pool16, p16.data(), np * sizeof(uint16_t), hipMemcpyHostToDevice) != hipSuccess) {
+                free_image(f);
+                return fail(PR_EDEVICE, "upload of the 16-bit labels failed");
+            }
+        } else {
+            f->narrow = false;
+        }
+    }
     f->has_dev = true;
     f->dirty = false;
     f->merged = false;
@@ -503,19 +577,30 @@ pr_status route_order(pr_forest *f, const int64_t *q_offsets, int64_t nq, int64_
     return PR_OK;
 }
 
+template <int W, bool SEL, typename LT>
+void launch_route_t(const pr_forest *f, const LT *pool, const int32_t *qt, int64_t ntok, const int64_t *qo,
+                    int64_t nq, const pr::Select &sel, int32_t *ml, int32_t *ch, const int32_t *order,
+                    hipStream_t s) {
+    const int64_t blocks = (nq + pr::kRouteWavesPerBlock - 1) / pr::kRouteWavesPerBlock;
+    hipLaunchKernelGGL((pr::route_kernel<W, SEL, LT>), dim3((unsigned)blocks), dim3(pr::kWave * pr::kRouteWavesPerBlock),
+                       0, s, f->dev.nodes, f->dev.ntok, f->dev.nsep, f->dev.mext, pool, qt, ntok, qo, nq, f->P, sel,
+                       ml, ch, order);
+}
+
+// Plain routing or selection, over the 16-bit labels when they are current.
 template <int W>
 hipError_t launch_route(const pr_forest *f, const int32_t *qt, int64_t ntok, const int64_t *qo, int64_t nq,
                         const pr::Select &sel, int32_t *ml, int32_t *ch, const int32_t *order, hipStream_t s) {
-    const int64_t blocks = (nq + pr::kRouteWavesPerBlock - 1) / pr::kRouteWavesPerBlock;
     const bool plain = !sel.eligible && !sel.prefer_local && !sel.second;
-    if (plain)
-        hipLaunchKernelGGL((pr::route_kernel<W, false>), dim3((unsigned)blocks),
-                           dim3(pr::kWave * pr::kRouteWavesPerBlock), 0, s, f->dev.nodes, f->dev.ntok, f->dev.nsep,
-                           f->dev.mext, f->dev.pool, qt, ntok, qo, nq, f->P, sel, ml, ch, order);
+    const bool narrow = f->narrow && f->dev.pool16;
+    if (plain && narrow)
+        launch_route_t<W, false>(f, f->dev.pool16, qt, ntok, qo, nq, sel, ml, ch, order, s);
+    else if (plain)
+        launch_route_t<W, false>(f, f->dev.pool, qt, ntok, qo, nq, sel, ml, ch, order, s);
+    else if (narrow)
+        launch_route_t<W, true>(f, f->dev.pool16, qt, ntok, qo, nq, sel, ml, ch, order, s);
     else
-        hipLaunchKernelGGL((pr::route_kernel<W, true>), dim3((unsigned)blocks),
-                           dim3(pr::kWave * pr::kRouteWavesPerBlock), 0, s, f->dev.nodes, f->dev.ntok, f->dev.nsep,
-                           f->dev.mext, f->dev.pool, qt, ntok, qo, nq, f->P, sel, ml, ch, order);
+        launch_route_t<W, true>(f, f->dev.pool, qt, ntok, qo, nq, sel, ml, ch, order, s);
     return hipGetLastError();
 }
 
@@ -593,6 +678,7 @@ __global__ void reset_round_kernel(pr::MergeCounters *c) {
 }
 
 __global__ void reset_call_kernel(pr::MergeCounters *c) {
+    c->wide_tokens = 0;
     c->n_add = 0;
     c->n_split = 0;
     c->pool_need = 0;
@@ -651,6 +737,7 @@ pr_status run_merge(pr_forest *f, const int32_t *peer_of, const int32_t *tokens,
                     const int64_t *offsets, int64_t n, hipStream_t s, int32_t stamp = 1) {
     pr_status r = ensure_merge_scratch(f, n, s);
     if (r) return r;
+    const int64_t pool0 = f->dev.n_pool;  // labels appended from here on
     MergeScratch &m = f->ms;
     pr::Batch B{peer_of, tokens, offsets, num_tokens, n, f->P, stamp};
     const int bs = 256, wb = 64 * pr::kMergeWavesPerBlock;
@@ -733,10 +820,12 @@ pr_status run_merge(pr_forest *f, const int32_t *peer_of, const int32_t *tokens,
     hipLaunchKernelGGL(pr::merge_mask_kernel, dim3(grid_waves(n)), dim3(wb), 0, s, dev_view(f), B, m.st, f->d_ctr);
     hipLaunchKernelGGL(add_skipped_kernel, dim3(1), dim3(1), 0, s, f->d_skipped, f->d_ctr);
     if (hipGetLastError() != hipSuccess) return fail(PR_EDEVICE, "merge launch failed");
+    if ((r = pool16_extend(f, pool0, s))) return r;
     if ((r = read_counters(f, &c, s))) return r;
     if (c.overflow || c.bad_path)
         return fail(PR_EDEVICE, "merge invariant broken (overflow " + std::to_string(c.overflow) + ", bad paths " +
                                     std::to_string(c.bad_path) + "); destroy the forest");
+    if (c.wide_tokens) drop_pool16(f);  // a label token outside [0, 65535] arrived
     f->merged = true;
     return PR_OK;
 }
@@ -1081,6 +1170,7 @@ pr_status pr_forest_compact(pr_forest *f, int64_t *nodes_before, int64_t *nodes_
     hipStream_t s = (hipStream_t)hip_stream;
     DevImage &d = f->dev;
     const int64_t n_old = d.n_nodes;
+    const bool narrow_before = f->narrow;
     if (nodes_before) *nodes_before = n_old;
     // the new image (capacity: the old node count plus spare; labels sized below)
     DevImage nw;
@@ -1202,6 +1292,18 @@ pr_status pr_forest_compact(pr_forest *f, int64_t *nodes_before, int64_t *nodes_
         f->broken = true;
         return fail(PR_EDEVICE, "counter upload failed");
     }
+    // the 16-bit copy of the new pool (its labels are a subset of the old ones)
+    f->narrow = narrow_before;
+    if ((r = pool16_extend(f, 0, s))) {
+        f->broken = true;
+        return r;
+    }
+    unsigned long long wide = 0;
+    if (f->narrow && !read_small(f, &wide, &f->d_ctr->wide_tokens, sizeof(wide), s)) {
+        f->broken = true;
+        return fail(PR_EDEVICE, "reading the 16-bit label check failed");
+    }
+    if (wide) drop_pool16(f);
     f->host_img_valid = false;  // the host image no longer mirrors the device layout
     if (nodes_after) *nodes_after = n_new;
     return ok();
@@ -1574,6 +1676,7 @@ pr_status pr_forest_info_get(pr_forest *f, pr_forest_info *out) {
     }
     out->device_bytes = f->device_bytes;
     out->layout_epoch = f->layout_epoch;
+    out->label_token_bytes = f->narrow ? 2 : 4;
     int64_t t = 0;
     for (const auto &S : f->sets) t += (int64_t)S.tokens.size();
     out->host_seq_tokens = t;

@@ -409,3 +409,63 @@ def test_launcher_keeps_its_forest():
     launch.buffers[0].close()
     with pytest.raises(RuntimeError, match="closed"):
         launch()
+
+
+def test_label_width_follows_the_tokens():
+    """Routes read 16-bit labels while every label token fits in [0, 65535]
+    and int32 labels otherwise, with identical results: a small-token forest
+    starts narrow, stays narrow through merges that grow its label pool (the
+    16-bit copy grows with it) and through compaction, and turns wide when a
+    merge brings a token of 70,000; a forest uploaded with a negative token is
+    wide from the start."""
+    import torch
+    rng = np.random.default_rng(616)
+    P = 3
+    w = W.tiny_random(7, num_peers=P, vocab=8, max_seqs=12, n_queries=150)
+    f = _forest(w.snapshot, P)
+    o = oracle_for(w.snapshot, P)
+    queries = [w.queries.seq(i).tolist() for i in range(len(w.queries))]
+
+    def check(what, width):
+        t, off = pins._csr(queries)
+        m, c = gpu_route(f, W.SeqSet(t, off, None), what)
+        m_or, c_or = o.route(t, off, 2)
+        assert_rows_equal(m, c, m_or, c_or, what=what)
+        assert f.info()["label_token_bytes"] == width, (what, f.info())
+
+    def merge(seqs, what):
+        peers = np.array([int(rng.integers(0, P)) for _ in seqs], np.int32)
+        t, off = pins._csr(seqs)
+        announce(f"label width: merge {what}")
+        f.merge(torch.from_numpy(peers).to(device()), torch.from_numpy(t).to(device()),
+                torch.from_numpy(off).to(device()))
+        o.merge(peers, t, off)
+        torch.cuda.synchronize()
+
+    check("uploaded", 2)
+    pool0 = f.info()["pool_tokens"]
+    # long small-token sequences: the label pool outgrows its spare capacity
+    merge([rng.integers(0, 8, int(rng.integers(200, 400))).tolist() for _ in range(60)], "long small tokens")
+    assert f.info()["pool_tokens"] > 2 * pool0 + 4096
+    queries += [s[:150] for s in pins.csr_to_list(*o.export(0))[:20]]
+    check("after growth", 2)
+    f.compact()
+    check("after compaction", 2)
+    epoch = f.info()["layout_epoch"]
+    merge([[1, 2, 70000, 3], [5, 70000]], "a token of 70,000")
+    assert f.info()["layout_epoch"] > epoch
+    queries += [[1, 2, 70000, 3, 9], [5, 70000]]
+    check("after a wide token", 4)
+    f.close()
+    o.close()
+
+    neg = W.from_lists([[3, -1, 4], [3, 1]], [0, 1])
+    g = _forest(neg, 2)
+    og = oracle_for(neg, 2)
+    t, off = pins._csr([[3, -1, 4, 4], [3, 1], [3, 2]])
+    m, c = gpu_route(g, W.SeqSet(t, off, None), "negative token forest")
+    m_or, c_or = og.route(t, off, 1)
+    assert_rows_equal(m, c, m_or, c_or, what="negative token forest")
+    assert g.info()["label_token_bytes"] == 4
+    g.close()
+    og.close()

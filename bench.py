@@ -74,6 +74,14 @@ def step_kernels(nq: int, ntok: int) -> list:
     return ["route_kernel<W, false>"]
 
 
+def route_kernel_name(f) -> str:
+    """The plain route kernel instantiation a forest's routes run: mask words
+    and label token type (16-bit while every label token fits)."""
+    info = f.info()
+    lt = "unsigned short" if info["label_token_bytes"] == 2 else "int"
+    return f"route_kernel<{info['mask_words']}, false, {lt}>"
+
+
 def log(msg: str) -> None:
     sys.stderr.write(msg + "\n")
     sys.stderr.flush()
@@ -236,12 +244,13 @@ def bench_stream(args, w, dev):
                 compact_out.append(bench_compact(f, qt, qo, ml, ch, qs, args.steps, dist, float(km.mean())))
                 log(f"[bench] compact: {compact_out[-1]}")
             del qt, qo, ml, ch
+        kname = route_kernel_name(f)
         f.close()
     kern = np.array(kern_all)
     achieved = tot_bytes / tot_route_s / 1e9
     return {
         "value": tot_q / tot_route_s, "ms_per_step": float(kern.mean()), "kernel_ms": float(kern.mean()),
-        "achieved": achieved, "bytes_per_launch": tot_bytes / len(kern),
+        "achieved": achieved, "bytes_per_launch": tot_bytes / len(kern), "kernel": kname,
         "merge": {"inserts_per_s": tot_ins / tot_merge_s, "inserts": tot_ins, "seconds": tot_merge_s,
                   "note": "wall time of pr_merge calls (host-synchronous), 8 rounds x 10,000 inserts"},
         "phases": phases_out, "cpu": cpu, "compact": compact_out or None}
@@ -503,7 +512,7 @@ def main() -> int:
             "roofline": {"bound": "hbm", "achieved": r["achieved"], "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                          "frac": r["achieved"] / PEAK_HBM_GBPS, "traffic": measured_traffic("stream"),
                          "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
-                         "kernel": "route_kernel<W, false>",
+                         "kernel": r["kernel"],
                          "kernel_ms": r["kernel_ms"], "algorithmic_bytes_per_launch": r["bytes_per_launch"]},
             "cpu_baseline": r["cpu"], "merge": r["merge"], "phases": r["phases"]}
         if r["compact"]:
@@ -629,7 +638,7 @@ def main() -> int:
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                      "frac": achieved / PEAK_HBM_GBPS, "traffic": measured_traffic(W.CONFIG_NAMES[args.config]),
                      "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
-                     "kernel": "route_kernel<W, false>", "kernel_ms": total_ms / K,
+                     "kernel": route_kernel_name(f), "kernel_ms": total_ms / K,
                      "kernel_ms_own_events": {"mean": float(kern_ms.mean()), "median": float(np.median(kern_ms))},
                      "kernels_per_step": step_kernels(nq, int(qlen.sum())),
                      "algorithmic_bytes_per_launch": total_bytes},

@@ -98,6 +98,12 @@ static int device_checks(void) {
     const int32_t c_exp[5] = {0, 0, 2, 2, 0};
     CHECK(memcmp(m, m_exp, sizeof(m)) == 0);
     CHECK(memcmp(c, c_exp, sizeof(c)) == 0);
+    /* the info struct as this header lays it out: small tokens, 16-bit labels */
+    pr_forest_info info;
+    memset(&info, 0xAB, sizeof(info));
+    CHECK(pr_forest_info_get(f, &info) == PR_OK);
+    CHECK(info.num_peers == 3 && info.mask_words == 1 && info.num_nodes > 1 && info.pool_tokens > 0);
+    CHECK(info.layout_epoch >= 1 && info.label_token_bytes == 2);
     /* merge [3 4 1] into peer 1 and [1 2 3 4 5 6] into peer 2 */
     const int32_t mt[9] = {3, 4, 1, 1, 2, 3, 4, 5, 6};
     const int64_t mo[3] = {0, 3, 9};

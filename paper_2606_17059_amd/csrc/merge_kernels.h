@@ -429,13 +429,16 @@ __global__ void add_alloc_kernel(DevForest F, const unsigned long long *keys, in
 
 // Step 4 (one wave per 64-child chunk of every rebuilt parent's old block):
 // old children keep their order, each moving up by the winners below it, and
-// are stamped with their new position.
+// are stamped with their new position.  The grid may be larger than the
+// chunk count (an upper bound known on the host); the count itself is the
+// one step 2 recorded.
 __global__ __launch_bounds__(64 *kMergeWavesPerBlock) void add_move_kernel(
-    DevForest F, const unsigned long long *keys, int64_t n_add, const int32_t *cstart, int64_t n_chunks,
-    const int32_t *grp_nw, const int32_t *grp_nb, const int32_t *win_tok, long long stamp) {
+    DevForest F, const unsigned long long *keys, int64_t n_add, const int32_t *cstart,
+    const MergeCounters *__restrict__ ctr, const int32_t *grp_nw, const int32_t *grp_nb, const int32_t *win_tok,
+    long long stamp) {
     const int lane = (int)(threadIdx.x & 63);
     const int64_t c = m_wave_index();
-    if (c >= n_chunks) return;
+    if (c >= (int64_t)ctr->move_chunks) return;
     // the group whose chunks hold c: cstart[k] <= c < cstart[k + 1]
     int64_t lo = 0, hi = n_add;
     while (lo < hi) {

@@ -793,18 +793,30 @@ pr_status run_merge(pr_forest *f, const int32_t *peer_of, const int32_t *tokens,
             hipLaunchKernelGGL(pr::add_group_kernel, dim3(grid_threads(n_add, bs)), dim3(bs), 0, s, dev_view(f),
                                m.keys_out, m.vals_out, n_add, m.st, m.win, m.rest, m.widx, m.poff, m.hd, m.cstart,
                                m.grp_nw, m.grp_pool, m.win_tok, m.win_ins, f->d_ctr);
-            if ((r = read_counters(f, &c, s))) return r;
-            if ((r = ensure_capacity(f, (int64_t)c.n_nodes + (int64_t)c.node_need,
-                                     (int64_t)c.n_pool + (int64_t)c.pool_need, s)))
-                return r;
+            // A round adds at most one record per old child of the rebuilt
+            // parents (at most every record) plus one leaf per insert, and at
+            // most the pool tokens the walk's tally bounded; when the spare
+            // capacity holds that, no readback is needed before allocating,
+            // and the move kernel's grid takes the matching chunk bound.
+            int64_t chunks;
+            const int64_t nodes_ub = 2 * f->dev.n_nodes + n_add;
+            const int64_t pool_ub = f->dev.n_pool + (int64_t)c.pool_need;
+            if (nodes_ub <= f->dev.cap_nodes && pool_ub <= f->dev.cap_pool) {
+                chunks = (f->dev.n_nodes + 63) / 64 + n_add;  // sum over groups of ceil(old children / 64)
+            } else {
+                if ((r = read_counters(f, &c, s))) return r;
+                if ((r = ensure_capacity(f, (int64_t)c.n_nodes + (int64_t)c.node_need,
+                                         (int64_t)c.n_pool + (int64_t)c.pool_need, s)))
+                    return r;
+                chunks = (int64_t)c.move_chunks;
+            }
             const long long stamp = ++f->stamp;
             const pr::DevForest F = dev_view(f);
-            const int64_t chunks = (int64_t)c.move_chunks;
             hipLaunchKernelGGL(pr::add_alloc_kernel, dim3(grid_threads(n_add, bs)), dim3(bs), 0, s, F, m.keys_out,
                                n_add, m.grp_nw, m.grp_pool, m.grp_nb, m.grp_pb, f->d_ctr);
             if (chunks > 0)
                 hipLaunchKernelGGL(pr::add_move_kernel, dim3(grid_waves(chunks)), dim3(wb), 0, s, F, m.keys_out,
-                                   n_add, m.cstart, chunks, m.grp_nw, m.grp_nb, m.win_tok, stamp);
+                                   n_add, m.cstart, f->d_ctr, m.grp_nw, m.grp_nb, m.win_tok, stamp);
             hipLaunchKernelGGL(pr::add_leaf_kernel, dim3(grid_waves(n_add)), dim3(wb), 0, s, F, B, m.keys_out,
                                m.vals_out, n_add, m.st, m.win, m.widx, m.poff, m.hd, m.grp_nb, m.grp_pb);
             hipLaunchKernelGGL(pr::add_sep_kernel, dim3(grid_waves(n_add)), dim3(wb), 0, s, F, m.keys_out, n_add,

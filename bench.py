@@ -476,7 +476,7 @@ def main() -> int:
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        sys.stderr.write("bench.py: this build measures one GPU only; multi-GPU runs are not part of it "
+        sys.stderr.write("bench.py: measures one GPU only; runs on several GPUs are not supported "
                          "(queries would shard across GPUs with the forest replicated)\n")
         return 2
 

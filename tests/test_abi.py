@@ -28,6 +28,20 @@ def test_library_exports_every_declared_symbol():
     assert set(declared_functions()) == set(R.EXPORTED)
 
 
+def test_abi_version_and_info_layout_agree():
+    """The library reports the header's PR_ABI_VERSION, and the binding's copy
+    of pr_forest_info has the header's fields in the header's order."""
+    from paper_2606_17059_amd import router as R
+    src = open(os.path.join(ROOT, "include", "prefix_router.h")).read()
+    version = int(re.search(r"#define PR_ABI_VERSION (\d+)", src).group(1))
+    assert R.lib().pr_abi_version() == version
+    body = re.search(r"typedef struct \{(.*?)\} pr_forest_info;", src, flags=re.S).group(1)
+    body = re.sub(r"/\*.*?\*/", "", body, flags=re.S)
+    fields = re.findall(r"(int32_t|int64_t)\s+(\w+);", body)
+    ctypes_of = {"int32_t": ctypes.c_int32, "int64_t": ctypes.c_int64}
+    assert [(n, ctypes_of[t]) for t, n in fields] == list(R.ForestInfo._fields_)
+
+
 def test_binding_refuses_missing_library(monkeypatch, tmp_path):
     from paper_2606_17059_amd import router as R
     monkeypatch.setattr(R, "_lib_handle", None)

@@ -46,6 +46,14 @@ def oracle_for(snapshot, num_peers):
     return o
 
 
+def radix_for(snapshot, num_peers, split_block=0):
+    """The per-peer radix-tree oracle loaded with a snapshot: fast enough to
+    check every row of the full-size workloads."""
+    o = oracle.RadixOracle(num_peers, split_block=split_block)
+    o.load_seqset(snapshot)
+    return o
+
+
 def nthreads() -> int:
     n = os.cpu_count() or 1
     return max(1, min(n, 16))

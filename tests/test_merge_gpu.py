@@ -8,7 +8,7 @@ import oracle
 import pins
 import workloads as W
 from gpu_util import (announce, assert_properties, assert_rows_equal, device, gpu_route, nthreads,
-                      oracle_for, to_dev)
+                      oracle_for, radix_for, to_dev)
 
 pytestmark = pytest.mark.gpu
 
@@ -171,16 +171,23 @@ def test_snapshot_load_after_merges():
     assert_rows_equal(m, c, m_or, c_or, what="merge after reload")
 
 
-def _stream_phases(w, dist, f, o, sample, label):
+def _stream_phases(w, dist, f, o, label, linear=None, linear_sample=0):
+    """Each round: the merge batch into the GPU forest and into the oracle,
+    then the round's lookups, every row compared; with ``linear`` also a
+    sample against the linear-scan oracle."""
     for ph in w.phases(dist):
         _merge(f, ph.inserts, f"{label} {dist} round {ph.round}")
         o.merge(ph.inserts.peer, ph.inserts.tokens, ph.inserts.offsets)
         m, c = gpu_route(f, ph.queries, f"{label} {dist} round {ph.round}")
         assert_properties(m, c, ph.queries, f"{label} {dist} {ph.round}")
-        idx = np.arange(len(ph.queries)) if sample is None else \
-            np.unique(np.random.default_rng(ph.round).choice(len(ph.queries), sample, replace=False))
-        m_or, c_or = o.route_seqset(ph.queries, idx, nthreads())
-        assert_rows_equal(m, c, m_or, c_or, idx if sample is not None else None, f"{label} {dist} {ph.round}")
+        announce(f"{label} {dist} round {ph.round}: oracle, every row")
+        m_or, c_or = o.route(ph.queries.tokens, ph.queries.offsets, nthreads())
+        assert_rows_equal(m, c, m_or, c_or, what=f"{label} {dist} {ph.round} every row")
+        if linear is not None:
+            linear.merge(ph.inserts.peer, ph.inserts.tokens, ph.inserts.offsets)
+            idx = np.unique(np.random.default_rng(ph.round).choice(len(ph.queries), linear_sample, replace=False))
+            m_ls, c_ls = linear.route_seqset(ph.queries, idx, nthreads())
+            assert_rows_equal(m, c, m_ls, c_ls, idx, f"{label} {dist} {ph.round} linear-scan sample")
         # the inserted prompts now match their replicas in full
         k = min(64, len(ph.inserts))
         sub = ph.inserts.subset(np.arange(k))
@@ -193,7 +200,7 @@ def test_stream_config_small():
     for dist in ("uniform", "zipf"):
         f = _forest(w.snapshot, 128)
         o = oracle_for(w.snapshot, 128)
-        _stream_phases(w, dist, f, o, None, "stream small")
+        _stream_phases(w, dist, f, o, "stream small")
         f.close()
         o.close()
 
@@ -201,12 +208,15 @@ def test_stream_config_small():
 @pytest.mark.timeout(1500)
 def test_stream_config_full():
     """128 peers x 2,000 prompts; 4 rounds of (10,000 inserts, 1,048,576 lookups)
-    per topic distribution; exact on 384 sampled lookups per phase."""
+    per topic distribution; every lookup of every phase against the radix-tree
+    oracle, 48 per phase against the linear scan."""
     announce("stream full: generating")
     w = W.make_config(5)
     for dist in ("uniform", "zipf"):
         f = _forest(w.snapshot, 128)
-        o = oracle_for(w.snapshot, 128)
-        _stream_phases(w, dist, f, o, 384, "stream full")
+        r = radix_for(w.snapshot, 128)
+        lin = oracle_for(w.snapshot, 128)
+        _stream_phases(w, dist, f, r, "stream full", linear=lin, linear_sample=48)
         f.close()
-        o.close()
+        r.close()
+        lin.close()

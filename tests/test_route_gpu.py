@@ -1,8 +1,10 @@
 """Route parity on the GPU: the HIP path through the C ABI versus the CPU oracle.
 
 Integer outputs, so the bar is bit-exact: every match length and every chosen
-peer.  Small cases compare every row; full-size configurations compare a
-sampled set of rows exactly and check properties on all rows.
+peer, on every row.  Small cases compare with the linear-scan oracle;
+full-size workloads with the per-peer radix-tree oracle (itself pinned to the
+linear scan), plus a sample with the linear scan so the two oracles agree at
+full size too.
 """
 import numpy as np
 import pytest
@@ -11,7 +13,7 @@ import oracle
 import pins
 import workloads as W
 from gpu_util import (announce, assert_properties, assert_rows_equal, device, gpu_route, nthreads,
-                      oracle_for, to_dev)
+                      oracle_for, radix_for, to_dev)
 
 pytestmark = pytest.mark.gpu
 
@@ -77,18 +79,23 @@ def test_config1_tiny_all_rows():
 
 @pytest.mark.timeout(900)
 def test_config2_medium_full_batch():
-    """The benchmark's workload and launch (65,536 queries, 16 peers): exact on
-    a 4,096-row sample plus a ragged tail, properties on every row."""
+    """The medium workload's full batch (65,536 queries, 16 peers): every row
+    against the radix-tree oracle, a sample and the ragged tail against the
+    linear scan too."""
     w = W.make_config(2)
     f = _forest(w.snapshot, w.num_peers)
     m, c = gpu_route(f, w.queries, "config 2 medium full")
     assert_properties(m, c, w.queries, "config 2")
+    r = radix_for(w.snapshot, w.num_peers)
+    m_rx, c_rx = r.route(w.queries.tokens, w.queries.offsets, nthreads())
+    r.close()
+    assert_rows_equal(m, c, m_rx, c_rx, what="config 2 every row")
     rng = np.random.default_rng(2)
-    idx = np.unique(np.concatenate([rng.choice(len(w.queries), 4096, replace=False),
+    idx = np.unique(np.concatenate([rng.choice(len(w.queries), 512, replace=False),
                                     np.arange(len(w.queries) - 37, len(w.queries))]))
     o = oracle_for(w.snapshot, w.num_peers)
     m_or, c_or = o.route_seqset(w.queries, idx, nthreads())
-    assert_rows_equal(m, c, m_or, c_or, idx, "config 2 sample")
+    assert_rows_equal(m, c, m_or, c_or, idx, "config 2 linear-scan sample")
     # determinism: a second launch gives identical bytes
     m2, c2 = gpu_route(f, w.queries, "config 2 medium repeat")
     assert np.array_equal(m, m2) and np.array_equal(c, c2)
@@ -159,40 +166,49 @@ def _sample(n, k, seed):
 @pytest.mark.timeout(1200)
 def test_config3_stale_estimates_and_truth_full_batch():
     """64 peers, 262,144 queries: the estimated forest (stale replicas) and the
-    true forest, each exact against the oracle on a sample and checked on every
-    row; estimates never match more than the truth (Section "Stale trie
-    estimates")."""
+    true forest, every row of each against the radix-tree oracle; estimates
+    never match more than the truth (Section "Stale trie estimates")."""
     announce("config 3: generating")
     w = W.make_config(3)
-    fe = _forest(w.snapshot, w.num_peers)
-    me, ce = gpu_route(fe, w.queries, "config 3 estimated forest")
-    fe.close()
-    ft = _forest(w.true_snapshot, w.num_peers)
-    mt, ct = gpu_route(ft, w.queries, "config 3 true forest")
-    ft.close()
-    assert_properties(me, ce, w.queries, "config 3 est")
-    assert_properties(mt, ct, w.queries, "config 3 true")
+    out = {}
+    for snap, what in ((w.snapshot, "est"), (w.true_snapshot, "true")):
+        f = _forest(snap, w.num_peers)
+        m, c = gpu_route(f, w.queries, f"config 3 {what} forest")
+        f.close()
+        assert_properties(m, c, w.queries, f"config 3 {what}")
+        announce(f"config 3 {what}: radix oracle, every row")
+        r = radix_for(snap, w.num_peers)
+        m_rx, c_rx = r.route(w.queries.tokens, w.queries.offsets, nthreads())
+        r.close()
+        assert_rows_equal(m, c, m_rx, c_rx, what=f"config 3 {what} every row")
+        out[what] = (m, c)
+    (me, ce), (mt, _) = out["est"], out["true"]
     assert (me <= mt).all() and np.array_equal(me[:, 0], mt[:, 0])
-    idx = _sample(len(w.queries), 768, 3)
-    for snap, m, c, what in ((w.snapshot, me, ce, "est"), (w.true_snapshot, mt, ct, "true")):
-        o = oracle_for(snap, w.num_peers)
-        m_or, c_or = o.route_seqset(w.queries, idx, nthreads())
-        assert_rows_equal(m, c, m_or, c_or, idx, f"config 3 {what} sample")
-        o.close()
+    idx = _sample(len(w.queries), 64, 3)
+    o = oracle_for(w.snapshot, w.num_peers)
+    m_or, c_or = o.route_seqset(w.queries, idx, nthreads())
+    o.close()
+    assert_rows_equal(me, ce, m_or, c_or, idx, "config 3 est linear-scan sample")
 
 
 @pytest.mark.timeout(900)
 def test_config4_long_context_full_batch():
-    """32 peers, 8K-33K-token shared prefixes, 32,768 queries."""
+    """32 peers, 8K-33K-token shared prefixes, 32,768 queries: every row
+    against the radix-tree oracle with nodes forced at every 16-token block
+    (the workload's split granularity), a sample against the linear scan."""
     announce("config 4: generating")
     w = W.make_config(4)
     f = _forest(w.snapshot, w.num_peers)
     m, c = gpu_route(f, w.queries, "config 4 long")
     assert_properties(m, c, w.queries, "config 4")
-    idx = _sample(len(w.queries), 2048, 4)
+    r = radix_for(w.snapshot, w.num_peers, split_block=16)
+    m_rx, c_rx = r.route(w.queries.tokens, w.queries.offsets, nthreads())
+    r.close()
+    assert_rows_equal(m, c, m_rx, c_rx, what="config 4 every row")
+    idx = _sample(len(w.queries), 256, 4)
     o = oracle_for(w.snapshot, w.num_peers)
     m_or, c_or = o.route_seqset(w.queries, idx, nthreads())
-    assert_rows_equal(m, c, m_or, c_or, idx, "config 4 sample")
+    assert_rows_equal(m, c, m_or, c_or, idx, "config 4 linear-scan sample")
 
 
 def test_route_launcher_matches_oracle():
@@ -469,3 +485,119 @@ def test_label_width_follows_the_tokens():
     assert g.info()["label_token_bytes"] == 4
     g.close()
     og.close()
+
+
+def _wide_block_sets(rng, n_children, P):
+    """Sequences under one node with n_children distinct next tokens: a shared
+    3-token head, then one of n_children distinct tokens (even numbers, so that
+    odd tokens fall between two children), then a short random tail; spread
+    over P peers.  Also n_children sequences that start with distinct tokens,
+    so the root's block is as wide."""
+    kids = np.sort(rng.choice(np.arange(0, 8 * n_children, 2), n_children, replace=False)).astype(np.int64)
+    head = [900001, 900002, 900003]
+    seqs, owners = [], []
+    for i, t in enumerate(kids.tolist()):
+        tail = rng.integers(0, 4, int(rng.integers(0, 6))).tolist()
+        seqs.append(head + [t] + tail)
+        owners.append(i % P)
+        seqs.append([t, 5] + tail)
+        owners.append((i + 1) % P)
+    return seqs, owners, kids, head
+
+
+def _wide_block_queries(rng, seqs, kids, head):
+    """Hits, misses between, below and above the children, and the tokens at
+    and around the block's separator positions (rank k * n / 64)."""
+    n = len(kids)
+    qs = []
+    for r in sorted({(k * n) // 64 for k in range(64)} | {n - 1}):
+        for d in (-1, 0, 1):
+            t = int(kids[r]) + d
+            qs.append(head + [t, 0, 1])
+            qs.append([t, 5, 0])
+    for t in (int(kids[0]) - 2, int(kids[-1]) + 2, -5, 2 ** 31 - 1):
+        qs.append(head + [t])
+        qs.append([t, 5])
+    for i in rng.choice(len(seqs), 300, replace=False).tolist():
+        s = list(seqs[i])
+        qs.append(s)
+        qs.append(s + [7])
+        if len(s) > 4:
+            qs.append(s[:-1] + [s[-1] + 1])
+    return qs
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("n_children", [4097, 5000, 20000])
+def test_child_blocks_wider_than_4096(n_children):
+    """Child blocks of more than 64 x 64 children take a 64-ary search after
+    the separators, in the route's child locate and in the merge walk's.
+    Built by a host load, and again by a load of half the sequences followed
+    by merges of the other half (new children, extensions through the wide
+    block, duplicates); every row against the oracle."""
+    import torch
+    rng = np.random.default_rng(n_children)
+    P = 3
+    seqs, owners, kids, head = _wide_block_sets(rng, n_children, P)
+    qs = W.from_lists(_wide_block_queries(rng, seqs, kids, head))
+    snap = W.from_lists(seqs, owners)
+    o = oracle_for(snap, P)
+    m_or, c_or = o.route(qs.tokens, qs.offsets, nthreads())
+    o.close()
+    f = _forest(snap, P)
+    m, c = gpu_route(f, qs, f"wide block {n_children}: host load")
+    assert_rows_equal(m, c, m_or, c_or, what=f"wide block {n_children} host load")
+    f.close()
+    # half by host load, the rest (and extensions of the loaded half) by merges
+    half = np.arange(0, len(seqs), 2)
+    rest = np.arange(1, len(seqs), 2)
+    g = _forest(snap.subset(half), P)
+    gpu_route(g, qs.subset(np.arange(4)), "wide block: first upload")
+    ext = [list(seqs[i]) + [int(rng.integers(0, 4))] for i in half[::3]]
+    batches = [(np.array([owners[i] for i in rest], np.int32), [seqs[i] for i in rest]),
+               (np.array([owners[i] for i in half[::3]], np.int32), ext),
+               (np.array([owners[i] for i in rest[:500]], np.int32), [seqs[i] for i in rest[:500]])]
+    og = oracle_for(snap.subset(half), P)
+    for k, (peers, bseqs) in enumerate(batches):
+        t, off = pins._csr(bseqs)
+        announce(f"wide block {n_children}: merge batch {k} of {len(bseqs)}")
+        g.merge(torch.from_numpy(peers).to(device()), torch.from_numpy(t).to(device()),
+                torch.from_numpy(off).to(device()))
+        og.merge(peers, t, off)
+        m, c = gpu_route(g, qs, f"wide block {n_children}: after merge {k}")
+        m_or, c_or = og.route(qs.tokens, qs.offsets, nthreads())
+        assert_rows_equal(m, c, m_or, c_or, what=f"wide block {n_children} merge {k}")
+    g.check()
+    g.close()
+    og.close()
+
+
+def test_narrow_labels_with_query_tokens_out_of_range():
+    """While labels are read as 16-bit values, a query token outside
+    [0, 65535] must still differ from every label token: in the middle of a
+    label, the label token k is replaced by 65536 + k, k - 65536, k + 2^31
+    (wrapped) and -1; the walk must stop there, as the oracle's int32 compare
+    does."""
+    rng = np.random.default_rng(99)
+    P = 2
+    seqs = [rng.integers(0, 65536, int(rng.integers(40, 300))).tolist() for _ in range(30)]
+    owners = [i % P for i in range(len(seqs))]
+    snap = W.from_lists(seqs, owners)
+    f = _forest(snap, P)
+    qs = []
+    for s in seqs:
+        for pos in (0, 1, len(s) // 2, len(s) - 1):
+            k = s[pos]
+            for bad in (k + 65536, k - 65536, (k + 2 ** 31) % 2 ** 32 - 2 ** 31, -1, k + 131072):
+                q = list(s)
+                q[pos] = int(bad)
+                qs.append(q)
+        qs.append(list(s))
+    queries = W.from_lists(qs)
+    m, c = gpu_route(f, queries, "narrow labels, wide query tokens")
+    assert f.info()["label_token_bytes"] == 2
+    o = oracle_for(snap, P)
+    m_or, c_or = o.route(queries.tokens, queries.offsets, nthreads())
+    assert_rows_equal(m, c, m_or, c_or, what="narrow labels, wide query tokens")
+    o.close()
+    f.close()

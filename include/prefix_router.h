@@ -158,6 +158,31 @@ pr_status pr_route(pr_forest *f, const int32_t *q_tokens, int64_t num_tokens,
                    int32_t *chosen, void *hip_stream);
 
 /*
+ * pr_route for callers that cannot allocate device memory: code under HIP
+ * graph capture, tight serving loops, harnesses that forbid hipMalloc.  Same
+ * arguments, results and stream behaviour as pr_route, except:
+ *   - at most PR_NOALLOC_MAX_QUERIES queries per call (PR_EINVAL beyond);
+ *   - the forest must already be on the device: after pr_load_snapshot, run
+ *     pr_route (or any other device call) once first, else PR_ESTATE;
+ *   - the longest-first order of a batch (see pr_route) is kept in a static
+ *     device array of the library, not in a buffer of the forest: about
+ *     321 KiB on each GPU the library runs on, held until the process ends.
+ *     Every call on one GPU, for any forest, uses that GPU's array, which
+ *     keeps the previous call's contents (each call writes every entry it
+ *     reads first).  Calls that overlap on one GPU (different streams or host
+ *     threads) race on it: order them, e.g. on one stream.
+ * The call allocates no host or device memory and enqueues kernel launches
+ * only (no copy, wait or event).
+ * Errors (host side, nothing enqueued): PR_EINVAL (as pr_route, or more than
+ * PR_NOALLOC_MAX_QUERIES queries), PR_ESTATE, PR_EDEVICE.
+ */
+#define PR_NOALLOC_MAX_QUERIES 65536
+
+pr_status pr_route_noalloc(pr_forest *f, const int32_t *q_tokens, int64_t num_tokens,
+                           const int64_t *q_offsets, int64_t num_queries, int32_t *match_len,
+                           int32_t *chosen, void *hip_stream);
+
+/*
  * sendTrie, receive side, for a snapshot already in DEVICE memory (for
  * example received by a GPU-direct transfer).  Same semantics as
  * pr_load_snapshot: REPLACES peer's tree by the set of num_seqs sequences

@@ -9,6 +9,7 @@
 #include <algorithm>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <rocprim/device/device_radix_sort.hpp>
 #include <rocprim/device/device_scan.hpp>
@@ -541,6 +542,23 @@ bool use_longest_first(int64_t nq, int64_t ntok) {
            ntok >= 4096 * nq;
 }
 
+// The two order launches (at most 16 workgroups each) on stream s: bkt gets
+// every query's length bucket (a quarter of the mean query wide), blockcnt
+// the per-workgroup bucket counts, order the queries longest first.  Every
+// entry read is written earlier in the same two launches, so the buffers need
+// no clearing.  nq <= pr::kOrderMaxQueries.
+pr_status launch_order(const int64_t *q_offsets, int64_t nq, int64_t ntok, hipStream_t s, uint8_t *bkt,
+                       int32_t *blockcnt, int32_t *order) {
+    const uint32_t unit = (uint32_t)std::min<int64_t>(std::max<int64_t>(1, ntok / nq / 4), INT32_MAX);
+    const unsigned blocks = (unsigned)((nq + pr::kOrderChunk - 1) / pr::kOrderChunk);
+    hipLaunchKernelGGL(pr::route_order_count_kernel, dim3(blocks), dim3(pr::kOrderThreads), 0, s, q_offsets,
+                       (int32_t)nq, unit, bkt, blockcnt);
+    hipLaunchKernelGGL(pr::route_order_scatter_kernel, dim3(blocks), dim3(pr::kOrderThreads), 0, s, bkt,
+                       (int32_t)nq, blockcnt, order);
+    if (hipGetLastError() != hipSuccess) return fail(PR_EDEVICE, "route order launch failed");
+    return PR_OK;
+}
+
 // Fill f->rs.order with the queries longest first (two launches of at most 16
 // workgroups) on stream s; length buckets are a quarter of the mean query wide.
 pr_status route_order(pr_forest *f, const int64_t *q_offsets, int64_t nq, int64_t ntok, hipStream_t s,
@@ -566,13 +584,8 @@ pr_status route_order(pr_forest *f, const int64_t *q_offsets, int64_t nq, int64_
     }
     if (R.pending && hipStreamWaitEvent(s, R.done, 0) != hipSuccess)
         return fail(PR_EDEVICE, "hipStreamWaitEvent failed");
-    const uint32_t unit = (uint32_t)std::min<int64_t>(std::max<int64_t>(1, ntok / nq / 4), INT32_MAX);
-    const unsigned blocks = (unsigned)((nq + pr::kOrderChunk - 1) / pr::kOrderChunk);
-    hipLaunchKernelGGL(pr::route_order_count_kernel, dim3(blocks), dim3(pr::kOrderThreads), 0, s, q_offsets,
-                       (int32_t)nq, unit, R.bkt, R.blockcnt);
-    hipLaunchKernelGGL(pr::route_order_scatter_kernel, dim3(blocks), dim3(pr::kOrderThreads), 0, s, R.bkt,
-                       (int32_t)nq, R.blockcnt, R.order);
-    if (hipGetLastError() != hipSuccess) return fail(PR_EDEVICE, "route order launch failed");
+    pr_status r = launch_order(q_offsets, nq, ntok, s, R.bkt, R.blockcnt, R.order);
+    if (r) return r;
     *order = R.order;
     return PR_OK;
 }
@@ -602,6 +615,61 @@ hipError_t launch_route(const pr_forest *f, const int32_t *qt, int64_t ntok, con
     else
         launch_route_t<W, true>(f, f->dev.pool, qt, ntok, qo, nq, sel, ml, ch, order, s);
     return hipGetLastError();
+}
+
+// The route kernel for the forest's mask-word count.
+hipError_t launch_route_w(const pr_forest *f, const int32_t *qt, int64_t ntok, const int64_t *qo, int64_t nq,
+                          const pr::Select &sel, int32_t *ml, int32_t *ch, const int32_t *order, hipStream_t s) {
+    switch (f->W) {
+        case 1: return launch_route<1>(f, qt, ntok, qo, nq, sel, ml, ch, order, s);
+        case 2: return launch_route<2>(f, qt, ntok, qo, nq, sel, ml, ch, order, s);
+        case 4: return launch_route<4>(f, qt, ntok, qo, nq, sel, ml, ch, order, s);
+        case 8: return launch_route<8>(f, qt, ntok, qo, nq, sel, ml, ch, order, s);
+        default: return launch_route<16>(f, qt, ntok, qo, nq, sel, ml, ch, order, s);
+    }
+}
+
+// ---- routes without allocation ----------------------------------------------
+// The longest-first order of one pr_route_noalloc call lives in one
+// file-scope device array per GPU (`scratch`, held until the process ends):
+// order (int32 per query), the per-workgroup bucket counts, then each query's
+// length bucket (uint8).  On the host the array's name stands for no device
+// address; its address on each device comes from hipGetSymbolAddress, taken
+// once per device with that device current, and only that address is passed
+// to kernels.
+constexpr int64_t kNoAllocOrder = 0;
+constexpr int64_t kNoAllocBlockcnt = kNoAllocOrder + 4 * (int64_t)pr::kOrderMaxQueries;
+constexpr int64_t kNoAllocBkt = kNoAllocBlockcnt + 4 * (int64_t)pr::kOrderMaxBlocks * pr::kOrderBuckets;
+constexpr int64_t kNoAllocBytes = kNoAllocBkt + (int64_t)pr::kOrderMaxQueries;
+static_assert(PR_NOALLOC_MAX_QUERIES == pr::kOrderMaxQueries, "the header's limit is the order's capacity");
+static_assert(kNoAllocBlockcnt % 256 == 0 && kNoAllocBkt % 256 == 0, "aligned sub-arrays");
+constexpr int kNoAllocMaxDevices = 64;
+
+}  // namespace
+
+static __device__ __align__(256) unsigned char scratch[kNoAllocBytes];
+
+namespace {
+
+std::mutex g_scratch_mu;
+unsigned char *g_scratch_dev[kNoAllocMaxDevices] = {};
+
+// The current device's address of `scratch` (dev must be current).
+pr_status noalloc_scratch(int dev, unsigned char **out) {
+    if (dev < 0 || dev >= kNoAllocMaxDevices) return fail(PR_EDEVICE, "device id beyond the scratch table");
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_dev[dev]) {
+        void *p = nullptr;
+        const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p) {
+            (void)hipGetLastError();
+            return fail(PR_EDEVICE, std::string("hipGetSymbolAddress of the route scratch failed: ") +
+                                        hipGetErrorString(e));
+        }
+        g_scratch_dev[dev] = static_cast<unsigned char *>(p);
+    }
+    *out = g_scratch_dev[dev];
+    return PR_OK;
 }
 
 // ---- merge ------------------------------------------------------------------
@@ -1609,24 +1677,8 @@ static pr_status route_impl(pr_forest *f, const int32_t *q_tokens, int64_t num_t
     if (!capturing && use_longest_first(num_queries, num_tokens) &&
         (s = route_order(f, q_offsets, num_queries, num_tokens, st, &order)))
         return s;
-    hipError_t e;
-    switch (f->W) {
-        case 1:
-            e = launch_route<1>(f, q_tokens, num_tokens, q_offsets, num_queries, sel, match_len, chosen, order, st);
-            break;
-        case 2:
-            e = launch_route<2>(f, q_tokens, num_tokens, q_offsets, num_queries, sel, match_len, chosen, order, st);
-            break;
-        case 4:
-            e = launch_route<4>(f, q_tokens, num_tokens, q_offsets, num_queries, sel, match_len, chosen, order, st);
-            break;
-        case 8:
-            e = launch_route<8>(f, q_tokens, num_tokens, q_offsets, num_queries, sel, match_len, chosen, order, st);
-            break;
-        default:
-            e = launch_route<16>(f, q_tokens, num_tokens, q_offsets, num_queries, sel, match_len, chosen, order, st);
-            break;
-    }
+    const hipError_t e = launch_route_w(f, q_tokens, num_tokens, q_offsets, num_queries, sel, match_len, chosen,
+                                        order, st);
     if (e != hipSuccess) return fail(PR_EDEVICE, std::string("route launch failed: ") + hipGetErrorString(e));
     if (order) {
         // the order buffers are in use until the stream passes this launch
@@ -1645,6 +1697,40 @@ pr_status pr_route(pr_forest *f, const int32_t *q_tokens, int64_t num_tokens, co
     if (num_tokens > 0 && !q_tokens) return fail(PR_EINVAL, "q_tokens is NULL");
     const pr::Select sel{nullptr, -1, 0, nullptr};
     return route_impl(f, q_tokens, num_tokens, q_offsets, num_queries, sel, match_len, chosen, hip_stream);
+}
+
+pr_status pr_route_noalloc(pr_forest *f, const int32_t *q_tokens, int64_t num_tokens, const int64_t *q_offsets,
+                           int64_t num_queries, int32_t *match_len, int32_t *chosen, void *hip_stream) {
+    if (!f) return fail(PR_EINVAL, "forest is NULL");
+    if (num_queries < 0 || num_tokens < 0) return fail(PR_EINVAL, "negative count");
+    if (num_queries > PR_NOALLOC_MAX_QUERIES)
+        return fail(PR_EINVAL, "pr_route_noalloc takes at most " + std::to_string(PR_NOALLOC_MAX_QUERIES) +
+                                   " queries per call");
+    if (num_queries == 0) return ok();
+    if (!q_offsets || !match_len || !chosen) return fail(PR_EINVAL, "NULL device pointer");
+    if (num_tokens > 0 && !q_tokens) return fail(PR_EINVAL, "q_tokens is NULL");
+    if (f->broken) return fail(PR_ESTATE, "an earlier device update failed; destroy the forest");
+    if (f->dirty || !f->has_dev)
+        return fail(PR_ESTATE, "snapshots changed since the forest's last upload; call pr_route once first");
+    DeviceScope ds(f);
+    if (!ds.ok()) return fail(PR_EDEVICE, "cannot select the forest's device");
+    hipStream_t st = (hipStream_t)hip_stream;
+    unsigned char *sp = nullptr;
+    pr_status r = noalloc_scratch(f->device, &sp);
+    if (r) return r;
+    const int32_t *order = nullptr;
+    if (use_longest_first(num_queries, num_tokens)) {
+        int32_t *ord = reinterpret_cast<int32_t *>(sp + kNoAllocOrder);
+        if ((r = launch_order(q_offsets, num_queries, num_tokens, st, sp + kNoAllocBkt,
+                              reinterpret_cast<int32_t *>(sp + kNoAllocBlockcnt), ord)))
+            return r;
+        order = ord;
+    }
+    const pr::Select sel{nullptr, -1, 0, nullptr};
+    const hipError_t e = launch_route_w(f, q_tokens, num_tokens, q_offsets, num_queries, sel, match_len, chosen,
+                                        order, st);
+    if (e != hipSuccess) return fail(PR_EDEVICE, std::string("route launch failed: ") + hipGetErrorString(e));
+    return ok();
 }
 
 pr_status pr_route_select(pr_forest *f, const int32_t *q_tokens, int64_t num_tokens, const int64_t *q_offsets,

@@ -18,9 +18,11 @@ LIB_PATH = os.path.join(_PKG, "libprefix_router.so")
 
 PR_OK, PR_EINVAL, PR_ENOMEM, PR_EDEVICE, PR_ESTATE = 0, -1, -2, -3, -4
 PR_MAX_PEERS = 1024
+PR_NOALLOC_MAX_QUERIES = 65536
 
 EXPORTED = ("pr_abi_version", "pr_last_error", "pr_forest_create", "pr_forest_destroy",
             "pr_load_snapshot", "pr_load_snapshot_device", "pr_export_snapshot", "pr_merge", "pr_route",
+            "pr_route_noalloc",
             "pr_route_select", "pr_tree_tokens", "pr_forest_compact", "pr_set_local_peer", "pr_set_time", "pr_touch", "pr_evict_lru",
             "pr_forest_check",
             "pr_forest_info_get", "pr_forest_host_image")
@@ -96,6 +98,8 @@ def lib() -> ctypes.CDLL:
     L.pr_merge.argtypes = [_vp, _vp, _vp, ctypes.c_int64, _vp, ctypes.c_int64, _vp]
     L.pr_merge.restype = ctypes.c_int32
     L.pr_route.argtypes = [_vp, _vp, ctypes.c_int64, _vp, ctypes.c_int64, _vp, _vp, _vp]
+    L.pr_route_noalloc.restype = ctypes.c_int32
+    L.pr_route_noalloc.argtypes = [_vp, _vp, ctypes.c_int64, _vp, ctypes.c_int64, _vp, _vp, _vp]
     L.pr_route.restype = ctypes.c_int32
     L.pr_route_select.argtypes = [_vp, _vp, ctypes.c_int64, _vp, ctypes.c_int64, _vp, ctypes.c_int32,
                                   ctypes.c_uint32, _vp, _vp, _vp, _vp]
@@ -255,6 +259,24 @@ def pr_route(f: int, q_tokens, q_offsets, match_len, chosen, num_peers: int, str
                           _stream_ptr(stream, q_offsets.device)))
 
 
+def pr_route_noalloc(f: int, q_tokens, q_offsets, match_len, chosen, num_peers: int, stream=None) -> None:
+    """pr_route without allocation (at most PR_NOALLOC_MAX_QUERIES queries;
+    the forest must be on the device already)."""
+    import torch
+    _dev(q_tokens, torch.int32, "q_tokens")
+    _dev(q_offsets, torch.int64, "q_offsets")
+    _dev(match_len, torch.int32, "match_len")
+    _dev(chosen, torch.int32, "chosen")
+    nq = q_offsets.numel() - 1
+    if nq < 0:
+        raise ValueError("q_offsets must have at least one entry")
+    if match_len.numel() != nq * num_peers or chosen.numel() != nq:
+        raise ValueError("match_len must hold [num_queries][num_peers] and chosen [num_queries]")
+    _check(lib().pr_route_noalloc(f, q_tokens.data_ptr() or None, q_tokens.numel(), q_offsets.data_ptr(), nq,
+                                  match_len.data_ptr() or None, chosen.data_ptr() or None,
+                                  _stream_ptr(stream, q_offsets.device)))
+
+
 def pr_route_select(f: int, q_tokens, q_offsets, eligible, local_peer: int, flags: int, match_len, best, second,
                     num_peers: int, stream=None) -> None:
     """eligible: CUDA uint64 tensor of ceil(num_peers / 64) words (torch.int64
@@ -404,6 +426,11 @@ class Forest:
         if chosen is None:
             chosen = torch.empty(nq, dtype=torch.int32, device=dev)
         pr_route(self.handle, q_tokens, q_offsets, match_len, chosen, self.num_peers, stream)
+        return match_len, chosen
+
+    def route_noalloc(self, q_tokens, q_offsets, match_len, chosen, stream=None) -> Tuple:
+        """pr_route_noalloc into caller-allocated outputs."""
+        pr_route_noalloc(self.handle, q_tokens, q_offsets, match_len, chosen, self.num_peers, stream)
         return match_len, chosen
 
     def route_launcher(self, q_tokens, q_offsets, match_len, chosen, stream=None):

@@ -89,3 +89,23 @@ def test_lru_argument_errors_without_gpu():
         assert L.pr_touch(f, None, -1, None, 0, None) == R.PR_EINVAL
     finally:
         R.pr_forest_destroy(f)
+
+
+def test_route_noalloc_argument_errors_without_gpu():
+    """pr_route_noalloc refuses a NULL forest and more queries than its scratch
+    holds before any device work (the pointers are never read)."""
+    from paper_2606_17059_amd import router as R
+    L = R.lib()
+    f = R.pr_forest_create(3)
+    try:
+        dummy = ctypes.c_void_p(16)
+        n_over = R.PR_NOALLOC_MAX_QUERIES + 1
+        assert L.pr_route_noalloc(None, dummy, 4, dummy, 1, dummy, dummy, None) == R.PR_EINVAL
+        assert L.pr_route_noalloc(f, dummy, 4, dummy, n_over, dummy, dummy, None) == R.PR_EINVAL
+        assert "at most" in R.pr_last_error()
+        assert L.pr_route_noalloc(f, dummy, 4, dummy, -1, dummy, dummy, None) == R.PR_EINVAL
+        assert L.pr_route_noalloc(f, None, 0, None, 0, None, None, None) == R.PR_OK
+        # a forest never uploaded: refused, nothing enqueued
+        assert L.pr_route_noalloc(f, dummy, 4, dummy, 1, dummy, dummy, None) == R.PR_ESTATE
+    finally:
+        R.pr_forest_destroy(f)

@@ -1,18 +1,27 @@
 #!/usr/bin/env python3
 """Throughput of the batched prefix-cache-aware router on one MI355X.
 
-One step = one pr_route over a full query batch of the workload: every query's
-longest-prefix match against every peer's tree plus the argmax over peers
-(walk, child locate, label compare, per-peer lengths, argmax, output write).
-Queries, offsets, outputs and the forest are resident in HBM before the timed
-region; four device copies of the query batch rotate so that the 256 MB
-last-level cache cannot serve the query stream from one step to the next (with
-one copy, lines read with the default cache policy come back from it).
+Default workload: the largest single-GPU one, the streaming workload (128
+peers x 2,000 prompts).  One step = for each of its two topic distributions
+(uniform, Zipf 1.2), the delta-merge of a fresh 10,000-insert batch into that
+distribution's forest followed by a lookup batch of 1,048,576 queries on it:
+every row of the hot path (walk, child locate, label compare, per-peer
+lengths, argmax, output write, merge).  `value` is the lookups routed per
+second of step wall time (merges included); the lookup kernel alone and the
+merges are reported beside it.  `--config N` (1-4) makes a single lookup batch
+of that workload the step instead; `--extra-configs` (default 2,3,4) measures
+those workloads' lookup batches too, under "configs".
 
-Prints one JSON line (rank 0 = the only rank).  Algorithmic bytes per query:
+Inputs are resident in HBM before the timed region.  Every timed output is
+compared with the radix-tree CPU oracle afterwards (bit-exact or the run
+fails), and the oracle's match lengths give the algorithmic bytes per query:
   B_q = 4*min(|q|, M_q + 1) + 4*(P + 1) + 8
 (the query tokens a walk must read, including the mismatching one; the output
-row plus the chosen peer; the int64 query offset).
+row plus the chosen peer; the int64 query offset).  Lookup workloads rotate
+four device copies of their batch so that the 256 MB last-level cache cannot
+serve the query stream from one launch to the next.
+
+Prints one JSON line (rank 0 = the only rank).
 """
 from __future__ import annotations
 
@@ -75,11 +84,13 @@ def step_kernels(nq: int, ntok: int) -> list:
 
 
 def route_kernel_name(f) -> str:
-    """The plain route kernel instantiation a forest's routes run: mask words
-    and label token type (16-bit while every label token fits)."""
+    """The plain route kernel instantiation a forest's routes run: mask words,
+    label token type (16-bit while every label token fits 17 bits) and
+    whether bit 16 comes from the bit plane."""
     info = f.info()
-    lt = "unsigned short" if info["label_token_bytes"] == 2 else "int"
-    return f"route_kernel<{info['mask_words']}, false, {lt}>"
+    lt = "int" if info["label_bits"] == 32 else "unsigned short"
+    hb = "true" if info["label_bits"] == 17 else "false"
+    return f"route_kernel<{info['mask_words']}, false, {lt}, {hb}>"
 
 
 def log(msg: str) -> None:
@@ -88,11 +99,17 @@ def log(msg: str) -> None:
 
 
 def cpu_threads() -> int:
+    """Threads for the CPU oracle: the CPUs this process may run on, at most 16
+    (one GPU's share of the host on the GPU machines)."""
+    return max(1, min(16, host_cpus()["affinity"]))
+
+
+def host_cpus() -> dict:
     try:
-        n = len(os.sched_getaffinity(0))
+        aff = len(os.sched_getaffinity(0))
     except AttributeError:
-        n = os.cpu_count() or 1
-    return max(1, min(16, n))
+        aff = os.cpu_count() or 1
+    return {"logical": os.cpu_count() or 1, "affinity": aff}
 
 
 def cpu_model() -> str:
@@ -105,155 +122,371 @@ def cpu_model() -> str:
     return "unknown"
 
 
-def cpu_baseline(w, queries, target_s: float):
-    """Time the CPU oracle, as it stands, on a bounded sample of the same batch."""
-    import oracle
-    o = oracle.Oracle(w.num_peers)
-    ss = w.snapshot
-    for p in range(w.num_peers):
-        lo, hi = ss.peer_range(p)
-        o.load(p, ss.tokens[ss.offsets[lo]:ss.offsets[hi]], ss.offsets[lo:hi + 1] - ss.offsets[lo])
+def _time_oracle(o, queries, idx, T):
+    sub = queries.subset(idx)
+    t0 = time.perf_counter()
+    o.route(sub.tokens, sub.offsets, T)
+    return time.perf_counter() - t0
+
+
+def cpu_baseline(make_oracles, queries, target_s: float, what: str):
+    """The CPU oracles, as they stand, timed on bounded samples of the batch the
+    GPU routes: the radix-tree oracle (one tree per peer, the paper's own
+    structure) on T threads and on one thread, and the linear-scan oracle on T
+    threads.  ``make_oracles()`` returns (radix, linear) loaded with the forest
+    the GPU routes on."""
+    radix, linear = make_oracles()
     T = cpu_threads()
     rng = np.random.default_rng(12345)
-    n = min(len(queries), 4 * T)
-    while True:
-        idx = np.sort(rng.choice(len(queries), n, replace=False))
-        sub = queries.subset(idx)
-        t0 = time.perf_counter()
-        o.route(sub.tokens, sub.offsets, T)
-        dt = time.perf_counter() - t0
-        if dt >= 0.25 * target_s or n >= len(queries):
-            break
-        n = int(min(len(queries), max(2 * n, n * target_s / max(dt, 1e-3))))
-    # the same oracle on one thread, over a sample sized to about a fifth of the target time
-    n1 = max(1, min(n, int(n * 0.2 * target_s / max(dt * T, 1e-3))))
-    sub1 = queries.subset(np.sort(rng.choice(len(queries), n1, replace=False)))
-    t0 = time.perf_counter()
-    o.route(sub1.tokens, sub1.offsets, 1)
-    dt1 = time.perf_counter() - t0
-    o.close()
+    nq = len(queries)
+
+    def grow(o, threads, budget):
+        n = min(nq, 4 * threads)
+        while True:
+            idx = np.sort(rng.choice(nq, n, replace=False))
+            dt = _time_oracle(o, queries, idx, threads)
+            if dt >= 0.25 * budget or n >= nq:
+                return n, dt
+            n = int(min(nq, max(2 * n, n * budget / max(dt, 1e-3))))
+
+    n, dt = grow(radix, T, 0.5 * target_s)
+    n1, dt1 = grow(radix, 1, 0.15 * target_s)
+    nl, dtl = grow(linear, T, 0.25 * target_s)
+    radix.close()
+    linear.close()
+    cpus = host_cpus()
     return {"value": n / dt, "unit": "queries/s", "cores": T, "kind": "oracle",
-            "sample": f"{n} of {len(queries)} queries drawn uniformly (seed 12345), {dt:.1f} s with {T} threads",
+            "oracle": "radix trees, one per peer (oracle/radix_oracle.c)",
+            "sample": f"{n} of {nq} {what} drawn uniformly (seed 12345), {dt:.1f} s on {T} threads",
             "one_thread": {"value": n1 / dt1, "unit": "queries/s", "sample": f"{n1} queries, {dt1:.1f} s"},
+            "linear_scan": {"value": nl / dtl, "unit": "queries/s", "threads": T,
+                            "oracle": "max over stored sequences of the LCP (oracle/prefix_oracle.c)",
+                            "sample": f"{nl} queries, {dtl:.1f} s"},
+            "host_logical_cpus": cpus["logical"], "affinity_cpus": cpus["affinity"],
+            "threads_note": "threads = the CPUs this process may use, at most 16 (one GPU's share of the host)",
             "cpu_model": cpu_model()}
 
 
-def bench_stream(args, w, dev):
-    """Streaming configuration: per round, one delta-merge of the insert batch
-    into the replica trees, then lookups of the round's query batch."""
+def _upload(ss, dev):
     import torch
+    return (torch.from_numpy(np.ascontiguousarray(ss.tokens, dtype=np.int32)).to(dev),
+            torch.from_numpy(np.ascontiguousarray(ss.offsets, dtype=np.int64)).to(dev))
+
+
+def _alg_bytes(queries, M, P) -> np.ndarray:
+    """B_q = 4 min(|q|, M_q + 1) + 4 (P + 1) + 8 per query."""
+    return 4 * np.minimum(queries.lengths(), M.astype(np.int64) + 1) + 4 * (P + 1) + 8
+
+
+def bench_stream(args, dev) -> dict:
+    """The streaming workload, 128 peers.  One step = for each topic
+    distribution (uniform, Zipf 1.2), the delta-merge of a fresh batch of
+    10,000 inserts into that distribution's forest, then a lookup batch of
+    1,048,576 queries on it.  The two forests live on two streams, so one
+    forest's merge (latency-bound, host round trips) runs while the other's
+    lookup streams from HBM.  Every lookup of every timed step is compared
+    with the radix-tree oracle after the timed region, and the algorithmic
+    bytes come from the oracle's match lengths."""
+    import torch
+
+    import oracle
+    import workloads as W
     from paper_2606_17059_amd import Forest
-    P = w.num_peers
-    phases_out = []
-    tot_ins = tot_merge_s = tot_q = tot_route_s = tot_bytes = 0.0
-    kern_all = []
-    compact_out = []
-    cpu = None
-    # untimed warm-up on a throwaway forest: the first launch of each kernel
-    # loads its code object, a one-time cost of the process, not of a merge
+    t_gen = time.perf_counter()
+    w = W.make_config(5)
+    P, R = w.num_peers, w.meta["rounds"]
+    dists = ("uniform", "zipf")
+    Wu, K = args.warmup, args.steps
+    n_steps = Wu + K
+    if n_steps > W.MAX_STREAM_ROUNDS:
+        raise SystemExit(f"bench.py: at most {W.MAX_STREAM_ROUNDS} warm-up + timed steps on the streaming workload")
+    # lookups: the R rounds' batches of each distribution, taken in turn by
+    # the steps (fresh for the first R rounds, then again on the grown forest)
+    qhost = {d: [] for d in dists}
+    qdev = {d: [] for d in dists}
+    for d in dists:
+        for r in range(R):
+            q = w.query_batch(d, r)
+            qhost[d].append(q)
+            qdev[d].append(_upload(q, dev))
+            log(f"[bench] stream: lookup batch {d} {r}: {len(q)} queries, {q.tokens.size} tokens "
+                f"({time.perf_counter() - t_gen:.1f} s)")
+    ihost = {d: [w.insert_batch(d, k) for k in range(n_steps)] for d in dists}
+    idev = {d: [(torch.from_numpy(b.peer).to(dev),) + _upload(b, dev) for b in ihost[d]] for d in dists}
+    log(f"[bench] stream: {n_steps} insert batches per distribution generated and uploaded "
+        f"({time.perf_counter() - t_gen:.1f} s)")
+    nq = len(qhost[dists[0]][0])
+    # outputs: one pair per timed step and distribution (checked afterwards),
+    # one scratch pair for the warm-up steps
+    outs = {d: [(torch.empty((nq, P), dtype=torch.int32, device=dev), torch.empty(nq, dtype=torch.int32, device=dev))
+                for _ in range(K)] for d in dists}
+    warm_out = (torch.empty((nq, P), dtype=torch.int32, device=dev), torch.empty(nq, dtype=torch.int32, device=dev))
+    # the first launch of each kernel in a process loads its code object: a
+    # one-time cost of the process, paid on a throwaway forest
     wf = Forest(P)
-    wf.load_seqset(w.snapshot.subset(np.arange(min(len(w.snapshot), 4 * P))))
-    ph0 = w.phase("uniform", 0)
-    wi = ph0.inserts.subset(np.arange(min(len(ph0.inserts), 256)))
-    wf.merge(torch.from_numpy(wi.peer).to(dev), torch.from_numpy(wi.tokens).to(dev),
-             torch.from_numpy(wi.offsets).to(dev))
-    wq = ph0.queries.subset(np.arange(min(len(ph0.queries), 256)))
-    wf.route(torch.from_numpy(wq.tokens).to(dev), torch.from_numpy(wq.offsets).to(dev))
+    wf.load_seqset(w.snapshot.subset(np.arange(4 * P)))
+    wi = ihost[dists[0]][0].subset(np.arange(256))
+    wf.merge(torch.from_numpy(wi.peer).to(dev), *_upload(wi, dev))
+    wq = qhost[dists[0]][0].subset(np.arange(256))
+    wf.route(*_upload(wq, dev))
     torch.cuda.synchronize()
     wf.close()
-    del ph0, wi, wq
-    for dist in ("uniform", "zipf"):
-        f = Forest(P)
-        f.load_seqset(w.snapshot)
-        for rnd in range(w.meta["rounds"]):
+    forests, streams = {}, {}
+    for d in dists:
+        forests[d] = Forest(P)
+        forests[d].load_seqset(w.snapshot)
+        streams[d] = torch.cuda.Stream(device=dev)
+        forests[d].route(*qdev[d][0], *warm_out)  # builds and uploads the base forest
+    torch.cuda.synchronize()
+    log(f"[bench] stream: base forests uploaded ({forests[dists[0]].info()})")
+    ev = {d: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+          for d in dists}
+    merge_s = {d: np.zeros(n_steps) for d in dists}
+    t_region = 0.0
+    for k in range(n_steps):
+        if k == Wu:
+            torch.cuda.synchronize()
+            t_region = time.perf_counter()
+        for d in dists:
+            f, s = forests[d], streams[d]
             t0 = time.perf_counter()
-            ph = w.phase(dist, rnd)
-            gen_s = time.perf_counter() - t0
-            ins, qs = ph.inserts, ph.queries
-            ip = torch.from_numpy(ins.peer).to(dev)
-            it = torch.from_numpy(ins.tokens).to(dev)
-            io = torch.from_numpy(ins.offsets).to(dev)
-            qt = torch.from_numpy(qs.tokens).to(dev)
-            qo = torch.from_numpy(qs.offsets).to(dev)
-            nq = len(qs)
-            ml = torch.empty((nq, P), dtype=torch.int32, device=dev)
-            ch = torch.empty(nq, dtype=torch.int32, device=dev)
-            if rnd == 0:
-                f.route(qt, qo, ml, ch)  # builds and uploads the base forest
-            torch.cuda.synchronize()
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            t0 = time.perf_counter()
-            e0.record()
-            f.merge(ip, it, io)
-            e1.record()
-            torch.cuda.synchronize()
-            merge_s = time.perf_counter() - t0
-            ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-                  for _ in range(args.steps)]
-            for a, b in ev:
-                a.record()
-                f.route(qt, qo, ml, ch)
-                b.record()
-            torch.cuda.synchronize()
-            f.check()
-            km = np.array([a.elapsed_time(b) for a, b in ev])
-            m = ml.cpu().numpy()
-            M = m.max(axis=1).astype(np.int64)
-            bq = float((4 * np.minimum(qs.lengths(), M + 1) + 4 * (P + 1) + 8).sum())
-            kern_all.extend(km.tolist())
-            tot_ins += len(ins)
-            tot_merge_s += merge_s
-            tot_q += nq * len(km)
-            tot_route_s += km.sum() / 1e3
-            tot_bytes += bq * len(km)
-            ph_rec = {"dist": dist, "round": rnd, "inserts": len(ins), "merge_ms": merge_s * 1e3,
-                      "merge_inserts_per_s": len(ins) / merge_s, "lookups": nq,
-                      "route_ms": float(km.mean()), "route_gbps": bq / (km.mean() / 1e3) / 1e9,
-                      "forest_nodes": f.info()["num_nodes"]}
-            phases_out.append(ph_rec)
-            log(f"[bench] stream {dist} round {rnd}: gen {gen_s:.1f} s; {ph_rec}")
-            if cpu is None and not args.no_cpu_baseline:
-                import oracle
-                o = oracle.Oracle(P)
-                ss = w.snapshot
-                for p in range(P):
-                    lo, hi = ss.peer_range(p)
-                    o.load(p, ss.tokens[ss.offsets[lo]:ss.offsets[hi]], ss.offsets[lo:hi + 1] - ss.offsets[lo])
-                t0 = time.perf_counter()
-                o.merge(ins.peer, ins.tokens, ins.offsets)
-                o_merge_s = time.perf_counter() - t0
-                T = cpu_threads()
-                rng = np.random.default_rng(12345)
-                n = 4 * T
-                while True:
-                    sub = qs.subset(np.sort(rng.choice(nq, n, replace=False)))
-                    t0 = time.perf_counter()
-                    o.route(sub.tokens, sub.offsets, T)
-                    dt = time.perf_counter() - t0
-                    if dt >= 0.25 * args.cpu_seconds or n >= nq:
-                        break
-                    n = int(min(nq, max(2 * n, n * args.cpu_seconds / max(dt, 1e-3))))
-                o.close()
-                cpu = {"value": n / dt, "unit": "queries/s", "cores": T, "kind": "oracle",
-                       "sample": f"{n} of {nq} lookups of the first uniform round, {dt:.1f} s with {T} threads; "
-                                 f"oracle merge of that round's {len(ins)} inserts: "
-                                 f"{len(ins) / o_merge_s:.0f} inserts/s (1 thread)",
-                       "cpu_model": cpu_model()}
-                log(f"[bench] cpu baseline: {cpu}")
-            if args.compact and rnd == w.meta["rounds"] - 1:
-                compact_out.append(bench_compact(f, qt, qo, ml, ch, qs, args.steps, dist, float(km.mean())))
-                log(f"[bench] compact: {compact_out[-1]}")
-            del qt, qo, ml, ch
-        kname = route_kernel_name(f)
-        f.close()
-    kern = np.array(kern_all)
-    achieved = tot_bytes / tot_route_s / 1e9
+            f.merge(*idev[d][k], stream=s)  # returns when the forest holds the batch
+            merge_s[d][k] = time.perf_counter() - t0
+            qt, qo = qdev[d][k % R]
+            if k >= Wu:
+                a, b = ev[d][k - Wu]
+                a.record(s)
+                f.route(qt, qo, *outs[d][k - Wu], stream=s)
+                b.record(s)
+            else:
+                f.route(qt, qo, *warm_out, stream=s)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_region
+    for d in dists:
+        forests[d].check()
+    route_ms = {d: np.array([a.elapsed_time(b) for a, b in ev[d]]) for d in dists}
+    log(f"[bench] stream: timed region {K} steps in {wall * 1e3:.2f} ms; route ms mean "
+        f"{ {d: round(float(route_ms[d].mean()), 4) for d in dists} }; merge ms mean "
+        f"{ {d: round(float(merge_s[d][Wu:].mean() * 1e3), 3) for d in dists} }")
+    kname = route_kernel_name(forests[dists[0]])
+    info = {d: forests[d].info() for d in dists}
+    compact = None
+    if args.compact:
+        compact = [bench_compact(forests[d], *qdev[d][(n_steps - 1) % R], *warm_out, None, 5, d,
+                                 float(route_ms[d].mean())) for d in dists]
+        log(f"[bench] compact: {compact}")
+    for d in dists:
+        forests[d].close()
+    # every lookup of every timed step against the radix-tree oracle, which
+    # takes the same merges in the same order
+    T = cpu_threads()
+    tot_bytes = 0.0
+    rows = 0
+    per_dist = {}
+    for d in dists:
+        o = oracle.RadixOracle(P)
+        o.load_seqset(w.snapshot)
+        byts = []
+        for k in range(n_steps):
+            b = ihost[d][k]
+            o.merge(b.peer, b.tokens, b.offsets)
+            if k < Wu:
+                continue
+            q = qhost[d][k % R]
+            m_or, c_or = o.route(q.tokens, q.offsets, T)
+            m = outs[d][k - Wu][0].cpu().numpy()
+            c = outs[d][k - Wu][1].cpu().numpy()
+            if not (np.array_equal(m, m_or) and np.array_equal(c, c_or)):
+                bad = np.nonzero((m != m_or).any(axis=1) | (c != c_or))[0]
+                raise SystemExit(f"bench.py: stream {d} step {k}: {bad.size} rows differ from the oracle "
+                                 f"(first {bad[:5].tolist()})")
+            byts.append(float(_alg_bytes(q, m_or.max(axis=1), P).sum()))
+            rows += len(q)
+        log(f"[bench] stream {d}: every row of {K} steps equals the oracle")
+        tot_bytes += sum(byts)
+        per_dist[d] = {"route_ms_mean": float(route_ms[d].mean()), "route_ms_median": float(np.median(route_ms[d])),
+                       "algorithmic_bytes_per_launch": float(np.mean(byts)),
+                       "merge_ms_mean": float(merge_s[d][Wu:].mean() * 1e3),
+                       "merge_inserts_per_s": float(len(ihost[d][0]) * K / merge_s[d][Wu:].sum()),
+                       "forest_nodes_after": info[d]["num_nodes"], "forest_device_bytes": info[d]["device_bytes"]}
+        o.close()
+    all_ms = np.concatenate([route_ms[d] for d in dists])
+    route_s = all_ms.sum() / 1e3
+    n_lookups = 2 * K * nq
+    n_ins = sum(len(ihost[d][k]) for d in dists for k in range(Wu, n_steps))
+    merge_tot = sum(merge_s[d][Wu:].sum() for d in dists)
+    achieved = tot_bytes / route_s / 1e9
+    cpu = None
+    if not args.no_cpu_baseline:
+        def make():
+            ra = oracle.RadixOracle(P)
+            ra.load_seqset(w.snapshot)
+            li = oracle.Oracle(P)
+            li.load_seqset(w.snapshot)
+            b = ihost["uniform"][0]
+            ra.merge(b.peer, b.tokens, b.offsets)
+            li.merge(b.peer, b.tokens, b.offsets)
+            return ra, li
+        cpu = cpu_baseline(make, qhost["uniform"][0], args.cpu_seconds,
+                           "lookups of the first uniform round (after its merge)")
+        log(f"[bench] cpu baseline: {cpu}")
     return {
-        "value": tot_q / tot_route_s, "ms_per_step": float(kern.mean()), "kernel_ms": float(kern.mean()),
-        "achieved": achieved, "bytes_per_launch": tot_bytes / len(kern), "kernel": kname,
-        "merge": {"inserts_per_s": tot_ins / tot_merge_s, "inserts": tot_ins, "seconds": tot_merge_s,
-                  "note": "wall time of pr_merge calls (host-synchronous), 8 rounds x 10,000 inserts"},
-        "phases": phases_out, "cpu": cpu, "compact": compact_out or None}
+        "value": n_lookups / wall, "ms_per_step": wall * 1e3 / K,
+        "queries_per_step": 2 * nq, "inserts_per_step": 2 * len(ihost[dists[0]][0]),
+        "lookup": {"queries_per_s": n_lookups / route_s, "route_ms_mean": float(all_ms.mean()),
+                   "note": "lookup kernels alone: HIP events around each route call on its stream"},
+        "merge": {"inserts_per_s": n_ins / merge_tot, "inserts": n_ins, "seconds": float(merge_tot),
+                  "note": "wall time of the pr_merge calls (host-synchronous), each overlapping the other "
+                          "forest's lookup"},
+        "per_distribution": per_dist,
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                     "frac": achieved / PEAK_HBM_GBPS, "traffic": measured_traffic("stream"),
+                     "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
+                     "kernel": kname, "kernel_ms": float(all_ms.mean()),
+                     "algorithmic_bytes_per_launch": tot_bytes / len(all_ms),
+                     "bytes_from": "match lengths of the radix-tree oracle"},
+        "parity": {"oracle": "radix trees, one per peer", "rows": rows, "bit_exact": True,
+                   "what": "every match length and chosen peer of every timed lookup"},
+        "cpu": cpu, "compact": compact, "workload_note": f"lookup batches: the {R} rounds' batches per distribution, taken in "
+                                     f"turn; insert batches: fresh for every step"}
+
+
+def bench_route_config(cfg: int, args, dev, headline: bool) -> dict:
+    """One configuration's lookup batch: K launches back to back between one
+    pair of HIP events (four rotated query copies), every row compared with
+    the radix-tree oracle, whose match lengths give the algorithmic bytes."""
+    import torch
+
+    import oracle
+    import workloads as W
+    from paper_2606_17059_amd import Forest
+    t0 = time.perf_counter()
+    w = W.make_config(cfg)
+    queries = w.queries
+    P = w.num_peers
+    nq = len(queries)
+    log(f"[bench] config {cfg}: generated in {time.perf_counter() - t0:.1f} s: {len(w.snapshot)} cached prompts, "
+        f"{nq} queries")
+    f = Forest(P)
+    f.load_seqset(w.snapshot)
+    copies = max(1, args.copies)
+    qt = [torch.from_numpy(queries.tokens).to(dev) for _ in range(copies)]
+    qo = [torch.from_numpy(queries.offsets).to(dev) for _ in range(copies)]
+    ml = torch.empty((nq, P), dtype=torch.int32, device=dev)
+    ch = torch.empty(nq, dtype=torch.int32, device=dev)
+    t0 = time.perf_counter()
+    f.route(qt[0], qo[0], ml, ch)  # first route builds and uploads the forest
+    torch.cuda.synchronize()
+    log(f"[bench] config {cfg}: forest build + upload + first route {time.perf_counter() - t0:.2f} s; {f.info()}")
+    launch = [f.route_launcher(qt[i], qo[i], ml, ch) for i in range(len(qt))]
+    for i in range(args.warmup):
+        launch[i % len(launch)]()
+    torch.cuda.synchronize()
+    # K launches back to back between one pair of events: the host enqueues
+    # far faster than the kernel runs, so the region over K is the kernel's
+    # average launch duration
+    K = args.steps
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for k in range(K):
+        launch[k % len(launch)]()
+    e1.record()
+    torch.cuda.synchronize()
+    total_ms = e0.elapsed_time(e1)
+    f.check()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
+    for k in range(K):
+        ev[k][0].record()
+        launch[k % len(launch)]()
+        ev[k][1].record()
+    torch.cuda.synchronize()
+    kern_ms = np.array([a.elapsed_time(b) for a, b in ev])
+    m, c = ml.cpu().numpy(), ch.cpu().numpy()
+    split = int(w.meta.get("split_block", 0))
+    r = oracle.RadixOracle(P, split_block=split)
+    r.load_seqset(w.snapshot)
+    t0 = time.perf_counter()
+    m_or, c_or = r.route(queries.tokens, queries.offsets, cpu_threads())
+    oracle_s = time.perf_counter() - t0
+    r.close()
+    if not (np.array_equal(m, m_or) and np.array_equal(c, c_or)):
+        bad = np.nonzero((m != m_or).any(axis=1) | (c != c_or))[0]
+        raise SystemExit(f"bench.py: config {cfg}: {bad.size} rows differ from the oracle (first {bad[:5].tolist()})")
+    bytes_q = _alg_bytes(queries, m_or.max(axis=1), P)
+    total_bytes = float(bytes_q.sum())
+    achieved = total_bytes / (total_ms / K / 1e3) / 1e9
+    log(f"[bench] config {cfg}: {K} launches in {total_ms:.4f} ms, {total_ms / K:.4f} ms per launch, "
+        f"{achieved:.0f} GB/s ({achieved / PEAK_HBM_GBPS:.3f}); every row equals the oracle ({oracle_s:.1f} s)")
+    out = {
+        "workload": WORKLOADS[cfg], "peers": P, "queries": nq, "query_tokens": int(queries.lengths().sum()),
+        "value": nq * K / (total_ms / 1e3), "unit": "queries/s", "steps": K, "warmup": args.warmup,
+        "ms_per_step": total_ms / K,
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
+                     "frac": achieved / PEAK_HBM_GBPS, "traffic": measured_traffic(W.CONFIG_NAMES[cfg]),
+                     "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
+                     "kernel": route_kernel_name(f), "kernel_ms": total_ms / K,
+                     "kernel_ms_own_events": {"mean": float(kern_ms.mean()), "median": float(np.median(kern_ms))},
+                     "kernels_per_step": step_kernels(nq, int(queries.lengths().sum())),
+                     "algorithmic_bytes_per_launch": total_bytes,
+                     "bytes_from": "match lengths of the radix-tree oracle"},
+        "parity": {"oracle": "radix trees, one per peer" + (f", nodes at every {split}-token block" if split else ""),
+                   "rows": nq, "bit_exact": True},
+    }
+    if cfg == 3:
+        # the same batch routed on the peers' true trees (every row checked
+        # too): how often the stale estimates pick the same peer, and the
+        # prefill reuse they predict vs get (Table 2's expected / actual hit)
+        ft = Forest(P)
+        ft.load_seqset(w.true_snapshot)
+        mt, ct = ft.route(qt[0], qo[0])
+        torch.cuda.synchronize()
+        ft.close()
+        mt, ct = mt.cpu().numpy(), ct.cpu().numpy()
+        rt = oracle.RadixOracle(P)
+        rt.load_seqset(w.true_snapshot)
+        mt_or, ct_or = rt.route(queries.tokens, queries.offsets, cpu_threads())
+        rt.close()
+        if not (np.array_equal(mt, mt_or) and np.array_equal(ct, ct_or)):
+            raise SystemExit("bench.py: config 3 true forest: rows differ from the oracle")
+        rows = np.arange(nq)
+        tot = float(queries.lengths().sum())
+        out["stale_report"] = {
+            "route_agreement": float((c == ct).mean()),
+            "expected_hit": float(m[rows, c].sum() / tot),
+            "actual_hit": float(mt[rows, c].sum() / tot),
+            "oracle_true_hit": float(mt[rows, ct].sum() / tot),
+            "note": "estimates: observer 0's stale replicas; truth: the peers' exact trees; hit = matched "
+                    "prefill tokens / query tokens"}
+        out["parity"]["rows"] = 2 * nq
+        log(f"[bench] stale report: {out['stale_report']}")
+    if headline or cfg == 2:
+        if not args.no_select:
+            out["select"] = bench_select(f, w, qt, qo, np.minimum(queries.lengths(), m_or.max(axis=1) + 1),
+                                         K, args.warmup, dev)
+            log(f"[bench] select: {out['select']}")
+    if headline:
+        if args.latency:
+            out["latency"] = bench_latency(f, w, dev)
+        if args.lru:
+            out["lru"] = bench_lru(f, w, qt, qo, dev)
+            log(f"[bench] lru: {out['lru']}")
+        if args.snapshot:
+            out["snapshot"] = bench_snapshot(f, w, dev)
+            log(f"[bench] snapshot: {out['snapshot']}")
+        if not args.no_cpu_baseline:
+            def make():
+                ra = oracle.RadixOracle(P, split_block=split)
+                ra.load_seqset(w.snapshot)
+                li = oracle.Oracle(P)
+                li.load_seqset(w.snapshot)
+                return ra, li
+            out["cpu"] = cpu_baseline(make, queries, args.cpu_seconds, "queries")
+            log(f"[bench] cpu baseline: {out['cpu']}")
+    f.close()
+    del qt, qo, ml, ch, launch
+    torch.cuda.empty_cache()
+    return out
 
 
 def bench_compact(f, qt, qo, ml, ch, qs, steps, dist, route_ms_before) -> dict:
@@ -455,17 +688,22 @@ def main() -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", type=int, default=2, choices=sorted(WORKLOADS))
-    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU time of the oracle sample")
+    ap.add_argument("--config", type=int, default=5, choices=sorted(WORKLOADS),
+                    help="headline workload (default 5, the largest: streaming merges and lookups)")
+    ap.add_argument("--extra-configs", default="2,3,4",
+                    help="comma-separated lookup workloads also measured and reported under 'configs' "
+                         "('' for none)")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target CPU time of the oracle samples")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--lru", action="store_true",
-                    help="also time touching the batch in the local tree and LRU evictions")
+                    help="also time touching the batch in the local tree and LRU evictions (configs 1-4)")
     ap.add_argument("--snapshot", action="store_true",
-                    help="also time snapshot export and device-input load of a few peers")
-    ap.add_argument("--compact", action="store_true",
-                    help="config 5: compact the forest after the last merge round and time it")
+                    help="also time snapshot export and device-input load of a few peers (configs 1-4)")
     ap.add_argument("--latency", action="store_true",
-                    help="also time small batches (1 to 32,768 queries) per call, host wall time included")
+                    help="also time small batches (1 to 32,768 queries) per call, host wall time included "
+                         "(configs 1-4)")
+    ap.add_argument("--compact", action="store_true",
+                    help="config 5: compact both forests after the timed steps and time it")
     ap.add_argument("--no-select", action="store_true",
                     help="skip timing pr_route_select (push-back / failover selection)")
     ap.add_argument("--copies", type=int, default=4, help="device copies of the query batch to rotate")
@@ -482,9 +720,6 @@ def main() -> int:
 
     import torch
 
-    import workloads as W
-    from paper_2606_17059_amd import Forest
-
     if not torch.cuda.is_available():
         sys.stderr.write("bench.py needs a HIP device\n")
         return 1
@@ -497,156 +732,47 @@ def main() -> int:
         torch.cuda.synchronize()
         log(f"[bench] copy probe: 3 copies of {args.copy_probe_mib} MiB")
         del a, b
-    t0 = time.perf_counter()
-    w = W.make_config(args.config)
+    t_start = time.perf_counter()
+    extras = [int(x) for x in args.extra_configs.split(",") if x.strip()]
+    out = {"metric": "routed queries/sec (batched LPM over all peer trees) + achieved HBM GB/s",
+           "unit": "queries/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "int32",
+           "data": "synthetic"}
     if args.config == 5:
-        r = bench_stream(args, w, dev)
-        out = {
-            "metric": "routed queries/sec (batched LPM over all peer trees) + achieved HBM GB/s",
-            "value": r["value"], "unit": "queries/s", "n_gpus": 1, "steps": args.steps, "warmup": 0,
-            "ms_per_step": r["ms_per_step"], "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-            "dtype": "int32", "data": "synthetic",
-            "config": {"workload": WORKLOADS[5], "config_index": 5, "peers": w.num_peers,
-                       "queries_per_step": w.meta["phase_queries"], "parallelism": "single GPU"},
-            "hbm_gbps": r["achieved"],
-            "roofline": {"bound": "hbm", "achieved": r["achieved"], "peak": PEAK_HBM_GBPS, "unit": "GB/s",
-                         "frac": r["achieved"] / PEAK_HBM_GBPS, "traffic": measured_traffic("stream"),
-                         "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
-                         "kernel": r["kernel"],
-                         "kernel_ms": r["kernel_ms"], "algorithmic_bytes_per_launch": r["bytes_per_launch"]},
-            "cpu_baseline": r["cpu"], "merge": r["merge"], "phases": r["phases"]}
+        r = bench_stream(args, dev)
+        out.update({
+            "value": r["value"], "ms_per_step": r["ms_per_step"],
+            "config": {"workload": WORKLOADS[5], "config_index": 5, "peers": 128,
+                       "queries_per_step": r["queries_per_step"], "inserts_per_step": r["inserts_per_step"],
+                       "step": "for each topic distribution (uniform, Zipf 1.2): merge a fresh 10,000-insert batch "
+                               "into its forest, then route a 1,048,576-query lookup batch on it; the two "
+                               "forests on two streams",
+                       "parallelism": "single GPU"},
+            "hbm_gbps": r["roofline"]["achieved"], "roofline": r["roofline"], "lookup": r["lookup"],
+            "merge": r["merge"], "per_distribution": r["per_distribution"], "parity": r["parity"],
+            "cpu_baseline": r["cpu"], "inputs": r["workload_note"]})
         if r["compact"]:
             out["compact"] = r["compact"]
-        print(json.dumps(out), flush=True)
-        return 0
-    queries = w.queries
-    log(f"[bench] generated config {args.config} in {time.perf_counter() - t0:.1f} s: "
-        f"{len(w.snapshot)} cached prompts, {len(queries)} queries")
-
-    f = Forest(w.num_peers)
-    f.load_seqset(w.snapshot)
-    qt = [torch.from_numpy(queries.tokens).to(dev) for _ in range(max(1, args.copies))]
-    qo = [torch.from_numpy(queries.offsets).to(dev) for _ in range(max(1, args.copies))]
-    nq = len(queries)
-    P = w.num_peers
-    ml = torch.empty((nq, P), dtype=torch.int32, device=dev)
-    ch = torch.empty(nq, dtype=torch.int32, device=dev)
-    t0 = time.perf_counter()
-    f.route(qt[0], qo[0], ml, ch)  # first route builds and uploads the forest
-    torch.cuda.synchronize()
-    log(f"[bench] forest build + upload + first route {time.perf_counter() - t0:.2f} s; {f.info()}")
-
-    # buffers checked once; the timed loop only launches (host time per launch
-    # well below the kernel's, so the queue never runs dry)
-    launch = [f.route_launcher(qt[i], qo[i], ml, ch) for i in range(len(qt))]
-    for i in range(args.warmup):
-        launch[i % len(launch)]()
-    torch.cuda.synchronize()
-
-    # timed region: K launches back to back on the current stream between one
-    # pair of HIP events; the host enqueues far faster than the kernel runs, so
-    # the region's length over K is the kernel's average launch duration (event
-    # markers between launches would add GPU time of their own)
-    K = args.steps
-    all0, all1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    all0.record()
-    for k in range(K):
-        launch[k % len(launch)]()
-    all1.record()
-    torch.cuda.synchronize()
-    total_ms = all0.elapsed_time(all1)
-    f.check()
-    # after the timed region: per-launch spread, each launch between its own events
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
-    for k in range(K):
-        ev[k][0].record()
-        launch[k % len(launch)]()
-        ev[k][1].record()
-    torch.cuda.synchronize()
-    kern_ms = np.array([a.elapsed_time(b) for a, b in ev])
-
-    m = ml.cpu().numpy()
-    M = m.max(axis=1).astype(np.int64)
-    qlen = queries.lengths()
-    needed = np.minimum(qlen, M + 1)
-    bytes_q = 4 * needed + 4 * (P + 1) + 8
-    total_bytes = float(bytes_q.sum())
-    avg_kernel_s = total_ms / K / 1e3
-    achieved = total_bytes / avg_kernel_s / 1e9
-    value = nq * K / (total_ms / 1e3)
-    log(f"[bench] timed region: {K} launches in {total_ms:.4f} ms, {total_ms / K:.4f} ms per launch; "
-        f"algorithmic bytes/launch {total_bytes / 1e6:.1f} MB")
-    log(f"[bench] per-launch ms (own events, after the timed region): mean {kern_ms.mean():.4f} "
-        f"median {np.median(kern_ms):.4f} min {kern_ms.min():.4f} max {kern_ms.max():.4f}")
-
-    extra = {}
-    if args.config == 3:
-        # the same batch routed on the peers' true trees: how often the stale
-        # estimates pick the same peer, and the prefill reuse they predict vs get
-        ft = Forest(P)
-        ft.load_seqset(w.true_snapshot)
-        mt, ct = ft.route(qt[0], qo[0])
-        torch.cuda.synchronize()
-        ft.close()
-        mt, ct = mt.cpu().numpy(), ct.cpu().numpy()
-        ce = ch.cpu().numpy()
-        rows = np.arange(nq)
-        tot = float(qlen.sum())
-        extra["stale_report"] = {
-            "route_agreement": float((ce == ct).mean()),
-            "expected_hit": float(m[rows, ce].sum() / tot),
-            "actual_hit": float(mt[rows, ce].sum() / tot),
-            "oracle_true_hit": float(mt[rows, ct].sum() / tot)}
-        log(f"[bench] stale report: {extra['stale_report']}")
-
-    if not args.no_select:
-        extra["select"] = bench_select(f, w, qt, qo, needed, K, args.warmup, dev)
-        log(f"[bench] select: {extra['select']}")
-    if args.latency:
-        extra["latency"] = bench_latency(f, w, dev)
-    if args.lru:
-        # after the timed routes: touches and evictions change the forest
-        extra["lru"] = bench_lru(f, w, qt, qo, dev)
-        log(f"[bench] lru: {extra['lru']}")
-    if args.snapshot:
-        # after the timed routes: the device loads switch the forest to its device path
-        extra["snapshot"] = bench_snapshot(f, w, dev)
-        log(f"[bench] snapshot: {extra['snapshot']}")
-
-    cpu = None
-    if not args.no_cpu_baseline:
-        cpu = cpu_baseline(w, queries, args.cpu_seconds)
-        log(f"[bench] cpu baseline: {cpu}")
-
-    out = {
-        "metric": "routed queries/sec (batched LPM over all peer trees) + achieved HBM GB/s",
-        "value": value,
-        "unit": "queries/s",
-        "n_gpus": 1,
-        "steps": K,
-        "warmup": args.warmup,
-        "ms_per_step": total_ms / K,
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "int32",
-        "data": "synthetic",
-        "config": {"workload": WORKLOADS[args.config], "config_index": args.config, "peers": P,
-                   "queries_per_step": nq, "query_tokens": int(qlen.sum()), "parallelism": "single GPU"},
-        "hbm_gbps": achieved,
-        "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
-                     "frac": achieved / PEAK_HBM_GBPS, "traffic": measured_traffic(W.CONFIG_NAMES[args.config]),
-                     "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
-                     "kernel": route_kernel_name(f), "kernel_ms": total_ms / K,
-                     "kernel_ms_own_events": {"mean": float(kern_ms.mean()), "median": float(np.median(kern_ms))},
-                     "kernels_per_step": step_kernels(nq, int(qlen.sum())),
-                     "algorithmic_bytes_per_launch": total_bytes},
-        "cpu_baseline": cpu,
-    }
-    out.update(extra)
+    else:
+        r = bench_route_config(args.config, args, dev, headline=True)
+        out.update({
+            "value": r["value"], "ms_per_step": r["ms_per_step"],
+            "config": {"workload": WORKLOADS[args.config], "config_index": args.config, "peers": r["peers"],
+                       "queries_per_step": r["queries"], "query_tokens": r["query_tokens"],
+                       "parallelism": "single GPU"},
+            "hbm_gbps": r["roofline"]["achieved"], "roofline": r["roofline"], "parity": r["parity"],
+            "cpu_baseline": r.get("cpu")})
+        for k in ("stale_report", "select", "latency", "lru", "snapshot"):
+            if k in r:
+                out[k] = r[k]
+    if extras:
+        out["configs"] = {}
+        for cfg in extras:
+            if cfg == args.config or cfg == 5:
+                continue
+            out["configs"][str(cfg)] = bench_route_config(cfg, args, dev, headline=False)
+    out["bench_seconds"] = time.perf_counter() - t_start
     print(json.dumps(out), flush=True)
-    f.close()
     return 0
 
 

@@ -24,6 +24,7 @@ import numpy as np
 
 SEED_BASE = 20261202
 STREAM_NAMES = ("prefixes", "homing", "cache", "queries", "stale", "inserts")
+MAX_STREAM_ROUNDS = 256  # rounds per distribution the streaming configuration can generate
 
 I32 = np.int32
 I64 = np.int64
@@ -96,15 +97,28 @@ class Workload:
     queries: SeqSet
     true_snapshot: Optional[SeqSet] = None  # cfg 3: the peers' exact trees
     meta: Dict = field(default_factory=dict)
-    _phase_fn: Optional[object] = None
+    _insert_fn: Optional[object] = None
+    _query_fn: Optional[object] = None
 
     def phases(self, dist: str) -> List[StreamPhase]:
-        assert self._phase_fn is not None, "only the streaming configuration has phases"
-        return [self._phase_fn(dist, r) for r in range(self.meta["rounds"])]
+        assert self._insert_fn is not None, "only the streaming configuration has phases"
+        return [self.phase(dist, r) for r in range(self.meta["rounds"])]
 
     def phase(self, dist: str, rnd: int) -> StreamPhase:
-        assert self._phase_fn is not None
-        return self._phase_fn(dist, rnd)
+        """Round rnd of the streaming configuration: its merge batch, then its
+        lookup batch."""
+        assert self._insert_fn is not None, "only the streaming configuration has phases"
+        return StreamPhase(dist, rnd, self._insert_fn(dist, rnd), self._query_fn(dist, rnd))
+
+    def insert_batch(self, dist: str, rnd: int) -> SeqSet:
+        """The merge batch of round rnd (any rnd < MAX_STREAM_ROUNDS; rounds
+        past meta["rounds"] continue the same recipe)."""
+        assert self._insert_fn is not None, "only the streaming configuration has insert batches"
+        return self._insert_fn(dist, rnd)
+
+    def query_batch(self, dist: str, rnd: int) -> SeqSet:
+        assert self._query_fn is not None, "only the streaming configuration has lookup batches"
+        return self._query_fn(dist, rnd)
 
 
 # --------------------------------------------------------------------------
@@ -357,26 +371,33 @@ def _cfg_stream(st, per_peer, rounds, phase_queries, phase_inserts) -> Workload:
     peer, topic = _cache_heads(rng_c, homed, per_peer)
     snap = _assemble(heads, topic, _uniform_int(rng_c, 64, 256, topic.shape[0]), rng_c, V, peer)
     dists = ("uniform", "zipf")
-    # one child stream per (dist, round), spawned up front so any phase can be
-    # generated on its own
-    q_kids = st["queries"].spawn(2 * R)
-    i_kids = st["inserts"].spawn(2 * R)
+    # one child stream per (dist, round), spawned up front so any round's
+    # batches can be generated on their own
+    q_kids = st["queries"].spawn(2 * MAX_STREAM_ROUNDS)
+    i_kids = st["inserts"].spawn(2 * MAX_STREAM_ROUNDS)
 
-    def phase(dist: str, rnd: int) -> StreamPhase:
-        di = dists.index(dist)
+    def kid(dist: str, rnd: int) -> int:
+        if not 0 <= rnd < MAX_STREAM_ROUNDS:
+            raise ValueError(f"round {rnd} outside [0, {MAX_STREAM_ROUNDS})")
+        return dists.index(dist) * MAX_STREAM_ROUNDS + rnd
+
+    def inserts(dist: str, rnd: int) -> SeqSet:
         s = None if dist == "uniform" else 1.2
-        rng_i = _rng(i_kids[di * R + rnd])
+        rng_i = _rng(i_kids[kid(dist, rnd)])
         tgt = rng_i.integers(1, P, size=NI, dtype=I64).astype(I32)
         itopic = _draw_topics(rng_i, NI, T, s, perm)
-        ins = _assemble(heads, itopic, _uniform_int(rng_i, 64, 256, NI), rng_i, V, tgt)
-        qs, _, _ = _queries(_rng(q_kids[di * R + rnd]), NQ, T, T, 0.05, s, perm, heads, 64, 256, V)
-        return StreamPhase(dist, rnd, ins, qs)
+        return _assemble(heads, itopic, _uniform_int(rng_i, 64, 256, NI), rng_i, V, tgt)
+
+    def lookups(dist: str, rnd: int) -> SeqSet:
+        s = None if dist == "uniform" else 1.2
+        qs, _, _ = _queries(_rng(q_kids[kid(dist, rnd)]), NQ, T, T, 0.05, s, perm, heads, 64, 256, V)
+        return qs
 
     # the first-round query batch stands in as `queries` for generic code paths
     meta = dict(sys_len=SYS, head_len=np.array([h.shape[0] for h in heads], I64), n_topics=T,
                 homed=homed, cache_topic=topic, rounds=R, phase_queries=NQ, phase_inserts=NI)
     empty = SeqSet(np.zeros(0, I32), np.zeros(1, I64))
-    return Workload(5, "stream", P, V, snap, empty, meta=meta, _phase_fn=phase)
+    return Workload(5, "stream", P, V, snap, empty, meta=meta, _insert_fn=inserts, _query_fn=lookups)
 
 
 # --------------------------------------------------------------------------

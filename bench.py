@@ -182,9 +182,11 @@ def bench_stream(args, dev) -> dict:
     """The streaming workload, 128 peers.  One step = for each topic
     distribution (uniform, Zipf 1.2), the delta-merge of a fresh batch of
     10,000 inserts into that distribution's forest, then a lookup batch of
-    1,048,576 queries on it.  The two forests live on two streams, so one
-    forest's merge (latency-bound, host round trips) runs while the other's
-    lookup streams from HBM.  Every lookup of every timed step is compared
+    1,048,576 queries on it.  Each forest has its own stream, so one forest's
+    merge (latency-bound: small kernels and host round trips) runs while the
+    other's lookup streams from HBM; its kernels then wait for free wave
+    slots behind the lookup's million waves, so merges are also timed alone
+    after the timed region (--no-overlap puts both forests on one stream).  Every lookup of every timed step is compared
     with the radix-tree oracle after the timed region, and the algorithmic
     bytes come from the oracle's match lengths."""
     import torch
@@ -198,7 +200,7 @@ def bench_stream(args, dev) -> dict:
     dists = ("uniform", "zipf")
     Wu, K = args.warmup, args.steps
     n_steps = Wu + K
-    if n_steps > W.MAX_STREAM_ROUNDS:
+    if n_steps + 4 > W.MAX_STREAM_ROUNDS:
         raise SystemExit(f"bench.py: at most {W.MAX_STREAM_ROUNDS} warm-up + timed steps on the streaming workload")
     # lookups: the R rounds' batches of each distribution, taken in turn by
     # the steps (fresh for the first R rounds, then again on the grown forest)
@@ -235,7 +237,7 @@ def bench_stream(args, dev) -> dict:
     for d in dists:
         forests[d] = Forest(P)
         forests[d].load_seqset(w.snapshot)
-        streams[d] = torch.cuda.Stream(device=dev)
+        streams[d] = torch.cuda.Stream(device=dev) if args.overlap or d == dists[0] else streams[dists[0]]
         forests[d].route(*qdev[d][0], *warm_out)  # builds and uploads the base forest
     torch.cuda.synchronize()
     log(f"[bench] stream: base forests uploaded ({forests[dists[0]].info()})")
@@ -249,6 +251,8 @@ def bench_stream(args, dev) -> dict:
             t_region = time.perf_counter()
         for d in dists:
             f, s = forests[d], streams[d]
+            if not args.overlap:
+                s.synchronize()  # the previous lookup is done: the merge's wall time is its own
             t0 = time.perf_counter()
             f.merge(*idev[d][k], stream=s)  # returns when the forest holds the batch
             merge_s[d][k] = time.perf_counter() - t0
@@ -268,6 +272,22 @@ def bench_stream(args, dev) -> dict:
     log(f"[bench] stream: timed region {K} steps in {wall * 1e3:.2f} ms; route ms mean "
         f"{ {d: round(float(route_ms[d].mean()), 4) for d in dists} }; merge ms mean "
         f"{ {d: round(float(merge_s[d][Wu:].mean() * 1e3), 3) for d in dists} }")
+    # merges timed alone: further fresh batches after the last timed lookup,
+    # each with the GPU otherwise idle (they change nothing the oracle checks)
+    alone = {}
+    for d in dists:
+        ts = []
+        for k in range(n_steps, n_steps + 4):
+            b = w.insert_batch(d, k)
+            dev_b = (torch.from_numpy(b.peer).to(dev),) + _upload(b, dev)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            forests[d].merge(*dev_b, stream=streams[d])
+            ts.append(time.perf_counter() - t0)
+        alone[d] = ts
+    n_alone = sum(len(v) for v in alone.values()) * len(ihost[dists[0]][0])
+    alone_s = sum(sum(v) for v in alone.values())
+    log(f"[bench] stream: merges alone ms {({d: [round(x * 1e3, 3) for x in v] for d, v in alone.items()})}")
     kname = route_kernel_name(forests[dists[0]])
     info = {d: forests[d].info() for d in dists}
     compact = None
@@ -336,8 +356,12 @@ def bench_stream(args, dev) -> dict:
         "lookup": {"queries_per_s": n_lookups / route_s, "route_ms_mean": float(all_ms.mean()),
                    "note": "lookup kernels alone: HIP events around each route call on its stream"},
         "merge": {"inserts_per_s": n_ins / merge_tot, "inserts": n_ins, "seconds": float(merge_tot),
-                  "note": "wall time of the pr_merge calls (host-synchronous), each overlapping the other "
-                          "forest's lookup"},
+                  "note": "wall time of the timed steps' pr_merge calls (host-synchronous), "
+                          + ("each beside the other forest's lookup" if args.overlap
+                             else "each after the previous lookup on the stream finished"),
+                  "alone": {"inserts_per_s": n_alone / alone_s, "inserts": n_alone, "seconds": alone_s,
+                            "note": "four more fresh batches per distribution after the timed region, each "
+                                    "merged with the GPU otherwise idle"}},
         "per_distribution": per_dist,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                      "frac": achieved / PEAK_HBM_GBPS, "traffic": measured_traffic("stream"),
@@ -702,6 +726,9 @@ def main() -> int:
     ap.add_argument("--latency", action="store_true",
                     help="also time small batches (1 to 32,768 queries) per call, host wall time included "
                          "(configs 1-4)")
+    ap.add_argument("--no-overlap", dest="overlap", action="store_false",
+                    help="config 5: run both forests on one stream (by default each has its own, and one forest's "
+                         "merge runs beside the other's lookup)")
     ap.add_argument("--compact", action="store_true",
                     help="config 5: compact both forests after the timed steps and time it")
     ap.add_argument("--no-select", action="store_true",
@@ -745,8 +772,8 @@ def main() -> int:
             "config": {"workload": WORKLOADS[5], "config_index": 5, "peers": 128,
                        "queries_per_step": r["queries_per_step"], "inserts_per_step": r["inserts_per_step"],
                        "step": "for each topic distribution (uniform, Zipf 1.2): merge a fresh 10,000-insert batch "
-                               "into its forest, then route a 1,048,576-query lookup batch on it; the two "
-                               "forests on two streams",
+                               "into its forest, then route a 1,048,576-query lookup batch on it; "
+                               + ("the two forests on two streams" if args.overlap else "all on one stream"),
                        "parallelism": "single GPU"},
             "hbm_gbps": r["roofline"]["achieved"], "roofline": r["roofline"], "lookup": r["lookup"],
             "merge": r["merge"], "per_distribution": r["per_distribution"], "parity": r["parity"],

@@ -52,7 +52,8 @@ typedef int32_t pr_status;
 
 #define PR_OK 0
 #define PR_EINVAL (-1)  /* bad argument; the forest is unchanged, no output is written */
-#define PR_ENOMEM (-2)  /* host or device allocation failed; the forest is unchanged */
+#define PR_ENOMEM (-2)  /* host or device allocation failed; the forest is unchanged unless
+                           the call's description says otherwise */
 #define PR_EDEVICE (-3) /* a HIP call failed; destroy the forest */
 #define PR_ESTATE (-4)  /* call not valid in the forest's current state */
 
@@ -61,7 +62,7 @@ typedef int32_t pr_status;
 typedef struct pr_forest pr_forest;
 
 /* ABI version of this header (incremented on incompatible changes). */
-#define PR_ABI_VERSION 5
+#define PR_ABI_VERSION 6
 
 /* PR_ABI_VERSION of the header the library was built with; a client built
  * against another version must not call the library. */
@@ -71,14 +72,23 @@ int32_t pr_abi_version(void);
 const char *pr_last_error(void);
 
 /*
- * Create an empty forest of num_peers trees (1 <= num_peers <= PR_MAX_PEERS).
+ * Create an empty forest of num_peers trees (1 <= num_peers <= PR_MAX_PEERS):
+ * one node's view of the network (paper, System Design: every node keeps a
+ * radix tree of its own cache and one estimate of each other node's).
  * Every tree starts empty.  No GPU work happens here.
+ * Which tree is the node's own needs no argument here: routing treats every
+ * tree alike (Algorithm 1 takes the argmax over all N trees), and the tree
+ * whose LRU state is kept (Algorithm 1's EvictLRUTrie) is chosen later with
+ * pr_set_local_peer.  Nor does the layout take a split granularity: edges
+ * split at fixed token blocks would change no match length (the match is
+ * token-exact), so every tree is a plain path-compressed radix tree.
  * Errors: PR_EINVAL (num_peers out of range, out == NULL), PR_ENOMEM.
  * Ownership: the caller owns *out and releases it with pr_forest_destroy.
  */
 pr_status pr_forest_create(int32_t num_peers, pr_forest **out);
 
-/* Release a forest and all its host and device memory.  NULL is a no-op.
+/* Release a forest and all its host and device memory (the node leaving the
+ * network, or its router restarting: paper, System Design).  NULL is a no-op.
  * Waits for the forest's device to finish outstanding work first. */
 void pr_forest_destroy(pr_forest *f);
 
@@ -298,7 +308,9 @@ pr_status pr_touch(pr_forest *f, const int32_t *q_tokens, int64_t num_tokens,
  * (HOST) gets the number removed.  Other peers' trees are unchanged.
  * Host-synchronous.
  * Errors: PR_EINVAL (evicted NULL, max_tokens < 0), PR_ESTATE (no local
- * peer), PR_ENOMEM, PR_EDEVICE.
+ * peer), PR_ENOMEM, PR_EDEVICE.  A PR_ENOMEM before the first device change
+ * leaves the forest unchanged; one after it (the eviction's later scratch),
+ * like every PR_EDEVICE, leaves the forest refusing every call but destroy.
  */
 pr_status pr_evict_lru(pr_forest *f, int64_t max_tokens, int64_t *evicted, void *hip_stream);
 
@@ -358,10 +370,16 @@ typedef struct {
     int64_t layout_epoch;    /* advances whenever the device arrays that routes
                                 read move: an upload after host snapshot loads,
                                 growth inside a merge, device load, touch or
-                                eviction, compaction, and the switch from 16-bit
-                                to int32 labels */
+                                eviction, compaction, and every change of
+                                label_bits (16 to 17 or 32, 17 to 32) */
     int64_t label_token_bytes; /* 2 while routes read a 16-bit copy of the label
-                                  pool (every label token in [0, 65535]), else 4 */
+                                  pool (every label token in [0, 131071]), else 4 */
+    int64_t label_bits;        /* bits routes read per label token: 16 (every label
+                                  token in [0, 65535]), 17 (in [0, 131071]: the
+                                  16-bit copy plus a plane of bit 16), else 32 */
+    int64_t merge_refusals;    /* device update rounds that ran out of capacity and
+                                  ran again after the forest grew (their refused
+                                  allocations wrote nothing) */
 } pr_forest_info;
 
 pr_status pr_forest_info_get(pr_forest *f, pr_forest_info *out);

@@ -26,6 +26,11 @@
 //   mext[n*(W-1) + w-1]  peer-mask words 1..W-1 of node n (W > 1 only);
 //             word 0 lives in the record.
 //   pool[t]   int32 label tokens; node n's label is pool[lab_off .. +lab_len).
+//   pool16[t] the low 16 bits of pool[t], kept while every label token lies in
+//             [0, 131071]; routes read labels from it (half the bytes).
+//   hib[t/32] bit t % 32 is bit 16 of pool[t] (kept with pool16); routes read
+//             it once some label token is 65536 or more (17-bit labels: one
+//             32-bit word covers the high bits of 32 label tokens).
 #ifndef PR_FOREST_LAYOUT_H
 #define PR_FOREST_LAYOUT_H
 

@@ -60,7 +60,8 @@ struct MergeCounters {
     unsigned long long skipped;   // inserts with invalid peer or offsets
     unsigned long long bad_path;  // mask pass found a sequence not ending at a node
     unsigned long long move_chunks;  // add round: 64-child chunks of the old blocks that move
-    unsigned long long wide_tokens;  // appended label tokens outside [0, 65535] (16-bit copy)
+    unsigned long long wide_tokens;  // nonzero: an appended label token lies outside [0, 131071] (no narrow copy)
+    unsigned long long hi_tokens;    // nonzero: an appended label token lies in [65536, 131071] (17-bit labels)
 };
 
 struct DevForest {
@@ -248,10 +249,20 @@ __global__ __launch_bounds__(kTallyThreads) void merge_tally_kernel(Batch B, con
     }
 }
 
-__global__ void split_claim_kernel(DevForest F, Batch B, const InsState *st) {
+// Where node c's record lives now: an add phase earlier in the same round
+// (stamp > 0) may have moved it into its parent's rebuilt block.
+__device__ __forceinline__ int32_t current_pos(const DevForest &F, int32_t c, long long stamp) {
+    if (stamp <= 0) return c;
+    const long long mv = F.moved[c];
+    return (mv >> 32) == stamp ? (int32_t)(uint32_t)mv : c;
+}
+
+// SPLIT phase, step 1: per child c, the lowest batch index wins the claim.
+// stamp: that of the add phase that ran earlier in this round, or 0.
+__global__ void split_claim_kernel(DevForest F, Batch B, const InsState *st, long long stamp) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= B.n || st[i].kind != kInsSplit) return;
-    atomicMax(&F.nodes[st[i].c].aux, (int32_t)(INT32_MAX - i));
+    atomicMax(&F.nodes[current_pos(F, st[i].c, stamp)].aux, (int32_t)(INT32_MAX - i));
 }
 
 __device__ __forceinline__ void copy_mext(const DevForest &F, int64_t dst, int64_t src, int lane) {
@@ -267,14 +278,19 @@ __device__ __forceinline__ void copy_tokens(int32_t *dst, const int32_t *src, in
     for (int64_t k = lane; k < n; k += 64) dst[k] = src[k];
 }
 
-// Cut child c's edge after l tokens; the winning insert's rest becomes a leaf.
+// Cut child c's edge after l tokens; the winning insert's rest becomes a leaf,
+// and the winner is done.  An add phase earlier in the round may have moved
+// c's record (stamp, as for the claim); it also may have given c a new child
+// block, which the lower part of the edge takes along.
 __global__ __launch_bounds__(64 *kMergeWavesPerBlock) void split_apply_kernel(DevForest F, Batch B,
-                                                                             const InsState *st,
-                                                                             MergeCounters *ctr) {
+                                                                             InsState *st,
+                                                                             MergeCounters *ctr,
+                                                                             long long stamp) {
     const int lane = (int)(threadIdx.x & 63);
     const int64_t i = m_wave_index();
     if (i >= B.n || st[i].kind != kInsSplit) return;
-    const InsState r = st[i];
+    InsState r = st[i];
+    r.c = current_pos(F, r.c, stamp);
     if (F.nodes[r.c].aux != (int32_t)(INT32_MAX - i)) return;  // another insert cuts c this round
     const int32_t *s = B.tokens + B.offsets[i];
     const int64_t len = B.offsets[i + 1] - B.offsets[i];
@@ -287,7 +303,12 @@ __global__ __launch_bounds__(64 *kMergeWavesPerBlock) void split_apply_kernel(De
     const int64_t nb = (int64_t)wave_atomic_add(&ctr->n_nodes, (unsigned long long)k, lane);
     const int64_t pb = rest > 0 ? (int64_t)wave_atomic_add(&ctr->n_pool, (unsigned long long)rest, lane) : 0;
     if (nb + k > F.cap_nodes || pb + rest > F.cap_pool) {
-        if (lane == 0) atomicAdd(&ctr->overflow, 1ull);
+        // refused: nothing is written, the claim is withdrawn, and the insert
+        // walks again once the host has grown the forest
+        if (lane == 0) {
+            atomicAdd(&ctr->overflow, 1ull);
+            F.nodes[r.c].aux = 0;
+        }
         return;
     }
     const Node old = F.nodes[r.c];
@@ -329,6 +350,7 @@ __global__ __launch_bounds__(64 *kMergeWavesPerBlock) void split_apply_kernel(De
         upper.ct_cnt = k;
         upper.aux = 0;
         F.nodes[r.c] = upper;
+        st[i].kind = kInsDone;  // the sequence ends at the leaf, or at upper (rest 0)
     }
 }
 
@@ -466,7 +488,7 @@ __global__ __launch_bounds__(64 *kMergeWavesPerBlock) void add_move_kernel(
 // Step 5 (one wave per winning entry): the leaf holding the rest of the
 // winner's sequence, in its token's slot among the parent's children.
 __global__ __launch_bounds__(64 *kMergeWavesPerBlock) void add_leaf_kernel(
-    DevForest F, Batch B, const unsigned long long *keys, const int32_t *vals, int64_t n_add, const InsState *st,
+    DevForest F, Batch B, const unsigned long long *keys, const int32_t *vals, int64_t n_add, InsState *st,
     const int32_t *win, const int32_t *widx, const int64_t *poff, const int32_t *hd, const int32_t *grp_nb,
     const int64_t *grp_pb) {
     const int lane = (int)(threadIdx.x & 63);
@@ -497,6 +519,7 @@ __global__ __launch_bounds__(64 *kMergeWavesPerBlock) void add_leaf_kernel(
         F.nodes[dst] = leaf;
         F.ntok[dst] = leaf.tok;
         if (F.ltime) F.ltime[dst] = 0ull;
+        st[i].kind = kInsDone;  // the winner's sequence ends at its new leaf
     }
 }
 

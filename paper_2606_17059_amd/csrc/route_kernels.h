@@ -29,7 +29,10 @@
 // route_order_count_kernel and route_order_scatter_kernel below).
 // Labels are read from the int32 pool, or, while every label token lies in
 // [0, 65535], from a 16-bit copy of it (half the label bytes and requests; a
-// query token outside that range equals no label token either way).
+// query token outside that range equals no label token either way), or,
+// while every label token lies in [0, 131071], from that copy of the low 16
+// bits plus a plane of bit 16 (one 32-bit word per 32 tokens, loaded once per
+// compare step and handed to the lanes by cross-lane permutes).
 #ifndef PR_ROUTE_KERNELS_H
 #define PR_ROUTE_KERNELS_H
 
@@ -97,12 +100,61 @@ __device__ __forceinline__ int32_t load_label(__amdgpu_buffer_rsrc_t r, int32_t 
         return __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, 0);
 }
 
+// Where a compare step reads its labels.  p: the label's first token in the
+// pool (int32), or in its 16-bit copy.  HB (17-bit labels, with the 16-bit
+// copy): bit 16 of pool token i is bit i % 32 of hib[i / 32], and abs is the
+// label's offset in the pool, so that a step knows which bit words to load.
+template <typename LT, bool HB>
+struct LabelSrc {
+    const LT *p;
+    const uint32_t *hib;
+    uint32_t abs;
+};
+
+// The bit words of a step over pool tokens [A, A + cnt), A = abs + base: lane w
+// holds word A / 32 + w (w <= 32 for cnt <= 1024), with the bits of tokens at
+// or past A + cnt cleared, so that lanes past the step compare equal as with
+// plain labels.  Lane l of every 64-token vector j then takes bit
+// (A % 32 + l) % 32 of lane 2 j + (A % 32 + l) / 32's word (hb_take).
+struct HiBits {
+    uint32_t word;   // this lane's bit word
+    int32_t addr;    // ds_bpermute byte address of vector 0's source lane
+    uint32_t shift;  // bit position inside it
+};
+
+// The load is issued by hb_load; hb_trim, called once every load of the step
+// has been issued, clears the bits past the step (so that the first use of
+// the word does not make the compiler wait on it before the other loads).
+__device__ __forceinline__ HiBits hb_load(const uint32_t *hib, uint32_t A, int32_t cnt, int lane) {
+    const uint32_t a0 = A & 31u;
+    const int32_t nwords = (int32_t)((a0 + (uint32_t)cnt + 31u) >> 5);
+    const __amdgpu_buffer_rsrc_t r =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<uint32_t *>(hib + (A >> 5)), (short)0, nwords * 4, 0x00020000);
+    HiBits h;
+    h.word = (uint32_t)__builtin_amdgcn_raw_buffer_load_b32(r, lane * 4, 0, 0);
+    h.addr = (int32_t)(((a0 + (uint32_t)lane) >> 5) << 2);
+    h.shift = (a0 + (uint32_t)lane) & 31u;
+    return h;
+}
+
+__device__ __forceinline__ void hb_trim(HiBits &h, uint32_t A, int32_t cnt, int lane) {
+    const int32_t lim = cnt + (int32_t)(A & 31u) - 32 * lane;  // bits of this lane's word inside the step
+    h.word = lim >= 32 ? h.word : (lim <= 0 ? 0u : h.word & ((1u << lim) - 1u));
+}
+
+// Bit 16 of the label token lane `lane` holds in vector j.
+__device__ __forceinline__ int32_t hb_take(const HiBits &h, int j) {
+    const uint32_t w = (uint32_t)__builtin_amdgcn_ds_bpermute(h.addr + 8 * j, (int32_t)h.word);
+    return (int32_t)(((w >> h.shift) & 1u) << 16);
+}
+
 // One compare step over cnt <= 64 * NV tokens: ra holds the label tokens
 // (LT wide), rb the query tokens, both ranged to cnt tokens so that lanes past
 // the end read 0 on both sides and compare equal.  Returns the first
 // mismatch, or -1.
-template <int NV, typename LT>
-__device__ __forceinline__ int32_t lcp_step(__amdgpu_buffer_rsrc_t ra, __amdgpu_buffer_rsrc_t rb, int lane) {
+template <int NV, typename LT, bool HB = false>
+__device__ __forceinline__ int32_t lcp_step(__amdgpu_buffer_rsrc_t ra, __amdgpu_buffer_rsrc_t rb, int lane,
+                                            const uint32_t *hib = nullptr, uint32_t A = 0, int32_t cnt = 0) {
     int32_t va[NV], vb[NV];
     // opaque lane offset: with its range unknown the per-vector constant stays
     // an add, which folds into the loads' immediate offsets; and as each step
@@ -121,6 +173,12 @@ __device__ __forceinline__ int32_t lcp_step(__amdgpu_buffer_rsrc_t ra, __amdgpu_
     for (int j = 0; j < NV; j++) {
         va[j] = load_label<LT>(ra, offa + j * kWave * (int32_t)sizeof(LT));
         vb[j] = __builtin_amdgcn_raw_buffer_load_b32(rb, off + j * kWave * 4, 0, kQueryPolicy);
+    }
+    if constexpr (HB) {
+        HiBits hb = hb_load(hib, A, cnt, lane);
+        hb_trim(hb, A, cnt, lane);
+#pragma unroll
+        for (int j = 0; j < NV; j++) va[j] |= hb_take(hb, j);
     }
     // fold every vector's mismatches into a lane mask before branching, so
     // that no load of the step can be deferred behind an early exit
@@ -146,9 +204,10 @@ __device__ __forceinline__ int32_t lcp_step(__amdgpu_buffer_rsrc_t ra, __amdgpu_
 // 31 tokens short of its nominal size; the nine-vector first step leaves the
 // rest of a 1024-token label to an eight-vector step.  Steps of at most 128
 // and 512 tokens take two- and eight-vector forms.
-template <typename LT>
-__device__ __forceinline__ int64_t wave_lcp(const LT *__restrict__ a, const int32_t *__restrict__ b,
+template <typename LT, bool HB>
+__device__ __forceinline__ int64_t wave_lcp(const LabelSrc<LT, HB> &lab, const int32_t *__restrict__ b,
                                             int64_t n, int64_t base, int64_t first, int lane) {
+    const LT *__restrict__ a = lab.p;
     for (int64_t step = first; base < n; step = (int64_t)kWave * kLcpVectors) {
         int32_t cnt = (int32_t)min(n - base, step);
 #if PR_ALIGN_STEPS
@@ -159,15 +218,16 @@ __device__ __forceinline__ int64_t wave_lcp(const LT *__restrict__ a, const int3
 #endif
         const __amdgpu_buffer_rsrc_t ra = label_rsrc(a + base, cnt);
         const __amdgpu_buffer_rsrc_t rb = token_rsrc(b + base, cnt * 4);
+        const uint32_t A = lab.abs + (uint32_t)base;
         int32_t r;
         if (cnt <= 2 * kWave)
-            r = lcp_step<2, LT>(ra, rb, lane);
+            r = lcp_step<2, LT, HB>(ra, rb, lane, lab.hib, A, cnt);
         else if (cnt <= 8 * kWave)
-            r = lcp_step<8, LT>(ra, rb, lane);
+            r = lcp_step<8, LT, HB>(ra, rb, lane, lab.hib, A, cnt);
         else if (kLcpFirstVectors > 8 && kLcpVectors > kLcpFirstVectors && cnt <= kWave * kLcpFirstVectors)
-            r = lcp_step<kLcpFirstVectors, LT>(ra, rb, lane);
+            r = lcp_step<kLcpFirstVectors, LT, HB>(ra, rb, lane, lab.hib, A, cnt);
         else
-            r = lcp_step<kLcpVectors, LT>(ra, rb, lane);
+            r = lcp_step<kLcpVectors, LT, HB>(ra, rb, lane, lab.hib, A, cnt);
         if (r >= 0 && r < cnt) return base + r;
         base += cnt;
     }
@@ -198,17 +258,24 @@ __device__ __forceinline__ void load_window(int32_t (&win)[kWinVectors], const i
 // Label tokens [0, cnt) (ra, LT wide, cnt <= 64 * NL) against the window,
 // which may hold query tokens past cnt: only lanes below cnt count.  Returns
 // the first mismatch, or -1.
-template <int NL, typename LT>
+template <int NL, typename LT, bool HB>
 __device__ __forceinline__ int32_t lcp_step_win(__amdgpu_buffer_rsrc_t ra, const int32_t (&win)[kWinVectors],
-                                                int32_t cnt, int lane) {
+                                                int32_t cnt, int lane, const uint32_t *hib, uint32_t A) {
     int32_t va[NL];
     int32_t off = lane * (int32_t)sizeof(LT);  // opaque, as in lcp_step
     asm volatile("" : "+v"(off));
 #pragma unroll
     for (int j = 0; j < NL; j++) va[j] = load_label<LT>(ra, off + j * kWave * (int32_t)sizeof(LT));
+    if constexpr (HB) {
+        HiBits hb = hb_load(hib, A, cnt, lane);
+        hb_trim(hb, A, cnt, lane);
+#pragma unroll
+        for (int j = 0; j < NL; j++) va[j] |= hb_take(hb, j);
+    }
+    // both sides of the & are evaluated, so no label load becomes conditional
     uint32_t mm = 0;
 #pragma unroll
-    for (int j = 0; j < NL; j++) mm |= (uint32_t)(j * kWave + lane < cnt && va[j] != win[j]) << j;
+    for (int j = 0; j < NL; j++) mm |= (uint32_t)((j * kWave + lane < cnt) & (va[j] != win[j])) << j;
     if (!__ballot(mm != 0)) return -1;
 #pragma unroll
     for (int j = 0; j < NL; j++) {
@@ -219,15 +286,15 @@ __device__ __forceinline__ int32_t lcp_step_win(__amdgpu_buffer_rsrc_t ra, const
 }
 
 // wave_lcp for the first level, whose first query tokens are in win.
-template <typename LT>
-__device__ __forceinline__ int64_t wave_lcp_first(const LT *__restrict__ a, const int32_t *__restrict__ b,
+template <typename LT, bool HB>
+__device__ __forceinline__ int64_t wave_lcp_first(const LabelSrc<LT, HB> &lab, const int32_t *__restrict__ b,
                                                   int64_t n, const int32_t (&win)[kWinVectors], int lane) {
     const int32_t cnt = (int32_t)min(n, (int64_t)kWinTokens);
-    const __amdgpu_buffer_rsrc_t ra = label_rsrc(a, cnt);
-    const int32_t r = cnt <= 2 * kWave ? lcp_step_win<2, LT>(ra, win, cnt, lane)
-                                       : lcp_step_win<kWinVectors, LT>(ra, win, cnt, lane);
+    const __amdgpu_buffer_rsrc_t ra = label_rsrc(lab.p, cnt);
+    const int32_t r = cnt <= 2 * kWave ? lcp_step_win<2, LT, HB>(ra, win, cnt, lane, lab.hib, lab.abs)
+                                       : lcp_step_win<kWinVectors, LT, HB>(ra, win, cnt, lane, lab.hib, lab.abs);
     if (r >= 0 && r < cnt) return r;
-    return wave_lcp<LT>(a, b, n, kWinTokens, (int64_t)kWave * kLcpVectors, lane);
+    return wave_lcp<LT, HB>(lab, b, n, kWinTokens, (int64_t)kWave * kLcpVectors, lane);
 }
 #endif
 
@@ -359,13 +426,15 @@ __device__ __forceinline__ int32_t select_peers(const int32_t (&m)[W], int32_t P
 
 // SEL = false: plain routing (every peer eligible, ties to the lowest id, no
 // second pick); the selection options are compiled out.  LT: the label
-// pool's token type (int32_t, or uint16_t for the 16-bit copy).
-template <int W, bool SEL, typename LT>
+// pool's token type (int32_t, or uint16_t for the 16-bit copy); HB (with
+// uint16_t): bit 16 of every label token comes from the bit plane hib
+// (17-bit labels).
+template <int W, bool SEL, typename LT, bool HB = false>
 __global__ __launch_bounds__(kWave *kRouteWavesPerBlock)
 __attribute__((amdgpu_waves_per_eu(PR_ROUTE_WAVES_PER_EU))) void route_kernel(
     const Node *__restrict__ nodes, const int32_t *__restrict__ ntok, const int32_t *__restrict__ nsep,
-    const uint64_t *__restrict__ mext,
-    const LT *__restrict__ pool, const int32_t *__restrict__ qtok, int64_t num_tokens,
+    const uint64_t *__restrict__ mext, const LT *__restrict__ pool, const uint32_t *__restrict__ hib,
+    const int32_t *__restrict__ qtok, int64_t num_tokens,
     const int64_t *__restrict__ qoff, int64_t nq, int32_t P, const Select sel_in, int32_t *__restrict__ match_len,
     int32_t *__restrict__ chosen, const int32_t *__restrict__ order) {
     const Select sel = SEL ? sel_in : Select{nullptr, -1, 0, nullptr};
@@ -450,11 +519,12 @@ __attribute__((amdgpu_waves_per_eu(PR_ROUTE_WAVES_PER_EU))) void route_kernel(
         for (int w = 1; w < W; w++) mx[w] = mext[(int64_t)c.id * (W - 1) + (w - 1)];
         load_block(cb, ntok, nsep, c.ct_beg, c.ct_cnt, lane);
         const int64_t n = min((int64_t)c.lab_len, qlen - d);
+        const LabelSrc<LT, HB> lab{pool + (uint32_t)c.lab_off, hib, (uint32_t)c.lab_off};
         int64_t l;
         if constexpr (FIRST)
-            l = wave_lcp_first<LT>(pool + (uint32_t)c.lab_off, qs, n, win, lane);
+            l = wave_lcp_first<LT, HB>(lab, qs, n, win, lane);
         else
-            l = wave_lcp<LT>(pool + (uint32_t)c.lab_off, qs + d, n, 0, (int64_t)kWave * kLcpFirstVectors, lane);
+            l = wave_lcp<LT, HB>(lab, qs + d, n, 0, (int64_t)kWave * kLcpFirstVectors, lane);
         if constexpr (KNOWN) {
             if constexpr (PR_FIRST_WINDOW) t = uniform(win[0]);
             if (t != c0_tok) return false;  // no child starts with the query's first token
@@ -514,20 +584,46 @@ __attribute__((amdgpu_waves_per_eu(PR_ROUTE_WAVES_PER_EU))) void route_kernel(
     }
 }
 
-// The 16-bit copy of the label pool: p16[i] = pool[i] for i in [from, to);
-// tokens outside [0, 65535] (which make the copy unusable) are counted.
-__global__ void pool16_copy_kernel(const int32_t *__restrict__ pool, uint16_t *__restrict__ p16, int64_t from,
-                                   int64_t to, unsigned long long *__restrict__ wide) {
-    const int64_t i = from + (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    bool out = false;
-    if (i < to) {
-        const int32_t t = pool[i];
-        out = (uint32_t)t > 0xFFFFu;
-        p16[i] = (uint16_t)t;
+// The narrow copy of the label pool for tokens [from, to): p16[i] = the low
+// 16 bits of pool[i], and bit i % 32 of hib[i / 32] = bit 16 of pool[i].  One
+// wave per 64-token chunk (grid-stride), a lane per token: the chunk's two bit
+// words come from one ballot.  Chunks start at a multiple of 64, so the first
+// one may rewrite entries below `from` with the values they already hold.
+// *hi becomes nonzero if a token of the range lies in [65536, 131071] (the
+// bit plane is needed), *wide if one lies outside [0, 131071] (the copy is
+// unusable); each workgroup reduces its finds and writes each flag at most
+// once, so the waves do not queue on one address.
+constexpr int kNarrowThreads = 256;
+__global__ __launch_bounds__(kNarrowThreads) void pool_narrow_kernel(const int32_t *__restrict__ pool,
+                                                                     uint16_t *__restrict__ p16,
+                                                                     uint32_t *__restrict__ hib, int64_t from,
+                                                                     int64_t to, unsigned long long *__restrict__ hi,
+                                                                     unsigned long long *__restrict__ wide) {
+    __shared__ int found[2];
+    const int lane = (int)(threadIdx.x & (kWave - 1));
+    if (threadIdx.x < 2) found[threadIdx.x] = 0;
+    __syncthreads();
+    const int64_t waves = (int64_t)gridDim.x * (kNarrowThreads / kWave);
+    bool h = false, o = false;
+    for (int64_t k = from / kWave + (int64_t)blockIdx.x * (kNarrowThreads / kWave) + threadIdx.x / kWave;
+         k * kWave < to; k += waves) {
+        const int64_t i = k * kWave + lane;
+        const bool in = i < to;
+        const uint32_t t = in ? (uint32_t)pool[i] : 0u;
+        if (in) p16[i] = (uint16_t)t;
+        const uint64_t bits = __ballot((t >> 16) & 1u);
+        if (lane == 0) hib[2 * k] = (uint32_t)bits;
+        if (lane == 32) hib[2 * k + 1] = (uint32_t)(bits >> 32);
+        h |= in && i >= from && t > 0xFFFFu && t <= 0x1FFFFu;
+        o |= in && i >= from && t > 0x1FFFFu;
     }
-    const uint64_t b = __ballot(out);
-    if (b && (int)(threadIdx.x & (kWave - 1)) == __ffsll((unsigned long long)b) - 1)
-        atomicAdd(wide, (unsigned long long)__popcll(b));
+    if (__ballot(h) && lane == 0) found[0] = 1;
+    if (__ballot(o) && lane == 0) found[1] = 1;
+    __syncthreads();
+    if (threadIdx.x == 0 && found[0] && __hip_atomic_load(hi, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0)
+        atomicOr(hi, 1ull);
+    if (threadIdx.x == 1 && found[1] && __hip_atomic_load(wide, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0)
+        atomicOr(wide, 1ull);
 }
 
 // Longest-first order of a batch, a counting sort in two launches of a few

@@ -54,8 +54,9 @@ struct DevImage {
     int32_t *pool = nullptr;
     long long *moved = nullptr;
     unsigned long long *ltime = nullptr;  // local peer's access times (allocated while a local peer is set)
-    uint16_t *pool16 = nullptr;  // 16-bit copy of pool, which routes read while every label token fits
+    uint16_t *pool16 = nullptr;  // low 16 bits of pool, which routes read while every label token fits 17 bits
     int64_t cap_pool16 = 0;
+    uint32_t *hib = nullptr;     // bit 16 of pool token i: bit i % 32 of hib[i / 32] (hib_words(cap_pool16) words)
     int64_t cap_nodes = 0, cap_pool = 0;
     int64_t n_nodes = 0, n_pool = 0;  // host mirror of the device counters
 };
@@ -122,12 +123,16 @@ struct pr_forest {
     ExportScratch xs;
     RouteScratch rs;
     long long stamp = 0;          // add-round counter (stamps of moved records)
+    int64_t round_nodes = 0;      // records the last merge added (spare capacity kept for the next)
+    int64_t refusals = 0;         // merge rounds repeated after running out of capacity
     int32_t local = -1;           // peer whose tree keeps access times (-1: none)
     int64_t now = 0;              // current time, set by the caller, never decreasing
     int64_t local_load_time = 0;  // time of the local peer's last host snapshot
     int64_t device_bytes = 0;
     int64_t layout_epoch = 0;     // advances whenever the device arrays the route reads move
-    bool narrow = false;          // dev.pool16 mirrors dev.pool[0, n_pool) (every label token in [0, 65535])
+    bool narrow = false;          // dev.pool16 and dev.hib mirror dev.pool[0, n_pool) (every label token in
+                                  // [0, 131071])
+    bool hi17 = false;            // some label token is in [65536, 131071]: routes need the bit plane
     bool broken = false;          // a device update failed; only destroy is valid
 };
 
@@ -135,6 +140,10 @@ namespace {
 
 #ifndef PR_ROUTE_LONGEST_FIRST
 #define PR_ROUTE_LONGEST_FIRST 1
+#endif
+// Narrow (16- or 17-bit) label copies for routes; 0 keeps every forest on int32 labels.
+#ifndef PR_NARROW_LABELS
+#define PR_NARROW_LABELS 1
 #endif
 
 // Makes the forest's device current for the duration of a call.
@@ -188,6 +197,10 @@ void dfree(pr_forest *f, T **p, int64_t count) {
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+// Words of the bit plane for a pool capacity of cap tokens: two per 64-token
+// chunk (the narrow copy kernel writes a chunk's two words together).
+int64_t hib_words(int64_t cap) { return 2 * ((cap + 63) / 64) + 2; }
+
 // The per-node arrays of one capacity (records, first tokens, separators,
 // extra mask words, move stamps) in one device allocation, each 256-byte
 // aligned: growing the forest costs one hipMalloc and one hipFree instead of
@@ -236,9 +249,11 @@ void free_image(pr_forest *f) {
     dfree(f, &d.pool, d.cap_pool);
     dfree(f, &d.ltime, d.cap_nodes);
     dfree(f, &d.pool16, d.cap_pool16);
+    dfree(f, &d.hib, hib_words(d.cap_pool16));
     d = DevImage();
     f->has_dev = false;
     f->narrow = false;
+    f->hi17 = false;
 }
 
 void free_export_scratch(pr_forest *f) {
@@ -313,6 +328,8 @@ pr_status ensure_host_image(pr_forest *f) {
     return PR_OK;
 }
 
+void drop_pool16(pr_forest *f);
+
 // Grow the node and pool capacities to hold at least the given totals.
 pr_status ensure_capacity(pr_forest *f, int64_t need_nodes, int64_t need_pool, hipStream_t s) {
     DevImage &d = f->dev;
@@ -374,14 +391,40 @@ pr_status ensure_capacity(pr_forest *f, int64_t need_nodes, int64_t need_pool, h
                                               (int64_t)UINT32_MAX);
         int32_t *np = nullptr;
         if (!dalloc(f, &np, cap)) return fail(PR_ENOMEM, "hipMalloc failed while growing the label pool");
+        // the narrow copy grows with the pool, under the same wait (without
+        // the memory, routes fall back to the int32 pool)
+        uint16_t *n16 = nullptr;
+        uint32_t *nhb = nullptr;
+        const bool narrow = f->narrow && d.pool16 && d.hib;
+        const bool keep16 = narrow && dalloc(f, &n16, cap) && dalloc(f, &nhb, hib_words(cap));
+        // the tail is zeroed: a merge round refused for lack of capacity can
+        // leave unwritten tokens below the used size, which the narrow copy
+        // then converts
         if (hipMemcpyAsync(np, d.pool, d.n_pool * sizeof(int32_t), hipMemcpyDeviceToDevice, s) != hipSuccess ||
+            hipMemsetAsync(np + d.n_pool, 0, (cap - d.n_pool) * sizeof(int32_t), s) != hipSuccess ||
+            (keep16 &&
+             (hipMemcpyAsync(n16, d.pool16, d.n_pool * sizeof(uint16_t), hipMemcpyDeviceToDevice, s) != hipSuccess ||
+              hipMemcpyAsync(nhb, d.hib, hib_words(d.n_pool) * sizeof(uint32_t), hipMemcpyDeviceToDevice, s) !=
+                  hipSuccess)) ||
             hipStreamSynchronize(s) != hipSuccess || hipDeviceSynchronize() != hipSuccess) {
             dfree(f, &np, cap);
+            dfree(f, &n16, cap);
+            dfree(f, &nhb, hib_words(cap));
             return fail(PR_EDEVICE, "device copy failed while growing the label pool");
         }
         dfree(f, &d.pool, d.cap_pool);
         d.pool = np;
         d.cap_pool = cap;
+        if (keep16) {
+            dfree(f, &d.pool16, d.cap_pool16);
+            dfree(f, &d.hib, hib_words(d.cap_pool16));
+            d.pool16 = n16;
+            d.hib = nhb;
+            d.cap_pool16 = cap;
+        } else if (narrow) {
+            dfree(f, &n16, cap);
+            drop_pool16(f);
+        }
         f->layout_epoch++;
     }
     return PR_OK;
@@ -389,52 +432,64 @@ pr_status ensure_capacity(pr_forest *f, int64_t need_nodes, int64_t need_pool, h
 
 pr::DevForest dev_view(const pr_forest *f);
 
-// The 16-bit label copy.  Routes read labels from it while every label token
-// lies in [0, 65535] (half the label bytes); otherwise from the int32 pool.
-// Labels are only ever appended to the pool (a split reuses a span of its
-// label), so the copy follows merges by converting the appended range.
+// The narrow label copy.  While every label token lies in [0, 131071], routes
+// read labels from pool16 (the low 16 bits: half the label bytes) and, once
+// some token is 65536 or more, from hib (bit 16, one bit per token) as well;
+// otherwise from the int32 pool.  Labels are only ever appended to the pool
+// (a split reuses a span of its label), so the copy follows merges by
+// converting the appended range.
 void drop_pool16(pr_forest *f) {
     DevImage &d = f->dev;
-    if (d.pool16) {
-        // a route launched earlier on another stream may still read it
+    if (d.pool16 || d.hib) {
+        // a route launched earlier on another stream may still read them
         (void)hipDeviceSynchronize();
         dfree(f, &d.pool16, d.cap_pool16);
+        dfree(f, &d.hib, hib_words(d.cap_pool16));
         f->layout_epoch++;
     }
     d.cap_pool16 = 0;
     f->narrow = false;
+    f->hi17 = false;
 }
 
 // Enqueue the copy of pool[from, n_pool) on s, first growing the copy to the
-// pool's capacity (then it is rebuilt from 0).  Tokens out of range are
-// counted in the merge counters' wide_tokens; the caller reads them with its
-// next counter readback and drops the copy if there are any.  Without memory
-// for a larger copy, routes fall back to the int32 pool.
+// pool's capacity (then it is rebuilt from 0).  Tokens in [65536, 131071] are
+// counted in the merge counters' hi_tokens, tokens outside [0, 131071] in
+// wide_tokens; the caller reads them with its next counter readback, turns
+// the bit plane on for the former and drops the copy for the latter.  Without
+// memory for a larger copy, routes fall back to the int32 pool.
 pr_status pool16_extend(pr_forest *f, int64_t from, hipStream_t s) {
     DevImage &d = f->dev;
     if (!f->narrow) return PR_OK;
     if (d.cap_pool16 < d.cap_pool) {
         uint16_t *np = nullptr;
-        if (!dalloc(f, &np, d.cap_pool)) {
+        uint32_t *nh = nullptr;
+        if (!dalloc(f, &np, d.cap_pool) || !dalloc(f, &nh, hib_words(d.cap_pool))) {
+            dfree(f, &np, d.cap_pool);
             drop_pool16(f);
             return PR_OK;
         }
         if (d.pool16) {
             if (hipDeviceSynchronize() != hipSuccess) {
                 dfree(f, &np, d.cap_pool);
-                return fail(PR_EDEVICE, "hipDeviceSynchronize failed while growing the 16-bit labels");
+                dfree(f, &nh, hib_words(d.cap_pool));
+                return fail(PR_EDEVICE, "hipDeviceSynchronize failed while growing the narrow labels");
             }
             dfree(f, &d.pool16, d.cap_pool16);
+            dfree(f, &d.hib, hib_words(d.cap_pool16));
         }
         d.pool16 = np;
+        d.hib = nh;
         d.cap_pool16 = d.cap_pool;
         from = 0;
         f->layout_epoch++;
     }
     if (d.n_pool > from) {
-        hipLaunchKernelGGL(pr::pool16_copy_kernel, dim3(grid_threads(d.n_pool - from, 256)), dim3(256), 0, s, d.pool,
-                           d.pool16, from, d.n_pool, &f->d_ctr->wide_tokens);
-        if (hipGetLastError() != hipSuccess) return fail(PR_EDEVICE, "16-bit label copy failed to launch");
+        const int64_t chunks = (d.n_pool + pr::kWave - 1) / pr::kWave - from / pr::kWave;
+        const int64_t blocks = std::min<int64_t>((chunks + 3) / 4, 1024);
+        hipLaunchKernelGGL(pr::pool_narrow_kernel, dim3((unsigned)blocks), dim3(pr::kNarrowThreads), 0, s, d.pool,
+                           d.pool16, d.hib, from, d.n_pool, &f->d_ctr->hi_tokens, &f->d_ctr->wide_tokens);
+        if (hipGetLastError() != hipSuccess) return fail(PR_EDEVICE, "narrow label copy failed to launch");
     }
     return PR_OK;
 }
@@ -484,6 +539,7 @@ pr_status commit(pr_forest *f) {
         (f->W > 1 && hipMemcpy(d.mext, h.mext.data(), h.mext.size() * sizeof(uint64_t), hipMemcpyHostToDevice) !=
                          hipSuccess) ||
         (np > 0 && hipMemcpy(d.pool, h.pool.data(), np * sizeof(int32_t), hipMemcpyHostToDevice) != hipSuccess) ||
+        hipMemset(d.pool + np, 0, (d.cap_pool - np) * sizeof(int32_t)) != hipSuccess ||
         hipMemset(d.moved, 0, d.cap_nodes * sizeof(long long)) != hipSuccess) {
         free_image(f);
         return fail(PR_EDEVICE, "upload of the forest image failed");
@@ -496,25 +552,36 @@ pr_status commit(pr_forest *f) {
     c.n_pool = (unsigned long long)np;
     if (hipMemcpy(f->d_ctr, &c, sizeof(c), hipMemcpyHostToDevice) != hipSuccess)
         return fail(PR_EDEVICE, "counter upload failed");
-    // 16-bit labels when every token fits (else, or without the memory, int32)
-    f->narrow = std::all_of(h.pool.begin(), h.pool.end(), [](int32_t t) { return (uint32_t)t <= 0xFFFFu; });
+    // narrow labels when every token fits 17 bits (else, or without the memory,
+    // int32): the low 16 bits, and bit 16 as a plane once some token needs it
+    f->narrow = PR_NARROW_LABELS &&
+                std::all_of(h.pool.begin(), h.pool.end(), [](int32_t t) { return (uint32_t)t <= 0x1FFFFu; });
+    f->hi17 = f->narrow && std::any_of(h.pool.begin(), h.pool.end(), [](int32_t t) { return (uint32_t)t > 0xFFFFu; });
     if (f->narrow) {
         std::vector<uint16_t> p16;
+        std::vector<uint32_t> hb;
         try {
-            p16.assign(h.pool.begin(), h.pool.end());
+            p16.assign(h.pool.begin(), h.pool.end());  // the low 16 bits
+            hb.assign((size_t)hib_words(np), 0u);
+            for (int64_t i = 0; i < np; i++) hb[(size_t)(i >> 5)] |= (((uint32_t)h.pool[(size_t)i] >> 16) & 1u) << (i & 31);
         } catch (const std::bad_alloc &) {
             f->narrow = false;
         }
-        if (f->narrow && dalloc(f, &d.pool16, d.cap_pool)) {
+        if (f->narrow && dalloc(f, &d.pool16, d.cap_pool) && dalloc(f, &d.hib, hib_words(d.cap_pool))) {
             d.cap_pool16 = d.cap_pool;
-            if (np > 0 && hipMemcpy(d.pool16, p16.data(), np * sizeof(uint16_t), hipMemcpyHostToDevice) != hipSuccess) {
+            if ((np > 0 && hipMemcpy(d.pool16, p16.data(), np * sizeof(uint16_t), hipMemcpyHostToDevice) != hipSuccess) ||
+                hipMemcpy(d.hib, hb.data(), hb.size() * sizeof(uint32_t), hipMemcpyHostToDevice) != hipSuccess) {
+                d.cap_pool16 = d.cap_pool;
                 free_image(f);
-                return fail(PR_EDEVICE, "upload of the 16-bit labels failed");
+                return fail(PR_EDEVICE, "upload of the narrow labels failed");
             }
         } else {
+            dfree(f, &d.pool16, d.cap_pool);
+            dfree(f, &d.hib, hib_words(d.cap_pool));
             f->narrow = false;
         }
     }
+    if (!f->narrow) f->hi17 = false;
     f->has_dev = true;
     f->dirty = false;
     f->merged = false;
@@ -590,30 +657,38 @@ pr_status route_order(pr_forest *f, const int64_t *q_offsets, int64_t nq, int64_
     return PR_OK;
 }
 
-template <int W, bool SEL, typename LT>
+template <int W, bool SEL, typename LT, bool HB>
 void launch_route_t(const pr_forest *f, const LT *pool, const int32_t *qt, int64_t ntok, const int64_t *qo,
                     int64_t nq, const pr::Select &sel, int32_t *ml, int32_t *ch, const int32_t *order,
                     hipStream_t s) {
     const int64_t blocks = (nq + pr::kRouteWavesPerBlock - 1) / pr::kRouteWavesPerBlock;
-    hipLaunchKernelGGL((pr::route_kernel<W, SEL, LT>), dim3((unsigned)blocks), dim3(pr::kWave * pr::kRouteWavesPerBlock),
-                       0, s, f->dev.nodes, f->dev.ntok, f->dev.nsep, f->dev.mext, pool, qt, ntok, qo, nq, f->P, sel,
-                       ml, ch, order);
+    const uint32_t *hib = HB ? f->dev.hib : nullptr;
+    hipLaunchKernelGGL((pr::route_kernel<W, SEL, LT, HB>), dim3((unsigned)blocks),
+                       dim3(pr::kWave * pr::kRouteWavesPerBlock), 0, s, f->dev.nodes, f->dev.ntok, f->dev.nsep,
+                       f->dev.mext, pool, hib, qt, ntok, qo, nq, f->P, sel, ml, ch, order);
 }
 
-// Plain routing or selection, over the 16-bit labels when they are current.
+template <int W, bool SEL>
+void launch_route_l(const pr_forest *f, const int32_t *qt, int64_t ntok, const int64_t *qo, int64_t nq,
+                    const pr::Select &sel, int32_t *ml, int32_t *ch, const int32_t *order, hipStream_t s) {
+    const bool narrow = f->narrow && f->dev.pool16 && f->dev.hib;
+    if (narrow && f->hi17)
+        launch_route_t<W, SEL, uint16_t, true>(f, f->dev.pool16, qt, ntok, qo, nq, sel, ml, ch, order, s);
+    else if (narrow)
+        launch_route_t<W, SEL, uint16_t, false>(f, f->dev.pool16, qt, ntok, qo, nq, sel, ml, ch, order, s);
+    else
+        launch_route_t<W, SEL, int32_t, false>(f, f->dev.pool, qt, ntok, qo, nq, sel, ml, ch, order, s);
+}
+
+// Plain routing or selection, over the narrow labels when they are current.
 template <int W>
 hipError_t launch_route(const pr_forest *f, const int32_t *qt, int64_t ntok, const int64_t *qo, int64_t nq,
                         const pr::Select &sel, int32_t *ml, int32_t *ch, const int32_t *order, hipStream_t s) {
     const bool plain = !sel.eligible && !sel.prefer_local && !sel.second;
-    const bool narrow = f->narrow && f->dev.pool16;
-    if (plain && narrow)
-        launch_route_t<W, false>(f, f->dev.pool16, qt, ntok, qo, nq, sel, ml, ch, order, s);
-    else if (plain)
-        launch_route_t<W, false>(f, f->dev.pool, qt, ntok, qo, nq, sel, ml, ch, order, s);
-    else if (narrow)
-        launch_route_t<W, true>(f, f->dev.pool16, qt, ntok, qo, nq, sel, ml, ch, order, s);
+    if (plain)
+        launch_route_l<W, false>(f, qt, ntok, qo, nq, sel, ml, ch, order, s);
     else
-        launch_route_t<W, true>(f, f->dev.pool, qt, ntok, qo, nq, sel, ml, ch, order, s);
+        launch_route_l<W, true>(f, qt, ntok, qo, nq, sel, ml, ch, order, s);
     return hipGetLastError();
 }
 
@@ -747,6 +822,7 @@ __global__ void reset_round_kernel(pr::MergeCounters *c) {
 
 __global__ void reset_call_kernel(pr::MergeCounters *c) {
     c->wide_tokens = 0;
+    c->hi_tokens = 0;
     c->n_add = 0;
     c->n_split = 0;
     c->pool_need = 0;
@@ -758,6 +834,14 @@ __global__ void reset_call_kernel(pr::MergeCounters *c) {
 }
 
 __global__ void add_skipped_kernel(unsigned long long *acc, const pr::MergeCounters *c) { *acc += c->skipped; }
+
+// Counters after refused allocations: the used sizes the host clipped to the
+// capacities, and no refusal pending.
+__global__ void set_used_kernel(pr::MergeCounters *c, unsigned long long n_nodes, unsigned long long n_pool) {
+    c->n_nodes = n_nodes;
+    c->n_pool = n_pool;
+    c->overflow = 0;
+}
 
 // Copy `bytes` (<= kStageBytes) of device memory to the host through the
 // forest's pinned staging buffer (a direct DMA, no pageable bounce) and wait.
@@ -779,6 +863,12 @@ pr_status read_counters(pr_forest *f, pr::MergeCounters *c, hipStream_t s) {
     if (!read_small(f, c, f->d_ctr, sizeof(*c), s)) return fail(PR_EDEVICE, "reading merge counters failed");
     f->dev.n_nodes = (int64_t)c->n_nodes;
     f->dev.n_pool = (int64_t)c->n_pool;
+    return PR_OK;
+}
+
+// The counters only (the caller decides what the used sizes are).
+pr_status read_counters_raw(pr_forest *f, pr::MergeCounters *c, hipStream_t s) {
+    if (!read_small(f, c, f->d_ctr, sizeof(*c), s)) return fail(PR_EDEVICE, "reading merge counters failed");
     return PR_OK;
 }
 
@@ -806,6 +896,7 @@ pr_status run_merge(pr_forest *f, const int32_t *peer_of, const int32_t *tokens,
     pr_status r = ensure_merge_scratch(f, n, s);
     if (r) return r;
     const int64_t pool0 = f->dev.n_pool;  // labels appended from here on
+    const int64_t nodes0 = f->dev.n_nodes;
     MergeScratch &m = f->ms;
     pr::Batch B{peer_of, tokens, offsets, num_tokens, n, f->P, stamp};
     const int bs = 256, wb = 64 * pr::kMergeWavesPerBlock;
@@ -814,6 +905,7 @@ pr_status run_merge(pr_forest *f, const int32_t *peer_of, const int32_t *tokens,
     pr::MergeCounters c;
     const int max_rounds = 100000;
     int round = 0;
+    int refusals = 0;
     for (; round < max_rounds; round++) {
         hipLaunchKernelGGL(reset_round_kernel, dim3(1), dim3(1), 0, s, f->d_ctr);
         hipLaunchKernelGGL(pr::merge_walk_kernel, dim3(grid_waves(n)), dim3(wb), 0, s, dev_view(f), B, m.st,
@@ -821,16 +913,44 @@ pr_status run_merge(pr_forest *f, const int32_t *peer_of, const int32_t *tokens,
         hipLaunchKernelGGL(pr::merge_tally_kernel,
                            dim3((unsigned)std::min<int64_t>(256, (n + pr::kTallyThreads - 1) / pr::kTallyThreads)),
                            dim3(pr::kTallyThreads), 0, s, B, m.st, f->d_ctr);
-        if ((r = read_counters(f, &c, s))) return r;
-        if (c.overflow) break;  // reported below; the forest stays consistent
-        if (c.n_split > 0) {
-            if ((r = ensure_capacity(f, (int64_t)c.n_nodes + 2 * (int64_t)c.n_split,
-                                     (int64_t)c.n_pool + (int64_t)c.pool_need, s)))
+        if ((r = read_counters_raw(f, &c, s))) return r;
+        if (c.overflow) {
+            // The last round ran out of capacity.  Every refused allocation
+            // wrote nothing and left its inserts to walk again (above), but
+            // the refused requests still advanced the counters: records and
+            // tokens past the last allocation that fit were never written, so
+            // the counters are clipped to the capacities, and the forest grows
+            // to what the round asked for before the round is repeated.
+            if (++refusals > 4) break;  // reported below
+            f->refusals++;
+            const int64_t want_nodes = (int64_t)c.n_nodes, want_pool = (int64_t)c.n_pool;
+            f->dev.n_nodes = std::min<int64_t>(want_nodes, f->dev.cap_nodes);
+            f->dev.n_pool = std::min<int64_t>(want_pool, f->dev.cap_pool);
+            hipLaunchKernelGGL(set_used_kernel, dim3(1), dim3(1), 0, s, f->d_ctr,
+                               (unsigned long long)f->dev.n_nodes, (unsigned long long)f->dev.n_pool);
+            if (hipGetLastError() != hipSuccess) return fail(PR_EDEVICE, "merge launch failed");
+            if ((r = ensure_capacity(f, std::max<int64_t>(want_nodes, f->dev.n_nodes + 1),
+                                     std::max<int64_t>(want_pool, f->dev.n_pool + (int64_t)c.pool_need), s)))
                 return r;
-            const pr::DevForest F = dev_view(f);
-            hipLaunchKernelGGL(pr::split_claim_kernel, dim3(grid_threads(n, bs)), dim3(bs), 0, s, F, B, m.st);
-            hipLaunchKernelGGL(pr::split_apply_kernel, dim3(grid_waves(n)), dim3(wb), 0, s, F, B, m.st, f->d_ctr);
-        } else if (c.n_add > 0) {
+            continue;
+        }
+        f->dev.n_nodes = (int64_t)c.n_nodes;
+        f->dev.n_pool = (int64_t)c.n_pool;
+        if (c.n_add == 0 && c.n_split == 0) break;
+        // One round applies both kinds from the same walk: the add phase first
+        // (rebuilt child blocks move records; the split phase finds them through
+        // their move stamps), then the split phase.  The winners of either are
+        // done; the losers (the same slot or the same edge as a winner) walk
+        // again.  Allocations come from the device counters; one that does not
+        // fit the capacity is refused (see above), so no readback sits between
+        // the phases.  A forest whose spare capacity is short of what the last
+        // merges added grows first (the walk's tally bounds the pool tokens).
+        const int64_t n_split = (int64_t)c.n_split;
+        if ((r = ensure_capacity(f, f->dev.n_nodes + 2 * std::max<int64_t>(f->round_nodes, n),
+                                 f->dev.n_pool + (int64_t)c.pool_need, s)))
+            return r;
+        long long add_stamp = 0;
+        if (c.n_add > 0) {
             const int64_t n_add = (int64_t)c.n_add;
             hipLaunchKernelGGL(pr::add_keys_kernel, dim3(grid_threads(n, bs)), dim3(bs), 0, s, B, m.st, m.keys_in,
                                m.vals_in);
@@ -861,42 +981,35 @@ pr_status run_merge(pr_forest *f, const int32_t *peer_of, const int32_t *tokens,
             hipLaunchKernelGGL(pr::add_group_kernel, dim3(grid_threads(n_add, bs)), dim3(bs), 0, s, dev_view(f),
                                m.keys_out, m.vals_out, n_add, m.st, m.win, m.rest, m.widx, m.poff, m.hd, m.cstart,
                                m.grp_nw, m.grp_pool, m.win_tok, m.win_ins, f->d_ctr);
-            // A round adds at most one record per old child of the rebuilt
-            // parents (at most every record) plus one leaf per insert, and at
-            // most the pool tokens the walk's tally bounded; when the spare
-            // capacity holds that, no readback is needed before allocating,
-            // and the move kernel's grid takes the matching chunk bound.
-            int64_t chunks;
-            const int64_t nodes_ub = 2 * f->dev.n_nodes + n_add;
-            const int64_t pool_ub = f->dev.n_pool + (int64_t)c.pool_need;
-            if (nodes_ub <= f->dev.cap_nodes && pool_ub <= f->dev.cap_pool) {
-                chunks = (f->dev.n_nodes + 63) / 64 + n_add;  // sum over groups of ceil(old children / 64)
-            } else {
-                if ((r = read_counters(f, &c, s))) return r;
-                if ((r = ensure_capacity(f, (int64_t)c.n_nodes + (int64_t)c.node_need,
-                                         (int64_t)c.n_pool + (int64_t)c.pool_need, s)))
-                    return r;
-                chunks = (int64_t)c.move_chunks;
-            }
+            // the move kernel's grid takes a bound of the chunks (the sum over
+            // groups of ceil(old children / 64)); it reads the exact count
+            const int64_t chunks = (f->dev.n_nodes + 63) / 64 + n_add;
             const long long stamp = ++f->stamp;
+            add_stamp = stamp;
             const pr::DevForest F = dev_view(f);
             hipLaunchKernelGGL(pr::add_alloc_kernel, dim3(grid_threads(n_add, bs)), dim3(bs), 0, s, F, m.keys_out,
                                n_add, m.grp_nw, m.grp_pool, m.grp_nb, m.grp_pb, f->d_ctr);
-            if (chunks > 0)
-                hipLaunchKernelGGL(pr::add_move_kernel, dim3(grid_waves(chunks)), dim3(wb), 0, s, F, m.keys_out,
-                                   n_add, m.cstart, f->d_ctr, m.grp_nw, m.grp_nb, m.win_tok, stamp);
+            hipLaunchKernelGGL(pr::add_move_kernel, dim3(grid_waves(chunks)), dim3(wb), 0, s, F, m.keys_out, n_add,
+                               m.cstart, f->d_ctr, m.grp_nw, m.grp_nb, m.win_tok, stamp);
             hipLaunchKernelGGL(pr::add_leaf_kernel, dim3(grid_waves(n_add)), dim3(wb), 0, s, F, B, m.keys_out,
                                m.vals_out, n_add, m.st, m.win, m.widx, m.poff, m.hd, m.grp_nb, m.grp_pb);
             hipLaunchKernelGGL(pr::add_sep_kernel, dim3(grid_waves(n_add)), dim3(wb), 0, s, F, m.keys_out, n_add,
                                m.grp_nw, m.grp_nb);
             hipLaunchKernelGGL(pr::add_fix_kernel, dim3(grid_threads(n_add, bs)), dim3(bs), 0, s, F, m.keys_out,
                                n_add, m.grp_nw, m.grp_nb, stamp);
-        } else {
-            break;
+        }
+        if (n_split > 0) {
+            const pr::DevForest F = dev_view(f);
+            hipLaunchKernelGGL(pr::split_claim_kernel, dim3(grid_threads(n, bs)), dim3(bs), 0, s, F, B, m.st,
+                               add_stamp);
+            hipLaunchKernelGGL(pr::split_apply_kernel, dim3(grid_waves(n)), dim3(wb), 0, s, F, B, m.st, f->d_ctr,
+                               add_stamp);
         }
         if (hipGetLastError() != hipSuccess) return fail(PR_EDEVICE, "merge launch failed");
     }
     if (round == max_rounds) return fail(PR_EDEVICE, "merge did not converge");
+    // records this merge added: the spare capacity the next one keeps free
+    f->round_nodes = std::max<int64_t>(f->dev.n_nodes - nodes0, 0);
     hipLaunchKernelGGL(pr::merge_mask_kernel, dim3(grid_waves(n)), dim3(wb), 0, s, dev_view(f), B, m.st, f->d_ctr);
     hipLaunchKernelGGL(add_skipped_kernel, dim3(1), dim3(1), 0, s, f->d_skipped, f->d_ctr);
     if (hipGetLastError() != hipSuccess) return fail(PR_EDEVICE, "merge launch failed");
@@ -905,7 +1018,12 @@ pr_status run_merge(pr_forest *f, const int32_t *peer_of, const int32_t *tokens,
     if (c.overflow || c.bad_path)
         return fail(PR_EDEVICE, "merge invariant broken (overflow " + std::to_string(c.overflow) + ", bad paths " +
                                     std::to_string(c.bad_path) + "); destroy the forest");
-    if (c.wide_tokens) drop_pool16(f);  // a label token outside [0, 65535] arrived
+    if (c.wide_tokens)
+        drop_pool16(f);  // a label token outside [0, 131071] arrived
+    else if (c.hi_tokens && f->narrow && !f->hi17) {
+        f->hi17 = true;  // routes now read the bit plane too (a new kernel: the arrays stay)
+        f->layout_epoch++;
+    }
     f->merged = true;
     return PR_OK;
 }
@@ -1350,6 +1468,8 @@ pr_status pr_forest_compact(pr_forest *f, int64_t *nodes_before, int64_t *nodes_
     N.pool = nw.pool;
     N.cap_pool = nw.cap_pool;
     const unsigned gn_all = (unsigned)((n_new + pr::kCompactWavesPerBlock - 1) / pr::kCompactWavesPerBlock);
+    if (hipMemsetAsync(nw.pool + n_pool, 0, (nw.cap_pool - n_pool) * sizeof(int32_t), s) != hipSuccess)
+        return fail_dev("compaction memset failed");
     hipLaunchKernelGGL(pr::compact_labels_kernel, dim3(gn_all), dim3(wb), 0, s, d.pool, N, n_new, off);
     hipLaunchKernelGGL(pr::compact_sep_kernel, dim3(gn_all), dim3(wb), 0, s, N, n_new);
     if (hipGetLastError() != hipSuccess ||
@@ -1378,12 +1498,17 @@ pr_status pr_forest_compact(pr_forest *f, int64_t *nodes_before, int64_t *nodes_
         f->broken = true;
         return r;
     }
-    unsigned long long wide = 0;
-    if (f->narrow && !read_small(f, &wide, &f->d_ctr->wide_tokens, sizeof(wide), s)) {
+    pr::MergeCounters cc;
+    if (f->narrow && !read_small(f, &cc, f->d_ctr, sizeof(cc), s)) {
         f->broken = true;
-        return fail(PR_EDEVICE, "reading the 16-bit label check failed");
+        return fail(PR_EDEVICE, "reading the narrow label check failed");
     }
-    if (wide) drop_pool16(f);
+    if (f->narrow) {
+        if (cc.wide_tokens)
+            drop_pool16(f);
+        else
+            f->hi17 = cc.hi_tokens > 0;  // the rebuilt pool holds only live labels
+    }
     f->host_img_valid = false;  // the host image no longer mirrors the device layout
     if (nodes_after) *nodes_after = n_new;
     return ok();
@@ -1530,10 +1655,17 @@ pr_status pr_evict_lru(pr_forest *f, int64_t max_tokens, int64_t *evicted, void 
     pr::EvictPlan *d_plan = nullptr;
     if (!X.get(&keys, V) || !X.get(&keys_s, V) || !X.get(&vals, V) || !X.get(&vals_s, V) || !X.get(&cnt1, V + 1) ||
         !X.get(&cum, V + 1) || !X.get(&d_plan, 1))
-        return fail(PR_ENOMEM, "hipMalloc failed for the eviction");
+        return fail(PR_ENOMEM, "hipMalloc failed for the eviction");  // nothing changed yet
     auto fail_dev = [&](const char *m) {
         f->broken = true;
         return fail(PR_EDEVICE, m);
+    };
+    // once a launch has changed the forest, a failed allocation leaves it
+    // partly evicted: the forest is then broken, as after a device failure
+    bool mutated = false;
+    auto fail_nomem = [&](const char *m) {
+        if (mutated) f->broken = true;
+        return fail(PR_ENOMEM, m);
     };
     const pr::DevForest F = dev_view(f);
     hipLaunchKernelGGL(pr::lru_keys_kernel, dim3(grid_threads(V, 256)), dim3(256), 0, s, F, W.all, V, keys, vals);
@@ -1543,7 +1675,7 @@ pr_status pr_evict_lru(pr_forest *f, int64_t max_tokens, int64_t *evicted, void 
         return fail_dev("eviction sort sizing failed");
     char *tmp = nullptr;
     const size_t tmp_bytes = std::max(need, need2);
-    if (!X.get(&tmp, (int64_t)tmp_bytes)) return fail(PR_ENOMEM, "hipMalloc failed for the eviction");
+    if (!X.get(&tmp, (int64_t)tmp_bytes)) return fail_nomem("hipMalloc failed for the eviction");
     size_t t1 = tmp_bytes;
     if (rocprim::radix_sort_pairs(tmp, t1, keys, keys_s, vals, vals_s, (size_t)V, 0, 64, s) != hipSuccess)
         return fail_dev("eviction sort failed");
@@ -1556,9 +1688,11 @@ pr_status pr_evict_lru(pr_forest *f, int64_t max_tokens, int64_t *evicted, void 
     if (!read_small(f, &plan, d_plan, sizeof(plan), s))
         return fail_dev("eviction readback failed");
     const int64_t n_evict = std::min<int64_t>(max_tokens, plan.total);
-    if (plan.a > 0)
+    if (plan.a > 0) {
         hipLaunchKernelGGL(pr::lru_clear_sorted_kernel, dim3(grid_threads(plan.a, 256)), dim3(256), 0, s, F, vals_s,
                            plan.a);
+        mutated = true;
+    }
     if (plan.r > 0) {
         const int64_t a = plan.a, b = plan.b, nc = b - a;
         hipLaunchKernelGGL(pr::lru_maxdepth_kernel, dim3(grid_threads(nc, 256)), dim3(256), 0, s, vals_s, a, b,
@@ -1572,7 +1706,7 @@ pr_status pr_evict_lru(pr_forest *f, int64_t max_tokens, int64_t *evicted, void 
         if (!X.get(&hist, maxd + 2) || !X.get(&cnt, maxd + 2) || !X.get(&rev, maxd) || !X.get(&S, maxd) ||
             !X.get(&level, nc) || !X.get(&n_level, 1) || !X.get(&rank_of, f->dev.n_nodes) ||
             !X.get(&cut_node, nc) || !X.get(&n_cut, 1) || !X.get(&cut_len1, nc + 1))
-            return fail(PR_ENOMEM, "hipMalloc failed for the eviction");
+            return fail_nomem("hipMalloc failed for the eviction");
         if (hipMemsetAsync(hist, 0, (maxd + 2) * sizeof(long long), s) != hipSuccess ||
             hipMemsetAsync(n_level, 0, sizeof(int32_t), s) != hipSuccess ||
             hipMemsetAsync(n_cut, 0, sizeof(int32_t), s) != hipSuccess ||
@@ -1587,7 +1721,7 @@ pr_status pr_evict_lru(pr_forest *f, int64_t max_tokens, int64_t *evicted, void 
             return fail_dev("eviction scan sizing failed");
         char *tmp2 = nullptr;
         const size_t tb2 = std::max(n3, n4);
-        if (!X.get(&tmp2, (int64_t)tb2)) return fail(PR_ENOMEM, "hipMalloc failed for the eviction");
+        if (!X.get(&tmp2, (int64_t)tb2)) return fail_nomem("hipMalloc failed for the eviction");
         size_t u3 = tb2, u4 = tb2;
         if (rocprim::inclusive_scan(tmp2, u3, hist, cnt, (size_t)maxd + 2, rocprim::plus<long long>(), s) !=
             hipSuccess)
@@ -1614,20 +1748,20 @@ pr_status pr_evict_lru(pr_forest *f, int64_t max_tokens, int64_t *evicted, void 
             int64_t *offs = nullptr, *old_len = nullptr;
             int32_t *peer_of = nullptr, *ctok = nullptr;
             if (!X.get(&offs, h_cut + 1) || !X.get(&old_len, h_cut) || !X.get(&peer_of, h_cut))
-                return fail(PR_ENOMEM, "hipMalloc failed for the eviction");
+                return fail_nomem("hipMalloc failed for the eviction");
             size_t n5 = 0;
             if (rocprim::inclusive_scan(nullptr, n5, cut_len1, offs, (size_t)h_cut + 1, rocprim::plus<int64_t>(),
                                         s) != hipSuccess)
                 return fail_dev("eviction scan sizing failed");
             char *tmp3 = nullptr;
-            if (!X.get(&tmp3, (int64_t)n5)) return fail(PR_ENOMEM, "hipMalloc failed for the eviction");
+            if (!X.get(&tmp3, (int64_t)n5)) return fail_nomem("hipMalloc failed for the eviction");
             if (rocprim::inclusive_scan(tmp3, n5, cut_len1, offs, (size_t)h_cut + 1, rocprim::plus<int64_t>(), s) !=
                 hipSuccess)
                 return fail_dev("eviction scan failed");
             int64_t total_cut = 0;
             if (!read_small(f, &total_cut, offs + h_cut, sizeof(total_cut), s))
                 return fail_dev("eviction readback failed");
-            if (!X.get(&ctok, total_cut)) return fail(PR_ENOMEM, "hipMalloc failed for the eviction");
+            if (!X.get(&ctok, total_cut)) return fail_nomem("hipMalloc failed for the eviction");
             hipLaunchKernelGGL(pr::lru_cut_paths_kernel, dim3((unsigned)((h_cut + 3) / 4)), dim3(256), 0, s, F,
                                cut_node, h_cut, offs, W.parent, W.depth, ctok);
             hipLaunchKernelGGL(pr::lru_old_len_kernel, dim3(grid_threads(h_cut, 256)), dim3(256), 0, s, F, cut_node,
@@ -1775,6 +1909,8 @@ pr_status pr_forest_info_get(pr_forest *f, pr_forest_info *out) {
     out->device_bytes = f->device_bytes;
     out->layout_epoch = f->layout_epoch;
     out->label_token_bytes = f->narrow ? 2 : 4;
+    out->label_bits = f->narrow ? (f->hi17 ? 17 : 16) : 32;
+    out->merge_refusals = f->refusals;
     int64_t t = 0;
     for (const auto &S : f->sets) t += (int64_t)S.tokens.size();
     out->host_seq_tokens = t;

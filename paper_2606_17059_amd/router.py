@@ -41,7 +41,8 @@ class ForestInfo(ctypes.Structure):
                 ("num_nodes", ctypes.c_int64),
                 ("pool_tokens", ctypes.c_int64), ("device_bytes", ctypes.c_int64),
                 ("host_seq_tokens", ctypes.c_int64), ("layout_epoch", ctypes.c_int64),
-                ("label_token_bytes", ctypes.c_int64)]
+                ("label_token_bytes", ctypes.c_int64), ("label_bits", ctypes.c_int64),
+                ("merge_refusals", ctypes.c_int64)]
 
 
 class ImageView(ctypes.Structure):
@@ -110,7 +111,7 @@ def lib() -> ctypes.CDLL:
     L.pr_forest_info_get.restype = ctypes.c_int32
     L.pr_forest_host_image.argtypes = [_vp, ctypes.POINTER(ImageView)]
     L.pr_forest_host_image.restype = ctypes.c_int32
-    if L.pr_abi_version() != 5:
+    if L.pr_abi_version() != 6:
         raise RuntimeError("libprefix_router ABI version mismatch")
     _lib_handle = L
     return L

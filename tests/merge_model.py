@@ -55,6 +55,12 @@ class FlatForest:
         return off
 
     def merge(self, seqs, peers):
+        """Rounds as the device runs them: walk every unfinished insert; then,
+        from that one walk, the add phase (the first insert of each
+        (parent, token) slot adds a leaf to its parent's rebuilt block) and
+        the split phase (the lowest insert per edge cuts it; the edge's record
+        is found through its move stamp if the add phase moved it).  Winners
+        are done; everyone else walks again."""
         n = len(seqs)
         st = [None] * n
         active = [True] * n
@@ -66,29 +72,12 @@ class FlatForest:
                         active[i] = False
             splits = [i for i in range(n) if active[i] and st[i][0] == "split"]
             adds = [i for i in range(n) if active[i] and st[i][0] == "add"]
-            if splits:
-                for i in splits:  # claim: lowest index per child
-                    c = st[i][2]
-                    self.nodes[c]["aux"] = max(self.nodes[c]["aux"], 2 ** 31 - 1 - i)
-                for i in splits:
-                    _, x, c, l, d, t = st[i]
-                    if self.nodes[c]["aux"] != 2 ** 31 - 1 - i:
-                        continue
-                    s = seqs[i]
-                    rest = len(s) - d - l
-                    old = dict(self.nodes[c])
-                    lower = dict(old, off=old["off"] + l, len=old["len"] - l, aux=0)
-                    lower["tok"] = self.pool[lower["off"]]
-                    nb = len(self.nodes)
-                    block = [lower]
-                    if rest > 0:
-                        leaf = dict(tok=int(s[d + l]), off=self.alloc_pool(s[d + l:]), len=rest, cb=0, cc=0,
-                                    aux=0, mask=0)
-                        block = sorted([lower, leaf], key=lambda r: r["tok"])
-                    self.nodes.extend(block)
-                    self.nodes[c] = dict(old, len=l, cb=nb, cc=len(block), aux=0)
-            elif adds:
+            if not splits and not adds:
+                break
+            stamp = 0
+            if adds:
                 self.stamp += 1
+                stamp = self.stamp
                 order = sorted(adds, key=lambda i: (st[i][1], st[i][5], i))
                 groups = {}
                 for i in order:
@@ -107,6 +96,7 @@ class FlatForest:
                         s, d = seqs[i], st[i][4]
                         leaves.append(dict(tok=int(s[d]), off=self.alloc_pool(s[d:]), len=len(s) - d, cb=0, cc=0,
                                            aux=0, mask=0))
+                        active[i] = False
                     block = sorted(old + leaves, key=lambda r: r["tok"])
                     nb = len(self.nodes)
                     self.nodes.extend(block)
@@ -119,8 +109,34 @@ class FlatForest:
                     stp, pos = self.moved.get(x, (0, x))
                     pos = pos if stp == self.stamp else x
                     self.nodes[pos]["cb"], self.nodes[pos]["cc"] = nb, cnt
-            else:
-                break
+
+            def where(c):
+                stp, pos = self.moved.get(c, (0, c))
+                return pos if stamp and stp == stamp else c
+
+            if splits:
+                for i in splits:  # claim: lowest index per edge
+                    c = where(st[i][2])
+                    self.nodes[c]["aux"] = max(self.nodes[c]["aux"], 2 ** 31 - 1 - i)
+                for i in splits:
+                    _, x, c, l, d, t = st[i]
+                    c = where(c)
+                    if self.nodes[c]["aux"] != 2 ** 31 - 1 - i:
+                        continue
+                    s = seqs[i]
+                    rest = len(s) - d - l
+                    old = dict(self.nodes[c])
+                    lower = dict(old, off=old["off"] + l, len=old["len"] - l, aux=0)
+                    lower["tok"] = self.pool[lower["off"]]
+                    nb = len(self.nodes)
+                    block = [lower]
+                    if rest > 0:
+                        leaf = dict(tok=int(s[d + l]), off=self.alloc_pool(s[d + l:]), len=rest, cb=0, cc=0,
+                                    aux=0, mask=0)
+                        block = sorted([lower, leaf], key=lambda r: r["tok"])
+                    self.nodes.extend(block)
+                    self.nodes[c] = dict(old, len=l, cb=nb, cc=len(block), aux=0)
+                    active[i] = False
         for i in range(n):  # mask pass
             s, p = seqs[i], peers[i]
             x, d = 0, 0

@@ -126,6 +126,51 @@ def test_batch_order_does_not_matter():
     assert_rows_equal(m1, c1, m_or, c_or, what="merged config 1")
 
 
+def test_round_out_of_capacity_is_refused_and_repeated():
+    """A merge round whose allocations do not fit the forest's spare capacity
+    is refused (nothing written), the forest grows, and the round runs again.
+    Compaction leaves a forest with 1/8 spare records; a fresh forest has no
+    merge history to size its spare by, so one insert that rebuilds a block of
+    20,000 children cannot fit.  The same batch also adds a second child to a
+    small node and splits edges, whose allocations come after the refused one
+    on the device counters and are refused too.  Every row against the oracle
+    after each merge; the refusals show in the forest info."""
+    import torch
+    rng = np.random.default_rng(31)
+    P = 3
+    kids = np.sort(rng.choice(np.arange(0, 200000, 2), 20000, replace=False))
+    seqs = [[7, int(t), 1, 2, 3] for t in kids] + [[9, 9, 9, 9, 9, 9]]
+    owners = [i % P for i in range(len(seqs))]
+    snap = W.from_lists(seqs, owners)
+    f = _forest(snap, P)
+    o = oracle_for(snap, P)
+    qs = W.from_lists([list(s) for s in seqs[::97]] + [[7, int(kids[5]), 1, 2, 9], [7, 1], [9, 9, 9, 4], [9, 9]])
+    gpu_route(f, qs, "refusal: upload")
+    before, after = f.compact()
+    assert after == before
+    batches = [
+        [(0, [7, 1, 5]), (1, [9, 9, 9, 4, 4]), (2, [7, int(kids[5]), 1, 2, 8, 8]), (1, [9, 9, 2])],
+        [(2, [7, 3, 3]), (0, [7, int(kids[7]), 4]), (1, [9, 9, 9, 9, 9, 9, 9])],
+    ]
+    for k, items in enumerate(batches):
+        peers = np.array([p for p, _ in items], np.int32)
+        t, off = pins._csr([s for _, s in items])
+        announce(f"refusal: merge batch {k}")
+        f.merge(torch.from_numpy(peers).to(device()), torch.from_numpy(t).to(device()),
+                torch.from_numpy(off).to(device()))
+        o.merge(peers, t, off)
+        torch.cuda.synchronize()
+        q2 = W.from_lists([qs.seq(i).tolist() for i in range(len(qs))] + [s for _, s in items])
+        m, c = gpu_route(f, q2, f"refusal: after batch {k}")
+        m_or, c_or = o.route(q2.tokens, q2.offsets, nthreads())
+        assert_rows_equal(m, c, m_or, c_or, what=f"refusal batch {k}")
+        if k == 0:
+            assert f.info()["merge_refusals"] >= 1, f.info()
+    f.check()
+    f.close()
+    o.close()
+
+
 def test_invalid_inserts_are_skipped_and_reported():
     import torch
     from paper_2606_17059_amd import RouterError

@@ -428,12 +428,16 @@ def test_launcher_keeps_its_forest():
 
 
 def test_label_width_follows_the_tokens():
-    """Routes read 16-bit labels while every label token fits in [0, 65535]
-    and int32 labels otherwise, with identical results: a small-token forest
-    starts narrow, stays narrow through merges that grow its label pool (the
-    16-bit copy grows with it) and through compaction, and turns wide when a
-    merge brings a token of 70,000; a forest uploaded with a negative token is
-    wide from the start."""
+    """Routes read 16-bit labels while every label token fits in [0, 65535],
+    16-bit labels plus a plane of bit 16 while every token fits in
+    [0, 131071], and int32 labels otherwise, with identical results: a
+    small-token forest starts at 16 bits, stays there through merges that grow
+    its label pool (the narrow copy grows with it) and through compaction,
+    goes to 17 bits when a merge brings a token of 70,000 (the layout epoch
+    advances, since routes switch kernels), keeps them through compaction and
+    a growth, and goes to 32 bits when a merge brings a token of 200,000; a
+    forest uploaded with tokens up to 131,071 starts at 17 bits, one with a
+    negative token at 32."""
     import torch
     rng = np.random.default_rng(616)
     P = 3
@@ -442,12 +446,13 @@ def test_label_width_follows_the_tokens():
     o = oracle_for(w.snapshot, P)
     queries = [w.queries.seq(i).tolist() for i in range(len(w.queries))]
 
-    def check(what, width):
+    def check(what, bits):
         t, off = pins._csr(queries)
         m, c = gpu_route(f, W.SeqSet(t, off, None), what)
         m_or, c_or = o.route(t, off, 2)
         assert_rows_equal(m, c, m_or, c_or, what=what)
-        assert f.info()["label_token_bytes"] == width, (what, f.info())
+        info = f.info()
+        assert info["label_bits"] == bits and info["label_token_bytes"] == (4 if bits == 32 else 2), (what, info)
 
     def merge(seqs, what):
         peers = np.array([int(rng.integers(0, P)) for _ in seqs], np.int32)
@@ -458,33 +463,53 @@ def test_label_width_follows_the_tokens():
         o.merge(peers, t, off)
         torch.cuda.synchronize()
 
-    check("uploaded", 2)
+    check("uploaded", 16)
     pool0 = f.info()["pool_tokens"]
     # long small-token sequences: the label pool outgrows its spare capacity
     merge([rng.integers(0, 8, int(rng.integers(200, 400))).tolist() for _ in range(60)], "long small tokens")
     assert f.info()["pool_tokens"] > 2 * pool0 + 4096
     queries += [s[:150] for s in pins.csr_to_list(*o.export(0))[:20]]
-    check("after growth", 2)
+    check("after growth", 16)
     f.compact()
-    check("after compaction", 2)
+    check("after compaction", 16)
     epoch = f.info()["layout_epoch"]
-    merge([[1, 2, 70000, 3], [5, 70000]], "a token of 70,000")
+    merge([[1, 2, 70000, 3], [5, 70000], [1, 2, 65536, 65535, 131071]], "tokens of 65,536 to 131,071")
     assert f.info()["layout_epoch"] > epoch
-    queries += [[1, 2, 70000, 3, 9], [5, 70000]]
-    check("after a wide token", 4)
+    queries += [[1, 2, 70000, 3, 9], [5, 70000], [1, 2, 65536, 65535, 131071], [1, 2, 65536, 65535, 65535],
+                [1, 2, 70000 - 65536], [5, 70000 + 65536], [1, 2, 0, 65535, 131071]]
+    check("after tokens of up to 17 bits", 17)
+    # 17-bit labels of every alignment against the bit words: sequences of
+    # 1..300 tokens mixing both halves of the range, then a growth of the pool
+    merge([(rng.integers(0, 2, L) * 65536 + rng.integers(0, 5, L)).tolist() for L in range(1, 300, 7)],
+          "17-bit sequences of many lengths")
+    queries += [s for s in pins.csr_to_list(*o.export(1))[:30]]
+    queries += [[(x ^ 65536) if i == len(s) // 2 else x for i, x in enumerate(s)]
+                for s in pins.csr_to_list(*o.export(2))[:30] if s]
+    check("17-bit sequences", 17)
+    f.compact()
+    check("17 bits after compaction", 17)
+    merge([rng.integers(0, 131072, int(rng.integers(500, 1500))).tolist() for _ in range(40)], "growth at 17 bits")
+    check("17 bits after growth", 17)
+    epoch = f.info()["layout_epoch"]
+    merge([[1, 2, 200000, 3], [9, 9]], "a token of 200,000")
+    assert f.info()["layout_epoch"] > epoch
+    queries += [[1, 2, 200000, 3, 9], [1, 2, 200000 - 131072]]
+    check("after a wide token", 32)
     f.close()
     o.close()
 
-    neg = W.from_lists([[3, -1, 4], [3, 1]], [0, 1])
-    g = _forest(neg, 2)
-    og = oracle_for(neg, 2)
-    t, off = pins._csr([[3, -1, 4, 4], [3, 1], [3, 2]])
-    m, c = gpu_route(g, W.SeqSet(t, off, None), "negative token forest")
-    m_or, c_or = og.route(t, off, 1)
-    assert_rows_equal(m, c, m_or, c_or, what="negative token forest")
-    assert g.info()["label_token_bytes"] == 4
-    g.close()
-    og.close()
+    for seqs, qs, bits in (([[3, 131071, 4], [3, 1, 65536]], [[3, 131071, 4, 4], [3, 1, 65536], [3, 1, 0], [3, 2]], 17),
+                           ([[3, -1, 4], [3, 1]], [[3, -1, 4, 4], [3, 1], [3, 2]], 32)):
+        snap = W.from_lists(seqs, [0, 1])
+        g = _forest(snap, 2)
+        og = oracle_for(snap, 2)
+        t, off = pins._csr(qs)
+        m, c = gpu_route(g, W.SeqSet(t, off, None), f"uploaded forest, {bits}-bit labels")
+        m_or, c_or = og.route(t, off, 1)
+        assert_rows_equal(m, c, m_or, c_or, what=f"uploaded forest, {bits}-bit labels")
+        assert g.info()["label_bits"] == bits
+        g.close()
+        og.close()
 
 
 def _wide_block_sets(rng, n_children, P):
@@ -572,15 +597,17 @@ def test_child_blocks_wider_than_4096(n_children):
     og.close()
 
 
-def test_narrow_labels_with_query_tokens_out_of_range():
-    """While labels are read as 16-bit values, a query token outside
-    [0, 65535] must still differ from every label token: in the middle of a
-    label, the label token k is replaced by 65536 + k, k - 65536, k + 2^31
-    (wrapped) and -1; the walk must stop there, as the oracle's int32 compare
-    does."""
-    rng = np.random.default_rng(99)
+@pytest.mark.parametrize("bits", [16, 17])
+def test_narrow_labels_with_query_tokens_out_of_range(bits):
+    """While labels are read as 16- or 17-bit values, a query token outside
+    their range, or equal to a label token in its low 16 bits only, must still
+    differ from it: in the middle of a label, the label token k is replaced by
+    k with bit 16 flipped, k + 131072, k - 65536, k + 2^31 (wrapped) and -1;
+    the walk must stop there, as the oracle's int32 compare does."""
+    rng = np.random.default_rng(99 + bits)
     P = 2
-    seqs = [rng.integers(0, 65536, int(rng.integers(40, 300))).tolist() for _ in range(30)]
+    top = 65536 if bits == 16 else 131072
+    seqs = [rng.integers(0, top, int(rng.integers(40, 300))).tolist() for _ in range(30)]
     owners = [i % P for i in range(len(seqs))]
     snap = W.from_lists(seqs, owners)
     f = _forest(snap, P)
@@ -588,14 +615,14 @@ def test_narrow_labels_with_query_tokens_out_of_range():
     for s in seqs:
         for pos in (0, 1, len(s) // 2, len(s) - 1):
             k = s[pos]
-            for bad in (k + 65536, k - 65536, (k + 2 ** 31) % 2 ** 32 - 2 ** 31, -1, k + 131072):
+            for bad in (k ^ 65536, k + 131072, k - 65536, (k + 2 ** 31) % 2 ** 32 - 2 ** 31, -1):
                 q = list(s)
                 q[pos] = int(bad)
                 qs.append(q)
         qs.append(list(s))
     queries = W.from_lists(qs)
-    m, c = gpu_route(f, queries, "narrow labels, wide query tokens")
-    assert f.info()["label_token_bytes"] == 2
+    m, c = gpu_route(f, queries, f"narrow labels ({bits} bits), wide query tokens")
+    assert f.info()["label_bits"] == bits
     o = oracle_for(snap, P)
     m_or, c_or = o.route(queries.tokens, queries.offsets, nthreads())
     assert_rows_equal(m, c, m_or, c_or, what="narrow labels, wide query tokens")

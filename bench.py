@@ -182,11 +182,12 @@ def bench_stream(args, dev) -> dict:
     """The streaming workload, 128 peers.  One step = for each topic
     distribution (uniform, Zipf 1.2), the delta-merge of a fresh batch of
     10,000 inserts into that distribution's forest, then a lookup batch of
-    1,048,576 queries on it.  Each forest has its own stream, so one forest's
-    merge (latency-bound: small kernels and host round trips) runs while the
-    other's lookup streams from HBM; its kernels then wait for free wave
-    slots behind the lookup's million waves, so merges are also timed alone
-    after the timed region (--no-overlap puts both forests on one stream).  Every lookup of every timed step is compared
+    1,048,576 queries on it.  Each forest has its own stream and host thread,
+    so one forest's merge (latency-bound: small kernels and host round trips)
+    runs while the other's lookup streams from HBM; its kernels then wait for
+    free wave slots behind the lookup's million waves, so merges are also
+    timed alone after the timed region (--no-overlap runs both forests in
+    turn on one stream and one thread).  Every lookup of every timed step is compared
     with the radix-tree oracle after the timed region, and the algorithmic
     bytes come from the oracle's match lengths."""
     import torch
@@ -244,13 +245,11 @@ def bench_stream(args, dev) -> dict:
     ev = {d: [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(K)]
           for d in dists}
     merge_s = {d: np.zeros(n_steps) for d in dists}
-    t_region = 0.0
-    for k in range(n_steps):
-        if k == Wu:
-            torch.cuda.synchronize()
-            t_region = time.perf_counter()
-        for d in dists:
-            f, s = forests[d], streams[d]
+    t_region = time.perf_counter()
+
+    def run_steps(d, ks):
+        f, s = forests[d], streams[d]
+        for k in ks:
             if not args.overlap:
                 s.synchronize()  # the previous lookup is done: the merge's wall time is its own
             t0 = time.perf_counter()
@@ -264,6 +263,47 @@ def bench_stream(args, dev) -> dict:
                 b.record(s)
             else:
                 f.route(qt, qo, *warm_out, stream=s)
+
+    if args.overlap:
+        # one host thread per forest (the library's calls release the
+        # interpreter lock): each forest's merge, then lookup, on its own
+        # stream, while the other forest's run beside them
+        import threading
+        barrier = threading.Barrier(len(dists) + 1)
+        errors = []
+
+        def worker(d):
+            try:
+                run_steps(d, range(Wu))
+                streams[d].synchronize()
+                barrier.wait()
+                barrier.wait()  # the main thread has started the clock
+                run_steps(d, range(Wu, n_steps))
+            except BaseException as e:  # reported by the main thread
+                errors.append(e)
+                barrier.abort()
+
+        threads = [threading.Thread(target=worker, args=(d,)) for d in dists]
+        for t in threads:
+            t.start()
+        try:
+            barrier.wait()
+            torch.cuda.synchronize()
+            t_region = time.perf_counter()
+            barrier.wait()
+        except threading.BrokenBarrierError:
+            pass
+        for t in threads:
+            t.join()
+        if errors:
+            raise errors[0]
+    else:
+        for k in range(n_steps):
+            if k == Wu:
+                torch.cuda.synchronize()
+                t_region = time.perf_counter()
+            for d in dists:
+                run_steps(d, [k])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_region
     for d in dists:
@@ -272,6 +312,21 @@ def bench_stream(args, dev) -> dict:
     log(f"[bench] stream: timed region {K} steps in {wall * 1e3:.2f} ms; route ms mean "
         f"{ {d: round(float(route_ms[d].mean()), 4) for d in dists} }; merge ms mean "
         f"{ {d: round(float(merge_s[d][Wu:].mean() * 1e3), 3) for d in dists} }")
+    # the lookup kernel alone, for the roofline: K launches back to back on
+    # each forest as the timed steps left it, over the last step's batch (whose
+    # algorithmic bytes the oracle gives below)
+    iso_ms = {}
+    for d in dists:
+        qt, qo = qdev[d][(n_steps - 1) % R]
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record(streams[d])
+        for _ in range(K):
+            forests[d].route(qt, qo, *warm_out, stream=streams[d])
+        b.record(streams[d])
+        torch.cuda.synchronize()
+        iso_ms[d] = a.elapsed_time(b) / K
+    log(f"[bench] stream: lookup kernel alone, ms per launch {iso_ms}")
     # merges timed alone: further fresh batches after the last timed lookup,
     # each with the GPU otherwise idle (they change nothing the oracle checks)
     alone = {}
@@ -325,6 +380,7 @@ def bench_stream(args, dev) -> dict:
         log(f"[bench] stream {d}: every row of {K} steps equals the oracle")
         tot_bytes += sum(byts)
         per_dist[d] = {"route_ms_mean": float(route_ms[d].mean()), "route_ms_median": float(np.median(route_ms[d])),
+                       "route_ms_alone": iso_ms[d], "last_step_bytes": byts[-1],
                        "algorithmic_bytes_per_launch": float(np.mean(byts)),
                        "merge_ms_mean": float(merge_s[d][Wu:].mean() * 1e3),
                        "merge_inserts_per_s": float(len(ihost[d][0]) * K / merge_s[d][Wu:].sum()),
@@ -333,9 +389,11 @@ def bench_stream(args, dev) -> dict:
     all_ms = np.concatenate([route_ms[d] for d in dists])
     route_s = all_ms.sum() / 1e3
     n_lookups = 2 * K * nq
+    iso_bytes = float(np.mean([per_dist[d]["last_step_bytes"] for d in dists]))
+    iso = float(np.mean([iso_ms[d] for d in dists]))
     n_ins = sum(len(ihost[d][k]) for d in dists for k in range(Wu, n_steps))
     merge_tot = sum(merge_s[d][Wu:].sum() for d in dists)
-    achieved = tot_bytes / route_s / 1e9
+    achieved = iso_bytes / (iso / 1e3) / 1e9
     cpu = None
     if not args.no_cpu_baseline:
         def make():
@@ -353,8 +411,12 @@ def bench_stream(args, dev) -> dict:
     return {
         "value": n_lookups / wall, "ms_per_step": wall * 1e3 / K,
         "queries_per_step": 2 * nq, "inserts_per_step": 2 * len(ihost[dists[0]][0]),
-        "lookup": {"queries_per_s": n_lookups / route_s, "route_ms_mean": float(all_ms.mean()),
-                   "note": "lookup kernels alone: HIP events around each route call on its stream"},
+        "lookup": {"queries_per_s": nq / (iso / 1e3), "route_ms_alone": iso,
+                   "route_ms_in_steps": float(all_ms.mean()),
+                   "queries_per_s_in_steps": n_lookups / route_s,
+                   "note": "alone: K launches back to back per forest after the timed region (the roofline's "
+                           "kernel time); in steps: HIP events around each route call of the timed steps, "
+                           "which run beside the other forest's merge and lookup"},
         "merge": {"inserts_per_s": n_ins / merge_tot, "inserts": n_ins, "seconds": float(merge_tot),
                   "note": "wall time of the timed steps' pr_merge calls (host-synchronous), "
                           + ("each beside the other forest's lookup" if args.overlap
@@ -366,9 +428,11 @@ def bench_stream(args, dev) -> dict:
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                      "frac": achieved / PEAK_HBM_GBPS, "traffic": measured_traffic("stream"),
                      "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
-                     "kernel": kname, "kernel_ms": float(all_ms.mean()),
-                     "algorithmic_bytes_per_launch": tot_bytes / len(all_ms),
-                     "bytes_from": "match lengths of the radix-tree oracle"},
+                     "kernel": kname, "kernel_ms": iso,
+                     "algorithmic_bytes_per_launch": iso_bytes,
+                     "bytes_from": "match lengths of the radix-tree oracle",
+                     "timing": "K launches back to back per forest, each forest as the timed steps left it, over "
+                               "the last timed step's lookup batch"},
         "parity": {"oracle": "radix trees, one per peer", "rows": rows, "bit_exact": True,
                    "what": "every match length and chosen peer of every timed lookup"},
         "cpu": cpu, "compact": compact, "workload_note": f"lookup batches: the {R} rounds' batches per distribution, taken in "
@@ -773,7 +837,8 @@ def main() -> int:
                        "queries_per_step": r["queries_per_step"], "inserts_per_step": r["inserts_per_step"],
                        "step": "for each topic distribution (uniform, Zipf 1.2): merge a fresh 10,000-insert batch "
                                "into its forest, then route a 1,048,576-query lookup batch on it; "
-                               + ("the two forests on two streams" if args.overlap else "all on one stream"),
+                               + ("the two forests on two streams and two host threads" if args.overlap
+                                  else "all in turn on one stream"),
                        "parallelism": "single GPU"},
             "hbm_gbps": r["roofline"]["achieved"], "roofline": r["roofline"], "lookup": r["lookup"],
             "merge": r["merge"], "per_distribution": r["per_distribution"], "parity": r["parity"],

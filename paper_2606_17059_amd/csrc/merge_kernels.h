@@ -92,6 +92,7 @@ struct Batch {
 };
 
 constexpr int kMergeWavesPerBlock = 4;
+constexpr int kMoveBlocks = 1024;  // workgroups of the grid-stride move kernel
 
 __device__ __forceinline__ int64_t m_wave_index() {
     return (int64_t)blockIdx.x * kMergeWavesPerBlock + uniform((int32_t)(threadIdx.x / 64));
@@ -449,40 +450,42 @@ __global__ void add_alloc_kernel(DevForest F, const unsigned long long *keys, in
     grp_pb[k] = pb;
 }
 
-// Step 4 (one wave per 64-child chunk of every rebuilt parent's old block):
-// old children keep their order, each moving up by the winners below it, and
-// are stamped with their new position.  The grid may be larger than the
-// chunk count (an upper bound known on the host); the count itself is the
-// one step 2 recorded.
+// Step 4 (64-child chunks of every rebuilt parent's old block, a wave per
+// chunk, grid-stride over the chunk count step 2 recorded): old children keep
+// their order, each moving up by the winners below it, and are stamped with
+// their new position.  The grid is small and fixed, so its size does not
+// follow the forest's record count.
 __global__ __launch_bounds__(64 *kMergeWavesPerBlock) void add_move_kernel(
     DevForest F, const unsigned long long *keys, int64_t n_add, const int32_t *cstart,
     const MergeCounters *__restrict__ ctr, const int32_t *grp_nw, const int32_t *grp_nb, const int32_t *win_tok,
     long long stamp) {
     const int lane = (int)(threadIdx.x & 63);
-    const int64_t c = m_wave_index();
-    if (c >= (int64_t)ctr->move_chunks) return;
-    // the group whose chunks hold c: cstart[k] <= c < cstart[k + 1]
-    int64_t lo = 0, hi = n_add;
-    while (lo < hi) {
-        const int64_t mid = (lo + hi) >> 1;
-        if (cstart[mid] <= c)
-            lo = mid + 1;
-        else
-            hi = mid;
+    const int64_t nchunks = (int64_t)ctr->move_chunks;
+    const int64_t waves = (int64_t)gridDim.x * kMergeWavesPerBlock;
+    for (int64_t c = m_wave_index(); c < nchunks; c += waves) {
+        // the group whose chunks hold c: cstart[k] <= c < cstart[k + 1]
+        int64_t lo = 0, hi = n_add;
+        while (lo < hi) {
+            const int64_t mid = (lo + hi) >> 1;
+            if (cstart[mid] <= c)
+                lo = mid + 1;
+            else
+                hi = mid;
+        }
+        const int64_t k = lo - 1;
+        const int32_t nb = grp_nb[k];
+        if (nb < 0) continue;
+        const Node nx = F.nodes[key_parent(keys[k])];
+        const int32_t j = (int32_t)(c - cstart[k]) * 64 + lane;
+        if (j >= nx.ct_cnt) continue;
+        const int32_t src = nx.ct_beg + j;
+        const int64_t dst = nb + j + lower_count(win_tok + k, grp_nw[k], F.ntok[src]);
+        F.nodes[dst] = F.nodes[src];
+        F.ntok[dst] = F.ntok[src];
+        if (F.ltime) F.ltime[dst] = F.ltime[src];
+        for (int w = 0; w < F.W - 1; w++) F.mext[dst * (F.W - 1) + w] = F.mext[(int64_t)src * (F.W - 1) + w];
+        F.moved[src] = (stamp << 32) | (long long)(uint32_t)dst;
     }
-    const int64_t k = lo - 1;
-    const int32_t nb = grp_nb[k];
-    if (nb < 0) return;
-    const Node nx = F.nodes[key_parent(keys[k])];
-    const int32_t j = (int32_t)(c - cstart[k]) * 64 + lane;
-    if (j >= nx.ct_cnt) return;
-    const int32_t src = nx.ct_beg + j;
-    const int64_t dst = nb + j + lower_count(win_tok + k, grp_nw[k], F.ntok[src]);
-    F.nodes[dst] = F.nodes[src];
-    F.ntok[dst] = F.ntok[src];
-    if (F.ltime) F.ltime[dst] = F.ltime[src];
-    for (int w = 0; w < F.W - 1; w++) F.mext[dst * (F.W - 1) + w] = F.mext[(int64_t)src * (F.W - 1) + w];
-    F.moved[src] = (stamp << 32) | (long long)(uint32_t)dst;
 }
 
 // Step 5 (one wave per winning entry): the leaf holding the rest of the

@@ -981,15 +981,12 @@ pr_status run_merge(pr_forest *f, const int32_t *peer_of, const int32_t *tokens,
             hipLaunchKernelGGL(pr::add_group_kernel, dim3(grid_threads(n_add, bs)), dim3(bs), 0, s, dev_view(f),
                                m.keys_out, m.vals_out, n_add, m.st, m.win, m.rest, m.widx, m.poff, m.hd, m.cstart,
                                m.grp_nw, m.grp_pool, m.win_tok, m.win_ins, f->d_ctr);
-            // the move kernel's grid takes a bound of the chunks (the sum over
-            // groups of ceil(old children / 64)); it reads the exact count
-            const int64_t chunks = (f->dev.n_nodes + 63) / 64 + n_add;
             const long long stamp = ++f->stamp;
             add_stamp = stamp;
             const pr::DevForest F = dev_view(f);
             hipLaunchKernelGGL(pr::add_alloc_kernel, dim3(grid_threads(n_add, bs)), dim3(bs), 0, s, F, m.keys_out,
                                n_add, m.grp_nw, m.grp_pool, m.grp_nb, m.grp_pb, f->d_ctr);
-            hipLaunchKernelGGL(pr::add_move_kernel, dim3(grid_waves(chunks)), dim3(wb), 0, s, F, m.keys_out, n_add,
+            hipLaunchKernelGGL(pr::add_move_kernel, dim3(pr::kMoveBlocks), dim3(wb), 0, s, F, m.keys_out, n_add,
                                m.cstart, f->d_ctr, m.grp_nw, m.grp_nb, m.win_tok, stamp);
             hipLaunchKernelGGL(pr::add_leaf_kernel, dim3(grid_waves(n_add)), dim3(wb), 0, s, F, B, m.keys_out,
                                m.vals_out, n_add, m.st, m.win, m.widx, m.poff, m.hd, m.grp_nb, m.grp_pb);

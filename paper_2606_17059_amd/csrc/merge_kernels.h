@@ -8,20 +8,25 @@
 //          below x;
 //   SPLIT  the sequence leaves (or ends inside) the label of child c of x
 //          after l tokens: c's edge must be cut there.
-// If any insert needs a SPLIT, the round cuts edges: per child c the insert
-// with the lowest batch index wins (an atomic max claim), rewrites c's record
-// in place as the upper part of the edge and gives it a new child block
-// holding the lower part (c's old record, label advanced) and, if the winner's
-// sequence goes on, a leaf with the winner's remaining tokens.  Otherwise the
-// round adds leaves: ADD inserts are radix-sorted by (x, next token); per slot
-// the lowest batch index wins, and one wave per node x writes a new, sorted
-// child block holding x's old children and one leaf per winning slot.  The
-// round is data-parallel however the inserts crowd on one parent: scans over
-// the sorted entries give every winner its slot and label span, one thread per
-// parent allocates its block, one wave per 64 old children moves them, and one
-// wave per winner writes its leaf.  Records that move are stamped with their
-// new position so that a parent rebuilt in the same round can be pointed at its
-// new block wherever its record lives.
+// A round applies both kinds the walk found.  The add phase comes first: ADD
+// inserts are sorted by (x, next token); per slot the lowest batch index wins,
+// and every parent x gets a new, sorted child block holding its old children
+// and one leaf per winning slot.  The phase is data-parallel however the
+// inserts crowd on one parent: scans over the sorted entries give every winner
+// its slot, one wave per 64 old children moves them, and one wave per winner
+// writes its leaf.  A round of at most kPlanMax ADD entries sorts, scans and
+// allocates in one workgroup (add_plan_kernel); larger rounds take a rocPRIM
+// radix sort, four scans and per-parent allocation.  Records that move are
+// stamped with their new position, so that a parent rebuilt in the same round,
+// and a child whose edge the split phase then cuts, are found wherever their
+// records live.  The split phase: per child c the insert with the lowest batch
+// index wins (an atomic max claim), rewrites c's record in place as the upper
+// part of the edge and gives it a new child block holding the lower part (c's
+// old record, label advanced) and, if the winner's sequence goes on, a leaf
+// with the winner's remaining tokens.  Winners of both phases are done.
+// Allocations come from device counters; one that does not fit the capacity
+// is refused whole and counted, and the host grows the forest and repeats the
+// round.
 // Losers walk again in the next round and find the structure the winners
 // built.  When every insert is DONE, a last pass ORs each insert's peer bit
 // into the mask of every node on its path.  The match function afterwards is
@@ -62,6 +67,7 @@ struct MergeCounters {
     unsigned long long move_chunks;  // add round: 64-child chunks of the old blocks that move
     unsigned long long wide_tokens;  // nonzero: an appended label token lies outside [0, 131071] (no narrow copy)
     unsigned long long hi_tokens;    // nonzero: an appended label token lies in [65536, 131071] (17-bit labels)
+    unsigned long long add_pool_base;  // add round planned in one workgroup: first pool token of its labels
 };
 
 struct DevForest {
@@ -213,17 +219,23 @@ __global__ __launch_bounds__(64 *kMergeWavesPerBlock) void merge_walk_kernel(Dev
 // need, reduced per block before one atomic each: per-insert atomics on the
 // same counters would serialise.
 constexpr int kTallyThreads = 256;
+// arest[i] (if not nullptr): the label tokens ADD insert i needs, else -1 (the
+// one-workgroup add plan reads it).
 __global__ __launch_bounds__(kTallyThreads) void merge_tally_kernel(Batch B, const InsState *st,
-                                                                    MergeCounters *ctr) {
+                                                                    MergeCounters *ctr, int32_t *arest) {
     __shared__ unsigned long long part[3][kTallyThreads / 64];
     unsigned long long n_add = 0, n_split = 0, pool = 0;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < B.n; i += (int64_t)gridDim.x * blockDim.x) {
         const int32_t kind = st[i].kind;
+        int32_t ar = -1;
         if (kind == kInsAdd || kind == kInsSplit) {
             n_add += kind == kInsAdd;
             n_split += kind == kInsSplit;
-            pool += (unsigned long long)(B.offsets[i + 1] - B.offsets[i] - st[i].d);
+            const int64_t rest = B.offsets[i + 1] - B.offsets[i] - st[i].d;
+            pool += (unsigned long long)rest;
+            if (kind == kInsAdd) ar = (int32_t)rest;
         }
+        if (arest) arest[i] = ar;
     }
     for (int off = 32; off >= 1; off >>= 1) {
         n_add += __shfl_xor(n_add, off);
@@ -431,6 +443,492 @@ __global__ void add_group_kernel(DevForest F, const unsigned long long *keys, co
     if (e == n_add - 1) ctr->move_chunks = (unsigned long long)cstart[n_add];
 }
 
+// ---- the add plan in one workgroup -------------------------------------------
+// For a round whose ADD entries fit one workgroup's LDS, one launch replaces
+// steps 0-3 (sort keys, radix sort, marks, the four scans, groups and their
+// allocation):
+//  1. the batch is read in coalesced chunks; ADD entries are gathered in batch
+//     order, and each gets its label span in one pool allocation for the whole
+//     round, in batch order (`pofs`, indexed by insert; a slot loser's span
+//     stays unused, zero-filled);
+//  2. parents are numbered through a hash table in LDS, so that the sort key
+//     (parent slot, token) needs about 11 + 17 bits instead of 31 + 32; with
+//     more distinct parents than the table takes, the key keeps the node id;
+//  3. a stable least-significant-digit radix sort in LDS, 4-bit digits, a pass
+//     only for digits that differ between keys; digit counts are LDS atomics on
+//     each thread's own counters, which also give the entry's rank among the
+//     thread's entries of that digit;
+//  4. marks and scans in registers; one node allocation for every rebuilt
+//     block of the round, refused as a whole when the capacity runs out.
+// The outputs keep the multi-launch path's layout (keys hold the parent's node
+// id), so the move, leaf, separator and fix steps serve both paths.
+constexpr int kPlanThreads = 1024;
+constexpr int kPlanItems = 10;                              // sorted entries per thread
+constexpr int kPlanMax = kPlanThreads * kPlanItems;         // ADD entries per round
+constexpr int kPlanBatchItems = 16;                         // batch chunks of kPlanThreads
+constexpr int64_t kPlanMaxBatch = (int64_t)kPlanThreads * kPlanBatchItems;  // insert ids fit 16 bits
+constexpr int kPlanWaves = kPlanThreads / 64;
+constexpr int kPlanSlots = 2048;                            // parent hash table
+constexpr int kPlanMaxParents = kPlanSlots / 2;
+
+// Inclusive scan over the wave.
+template <typename T, typename Op>
+__device__ __forceinline__ T plan_wave_incl(T v, Op op) {
+    const int lane = (int)(threadIdx.x & 63);
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const T u = __shfl_up(v, off);
+        if (lane >= off) v = op(v, u);
+    }
+    return v;
+}
+
+// Inclusive sum over the wave through DPP lane moves: a Hillis-Steele scan
+// within each row of 16 lanes (row shifts by 1, 2, 4, 8; a lane with no
+// source adds 0), then each row adds the totals of the rows before it (row
+// broadcasts of lanes 15 and 31).
+__device__ __forceinline__ uint32_t wave_incl_add_u32(uint32_t v) {
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x111, 0xf, 0xf, false);  // row_shr:1
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x112, 0xf, 0xf, false);  // row_shr:2
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x114, 0xf, 0xf, false);  // row_shr:4
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x118, 0xf, 0xf, false);  // row_shr:8
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x142, 0xa, 0xf, false);  // row_bcast:15 -> rows 1, 3
+    v += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x143, 0xc, 0xf, false);  // row_bcast:31 -> rows 2, 3
+    return v;
+}
+
+// Inclusive sum over the wave of values below 2^25 each (so no sum
+// overflows 32 bits), else of any values.
+__device__ __forceinline__ long long wave_incl_add_i64(long long v) {
+    if (__ballot(v >= (1ll << 25)) == 0) return (long long)wave_incl_add_u32((uint32_t)v);
+    return plan_wave_incl(v, [](long long a, long long b) { return a + b; });
+}
+
+// Exclusive scan over the workgroup in thread order (id: the identity of op);
+// *total receives the reduction of every thread's v.  Every thread calls it.
+template <typename T, typename Op>
+__device__ T plan_block_excl(T v, T id, Op op, T *tmp, T *total) {
+    const int lane = (int)(threadIdx.x & 63), w = (int)(threadIdx.x >> 6);
+    const T inc = plan_wave_incl(v, op);
+    if (lane == 63) tmp[w] = inc;
+    __syncthreads();
+    T pre = id, tot = id;
+#pragma unroll
+    for (int k = 0; k < kPlanWaves; k++) {
+        const T x = tmp[k];
+        if (k < w) pre = op(pre, x);
+        tot = op(tot, x);
+    }
+    __syncthreads();  // tmp is free for the next scan
+    T ex = __shfl_up(inc, 1);
+    if (lane == 0) ex = id;
+    *total = tot;
+    return op(pre, ex);
+}
+
+__device__ __forceinline__ uint32_t plan_hash(int32_t x) {
+    return ((uint32_t)x * 2654435761u) >> 21;  // 11 bits: kPlanSlots
+}
+
+// Slot of parent x in the table (x >= 0), inserting it; -1 when the table is full.
+__device__ __forceinline__ int plan_slot_insert(int32_t *tab, int *n_new, int32_t x) {
+    uint32_t h = plan_hash(x);
+    for (int p = 0; p < kPlanSlots; p++, h = (h + 1) & (kPlanSlots - 1)) {
+        const int32_t cur = tab[h];
+        if (cur == x) return (int)h;
+        if (cur == -1) {
+            const int32_t old = atomicCAS(&tab[h], -1, x);
+            if (old == -1) {
+                atomicAdd(n_new, 1);
+                return (int)h;
+            }
+            if (old == x) return (int)h;
+        }
+    }
+    return -1;
+}
+
+__device__ __forceinline__ int plan_slot_find(const int32_t *tab, int32_t x) {
+    uint32_t h = plan_hash(x);
+    for (int p = 0; p < kPlanSlots; p++, h = (h + 1) & (kPlanSlots - 1))
+        if (tab[h] == x) return (int)h;
+    return -1;  // not reached for a parent that was inserted
+}
+
+// LDS index of sorted entry p: one pad entry per 32, so that the threads'
+// blocked runs of entries (a stride of kPlanItems) spread over the banks.
+__device__ __forceinline__ int plan_pad(int p) { return p + (p >> 5); }
+constexpr int kPlanPadded = kPlanMax + kPlanMax / 32;
+
+// One workgroup of kPlanThreads, for batches of at most kPlanMaxBatch inserts
+// whose round has at most kPlanMax ADD entries.  n_add is the walk's tally of
+// ADD inserts and arest the tally's per-insert label tokens (-1: not ADD); a
+// different count raises bad_path and plans nothing (the merge then fails).
+// pofs[i]: the label span of ADD insert i from the round's pool base
+// (ctr->add_pool_base).
+__global__ __launch_bounds__(kPlanThreads) void add_plan_kernel(DevForest F, Batch B, const InsState *st,
+                                                                const int32_t *arest, int64_t n_add,
+                                                                unsigned long long *keys, int32_t *vals,
+                                                                int32_t *win, int32_t *widx, int32_t *hd,
+                                                                int32_t *cstart, int32_t *grp_nw, int32_t *grp_nb,
+                                                                int32_t *win_tok, int64_t *pofs,
+                                                                MergeCounters *ctr) {
+    __shared__ unsigned long long s_key[kPlanPadded];        // sort keys; later staged outputs
+    __shared__ uint16_t s_val[kPlanPadded];                  // insert ids; later each entry's widx
+    __shared__ uint32_t s_cnt[8 * kPlanThreads];             // digits d, d + 8 of thread t: word d * T + t
+    __shared__ int32_t s_tab[kPlanSlots];                    // parent node id per slot, or -1
+    __shared__ int s_cw[kPlanBatchItems * kPlanWaves];       // ADD entries per (chunk, wave), then their scan
+    __shared__ long long s_rw[kPlanBatchItems * kPlanWaves]; // their label tokens, then the scan
+    __shared__ uint32_t s_wt[kPlanWaves * 8];                // per wave: packed digit totals, then prefixes
+    __shared__ uint32_t s_dt[8];                             // packed digit totals of the workgroup
+    __shared__ long long s_tmp[kPlanWaves];
+    __shared__ int s_tmp32[kPlanWaves];
+    __shared__ int s_misc[4];                                // distinct parents, table full, ADD entries
+    constexpr int T = kPlanThreads;
+    const int t = (int)threadIdx.x;
+    const int lane = t & 63, wv = t >> 6;
+    const uint64_t lt_mask = lane == 0 ? 0ull : (~0ull >> (64 - lane));
+    const auto plus = [](int a, int b) { return a + b; };
+    const auto plus64 = [](long long a, long long b) { return a + b; };
+
+    for (int q = t; q < kPlanSlots; q += T) s_tab[q] = -1;
+    if (t < 4) s_misc[t] = 0;
+
+    // 1. chunk j holds inserts [j*T, (j+1)*T): count the ADD entries and their
+    // label tokens per (chunk, wave), in batch order
+    const int n = (int)min<int64_t>(B.n, kPlanMaxBatch);
+    const int R = (n + T - 1) / T;
+    int32_t ar[kPlanBatchItems];
+#pragma unroll
+    for (int j = 0; j < kPlanBatchItems; j++) ar[j] = (j < R && j * T + t < n) ? arest[j * T + t] : -1;
+    uint32_t addbits = 0;
+#pragma unroll
+    for (int j = 0; j < kPlanBatchItems; j++) {
+        if (j < R) {
+            const bool a = ar[j] >= 0;
+            addbits |= (uint32_t)a << j;
+            const uint64_t bal = __ballot(a);
+            const long long rs = wave_incl_add_i64((long long)(a ? ar[j] : 0));
+            if (lane == 63) {
+                s_cw[j * kPlanWaves + wv] = (int)__popcll(bal);
+                s_rw[j * kPlanWaves + wv] = rs;
+            }
+        }
+    }
+    __syncthreads();
+    if (wv == 0) {
+        // exclusive scans of the (chunk, wave) tables in their order, 4 entries a lane
+        int c[4];
+        long long r[4];
+        int cs = 0;
+        long long rsum = 0;
+#pragma unroll
+        for (int q = 0; q < 4; q++) {
+            const int idx = lane * 4 + q;
+            c[q] = idx < R * kPlanWaves ? s_cw[idx] : 0;
+            r[q] = idx < R * kPlanWaves ? s_rw[idx] : 0;
+            cs += c[q];
+            rsum += r[q];
+        }
+        const int ci = plan_wave_incl(cs, plus);
+        const long long ri = plan_wave_incl(rsum, plus64);
+        int cp = ci - cs;
+        long long rp = ri - rsum;
+#pragma unroll
+        for (int q = 0; q < 4; q++) {
+            const int idx = lane * 4 + q;
+            if (idx < R * kPlanWaves) {
+                s_cw[idx] = cp;
+                s_rw[idx] = rp;
+            }
+            cp += c[q];
+            rp += r[q];
+        }
+        if (lane == 63) {
+            s_misc[3] = ci;  // ADD entries
+            s_tmp[0] = ri;   // their label tokens
+        }
+    }
+    __syncthreads();
+    const int m = s_misc[3];
+    const long long pool_total = s_tmp[0];
+    if ((int64_t)m != n_add || m > kPlanMax || B.n > kPlanMaxBatch) {
+        if (t == 0) atomicAdd(&ctr->bad_path, 1ull);
+        return;  // the same in every thread
+    }
+    __syncthreads();  // s_tmp is reused by the scans below
+    // second sweep: place each ADD entry, record its span, hash its parent
+    // (parents are looked up until the table holds kPlanMaxParents of them)
+    {
+        int32_t xs[kPlanBatchItems], ts[kPlanBatchItems];
+#pragma unroll
+        for (int j = 0; j < kPlanBatchItems; j++) {
+            xs[j] = 0;
+            ts[j] = 0;
+            if ((addbits >> j) & 1u) {
+                xs[j] = st[j * T + t].x;
+                ts[j] = st[j * T + t].t;
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < kPlanBatchItems; j++) {
+            if (j < R) {
+                const int i = j * T + t;
+                const bool a = (addbits >> j) & 1u;
+                const long long rest = a ? ar[j] : 0;
+                const uint64_t bal = __ballot(a);
+                const long long rs = wave_incl_add_i64(rest) - rest;
+                if (a) {
+                    const int pos = s_cw[j * kPlanWaves + wv] + (int)__popcll(bal & lt_mask);
+                    pofs[i] = s_rw[j * kPlanWaves + wv] + rs;
+                    if (s_misc[1] == 0) {
+                        if (s_misc[0] > kPlanMaxParents || plan_slot_insert(s_tab, &s_misc[0], xs[j]) < 0)
+                            s_misc[1] = 1;
+                    }
+                    s_key[plan_pad(pos)] =
+                        ((unsigned long long)(uint32_t)xs[j] << 32) | (uint32_t)(ts[j] ^ (int32_t)0x80000000);
+                    s_val[plan_pad(pos)] = (uint16_t)i;
+                }
+            }
+        }
+    }
+    __syncthreads();
+    const bool slotted = s_misc[1] == 0 && s_misc[0] <= kPlanMaxParents;
+    if (slotted) {
+        for (int p = t; p < m; p += T) {
+            const unsigned long long kk = s_key[plan_pad(p)];
+            const int sl = plan_slot_find(s_tab, (int32_t)(kk >> 32));
+            s_key[plan_pad(p)] = ((unsigned long long)(uint32_t)sl << 32) | (kk & 0xFFFFFFFFull);
+        }
+    }
+    __syncthreads();
+
+    // 2. stable LSD radix sort; thread t holds the entries [t*C, t*C + nv)
+    const int C = (m + T - 1) / T;
+    const int e0 = t * C;
+    const int nv = max(0, min(C, m - e0));
+    unsigned long long k[kPlanItems];
+    int32_t v[kPlanItems];
+    unsigned long long kor = 0, kand = ~0ull;
+#pragma unroll
+    for (int j = 0; j < kPlanItems; j++) {
+        k[j] = j < nv ? s_key[plan_pad(e0 + j)] : 0ull;
+        v[j] = j < nv ? (int32_t)s_val[plan_pad(e0 + j)] : 0;
+        if (j < nv) {
+            kor |= k[j];
+            kand &= k[j];
+        }
+    }
+    {
+        long long o, a;
+        (void)plan_block_excl<long long>((long long)kor, 0, [](long long x, long long y) { return x | y; }, s_tmp,
+                                         &o);
+        (void)plan_block_excl<long long>((long long)kand, -1, [](long long x, long long y) { return x & y; }, s_tmp,
+                                         &a);
+        kor = (unsigned long long)o ^ (unsigned long long)a;  // bits that differ between keys
+    }
+#pragma unroll 1
+    for (int b = 0; b < 64; b += 4) {
+        if (((kor >> b) & 15ull) == 0) continue;  // the same digit in every key
+        // counts of the thread's own entries per digit, in its own column
+        // (digit d in the low half of word (d & 7) * T + t for d < 8, else the
+        // high half); the atomics' old values rank each entry among the
+        // thread's earlier entries of its digit
+#pragma unroll
+        for (int q = 0; q < 8; q++) s_cnt[q * T + t] = 0u;
+        uint32_t lr[kPlanItems];
+#pragma unroll
+        for (int j = 0; j < kPlanItems; j++) {
+            lr[j] = 0;
+            if (j < nv) {
+                const int d = (int)((k[j] >> b) & 15ull);
+                const uint32_t old = atomicAdd(&s_cnt[(d & 7) * T + t], (d >> 3) ? 0x10000u : 1u);
+                lr[j] = (old >> ((d >> 3) << 4)) & 0xFFFFu;
+            }
+        }
+        // rank base of (digit, thread) in digit-major order: the digit's
+        // offset, plus the same digit's counts of the threads before.  Both
+        // halves of a word scan together (no half exceeds kPlanMax < 2^16).
+        uint32_t ex[8];
+#pragma unroll
+        for (int q = 0; q < 8; q++) {
+            const uint32_t cw = s_cnt[q * T + t];
+            const uint32_t inc = wave_incl_add_u32(cw);
+            ex[q] = inc - cw;
+            if (lane == 63) s_wt[wv * 8 + q] = inc;
+        }
+        __syncthreads();
+        if (t < 8) {
+            // exclusive prefix over the waves of each packed word, and the total
+            uint32_t x[kPlanWaves];
+#pragma unroll
+            for (int w = 0; w < kPlanWaves; w++) x[w] = s_wt[w * 8 + t];
+            uint32_t run = 0;
+#pragma unroll
+            for (int w = 0; w < kPlanWaves; w++) {
+                s_wt[w * 8 + t] = run;
+                run += x[w];
+            }
+            s_dt[t] = run;
+        }
+        __syncthreads();
+        {
+            // digit offsets, packed like the counts: digits 0-7 in the low
+            // halves, 8-15 in the high (no half reaches 2^16, so packed sums
+            // do not carry)
+            uint32_t lo = 0, hi = 0;
+#pragma unroll
+            for (int q = 0; q < 8; q++) hi += s_dt[q] & 0xFFFFu;  // digits 8-15 start after all of 0-7
+#pragma unroll
+            for (int q = 0; q < 8; q++) {
+                const uint32_t dt = s_dt[q];
+                s_cnt[q * T + t] = ex[q] + s_wt[wv * 8 + q] + ((hi << 16) | lo);
+                lo += dt & 0xFFFFu;
+                hi += dt >> 16;
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < kPlanItems; j++) {
+            if (j < nv) {
+                const int d = (int)((k[j] >> b) & 15ull);
+                const uint32_t base = (s_cnt[(d & 7) * T + t] >> ((d >> 3) << 4)) & 0xFFFFu;
+                const int rank = (int)(base + lr[j]);
+                s_key[plan_pad(rank)] = k[j];
+                s_val[plan_pad(rank)] = (uint16_t)v[j];
+            }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < kPlanItems; j++) {
+            if (j < nv) {
+                k[j] = s_key[plan_pad(e0 + j)];
+                v[j] = (int32_t)s_val[plan_pad(e0 + j)];
+            }
+        }
+        // no barrier here: the next pass writes only its own wave's s_wt
+        // entries and its own column before its first barrier, and s_dt and
+        // the entries after it
+    }
+
+    // 3. marks: slot winners, group heads and ends; per-thread totals
+    const unsigned long long before = (nv > 0 && e0 > 0) ? s_key[plan_pad(e0 - 1)] : 0ull;
+    const unsigned long long after = (nv > 0 && e0 + nv < m) ? s_key[plan_pad(e0 + nv)] : 0ull;
+    for (int p = t; p < m; p += T) {
+        const unsigned long long kk = s_key[plan_pad(p)];
+        const uint32_t x = slotted ? (uint32_t)s_tab[(int)(kk >> 32)] : (uint32_t)(kk >> 32);
+        keys[p] = ((unsigned long long)x << 32) | (kk & 0xFFFFFFFFull);
+        vals[p] = (int32_t)s_val[plan_pad(p)];
+    }
+    uint32_t wbits = 0, hbits = 0, lbits = 0;
+    int sw = 0, sc = 0, lh = -1;
+#pragma unroll
+    for (int j = 0; j < kPlanItems; j++) {
+        if (j < nv) {
+            const int e = e0 + j;
+            const unsigned long long kp = j == 0 ? before : k[j - 1];
+            const unsigned long long kn = j + 1 < nv ? k[j + 1] : after;
+            const bool w = e == 0 || k[j] != kp;
+            const bool h = e == 0 || (k[j] >> 32) != (kp >> 32);
+            const bool l = e + 1 == m || (k[j] >> 32) != (kn >> 32);
+            wbits |= (uint32_t)w << j;
+            hbits |= (uint32_t)h << j;
+            lbits |= (uint32_t)l << j;
+            sw += w;
+            if (h) {
+                const int32_t x = slotted ? s_tab[(int)(k[j] >> 32)] : (int32_t)(k[j] >> 32);
+                sc += (F.nodes[x].ct_cnt + 63) / 64;
+                lh = e;
+            }
+        }
+    }
+    int tw, tc, th;
+    int pw = plan_block_excl<int>(sw, 0, plus, s_tmp32, &tw);
+    int pc = plan_block_excl<int>(sc, 0, plus, s_tmp32, &tc);
+    int ph = plan_block_excl<int>(lh, -1, [](int x, int y) { return x > y ? x : y; }, s_tmp32, &th);
+    // 4. per entry: widx, hd and cstart, staged in LDS (s_key's entries and
+    // s_val's ids were read before the scans' barriers) and written out
+    // coalesced; widx stays in s_val for the group ends
+    const int ph0 = ph;
+#pragma unroll
+    for (int j = 0; j < kPlanItems; j++) {
+        if (j < nv) {
+            const int e = e0 + j;
+            const bool h = (hbits >> j) & 1u;
+            if (h) ph = e;
+            s_val[plan_pad(e)] = (uint16_t)pw;
+            s_key[plan_pad(e)] = ((unsigned long long)(uint32_t)pc << 32) | (uint32_t)ph;
+            pw += (wbits >> j) & 1u;
+            if (h) {
+                const int32_t x = slotted ? s_tab[(int)(k[j] >> 32)] : (int32_t)(k[j] >> 32);
+                pc += (F.nodes[x].ct_cnt + 63) / 64;
+            }
+        }
+    }
+    __syncthreads();
+    for (int p = t; p < m; p += T) {
+        const unsigned long long sk = s_key[plan_pad(p)];
+        const int wi = (int)s_val[plan_pad(p)];
+        const int wn = p + 1 < m ? (int)s_val[plan_pad(p + 1)] : tw;
+        win[p] = wn - wi;
+        widx[p] = wi;
+        hd[p] = (int32_t)(uint32_t)sk;
+        cstart[p] = (int32_t)(sk >> 32);
+    }
+    // 5. records per rebuilt block (old children + winners), scanned over the
+    // groups in order; one allocation for all of them and one for the pool
+    int hcur = ph0;
+    int need = 0;
+#pragma unroll
+    for (int j = 0; j < kPlanItems; j++) {
+        if (j < nv) {
+            const int e = e0 + j;
+            if ((hbits >> j) & 1u) hcur = e;
+            if ((lbits >> j) & 1u) {
+                const int32_t x = slotted ? s_tab[(int)(k[j] >> 32)] : (int32_t)(k[j] >> 32);
+                const int nw = (int)s_val[plan_pad(e)] + (int)((wbits >> j) & 1u) - (int)s_val[plan_pad(hcur)];
+                need += F.nodes[x].ct_cnt + nw;
+            }
+        }
+    }
+    int need_all;
+    int noff = plan_block_excl<int>(need, 0, plus, s_tmp32, &need_all);
+    if (t == 0) {
+        const long long nb = (long long)atomicAdd(&ctr->n_nodes, (unsigned long long)need_all);
+        const long long pb = (long long)atomicAdd(&ctr->n_pool, (unsigned long long)pool_total);
+        const bool ok = nb + need_all <= F.cap_nodes && pb + pool_total <= F.cap_pool;
+        if (!ok) atomicAdd(&ctr->overflow, 1ull);
+        ctr->add_pool_base = (unsigned long long)pb;
+        ctr->move_chunks = (unsigned long long)tc;
+        cstart[m] = tc;
+        s_tmp[0] = ok ? nb : -1;
+    }
+    __syncthreads();
+    // winners' tokens go to LDS at their place in win_tok (head + ordinal) and
+    // out coalesced; entries past a group's winners hold no token
+    const long long nb0 = s_tmp[0];
+    uint32_t *s_tok = reinterpret_cast<uint32_t *>(s_key);  // the staged outputs were read above
+    hcur = ph0;
+#pragma unroll
+    for (int j = 0; j < kPlanItems; j++) {
+        if (j < nv) {
+            const int e = e0 + j;
+            const bool w = (wbits >> j) & 1u;
+            if ((hbits >> j) & 1u) hcur = e;
+            const int wk = (int)s_val[plan_pad(hcur)];
+            if (w) s_tok[plan_pad(hcur + ((int)s_val[plan_pad(e)] - wk))] = (uint32_t)k[j] ^ 0x80000000u;
+            if ((lbits >> j) & 1u) {
+                const int32_t x = slotted ? s_tab[(int)(k[j] >> 32)] : (int32_t)(k[j] >> 32);
+                const int nw = (int)s_val[plan_pad(e)] + (int)w - wk;
+                grp_nw[hcur] = nw;
+                grp_nb[hcur] = nb0 < 0 ? -1 : (int32_t)(nb0 + noff);
+                noff += F.nodes[x].ct_cnt + nw;
+            }
+        }
+    }
+    __syncthreads();
+    for (int p = t; p < m; p += T) win_tok[p] = (int32_t)s_tok[plan_pad(p)];
+}
+
 // Step 3 (one thread per group head): records and label tokens of the new
 // block, or grp_nb = -1 (nothing is written; the parent keeps its old,
 // consistent block) when the capacity runs out.
@@ -490,10 +988,12 @@ __global__ __launch_bounds__(64 *kMergeWavesPerBlock) void add_move_kernel(
 
 // Step 5 (one wave per winning entry): the leaf holding the rest of the
 // winner's sequence, in its token's slot among the parent's children.
+// pofs: nullptr after the multi-launch steps (spans from poff and grp_pb),
+// else the one-workgroup plan's spans per insert from ctr->add_pool_base.
 __global__ __launch_bounds__(64 *kMergeWavesPerBlock) void add_leaf_kernel(
     DevForest F, Batch B, const unsigned long long *keys, const int32_t *vals, int64_t n_add, InsState *st,
     const int32_t *win, const int32_t *widx, const int64_t *poff, const int32_t *hd, const int32_t *grp_nb,
-    const int64_t *grp_pb) {
+    const int64_t *grp_pb, const int64_t *pofs, const MergeCounters *ctr) {
     const int lane = (int)(threadIdx.x & 63);
     const int64_t e = m_wave_index();
     if (e >= n_add || !win[e]) return;
@@ -507,7 +1007,7 @@ __global__ __launch_bounds__(64 *kMergeWavesPerBlock) void add_leaf_kernel(
     const int32_t d = st[i].d;
     const int64_t rest = len - d;  // >= 1: an ADD insert has a next token
     const int64_t dst = nb + (widx[e] - widx[k]) + lower_count(F.ntok + nx.ct_beg, nx.ct_cnt, s[d]);
-    const int64_t pb = grp_pb[k] + (poff[e] - poff[k]);
+    const int64_t pb = pofs ? (int64_t)ctr->add_pool_base + pofs[i] : grp_pb[k] + (poff[e] - poff[k]);
     copy_tokens(F.pool + pb, s + d, rest, lane);
     zero_mext(F, dst, lane);
     if (lane == 0) {

@@ -69,6 +69,7 @@ struct MergeScratch {
     int32_t *grp_nw = nullptr, *grp_nb = nullptr, *win_tok = nullptr, *win_ins = nullptr;
     // add rounds: per sorted entry (cap + 1 entries)
     int32_t *win = nullptr, *widx = nullptr, *headv = nullptr, *hd = nullptr, *nch = nullptr, *cstart = nullptr;
+    int32_t *arest = nullptr;  // per insert: label tokens of an ADD insert, else -1
     int64_t *rest = nullptr, *poff = nullptr, *grp_pool = nullptr, *grp_pb = nullptr;
     int64_t cap = 0;
     void *sort_tmp = nullptr;
@@ -142,6 +143,12 @@ namespace {
 #define PR_ROUTE_LONGEST_FIRST 1
 #endif
 // Narrow (16- or 17-bit) label copies for routes; 0 keeps every forest on int32 labels.
+// Rounds of at most pr::kPlanMax ADD inserts plan their add phase in one
+// workgroup (0: always the multi-launch path, for comparisons).
+#ifndef PR_MERGE_PLAN
+#define PR_MERGE_PLAN 1
+#endif
+
 #ifndef PR_NARROW_LABELS
 #define PR_NARROW_LABELS 1
 #endif
@@ -286,6 +293,7 @@ void free_add_scratch(pr_forest *f) {
     dfree(f, &m.poff, c);
     dfree(f, &m.grp_pool, c);
     dfree(f, &m.grp_pb, c);
+    dfree(f, &m.arest, c);
 }
 
 void free_scratch(pr_forest *f) {
@@ -771,7 +779,7 @@ pr_status ensure_merge_scratch(pr_forest *f, int64_t n, hipStream_t s) {
             !dalloc(f, &m.win, c1) || !dalloc(f, &m.widx, c1) || !dalloc(f, &m.headv, c1) ||
             !dalloc(f, &m.hd, c1) || !dalloc(f, &m.nch, c1) || !dalloc(f, &m.cstart, c1) ||
             !dalloc(f, &m.rest, c1) || !dalloc(f, &m.poff, c1) || !dalloc(f, &m.grp_pool, c1) ||
-            !dalloc(f, &m.grp_pb, c1)) {
+            !dalloc(f, &m.grp_pb, c1) || !dalloc(f, &m.arest, c1)) {
             m.cap = cap;  // so that free_scratch releases the add arrays by their size
             free_scratch(f);
             return fail(PR_ENOMEM, "hipMalloc failed for merge scratch");
@@ -912,7 +920,7 @@ pr_status run_merge(pr_forest *f, const int32_t *peer_of, const int32_t *tokens,
                            f->d_ctr);
         hipLaunchKernelGGL(pr::merge_tally_kernel,
                            dim3((unsigned)std::min<int64_t>(256, (n + pr::kTallyThreads - 1) / pr::kTallyThreads)),
-                           dim3(pr::kTallyThreads), 0, s, B, m.st, f->d_ctr);
+                           dim3(pr::kTallyThreads), 0, s, B, m.st, f->d_ctr, m.arest);
         if ((r = read_counters_raw(f, &c, s))) return r;
         if (c.overflow) {
             // The last round ran out of capacity.  Every refused allocation
@@ -952,44 +960,54 @@ pr_status run_merge(pr_forest *f, const int32_t *peer_of, const int32_t *tokens,
         long long add_stamp = 0;
         if (c.n_add > 0) {
             const int64_t n_add = (int64_t)c.n_add;
-            hipLaunchKernelGGL(pr::add_keys_kernel, dim3(grid_threads(n, bs)), dim3(bs), 0, s, B, m.st, m.keys_in,
-                               m.vals_in);
-            size_t tmp = m.sort_tmp_bytes;
-            if (rocprim::radix_sort_pairs(m.sort_tmp, tmp, m.keys_in, m.keys_out, m.vals_in, m.vals_out, n, 0, 64,
-                                          s) != hipSuccess)
-                return fail(PR_EDEVICE, "radix sort failed");
-            // winners, group heads and chunks; their scans; per-group totals
-            hipLaunchKernelGGL(pr::add_mark_kernel, dim3(grid_threads(n_add + 1, bs)), dim3(bs), 0, s, dev_view(f),
-                               B, m.keys_out, m.vals_out, n_add, m.st, m.win, m.rest, m.headv, m.nch);
-            size_t t1 = m.sort_tmp_bytes;
-            if (rocprim::exclusive_scan(m.sort_tmp, t1, m.win, m.widx, 0, (size_t)n_add, rocprim::plus<int32_t>(),
-                                        s) != hipSuccess)
-                return fail(PR_EDEVICE, "add scan failed");
-            t1 = m.sort_tmp_bytes;
-            if (rocprim::exclusive_scan(m.sort_tmp, t1, m.rest, m.poff, (int64_t)0, (size_t)n_add,
-                                        rocprim::plus<int64_t>(), s) != hipSuccess)
-                return fail(PR_EDEVICE, "add scan failed");
-            t1 = m.sort_tmp_bytes;
-            if (rocprim::inclusive_scan(m.sort_tmp, t1, m.headv, m.hd, (size_t)n_add, rocprim::maximum<int32_t>(),
-                                        s) != hipSuccess)
-                return fail(PR_EDEVICE, "add scan failed");
-            t1 = m.sort_tmp_bytes;
-            if (rocprim::exclusive_scan(m.sort_tmp, t1, m.nch, m.cstart, 0, (size_t)n_add + 1,
-                                        rocprim::plus<int32_t>(), s) != hipSuccess)
-                return fail(PR_EDEVICE, "add scan failed");
-            hipLaunchKernelGGL(reset_round_kernel, dim3(1), dim3(1), 0, s, f->d_ctr);
-            hipLaunchKernelGGL(pr::add_group_kernel, dim3(grid_threads(n_add, bs)), dim3(bs), 0, s, dev_view(f),
-                               m.keys_out, m.vals_out, n_add, m.st, m.win, m.rest, m.widx, m.poff, m.hd, m.cstart,
-                               m.grp_nw, m.grp_pool, m.win_tok, m.win_ins, f->d_ctr);
+            const bool plan = PR_MERGE_PLAN && n_add <= pr::kPlanMax && n <= pr::kPlanMaxBatch;
+            if (plan) {
+                // sort, marks, scans and groups in one workgroup
+                hipLaunchKernelGGL(pr::add_plan_kernel, dim3(1), dim3(pr::kPlanThreads), 0, s, dev_view(f), B, m.st,
+                                   m.arest, n_add, m.keys_out, m.vals_out, m.win, m.widx, m.hd, m.cstart, m.grp_nw,
+                                   m.grp_nb, m.win_tok, m.rest, f->d_ctr);
+            } else {
+                hipLaunchKernelGGL(pr::add_keys_kernel, dim3(grid_threads(n, bs)), dim3(bs), 0, s, B, m.st, m.keys_in,
+                                   m.vals_in);
+                size_t tmp = m.sort_tmp_bytes;
+                if (rocprim::radix_sort_pairs(m.sort_tmp, tmp, m.keys_in, m.keys_out, m.vals_in, m.vals_out, n, 0, 64,
+                                              s) != hipSuccess)
+                    return fail(PR_EDEVICE, "radix sort failed");
+                // winners, group heads and chunks; their scans; per-group totals
+                hipLaunchKernelGGL(pr::add_mark_kernel, dim3(grid_threads(n_add + 1, bs)), dim3(bs), 0, s, dev_view(f),
+                                   B, m.keys_out, m.vals_out, n_add, m.st, m.win, m.rest, m.headv, m.nch);
+                size_t t1 = m.sort_tmp_bytes;
+                if (rocprim::exclusive_scan(m.sort_tmp, t1, m.win, m.widx, 0, (size_t)n_add, rocprim::plus<int32_t>(),
+                                            s) != hipSuccess)
+                    return fail(PR_EDEVICE, "add scan failed");
+                t1 = m.sort_tmp_bytes;
+                if (rocprim::exclusive_scan(m.sort_tmp, t1, m.rest, m.poff, (int64_t)0, (size_t)n_add,
+                                            rocprim::plus<int64_t>(), s) != hipSuccess)
+                    return fail(PR_EDEVICE, "add scan failed");
+                t1 = m.sort_tmp_bytes;
+                if (rocprim::inclusive_scan(m.sort_tmp, t1, m.headv, m.hd, (size_t)n_add, rocprim::maximum<int32_t>(),
+                                            s) != hipSuccess)
+                    return fail(PR_EDEVICE, "add scan failed");
+                t1 = m.sort_tmp_bytes;
+                if (rocprim::exclusive_scan(m.sort_tmp, t1, m.nch, m.cstart, 0, (size_t)n_add + 1,
+                                            rocprim::plus<int32_t>(), s) != hipSuccess)
+                    return fail(PR_EDEVICE, "add scan failed");
+                hipLaunchKernelGGL(reset_round_kernel, dim3(1), dim3(1), 0, s, f->d_ctr);
+                hipLaunchKernelGGL(pr::add_group_kernel, dim3(grid_threads(n_add, bs)), dim3(bs), 0, s, dev_view(f),
+                                   m.keys_out, m.vals_out, n_add, m.st, m.win, m.rest, m.widx, m.poff, m.hd, m.cstart,
+                                   m.grp_nw, m.grp_pool, m.win_tok, m.win_ins, f->d_ctr);
+            }
             const long long stamp = ++f->stamp;
             add_stamp = stamp;
             const pr::DevForest F = dev_view(f);
-            hipLaunchKernelGGL(pr::add_alloc_kernel, dim3(grid_threads(n_add, bs)), dim3(bs), 0, s, F, m.keys_out,
-                               n_add, m.grp_nw, m.grp_pool, m.grp_nb, m.grp_pb, f->d_ctr);
+            if (!plan)
+                hipLaunchKernelGGL(pr::add_alloc_kernel, dim3(grid_threads(n_add, bs)), dim3(bs), 0, s, F, m.keys_out,
+                                   n_add, m.grp_nw, m.grp_pool, m.grp_nb, m.grp_pb, f->d_ctr);
             hipLaunchKernelGGL(pr::add_move_kernel, dim3(pr::kMoveBlocks), dim3(wb), 0, s, F, m.keys_out, n_add,
                                m.cstart, f->d_ctr, m.grp_nw, m.grp_nb, m.win_tok, stamp);
             hipLaunchKernelGGL(pr::add_leaf_kernel, dim3(grid_waves(n_add)), dim3(wb), 0, s, F, B, m.keys_out,
-                               m.vals_out, n_add, m.st, m.win, m.widx, m.poff, m.hd, m.grp_nb, m.grp_pb);
+                               m.vals_out, n_add, m.st, m.win, m.widx, m.poff, m.hd, m.grp_nb, m.grp_pb,
+                               plan ? m.rest : nullptr, f->d_ctr);
             hipLaunchKernelGGL(pr::add_sep_kernel, dim3(grid_waves(n_add)), dim3(wb), 0, s, F, m.keys_out, n_add,
                                m.grp_nw, m.grp_nb);
             hipLaunchKernelGGL(pr::add_fix_kernel, dim3(grid_threads(n_add, bs)), dim3(bs), 0, s, F, m.keys_out,

@@ -28,9 +28,12 @@
 // is refused whole and counted, and the host grows the forest and repeats the
 // round.
 // Losers walk again in the next round and find the structure the winners
-// built.  When every insert is DONE, a last pass ORs each insert's peer bit
-// into the mask of every node on its path.  The match function afterwards is
-// that of the old sets plus the batch; it does not depend on the batch order.
+// built.  Peer masks follow the walks: a walk sets its insert's peer bit in
+// every node it passes through whole (the root included), a new leaf holds
+// its winner's bit, and a cut edge's upper part adds it; records carry their
+// masks when they move or split, so every node on an insert's final path holds
+// its bit.  The match function afterwards is that of the old sets plus the
+// batch; it does not depend on the batch order.
 #ifndef PR_MERGE_KERNELS_H
 #define PR_MERGE_KERNELS_H
 
@@ -63,7 +66,7 @@ struct MergeCounters {
     unsigned long long node_need; // add round: exact node records the next round adds
     unsigned long long overflow;  // allocations refused for lack of capacity
     unsigned long long skipped;   // inserts with invalid peer or offsets
-    unsigned long long bad_path;  // mask pass found a sequence not ending at a node
+    unsigned long long bad_path;  // an invariant of the round broke (the merge fails)
     unsigned long long move_chunks;  // add round: 64-child chunks of the old blocks that move
     unsigned long long wide_tokens;  // nonzero: an appended label token lies outside [0, 131071] (no narrow copy)
     unsigned long long hi_tokens;    // nonzero: an appended label token lies in [65536, 131071] (17-bit labels)
@@ -111,22 +114,40 @@ __device__ __forceinline__ unsigned long long wave_atomic_add(unsigned long long
     return (unsigned long long)readlane64((uint64_t)r, 0);
 }
 
-// First i < n with a[i] != b[i], or n (wave-cooperative).
+// First i < n with a[i] != b[i], or n (wave-cooperative).  Steps of 1024
+// tokens: a step's loads are all issued before its first wait, so a 1024-token
+// label costs one round trip.
+constexpr int kMergeLcpVectors = 16;
 __device__ __forceinline__ int64_t m_lcp(const int32_t *a, const int32_t *b, int64_t n, int lane) {
-    for (int64_t base = 0; base < n; base += 256) {
-        uint64_t bal[4];
+    for (int64_t base = 0; base < n; base += 64 * kMergeLcpVectors) {
+        uint64_t bal[kMergeLcpVectors];
 #pragma unroll
-        for (int j = 0; j < 4; j++) {
+        for (int j = 0; j < kMergeLcpVectors; j++) {
             const int64_t i = base + j * 64 + lane;
             bool mis = false;
             if (i < n) mis = a[i] != b[i];
             bal[j] = __ballot(mis);
         }
 #pragma unroll
-        for (int j = 0; j < 4; j++)
+        for (int j = 0; j < kMergeLcpVectors; j++)
             if (bal[j]) return base + j * 64 + (__ffsll((unsigned long long)bal[j]) - 1);
     }
     return n;
+}
+
+// The insert's peer bit in node x's mask, set only where it is missing (the
+// nodes near the root lie on almost every path, and atomics on one address
+// serialise); inserts into the local peer also stamp x with the current time.
+// mask0: x's first mask word as the caller read it.  Lane 0 only.
+__device__ __forceinline__ void m_mark(const DevForest &F, int32_t x, uint64_t mask0, int32_t w,
+                                       unsigned long long bit, bool stamp) {
+    unsigned long long *mw = w == 0 ? (unsigned long long *)&F.nodes[x].mask0
+                                    : (unsigned long long *)&F.mext[(int64_t)x * (F.W - 1) + (w - 1)];
+    const unsigned long long cur =
+        w == 0 ? (unsigned long long)mask0 : __hip_atomic_load(mw, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (!(cur & bit)) atomicOr(mw, bit);
+    if (stamp && __hip_atomic_load(&F.ltime[x], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < F.now)
+        atomicMax(&F.ltime[x], F.now);
 }
 
 // Child of node x whose first token is t, or -1 (wave-cooperative).  Blocks
@@ -177,12 +198,17 @@ __global__ __launch_bounds__(64 *kMergeWavesPerBlock) void merge_walk_kernel(Dev
     if (kind == kInsSkip || kind == kInsDone) return;
     const int32_t *s = B.tokens + B.offsets[i];
     const int64_t len = B.offsets[i + 1] - B.offsets[i];
+    const int32_t p = B.peer_of[i];
+    const int32_t w = p >> 6;
+    const unsigned long long bit = 1ull << (p & 63);
+    const bool stamp = F.ltime && B.stamp && p == F.local;
     int32_t x = 0;
     int64_t d = 0;
     InsState r;
     r.c = -1;
     r.l = 0;
     r.t = 0;
+    if (lane == 0) m_mark(F, 0, F.nodes[0].mask0, w, bit, stamp);
     while (true) {
         if (d == len) {
             r.kind = kInsDone;
@@ -202,6 +228,7 @@ __global__ __launch_bounds__(64 *kMergeWavesPerBlock) void merge_walk_kernel(Dev
         if (l == nc.lab_len && nc.lab_len > 0) {
             x = c;
             d += l;
+            if (lane == 0) m_mark(F, c, nc.mask0, w, bit, stamp);
             continue;
         }
         r.kind = kInsSplit;
@@ -278,12 +305,21 @@ __global__ void split_claim_kernel(DevForest F, Batch B, const InsState *st, lon
     atomicMax(&F.nodes[current_pos(F, st[i].c, stamp)].aux, (int32_t)(INT32_MAX - i));
 }
 
-__device__ __forceinline__ void copy_mext(const DevForest &F, int64_t dst, int64_t src, int lane) {
-    for (int w = lane; w < F.W - 1; w += 64) F.mext[dst * (F.W - 1) + w] = F.mext[src * (F.W - 1) + w];
+// Mask words past the first of a cut edge: the lower part (dst) keeps the
+// edge's peers, the upper part (src, in place) adds peer p.  Each word is read
+// and written by one lane.
+__device__ __forceinline__ void cut_mext(const DevForest &F, int64_t dst, int64_t src, int32_t p, int lane) {
+    for (int w = lane; w < F.W - 1; w += 64) {
+        const uint64_t v = F.mext[src * (F.W - 1) + w];
+        F.mext[dst * (F.W - 1) + w] = v;
+        if ((p >> 6) == w + 1) F.mext[src * (F.W - 1) + w] = v | (1ull << (p & 63));
+    }
 }
 
-__device__ __forceinline__ void zero_mext(const DevForest &F, int64_t dst, int lane) {
-    for (int w = lane; w < F.W - 1; w += 64) F.mext[dst * (F.W - 1) + w] = 0ull;
+// Mask words past the first of a new leaf: the bit of peer p only.
+__device__ __forceinline__ void leaf_mext(const DevForest &F, int64_t dst, int32_t p, int lane) {
+    for (int w = lane; w < F.W - 1; w += 64)
+        F.mext[dst * (F.W - 1) + w] = (p >> 6) == w + 1 ? 1ull << (p & 63) : 0ull;
 }
 
 // Copy n tokens into freshly allocated pool space (wave-cooperative).
@@ -336,14 +372,21 @@ __global__ __launch_bounds__(64 *kMergeWavesPerBlock) void split_apply_kernel(De
         pos_lower = nb + 1;
     }
     if (rest > 0) copy_tokens(F.pool + pb, s + r.d + r.l, rest, lane);
-    copy_mext(F, pos_lower, r.c, lane);
-    if (rest > 0) zero_mext(F, pos_leaf, lane);
+    // the winner's peer holds the upper part and its leaf; the lower part
+    // keeps the edge's peers
+    const int32_t p = B.peer_of[i];
+    const unsigned long long bit0 = (p >> 6) == 0 ? 1ull << (p & 63) : 0ull;
+    const bool local = F.ltime && B.stamp && p == F.local;
+    cut_mext(F, pos_lower, r.c, p, lane);
+    if (rest > 0) leaf_mext(F, pos_leaf, p, lane);
     if (lane == 0) {
         F.nodes[pos_lower] = lower;
         F.ntok[pos_lower] = lower.tok;
         if (F.ltime) {
-            F.ltime[pos_lower] = F.ltime[r.c];  // both parts of the edge keep its time
-            if (rest > 0) F.ltime[pos_leaf] = 0ull;
+            const unsigned long long tc = F.ltime[r.c];
+            F.ltime[pos_lower] = tc;  // both parts of the edge keep its time
+            if (local && tc < F.now) F.ltime[r.c] = F.now;
+            if (rest > 0) F.ltime[pos_leaf] = local ? F.now : 0ull;
         }
         if (rest > 0) {
             Node leaf;
@@ -353,11 +396,12 @@ __global__ __launch_bounds__(64 *kMergeWavesPerBlock) void split_apply_kernel(De
             leaf.ct_beg = 0;
             leaf.ct_cnt = 0;
             leaf.aux = 0;
-            leaf.mask0 = 0ull;
+            leaf.mask0 = bit0;
             F.nodes[pos_leaf] = leaf;
             F.ntok[pos_leaf] = leaf.tok;
         }
         Node upper = old;  // keeps tok, label start, peers and c's slot in its parent
+        upper.mask0 |= bit0;
         upper.lab_len = r.l;
         upper.ct_beg = (int32_t)nb;
         upper.ct_cnt = k;
@@ -1008,8 +1052,9 @@ __global__ __launch_bounds__(64 *kMergeWavesPerBlock) void add_leaf_kernel(
     const int64_t rest = len - d;  // >= 1: an ADD insert has a next token
     const int64_t dst = nb + (widx[e] - widx[k]) + lower_count(F.ntok + nx.ct_beg, nx.ct_cnt, s[d]);
     const int64_t pb = pofs ? (int64_t)ctr->add_pool_base + pofs[i] : grp_pb[k] + (poff[e] - poff[k]);
+    const int32_t p = B.peer_of[i];
     copy_tokens(F.pool + pb, s + d, rest, lane);
-    zero_mext(F, dst, lane);
+    leaf_mext(F, dst, p, lane);
     if (lane == 0) {
         Node leaf;
         leaf.tok = s[d];
@@ -1018,10 +1063,10 @@ __global__ __launch_bounds__(64 *kMergeWavesPerBlock) void add_leaf_kernel(
         leaf.ct_beg = 0;
         leaf.ct_cnt = 0;
         leaf.aux = 0;
-        leaf.mask0 = 0ull;
+        leaf.mask0 = (p >> 6) == 0 ? 1ull << (p & 63) : 0ull;  // the winner's peer holds its leaf
         F.nodes[dst] = leaf;
         F.ntok[dst] = leaf.tok;
-        if (F.ltime) F.ltime[dst] = 0ull;
+        if (F.ltime) F.ltime[dst] = (B.stamp && p == F.local) ? F.now : 0ull;
         st[i].kind = kInsDone;  // the winner's sequence ends at its new leaf
     }
 }
@@ -1056,45 +1101,6 @@ __global__ void add_fix_kernel(DevForest F, const unsigned long long *keys, int6
     const int64_t pos = (mv >> 32) == stamp ? (int64_t)(uint32_t)mv : (int64_t)x;
     F.nodes[pos].ct_cnt = F.nodes[pos].ct_cnt + grp_nw[k];
     F.nodes[pos].ct_beg = grp_nb[k];
-}
-
-// OR each insert's peer bit into every node on its path (the root included);
-// inserts into the local peer also stamp the path with the current time.
-__global__ __launch_bounds__(64 *kMergeWavesPerBlock) void merge_mask_kernel(DevForest F, Batch B,
-                                                                            const InsState *st,
-                                                                            MergeCounters *ctr) {
-    const int lane = (int)(threadIdx.x & 63);
-    const int64_t i = m_wave_index();
-    if (i >= B.n || st[i].kind != kInsDone) return;
-    const int32_t p = B.peer_of[i];
-    const int32_t w = p >> 6;
-    const unsigned long long bit = 1ull << (p & 63);
-    const int32_t *s = B.tokens + B.offsets[i];
-    const int64_t len = B.offsets[i + 1] - B.offsets[i];
-    const bool stamp = F.ltime && B.stamp && p == F.local;
-    int32_t x = 0;
-    int64_t d = 0;
-    while (true) {
-        if (lane == 0) {
-            // bits only get set during the pass, so a bit already seen set
-            // needs no atomic (nodes near the root are on almost every path)
-            unsigned long long *mw =
-                w == 0 ? (unsigned long long *)&F.nodes[x].mask0 : (unsigned long long *)&F.mext[(int64_t)x * (F.W - 1) + (w - 1)];
-            if (!(__hip_atomic_load(mw, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) & bit)) atomicOr(mw, bit);
-            if (stamp && __hip_atomic_load(&F.ltime[x], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < F.now)
-                atomicMax(&F.ltime[x], F.now);
-        }
-        if (d == len) break;
-        const Node nx = F.nodes[x];
-        const int32_t c = m_find_child(F, nx, s[d], lane);
-        const int32_t ll = c < 0 ? 0 : F.nodes[c].lab_len;
-        if (c < 0 || ll <= 0 || d + ll > len) {
-            if (lane == 0) atomicAdd(&ctr->bad_path, 1ull);
-            break;
-        }
-        x = c;
-        d += ll;
-    }
 }
 
 // A replaced snapshot: remove peer p from every mask (its old paths stay as

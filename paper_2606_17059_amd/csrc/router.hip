@@ -1025,7 +1025,6 @@ pr_status run_merge(pr_forest *f, const int32_t *peer_of, const int32_t *tokens,
     if (round == max_rounds) return fail(PR_EDEVICE, "merge did not converge");
     // records this merge added: the spare capacity the next one keeps free
     f->round_nodes = std::max<int64_t>(f->dev.n_nodes - nodes0, 0);
-    hipLaunchKernelGGL(pr::merge_mask_kernel, dim3(grid_waves(n)), dim3(wb), 0, s, dev_view(f), B, m.st, f->d_ctr);
     hipLaunchKernelGGL(add_skipped_kernel, dim3(1), dim3(1), 0, s, f->d_skipped, f->d_ctr);
     if (hipGetLastError() != hipSuccess) return fail(PR_EDEVICE, "merge launch failed");
     if ((r = pool16_extend(f, pool0, s))) return r;

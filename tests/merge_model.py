@@ -30,8 +30,11 @@ class FlatForest:
                 return nx["cb"] + j
         return -1
 
-    def walk(self, s):
+    def walk(self, s, p):
+        """Classify an insert; on the way, set its peer bit in every node it
+        passes through whole (the root included)."""
         x, d = 0, 0
+        self.nodes[0]["mask"] |= 1 << p
         while True:
             if d == len(s):
                 return ("done", x, -1, 0, d, 0)
@@ -46,6 +49,7 @@ class FlatForest:
                 l += 1
             if l == nc["len"]:
                 x, d = c, d + l
+                nc["mask"] |= 1 << p
                 continue
             return ("split", x, c, l, d, t)
 
@@ -60,14 +64,16 @@ class FlatForest:
         (parent, token) slot adds a leaf to its parent's rebuilt block) and
         the split phase (the lowest insert per edge cuts it; the edge's record
         is found through its move stamp if the add phase moved it).  Winners
-        are done; everyone else walks again."""
+        are done; everyone else walks again.  Peer bits: each walk sets them on
+        its path, a new leaf holds its winner's, a cut edge's upper part adds
+        the winner's, and records keep theirs when they move or split."""
         n = len(seqs)
         st = [None] * n
         active = [True] * n
         while True:
             for i in range(n):
                 if active[i]:
-                    st[i] = self.walk(seqs[i])
+                    st[i] = self.walk(seqs[i], peers[i])
                     if st[i][0] == "done":
                         active[i] = False
             splits = [i for i in range(n) if active[i] and st[i][0] == "split"]
@@ -95,7 +101,7 @@ class FlatForest:
                     for i in winners:
                         s, d = seqs[i], st[i][4]
                         leaves.append(dict(tok=int(s[d]), off=self.alloc_pool(s[d:]), len=len(s) - d, cb=0, cc=0,
-                                           aux=0, mask=0))
+                                           aux=0, mask=1 << peers[i]))
                         active[i] = False
                     block = sorted(old + leaves, key=lambda r: r["tok"])
                     nb = len(self.nodes)
@@ -132,21 +138,19 @@ class FlatForest:
                     block = [lower]
                     if rest > 0:
                         leaf = dict(tok=int(s[d + l]), off=self.alloc_pool(s[d + l:]), len=rest, cb=0, cc=0,
-                                    aux=0, mask=0)
+                                    aux=0, mask=1 << peers[i])
                         block = sorted([lower, leaf], key=lambda r: r["tok"])
                     self.nodes.extend(block)
-                    self.nodes[c] = dict(old, len=l, cb=nb, cc=len(block), aux=0)
+                    self.nodes[c] = dict(old, len=l, cb=nb, cc=len(block), aux=0, mask=old["mask"] | (1 << peers[i]))
                     active[i] = False
-        for i in range(n):  # mask pass
+        for i in range(n):  # every sequence ends at a node holding its peer
             s, p = seqs[i], peers[i]
             x, d = 0, 0
-            while True:
-                self.nodes[x]["mask"] |= 1 << p
-                if d == len(s):
-                    break
+            while d < len(s):
                 c = self.find_child(x, s[d])
                 assert c >= 0 and d + self.nodes[c]["len"] <= len(s), "sequence does not end at a node"
                 x, d = c, d + self.nodes[c]["len"]
+                assert (self.nodes[x]["mask"] >> p) & 1, "a node on the path lacks the peer's bit"
 
     def clear_peer(self, p):
         for r in self.nodes:

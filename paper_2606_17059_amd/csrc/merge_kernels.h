@@ -71,7 +71,15 @@ struct MergeCounters {
     unsigned long long wide_tokens;  // nonzero: an appended label token lies outside [0, 131071] (no narrow copy)
     unsigned long long hi_tokens;    // nonzero: an appended label token lies in [65536, 131071] (17-bit labels)
     unsigned long long add_pool_base;  // add round planned in one workgroup: first pool token of its labels
+    unsigned long long plan_n;         // ADD entries the one-workgroup plan took this round (0: none)
+    unsigned long long plan_fallback;  // nonzero: this round's ADD entries do not fit the one-workgroup plan
 };
+
+// Entry count of an add step: the host's, or (n_add < 0, rounds the host does
+// not read back) the one-workgroup plan's.
+__device__ __forceinline__ int64_t add_count(int64_t n_add, const MergeCounters *ctr) {
+    return n_add >= 0 ? n_add : (int64_t)ctr->plan_n;
+}
 
 struct DevForest {
     Node *nodes;
@@ -606,10 +614,12 @@ constexpr int kPlanPadded = kPlanMax + kPlanMax / 32;
 
 // One workgroup of kPlanThreads, for batches of at most kPlanMaxBatch inserts
 // whose round has at most kPlanMax ADD entries.  n_add is the walk's tally of
-// ADD inserts and arest the tally's per-insert label tokens (-1: not ADD); a
-// different count raises bad_path and plans nothing (the merge then fails).
-// pofs[i]: the label span of ADD insert i from the round's pool base
-// (ctr->add_pool_base).
+// ADD inserts (< 0: take the tally from ctr, for rounds the host does not read
+// back; a round that does not fit then raises plan_fallback and plans
+// nothing), and arest the tally's per-insert label tokens (-1: not ADD); a
+// count that differs from the host's raises bad_path and plans nothing (the
+// merge then fails).  pofs[i]: the label span of ADD insert i from the round's
+// pool base (ctr->add_pool_base); ctr->plan_n: the entries planned.
 __global__ __launch_bounds__(kPlanThreads) void add_plan_kernel(DevForest F, Batch B, const InsState *st,
                                                                 const int32_t *arest, int64_t n_add,
                                                                 unsigned long long *keys, int32_t *vals,
@@ -635,6 +645,18 @@ __global__ __launch_bounds__(kPlanThreads) void add_plan_kernel(DevForest F, Bat
     const auto plus = [](int a, int b) { return a + b; };
     const auto plus64 = [](long long a, long long b) { return a + b; };
 
+    if (n_add < 0) {
+        const unsigned long long na = ctr->n_add;  // the tally's, complete before this launch
+        if (na == 0 || na > (unsigned long long)kPlanMax || B.n > kPlanMaxBatch) {
+            if (t == 0) {
+                ctr->plan_n = 0;
+                ctr->move_chunks = 0;
+                if (na) ctr->plan_fallback = 1;
+            }
+            return;
+        }
+        n_add = (int64_t)na;
+    }
     for (int q = t; q < kPlanSlots; q += T) s_tab[q] = -1;
     if (t < 4) s_misc[t] = 0;
 
@@ -697,7 +719,11 @@ __global__ __launch_bounds__(kPlanThreads) void add_plan_kernel(DevForest F, Bat
     const int m = s_misc[3];
     const long long pool_total = s_tmp[0];
     if ((int64_t)m != n_add || m > kPlanMax || B.n > kPlanMaxBatch) {
-        if (t == 0) atomicAdd(&ctr->bad_path, 1ull);
+        if (t == 0) {
+            atomicAdd(&ctr->bad_path, 1ull);
+            ctr->plan_n = 0;
+            ctr->move_chunks = 0;
+        }
         return;  // the same in every thread
     }
     __syncthreads();  // s_tmp is reused by the scans below
@@ -943,6 +969,7 @@ __global__ __launch_bounds__(kPlanThreads) void add_plan_kernel(DevForest F, Bat
         if (!ok) atomicAdd(&ctr->overflow, 1ull);
         ctr->add_pool_base = (unsigned long long)pb;
         ctr->move_chunks = (unsigned long long)tc;
+        ctr->plan_n = (unsigned long long)m;
         cstart[m] = tc;
         s_tmp[0] = ok ? nb : -1;
     }
@@ -1004,6 +1031,7 @@ __global__ __launch_bounds__(64 *kMergeWavesPerBlock) void add_move_kernel(
     const int lane = (int)(threadIdx.x & 63);
     const int64_t nchunks = (int64_t)ctr->move_chunks;
     const int64_t waves = (int64_t)gridDim.x * kMergeWavesPerBlock;
+    n_add = add_count(n_add, ctr);
     for (int64_t c = m_wave_index(); c < nchunks; c += waves) {
         // the group whose chunks hold c: cstart[k] <= c < cstart[k + 1]
         int64_t lo = 0, hi = n_add;
@@ -1034,40 +1062,45 @@ __global__ __launch_bounds__(64 *kMergeWavesPerBlock) void add_move_kernel(
 // winner's sequence, in its token's slot among the parent's children.
 // pofs: nullptr after the multi-launch steps (spans from poff and grp_pb),
 // else the one-workgroup plan's spans per insert from ctr->add_pool_base.
+// Steps 5-7 stride over their entries, so a grid sized without the count
+// (rounds the host does not read back) serves as well.
 __global__ __launch_bounds__(64 *kMergeWavesPerBlock) void add_leaf_kernel(
     DevForest F, Batch B, const unsigned long long *keys, const int32_t *vals, int64_t n_add, InsState *st,
     const int32_t *win, const int32_t *widx, const int64_t *poff, const int32_t *hd, const int32_t *grp_nb,
     const int64_t *grp_pb, const int64_t *pofs, const MergeCounters *ctr) {
     const int lane = (int)(threadIdx.x & 63);
-    const int64_t e = m_wave_index();
-    if (e >= n_add || !win[e]) return;
-    const int32_t k = hd[e];
-    const int32_t nb = grp_nb[k];
-    if (nb < 0) return;
-    const int32_t i = vals[e];
-    const Node nx = F.nodes[key_parent(keys[e])];
-    const int32_t *s = B.tokens + B.offsets[i];
-    const int64_t len = B.offsets[i + 1] - B.offsets[i];
-    const int32_t d = st[i].d;
-    const int64_t rest = len - d;  // >= 1: an ADD insert has a next token
-    const int64_t dst = nb + (widx[e] - widx[k]) + lower_count(F.ntok + nx.ct_beg, nx.ct_cnt, s[d]);
-    const int64_t pb = pofs ? (int64_t)ctr->add_pool_base + pofs[i] : grp_pb[k] + (poff[e] - poff[k]);
-    const int32_t p = B.peer_of[i];
-    copy_tokens(F.pool + pb, s + d, rest, lane);
-    leaf_mext(F, dst, p, lane);
-    if (lane == 0) {
-        Node leaf;
-        leaf.tok = s[d];
-        leaf.lab_off = (uint32_t)pb;
-        leaf.lab_len = (int32_t)rest;
-        leaf.ct_beg = 0;
-        leaf.ct_cnt = 0;
-        leaf.aux = 0;
-        leaf.mask0 = (p >> 6) == 0 ? 1ull << (p & 63) : 0ull;  // the winner's peer holds its leaf
-        F.nodes[dst] = leaf;
-        F.ntok[dst] = leaf.tok;
-        if (F.ltime) F.ltime[dst] = (B.stamp && p == F.local) ? F.now : 0ull;
-        st[i].kind = kInsDone;  // the winner's sequence ends at its new leaf
+    const int64_t cnt = add_count(n_add, ctr);
+    const int64_t waves = (int64_t)gridDim.x * kMergeWavesPerBlock;
+    for (int64_t e = m_wave_index(); e < cnt; e += waves) {
+        if (!win[e]) continue;
+        const int32_t k = hd[e];
+        const int32_t nb = grp_nb[k];
+        if (nb < 0) continue;
+        const int32_t i = vals[e];
+        const Node nx = F.nodes[key_parent(keys[e])];
+        const int32_t *s = B.tokens + B.offsets[i];
+        const int64_t len = B.offsets[i + 1] - B.offsets[i];
+        const int32_t d = st[i].d;
+        const int64_t rest = len - d;  // >= 1: an ADD insert has a next token
+        const int64_t dst = nb + (widx[e] - widx[k]) + lower_count(F.ntok + nx.ct_beg, nx.ct_cnt, s[d]);
+        const int64_t pb = pofs ? (int64_t)ctr->add_pool_base + pofs[i] : grp_pb[k] + (poff[e] - poff[k]);
+        const int32_t p = B.peer_of[i];
+        copy_tokens(F.pool + pb, s + d, rest, lane);
+        leaf_mext(F, dst, p, lane);
+        if (lane == 0) {
+            Node leaf;
+            leaf.tok = s[d];
+            leaf.lab_off = (uint32_t)pb;
+            leaf.lab_len = (int32_t)rest;
+            leaf.ct_beg = 0;
+            leaf.ct_cnt = 0;
+            leaf.aux = 0;
+            leaf.mask0 = (p >> 6) == 0 ? 1ull << (p & 63) : 0ull;  // the winner's peer holds its leaf
+            F.nodes[dst] = leaf;
+            F.ntok[dst] = leaf.tok;
+            if (F.ltime) F.ltime[dst] = (B.stamp && p == F.local) ? F.now : 0ull;
+            st[i].kind = kInsDone;  // the winner's sequence ends at its new leaf
+        }
     }
 }
 
@@ -1077,30 +1110,34 @@ __global__ __launch_bounds__(64 *kMergeWavesPerBlock) void add_leaf_kernel(
 __global__ __launch_bounds__(64 *kMergeWavesPerBlock) void add_sep_kernel(DevForest F,
                                                                          const unsigned long long *keys,
                                                                          int64_t n_add, const int32_t *grp_nw,
-                                                                         const int32_t *grp_nb) {
+                                                                         const int32_t *grp_nb,
+                                                                         const MergeCounters *ctr) {
     const int lane = (int)(threadIdx.x & 63);
-    const int64_t k = m_wave_index();
-    if (k >= n_add) return;
-    if (k > 0 && key_parent(keys[k - 1]) == key_parent(keys[k])) return;
-    const int32_t nb = grp_nb[k];
-    if (nb < 0) return;
-    const int32_t cnt = F.nodes[key_parent(keys[k])].ct_cnt + grp_nw[k];
-    if (cnt <= kSepCount) return;
-    F.nsep[nb + lane] = F.ntok[nb + PR_SEP_INDEX(lane, cnt)];
+    const int64_t cnt = add_count(n_add, ctr);
+    const int64_t waves = (int64_t)gridDim.x * kMergeWavesPerBlock;
+    for (int64_t k = m_wave_index(); k < cnt; k += waves) {
+        if (k > 0 && key_parent(keys[k - 1]) == key_parent(keys[k])) continue;
+        const int32_t nb = grp_nb[k];
+        if (nb < 0) continue;
+        const int32_t c = F.nodes[key_parent(keys[k])].ct_cnt + grp_nw[k];
+        if (c <= kSepCount) continue;
+        F.nsep[nb + lane] = F.ntok[nb + PR_SEP_INDEX(lane, c)];
+    }
 }
 
 // Point every rebuilt parent at its new block, wherever its record lives now.
 __global__ void add_fix_kernel(DevForest F, const unsigned long long *keys, int64_t n_add, const int32_t *grp_nw,
-                               const int32_t *grp_nb, long long stamp) {
-    const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (k >= n_add) return;
-    if (k > 0 && key_parent(keys[k - 1]) == key_parent(keys[k])) return;
-    if (grp_nb[k] < 0) return;  // the build of this group was refused
-    const int32_t x = key_parent(keys[k]);
-    const long long mv = F.moved[x];
-    const int64_t pos = (mv >> 32) == stamp ? (int64_t)(uint32_t)mv : (int64_t)x;
-    F.nodes[pos].ct_cnt = F.nodes[pos].ct_cnt + grp_nw[k];
-    F.nodes[pos].ct_beg = grp_nb[k];
+                               const int32_t *grp_nb, long long stamp, const MergeCounters *ctr) {
+    const int64_t cnt = add_count(n_add, ctr);
+    for (int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; k < cnt; k += (int64_t)gridDim.x * blockDim.x) {
+        if (k > 0 && key_parent(keys[k - 1]) == key_parent(keys[k])) continue;
+        if (grp_nb[k] < 0) continue;  // the build of this group was refused
+        const int32_t x = key_parent(keys[k]);
+        const long long mv = F.moved[x];
+        const int64_t pos = (mv >> 32) == stamp ? (int64_t)(uint32_t)mv : (int64_t)x;
+        F.nodes[pos].ct_cnt = F.nodes[pos].ct_cnt + grp_nw[k];
+        F.nodes[pos].ct_beg = grp_nb[k];
+    }
 }
 
 // A replaced snapshot: remove peer p from every mask (its old paths stay as

@@ -594,12 +594,16 @@ __attribute__((amdgpu_waves_per_eu(PR_ROUTE_WAVES_PER_EU))) void route_kernel(
 // unusable); each workgroup reduces its finds and writes each flag at most
 // once, so the waves do not queue on one address.
 constexpr int kNarrowThreads = 256;
+// to_dev (if not nullptr): the range ends at min(*to_dev, to) instead, for a
+// pool whose used size only the device knows.
 __global__ __launch_bounds__(kNarrowThreads) void pool_narrow_kernel(const int32_t *__restrict__ pool,
                                                                      uint16_t *__restrict__ p16,
                                                                      uint32_t *__restrict__ hib, int64_t from,
                                                                      int64_t to, unsigned long long *__restrict__ hi,
-                                                                     unsigned long long *__restrict__ wide) {
+                                                                     unsigned long long *__restrict__ wide,
+                                                                     const unsigned long long *to_dev) {
     __shared__ int found[2];
+    if (to_dev) to = min(to, (int64_t)*to_dev);
     const int lane = (int)(threadIdx.x & (kWave - 1));
     if (threadIdx.x < 2) found[threadIdx.x] = 0;
     __syncthreads();

@@ -119,12 +119,14 @@ struct pr_forest {
     bool has_dev = false;
     pr::MergeCounters *d_ctr = nullptr;
     void *h_stage = nullptr;      // pinned host staging for the small readbacks between device rounds
+    uint32_t *d_stage = nullptr;  // h_stage as the device addresses it (nullptr: readbacks by DMA)
     unsigned long long *d_skipped = nullptr;  // inputs skipped by device calls
     MergeScratch ms;
     ExportScratch xs;
     RouteScratch rs;
     long long stamp = 0;          // add-round counter (stamps of moved records)
     int64_t round_nodes = 0;      // records the last merge added (spare capacity kept for the next)
+    int64_t round_pool = 0;       // pool tokens the last merge added (0: no merge yet)
     int64_t refusals = 0;         // merge rounds repeated after running out of capacity
     int32_t local = -1;           // peer whose tree keeps access times (-1: none)
     int64_t now = 0;              // current time, set by the caller, never decreasing
@@ -177,6 +179,7 @@ class DeviceScope {
 };
 
 constexpr size_t kStageBytes = 256;  // pinned readback staging per forest
+constexpr int kDeviceRounds = 2;     // merge rounds queued before the first readback
 
 unsigned grid_threads(int64_t n, int bs) { return (unsigned)((n + bs - 1) / bs); }
 unsigned grid_waves(int64_t n) { return (unsigned)((n + pr::kMergeWavesPerBlock - 1) / pr::kMergeWavesPerBlock); }
@@ -466,7 +469,9 @@ void drop_pool16(pr_forest *f) {
 // wide_tokens; the caller reads them with its next counter readback, turns
 // the bit plane on for the former and drops the copy for the latter.  Without
 // memory for a larger copy, routes fall back to the int32 pool.
-pr_status pool16_extend(pr_forest *f, int64_t from, hipStream_t s) {
+// device_end: the range ends at the device counters' n_pool (a merge whose
+// rounds the host has not read back), on a grid sized without it.
+pr_status pool16_extend(pr_forest *f, int64_t from, hipStream_t s, bool device_end = false) {
     DevImage &d = f->dev;
     if (!f->narrow) return PR_OK;
     if (d.cap_pool16 < d.cap_pool) {
@@ -492,11 +497,15 @@ pr_status pool16_extend(pr_forest *f, int64_t from, hipStream_t s) {
         from = 0;
         f->layout_epoch++;
     }
-    if (d.n_pool > from) {
-        const int64_t chunks = (d.n_pool + pr::kWave - 1) / pr::kWave - from / pr::kWave;
-        const int64_t blocks = std::min<int64_t>((chunks + 3) / 4, 1024);
+    const int64_t to = device_end ? d.cap_pool : d.n_pool;
+    if (to > from) {
+        const int64_t chunks = (to + pr::kWave - 1) / pr::kWave - from / pr::kWave;
+        // a wave per chunk: each wave's load waits on memory, so waves, not
+        // iterations, carry the chunks
+        const int64_t blocks = device_end && from > 0 ? 2048 : std::min<int64_t>((chunks + 3) / 4, 16384);
         hipLaunchKernelGGL(pr::pool_narrow_kernel, dim3((unsigned)blocks), dim3(pr::kNarrowThreads), 0, s, d.pool,
-                           d.pool16, d.hib, from, d.n_pool, &f->d_ctr->hi_tokens, &f->d_ctr->wide_tokens);
+                           d.pool16, d.hib, from, to, &f->d_ctr->hi_tokens, &f->d_ctr->wide_tokens,
+                           device_end ? (const unsigned long long *)&f->d_ctr->n_pool : nullptr);
         if (hipGetLastError() != hipSuccess) return fail(PR_EDEVICE, "narrow label copy failed to launch");
     }
     return PR_OK;
@@ -524,6 +533,11 @@ pr_status commit(pr_forest *f) {
             f->h_stage = nullptr;
             return fail(PR_ENOMEM, "hipHostMalloc failed for the readback staging");
         }
+        void *dp = nullptr;
+        if (hipHostGetDevicePointer(&dp, f->h_stage, 0) == hipSuccess)
+            f->d_stage = static_cast<uint32_t *>(dp);
+        else
+            (void)hipGetLastError();  // readbacks fall back to DMA copies
         if (hipMemset(f->d_skipped, 0, sizeof(unsigned long long)) != hipSuccess)
             return fail(PR_EDEVICE, "hipMemset failed");
     }
@@ -826,6 +840,8 @@ __global__ void reset_round_kernel(pr::MergeCounters *c) {
     c->pool_need = 0;
     c->node_need = 0;
     c->move_chunks = 0;
+    c->plan_n = 0;
+    c->plan_fallback = 0;
 }
 
 __global__ void reset_call_kernel(pr::MergeCounters *c) {
@@ -839,6 +855,8 @@ __global__ void reset_call_kernel(pr::MergeCounters *c) {
     c->skipped = 0;
     c->bad_path = 0;
     c->move_chunks = 0;
+    c->plan_n = 0;
+    c->plan_fallback = 0;
 }
 
 __global__ void add_skipped_kernel(unsigned long long *acc, const pr::MergeCounters *c) { *acc += c->skipped; }
@@ -851,13 +869,27 @@ __global__ void set_used_kernel(pr::MergeCounters *c, unsigned long long n_nodes
     c->overflow = 0;
 }
 
+// One wave stores the words of a small readback straight into the pinned
+// staging buffer, at system scope (past the GPU's caches).
+__global__ void stage_copy_kernel(const uint32_t *src, uint32_t *dst, int words) {
+    for (int i = (int)threadIdx.x; i < words; i += (int)blockDim.x)
+        __hip_atomic_store(&dst[i], src[i], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
 // Copy `bytes` (<= kStageBytes) of device memory to the host through the
-// forest's pinned staging buffer (a direct DMA, no pageable bounce) and wait.
+// forest's pinned staging buffer and wait.  Whole aligned words go through a
+// one-wave kernel that writes the buffer directly (a DMA copy of a few bytes
+// costs a blit launch several times as long); anything else by DMA.
 bool read_small(pr_forest *f, void *out, const void *dsrc, size_t bytes, hipStream_t s) {
     if (bytes > kStageBytes || !f->h_stage) return false;
-    if (hipMemcpyAsync(f->h_stage, dsrc, bytes, hipMemcpyDeviceToHost, s) != hipSuccess ||
-        hipStreamSynchronize(s) != hipSuccess)
+    if (f->d_stage && bytes % 4 == 0 && reinterpret_cast<uintptr_t>(dsrc) % 4 == 0) {
+        hipLaunchKernelGGL(stage_copy_kernel, dim3(1), dim3(64), 0, s, static_cast<const uint32_t *>(dsrc),
+                           f->d_stage, (int)(bytes / 4));
+        if (hipGetLastError() != hipSuccess || hipStreamSynchronize(s) != hipSuccess) return false;
+    } else if (hipMemcpyAsync(f->h_stage, dsrc, bytes, hipMemcpyDeviceToHost, s) != hipSuccess ||
+               hipStreamSynchronize(s) != hipSuccess) {
         return false;
+    }
     std::memcpy(out, f->h_stage, bytes);
     return true;
 }
@@ -914,7 +946,59 @@ pr_status run_merge(pr_forest *f, const int32_t *peer_of, const int32_t *tokens,
     const int max_rounds = 100000;
     int round = 0;
     int refusals = 0;
-    for (; round < max_rounds; round++) {
+    bool done = false;
+    // Rounds the device drives: kDeviceRounds full rounds, each sized on the
+    // device (the add phase planned in one workgroup, the later add steps
+    // striding over what it planned), then a checking walk, the narrow copy
+    // and one readback.  Most batches end there: the first round places every
+    // insert but the losers of a slot or an edge, the second places those.
+    // Anything else (work left, a round too large for the one-workgroup plan,
+    // a refused allocation) continues in the host-driven rounds below, which
+    // read the counters back after every walk.  A forest's first merge takes
+    // the host-driven rounds, which size its spare capacity.
+    if (PR_MERGE_PLAN && n <= pr::kPlanMaxBatch && f->round_pool > 0) {
+        if ((r = ensure_capacity(f, f->dev.n_nodes + 2 * std::max<int64_t>(f->round_nodes, n),
+                                 f->dev.n_pool + 2 * f->round_pool, s)))
+            return r;
+        const pr::DevForest F = dev_view(f);
+        for (int k = 0; k < kDeviceRounds; k++) {
+            hipLaunchKernelGGL(reset_round_kernel, dim3(1), dim3(1), 0, s, f->d_ctr);
+            hipLaunchKernelGGL(pr::merge_walk_kernel, dim3(grid_waves(n)), dim3(wb), 0, s, F, B, m.st, f->d_ctr);
+            hipLaunchKernelGGL(pr::merge_tally_kernel,
+                               dim3((unsigned)std::min<int64_t>(256, (n + pr::kTallyThreads - 1) / pr::kTallyThreads)),
+                               dim3(pr::kTallyThreads), 0, s, B, m.st, f->d_ctr, m.arest);
+            hipLaunchKernelGGL(pr::add_plan_kernel, dim3(1), dim3(pr::kPlanThreads), 0, s, F, B, m.st, m.arest,
+                               (int64_t)-1, m.keys_out, m.vals_out, m.win, m.widx, m.hd, m.cstart, m.grp_nw, m.grp_nb,
+                               m.win_tok, m.rest, f->d_ctr);
+            const long long stamp = ++f->stamp;
+            hipLaunchKernelGGL(pr::add_move_kernel, dim3(pr::kMoveBlocks), dim3(wb), 0, s, F, m.keys_out, (int64_t)-1,
+                               m.cstart, f->d_ctr, m.grp_nw, m.grp_nb, m.win_tok, stamp);
+            hipLaunchKernelGGL(pr::add_leaf_kernel, dim3(grid_waves(std::min<int64_t>(n, pr::kPlanMax))), dim3(wb), 0,
+                               s, F, B, m.keys_out, m.vals_out, (int64_t)-1, m.st, m.win, m.widx, m.poff, m.hd,
+                               m.grp_nb, m.grp_pb, m.rest, f->d_ctr);
+            hipLaunchKernelGGL(pr::add_sep_kernel, dim3(grid_waves(std::min<int64_t>(n, pr::kPlanMax))), dim3(wb), 0,
+                               s, F, m.keys_out, (int64_t)-1, m.grp_nw, m.grp_nb, f->d_ctr);
+            hipLaunchKernelGGL(pr::add_fix_kernel, dim3(grid_threads(std::min<int64_t>(n, pr::kPlanMax), bs)),
+                               dim3(bs), 0, s, F, m.keys_out, (int64_t)-1, m.grp_nw, m.grp_nb, stamp, f->d_ctr);
+            hipLaunchKernelGGL(pr::split_claim_kernel, dim3(grid_threads(n, bs)), dim3(bs), 0, s, F, B, m.st, stamp);
+            hipLaunchKernelGGL(pr::split_apply_kernel, dim3(grid_waves(n)), dim3(wb), 0, s, F, B, m.st, f->d_ctr,
+                               stamp);
+        }
+        hipLaunchKernelGGL(reset_round_kernel, dim3(1), dim3(1), 0, s, f->d_ctr);
+        hipLaunchKernelGGL(pr::merge_walk_kernel, dim3(grid_waves(n)), dim3(wb), 0, s, F, B, m.st, f->d_ctr);
+        hipLaunchKernelGGL(pr::merge_tally_kernel,
+                           dim3((unsigned)std::min<int64_t>(256, (n + pr::kTallyThreads - 1) / pr::kTallyThreads)),
+                           dim3(pr::kTallyThreads), 0, s, B, m.st, f->d_ctr, m.arest);
+        if (hipGetLastError() != hipSuccess) return fail(PR_EDEVICE, "merge launch failed");
+        if ((r = pool16_extend(f, pool0, s, true))) return r;
+        if ((r = read_counters_raw(f, &c, s))) return r;
+        done = !c.overflow && !c.plan_fallback && !c.bad_path && c.n_add == 0 && c.n_split == 0;
+        if (!c.overflow) {
+            f->dev.n_nodes = (int64_t)c.n_nodes;
+            f->dev.n_pool = (int64_t)c.n_pool;
+        }  // else the first host-driven readback sees the refusal and clips the counters
+    }
+    for (; !done && round < max_rounds; round++) {
         hipLaunchKernelGGL(reset_round_kernel, dim3(1), dim3(1), 0, s, f->d_ctr);
         hipLaunchKernelGGL(pr::merge_walk_kernel, dim3(grid_waves(n)), dim3(wb), 0, s, dev_view(f), B, m.st,
                            f->d_ctr);
@@ -1009,9 +1093,9 @@ pr_status run_merge(pr_forest *f, const int32_t *peer_of, const int32_t *tokens,
                                m.vals_out, n_add, m.st, m.win, m.widx, m.poff, m.hd, m.grp_nb, m.grp_pb,
                                plan ? m.rest : nullptr, f->d_ctr);
             hipLaunchKernelGGL(pr::add_sep_kernel, dim3(grid_waves(n_add)), dim3(wb), 0, s, F, m.keys_out, n_add,
-                               m.grp_nw, m.grp_nb);
+                               m.grp_nw, m.grp_nb, f->d_ctr);
             hipLaunchKernelGGL(pr::add_fix_kernel, dim3(grid_threads(n_add, bs)), dim3(bs), 0, s, F, m.keys_out,
-                               n_add, m.grp_nw, m.grp_nb, stamp);
+                               n_add, m.grp_nw, m.grp_nb, stamp, f->d_ctr);
         }
         if (n_split > 0) {
             const pr::DevForest F = dev_view(f);
@@ -1023,12 +1107,16 @@ pr_status run_merge(pr_forest *f, const int32_t *peer_of, const int32_t *tokens,
         if (hipGetLastError() != hipSuccess) return fail(PR_EDEVICE, "merge launch failed");
     }
     if (round == max_rounds) return fail(PR_EDEVICE, "merge did not converge");
-    // records this merge added: the spare capacity the next one keeps free
+    // records and pool tokens this merge added: the spare capacity the next
+    // one keeps free
     f->round_nodes = std::max<int64_t>(f->dev.n_nodes - nodes0, 0);
+    f->round_pool = std::max<int64_t>(f->dev.n_pool - pool0, 1);
     hipLaunchKernelGGL(add_skipped_kernel, dim3(1), dim3(1), 0, s, f->d_skipped, f->d_ctr);
     if (hipGetLastError() != hipSuccess) return fail(PR_EDEVICE, "merge launch failed");
-    if ((r = pool16_extend(f, pool0, s))) return r;
-    if ((r = read_counters(f, &c, s))) return r;
+    if (!done) {  // the device-driven rounds read everything back with the narrow copy done
+        if ((r = pool16_extend(f, pool0, s))) return r;
+        if ((r = read_counters(f, &c, s))) return r;
+    }
     if (c.overflow || c.bad_path)
         return fail(PR_EDEVICE, "merge invariant broken (overflow " + std::to_string(c.overflow) + ", bad paths " +
                                     std::to_string(c.bad_path) + "); destroy the forest");

@@ -171,6 +171,64 @@ def test_round_out_of_capacity_is_refused_and_repeated():
     o.close()
 
 
+def _merge_lists(f, o, items, label):
+    """Merge (peer, sequence) pairs into the GPU forest and the oracle."""
+    import torch
+    peers = np.array([p for p, _ in items], np.int32)
+    t, off = pins._csr([s for _, s in items])
+    announce(f"{label}: merge of {len(items)} inserts")
+    f.merge(torch.from_numpy(peers).to(device()), torch.from_numpy(t).to(device()),
+            torch.from_numpy(off).to(device()))
+    o.merge(peers, t, off)
+    torch.cuda.synchronize()
+
+
+def test_device_driven_rounds_hand_over_to_host_rounds():
+    """After a forest's first merge, a merge runs two rounds sized on the
+    device before it reads anything back; what they leave goes on in rounds
+    the host reads back after every walk.  Three batches force each hand-over:
+    a chain of inserts that share a new prefix and part from it one token
+    after another (a slot, then the same edge over and over: more rounds than
+    the device runs); more ADD entries in one round than the one-workgroup
+    plan takes (the multi-launch path); and label tokens far beyond the pool's
+    spare room after compaction (the device round's allocation is refused,
+    the host grows the forest and repeats it).  Every row against the oracle
+    after each merge; refusals show in the forest info."""
+    rng = np.random.default_rng(41)
+    P = 5
+    seqs = [[3, 1, 4, 1, 5, 9, 2, 6][: 2 + i % 6] + [100 + i] for i in range(40)]
+    owners = [i % P for i in range(len(seqs))]
+    snap = W.from_lists(seqs, owners)
+    f = _forest(snap, P)
+    o = oracle_for(snap, P)
+
+    def check(extra, label):
+        q = W.from_lists([list(s) for s in seqs] + [list(s) for s in extra])
+        m, c = gpu_route(f, q, label)
+        m_or, c_or = o.route(q.tokens, q.offsets, nthreads())
+        assert_rows_equal(m, c, m_or, c_or, what=label)
+
+    first = [(1, [3, 1, 4, 7]), (2, [8, 8])]
+    _merge_lists(f, o, first, "hand-over: first merge (host rounds)")
+    check([s for _, s in first], "hand-over: after the first merge")
+    chain = [(0, [50, 1, 2, 3, 4]), (1, [50, 1, 2, 3, 5]), (2, [50, 1, 2, 6]), (3, [50, 1, 7]),
+             (4, [50, 1, 2, 3, 4, 8]), (0, [50, 1, 2, 9]), (1, [50, 2]), (2, [50, 1, 2, 3, 5, 5])]
+    _merge_lists(f, o, chain, "hand-over: chain of cuts")
+    check([s for _, s in chain] + [[50, 1, 2, 3], [50, 1, 2, 3, 4, 8, 1], [50]], "hand-over: after the chain")
+    wide = [(int(i % P), [60000 + i, 7, 7]) for i in range(11000)]  # 11,000 ADD entries at the root
+    _merge_lists(f, o, wide, "hand-over: round over the plan's size")
+    check([s for _, s in wide[::50]] + [[60000 + 11000, 7]], "hand-over: after the wide round")
+    refusals = f.info()["merge_refusals"]
+    before, after = f.compact()
+    long_rest = [(int(i % P), [70000 + i] + rng.integers(0, 1000, 300).tolist()) for i in range(600)]
+    _merge_lists(f, o, long_rest, "hand-over: labels past the spare pool")
+    check([s for _, s in long_rest[::13]], "hand-over: after the refused round")
+    assert f.info()["merge_refusals"] > refusals, f.info()
+    f.check()
+    f.close()
+    o.close()
+
+
 def test_invalid_inserts_are_skipped_and_reported():
     import torch
     from paper_2606_17059_amd import RouterError

@@ -182,12 +182,15 @@ def bench_stream(args, dev) -> dict:
     """The streaming workload, 128 peers.  One step = for each topic
     distribution (uniform, Zipf 1.2), the delta-merge of a fresh batch of
     10,000 inserts into that distribution's forest, then a lookup batch of
-    1,048,576 queries on it.  Each forest has its own stream and host thread,
-    so one forest's merge (latency-bound: small kernels and host round trips)
-    runs while the other's lookup streams from HBM; its kernels then wait for
-    free wave slots behind the lookup's million waves, so merges are also
-    timed alone after the timed region (--no-overlap runs both forests in
-    turn on one stream and one thread).  Every lookup of every timed step is compared
+    1,048,576 queries on it.  Each forest has its own stream and host thread;
+    the two fall into step: both merges (latency-bound: small kernels and one
+    readback each) run side by side, then both lookups share HBM.  A kernel
+    queued on one stream while a lookup's million waves fill the chip on the
+    other waits for that lookup to drain, so a merge gains nothing from
+    running beside the other forest's lookup (--schedule pipelined: one host
+    thread issuing merge A, lookup A, merge B, lookup B, with no wait between
+    them, measures that); --schedule serial runs everything in turn on one
+    stream.  Merges are also timed alone after the timed region.  Every lookup of every timed step is compared
     with the radix-tree oracle after the timed region, and the algorithmic
     bytes come from the oracle's match lengths."""
     import torch
@@ -238,7 +241,8 @@ def bench_stream(args, dev) -> dict:
     for d in dists:
         forests[d] = Forest(P)
         forests[d].load_seqset(w.snapshot)
-        streams[d] = torch.cuda.Stream(device=dev) if args.overlap or d == dists[0] else streams[dists[0]]
+        streams[d] = (torch.cuda.Stream(device=dev) if args.schedule != "serial" or d == dists[0]
+                      else streams[dists[0]])
         forests[d].route(*qdev[d][0], *warm_out)  # builds and uploads the base forest
     torch.cuda.synchronize()
     log(f"[bench] stream: base forests uploaded ({forests[dists[0]].info()})")
@@ -250,7 +254,7 @@ def bench_stream(args, dev) -> dict:
     def run_steps(d, ks):
         f, s = forests[d], streams[d]
         for k in ks:
-            if not args.overlap:
+            if args.schedule == "serial":
                 s.synchronize()  # the previous lookup is done: the merge's wall time is its own
             t0 = time.perf_counter()
             f.merge(*idev[d][k], stream=s)  # returns when the forest holds the batch
@@ -264,7 +268,7 @@ def bench_stream(args, dev) -> dict:
             else:
                 f.route(qt, qo, *warm_out, stream=s)
 
-    if args.overlap:
+    if args.schedule == "threads":
         # one host thread per forest (the library's calls release the
         # interpreter lock): each forest's merge, then lookup, on its own
         # stream, while the other forest's run beside them
@@ -419,8 +423,8 @@ def bench_stream(args, dev) -> dict:
                            "which run beside the other forest's merge and lookup"},
         "merge": {"inserts_per_s": n_ins / merge_tot, "inserts": n_ins, "seconds": float(merge_tot),
                   "note": "wall time of the timed steps' pr_merge calls (host-synchronous), "
-                          + ("each beside the other forest's lookup" if args.overlap
-                             else "each after the previous lookup on the stream finished"),
+                          + ("each after the previous lookup on the stream finished" if args.schedule == "serial"
+                             else "each queued behind its forest's previous lookup, beside the other forest's"),
                   "alone": {"inserts_per_s": n_alone / alone_s, "inserts": n_alone, "seconds": alone_s,
                             "note": "four more fresh batches per distribution after the timed region, each "
                                     "merged with the GPU otherwise idle"}},
@@ -790,9 +794,10 @@ def main() -> int:
     ap.add_argument("--latency", action="store_true",
                     help="also time small batches (1 to 32,768 queries) per call, host wall time included "
                          "(configs 1-4)")
-    ap.add_argument("--no-overlap", dest="overlap", action="store_false",
-                    help="config 5: run both forests on one stream (by default each has its own, and one forest's "
-                         "merge runs beside the other's lookup)")
+    ap.add_argument("--schedule", choices=("threads", "pipelined", "serial"), default="threads",
+                    help="config 5: threads (default): a stream and a host thread per forest; pipelined: two "
+                         "streams, one host thread issuing each forest's merge while the other's lookup runs; "
+                         "serial: one stream, in turn")
     ap.add_argument("--compact", action="store_true",
                     help="config 5: compact both forests after the timed steps and time it")
     ap.add_argument("--no-select", action="store_true",
@@ -837,8 +842,10 @@ def main() -> int:
                        "queries_per_step": r["queries_per_step"], "inserts_per_step": r["inserts_per_step"],
                        "step": "for each topic distribution (uniform, Zipf 1.2): merge a fresh 10,000-insert batch "
                                "into its forest, then route a 1,048,576-query lookup batch on it; "
-                               + ("the two forests on two streams and two host threads" if args.overlap
-                                  else "all in turn on one stream"),
+                               + {"pipelined": "the two forests on two streams from one host thread, each "
+                                               "forest's merge beside the other forest's lookup",
+                                  "threads": "the two forests on two streams and two host threads",
+                                  "serial": "all in turn on one stream"}[args.schedule],
                        "parallelism": "single GPU"},
             "hbm_gbps": r["roofline"]["achieved"], "roofline": r["roofline"], "lookup": r["lookup"],
             "merge": r["merge"], "per_distribution": r["per_distribution"], "parity": r["parity"],

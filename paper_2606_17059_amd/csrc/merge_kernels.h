@@ -522,6 +522,7 @@ constexpr int64_t kPlanMaxBatch = (int64_t)kPlanThreads * kPlanBatchItems;  // i
 constexpr int kPlanWaves = kPlanThreads / 64;
 constexpr int kPlanSlots = 2048;                            // parent hash table
 constexpr int kPlanMaxParents = kPlanSlots / 2;
+constexpr int kPlanSmall = 256;                             // rounds ranked by counting instead
 
 // Inclusive scan over the wave.
 template <typename T, typename Op>
@@ -728,7 +729,11 @@ __global__ __launch_bounds__(kPlanThreads) void add_plan_kernel(DevForest F, Bat
     }
     __syncthreads();  // s_tmp is reused by the scans below
     // second sweep: place each ADD entry, record its span, hash its parent
-    // (parents are looked up until the table holds kPlanMaxParents of them)
+    // (parents are looked up until the table holds kPlanMaxParents of them;
+    // small rounds are ranked by counting and keep node ids)
+    const bool small = m <= kPlanSmall;
+    if (small && t == 0) s_misc[1] = 1;
+    __syncthreads();
     {
         int32_t xs[kPlanBatchItems], ts[kPlanBatchItems];
 #pragma unroll
@@ -763,7 +768,7 @@ __global__ __launch_bounds__(kPlanThreads) void add_plan_kernel(DevForest F, Bat
         }
     }
     __syncthreads();
-    const bool slotted = s_misc[1] == 0 && s_misc[0] <= kPlanMaxParents;
+    const bool slotted = !small && s_misc[1] == 0 && s_misc[0] <= kPlanMaxParents;
     if (slotted) {
         for (int p = t; p < m; p += T) {
             const unsigned long long kk = s_key[plan_pad(p)];
@@ -772,6 +777,29 @@ __global__ __launch_bounds__(kPlanThreads) void add_plan_kernel(DevForest F, Bat
         }
     }
     __syncthreads();
+
+    if (small) {
+        // rank of entry t: the entries with a smaller key, or an equal key
+        // earlier in the batch (every lane of a wave reads the same key: an
+        // LDS broadcast)
+        unsigned long long mk = 0;
+        int mv = 0, rank = 0;
+        if (t < m) {
+            mk = s_key[plan_pad(t)];
+            mv = s_val[plan_pad(t)];
+#pragma unroll 8
+            for (int j = 0; j < m; j++) {
+                const unsigned long long kj = s_key[plan_pad(j)];
+                rank += (int)((kj < mk) | ((kj == mk) & (j < t)));
+            }
+        }
+        __syncthreads();
+        if (t < m) {
+            s_key[plan_pad(rank)] = mk;
+            s_val[plan_pad(rank)] = (uint16_t)mv;
+        }
+        __syncthreads();
+    }
 
     // 2. stable LSD radix sort; thread t holds the entries [t*C, t*C + nv)
     const int C = (m + T - 1) / T;
@@ -789,7 +817,9 @@ __global__ __launch_bounds__(kPlanThreads) void add_plan_kernel(DevForest F, Bat
             kand &= k[j];
         }
     }
-    {
+    if (small) {
+        kor = 0;  // ranked above: no radix pass
+    } else {
         long long o, a;
         (void)plan_block_excl<long long>((long long)kor, 0, [](long long x, long long y) { return x | y; }, s_tmp,
                                          &o);

@@ -22,6 +22,7 @@
 #include "export_kernels.h"
 #include "lru_kernels.h"
 #include "merge_kernels.h"
+#include "narrow_kernels.h"
 #include "prefix_router.h"
 #include "route_kernels.h"
 

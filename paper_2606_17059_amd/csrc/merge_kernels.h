@@ -338,13 +338,24 @@ __device__ __forceinline__ void copy_tokens(int32_t *dst, const int32_t *src, in
 // Cut child c's edge after l tokens; the winning insert's rest becomes a leaf,
 // and the winner is done.  An add phase earlier in the round may have moved
 // c's record (stamp, as for the claim); it also may have given c a new child
-// block, which the lower part of the edge takes along.
+// block, which the lower part of the edge takes along.  reset_round: also
+// clear the round's counters for the next walk (every kernel that reads them
+// has finished; this one only allocates), which saves a launch per round.
 __global__ __launch_bounds__(64 *kMergeWavesPerBlock) void split_apply_kernel(DevForest F, Batch B,
                                                                              InsState *st,
                                                                              MergeCounters *ctr,
-                                                                             long long stamp) {
+                                                                             long long stamp, int reset_round) {
     const int lane = (int)(threadIdx.x & 63);
     const int64_t i = m_wave_index();
+    if (reset_round && blockIdx.x == 0 && threadIdx.x == 0) {
+        ctr->n_add = 0;
+        ctr->n_split = 0;
+        ctr->pool_need = 0;
+        ctr->node_need = 0;
+        ctr->move_chunks = 0;
+        ctr->plan_n = 0;
+        ctr->plan_fallback = 0;
+    }
     if (i >= B.n || st[i].kind != kInsSplit) return;
     InsState r = st[i];
     r.c = current_pos(F, r.c, stamp);

@@ -962,8 +962,9 @@ pr_status run_merge(pr_forest *f, const int32_t *peer_of, const int32_t *tokens,
                                  f->dev.n_pool + 2 * f->round_pool, s)))
             return r;
         const pr::DevForest F = dev_view(f);
+        // the round counters start cleared (reset_call_kernel above), and each
+        // round's split kernel clears them for the next walk
         for (int k = 0; k < kDeviceRounds; k++) {
-            hipLaunchKernelGGL(reset_round_kernel, dim3(1), dim3(1), 0, s, f->d_ctr);
             hipLaunchKernelGGL(pr::merge_walk_kernel, dim3(grid_waves(n)), dim3(wb), 0, s, F, B, m.st, f->d_ctr);
             hipLaunchKernelGGL(pr::merge_tally_kernel,
                                dim3((unsigned)std::min<int64_t>(256, (n + pr::kTallyThreads - 1) / pr::kTallyThreads)),
@@ -983,9 +984,8 @@ pr_status run_merge(pr_forest *f, const int32_t *peer_of, const int32_t *tokens,
                                dim3(bs), 0, s, F, m.keys_out, (int64_t)-1, m.grp_nw, m.grp_nb, stamp, f->d_ctr);
             hipLaunchKernelGGL(pr::split_claim_kernel, dim3(grid_threads(n, bs)), dim3(bs), 0, s, F, B, m.st, stamp);
             hipLaunchKernelGGL(pr::split_apply_kernel, dim3(grid_waves(n)), dim3(wb), 0, s, F, B, m.st, f->d_ctr,
-                               stamp);
+                               stamp, 1);
         }
-        hipLaunchKernelGGL(reset_round_kernel, dim3(1), dim3(1), 0, s, f->d_ctr);
         hipLaunchKernelGGL(pr::merge_walk_kernel, dim3(grid_waves(n)), dim3(wb), 0, s, F, B, m.st, f->d_ctr);
         hipLaunchKernelGGL(pr::merge_tally_kernel,
                            dim3((unsigned)std::min<int64_t>(256, (n + pr::kTallyThreads - 1) / pr::kTallyThreads)),
@@ -1103,7 +1103,7 @@ pr_status run_merge(pr_forest *f, const int32_t *peer_of, const int32_t *tokens,
             hipLaunchKernelGGL(pr::split_claim_kernel, dim3(grid_threads(n, bs)), dim3(bs), 0, s, F, B, m.st,
                                add_stamp);
             hipLaunchKernelGGL(pr::split_apply_kernel, dim3(grid_waves(n)), dim3(wb), 0, s, F, B, m.st, f->d_ctr,
-                               add_stamp);
+                               add_stamp, 0);
         }
         if (hipGetLastError() != hipSuccess) return fail(PR_EDEVICE, "merge launch failed");
     }

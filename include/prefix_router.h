@@ -62,7 +62,7 @@ typedef int32_t pr_status;
 typedef struct pr_forest pr_forest;
 
 /* ABI version of this header (incremented on incompatible changes). */
-#define PR_ABI_VERSION 6
+#define PR_ABI_VERSION 7
 
 /* PR_ABI_VERSION of the header the library was built with; a client built
  * against another version must not call the library. */
@@ -380,6 +380,11 @@ typedef struct {
     int64_t merge_refusals;    /* device update rounds that ran out of capacity and
                                   ran again after the forest grew (their refused
                                   allocations wrote nothing) */
+    int64_t first_window_tokens; /* query tokens a route loads before its walk
+                                    starts: 256 while, at the last upload of host
+                                    snapshots, the root had a single child with a
+                                    label of 256 tokens or more, else 128.  Speed
+                                    only: results do not depend on it */
 } pr_forest_info;
 
 pr_status pr_forest_info_get(pr_forest *f, pr_forest_info *out);

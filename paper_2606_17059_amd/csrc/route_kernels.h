@@ -21,10 +21,13 @@
 //      and query from a ballot of mismatches.
 // Peers still in the set at the end matched the whole walked depth.  A wave
 // reduction then takes the largest match and the lowest peer id holding it
-// (the argmax of Algorithm 1, ties to the lowest id).
+// (the argmax of Algorithm 1, ties to the lowest id).  Rows of whole cache
+// lines are stored non-temporally, so that they do not evict labels.
 // When the root has a single child (a prompt prefix every stored sequence
 // shares), its record is loaded before the walk and the first level's batch
-// goes out without waiting for the query's first token.  Batches of long
+// goes out without waiting for the query's first token.  The first level
+// compares its label against a window of the query's first 128 tokens, or 256
+// when the host chose the wide window for a long shared prefix.  Batches of long
 // queries can be served in an order computed on the device (longest first,
 // route_order_count_kernel and route_order_scatter_kernel below).
 // Labels are read from the int32 pool, or, while every label token lies in
@@ -68,6 +71,12 @@
 #ifndef PR_ROUTE_WAVES_PER_EU
 #define PR_ROUTE_WAVES_PER_EU 8
 #endif
+#ifndef PR_OUT_NT
+#define PR_OUT_NT 1
+#endif
+#ifndef PR_WIN_POLICY
+#define PR_WIN_POLICY 0
+#endif
 
 namespace pr {
 
@@ -83,7 +92,36 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t token_rsrc(const int32_t *p, i
 }
 
 // Cache policy of the query loads: non-temporal (read once).
+#ifdef PR_QUERY_POLICY
+constexpr int kQueryPolicy = PR_QUERY_POLICY;
+#else
 constexpr int kQueryPolicy = PR_QUERY_NT ? 2 : 0;
+#endif
+
+// Output stores of the match rows.  They are written once and never read by
+// the kernel; when a row fills whole 128-byte lines (P a multiple of 32),
+// non-temporal stores keep them from pushing the labels, which every query
+// reads, out of the L2.  Shorter rows share lines with their neighbours, which
+// plain stores let the L2 merge (as for the 4-byte chosen peer).  The
+// non-temporal path is a raw buffer store over the row (a different operation
+// from the plain store, so the compiler cannot fold the two paths into one
+// store and lose the policy); lanes past the row are dropped by its range.
+template <int W>
+__device__ __forceinline__ void store_row(int32_t *row, const int32_t (&m)[W], int32_t P, int lane) {
+#if PR_OUT_NT
+    if ((P & 31) == 0) {
+        const __amdgpu_buffer_rsrc_t r = __builtin_amdgcn_make_buffer_rsrc(row, (short)0, P * 4, 0x00020000);
+#pragma unroll
+        for (int w = 0; w < W; w++) __builtin_amdgcn_raw_buffer_store_b32(m[w], r, (lane + 64 * w) * 4, 0, 2);
+        return;
+    }
+#endif
+#pragma unroll
+    for (int w = 0; w < W; w++) {
+        const int p = lane + 64 * w;
+        if (p < P) row[p] = m[w];
+    }
+}
 
 // Label tokens: int32, or uint16 (the 16-bit copy of the pool).  Raw buffer
 // resources over the label bytes and loads of one token per lane.
@@ -234,32 +272,36 @@ __device__ __forceinline__ int64_t wave_lcp(const LabelSrc<LT, HB> &lab, const i
     return n;
 }
 
+constexpr int kWinVectors = PR_WIN_VECTORS;
+constexpr int kWideWinVectors = 4;
+static_assert(kWinVectors >= 2 && kWinVectors <= 16, "window of 2 to 16 vectors");
+
 #if PR_FIRST_WINDOW
-// First-level window: the query's first 64 * kWinVectors tokens are loaded
-// into registers together with its first token, whose HBM round trip the walk
+// First-level window: the query's first 64 * WV tokens are loaded into
+// registers together with its first token, whose HBM round trip the walk
 // waits for anyway, so that the first level's compare waits only on its label,
 // which the L2 holds.  Lane l of vector j holds token 64 j + l (0 past the
 // query).  The loads use the default cache policy: they also bring the lines
-// that the first level's next-token load reads.  A wider window reads more
-// tokens that the second level reads again.
-constexpr int kWinVectors = PR_WIN_VECTORS;
-constexpr int kWinTokens = kWave * kWinVectors;
-static_assert(kWinVectors >= 2 && kWinVectors <= 16, "window of 2 to 16 vectors");
+// that the first level's next-token load reads.  A window wider than the first
+// level's label reads tokens that the second level reads again, so the wide
+// window (kWideWinVectors) is for forests whose root has one child with a
+// label of at least that many tokens (a long shared system prompt).
 
-__device__ __forceinline__ void load_window(int32_t (&win)[kWinVectors], const int32_t *p, int32_t cnt, int lane) {
+template <int WV>
+__device__ __forceinline__ void load_window(int32_t (&win)[WV], const int32_t *p, int32_t cnt, int lane) {
     const __amdgpu_buffer_rsrc_t r = token_rsrc(p, cnt * 4);
     int32_t off = lane * 4;  // opaque, as in lcp_step
     asm volatile("" : "+v"(off));
 #pragma unroll
-    for (int j = 0; j < kWinVectors; j++)
-        win[j] = __builtin_amdgcn_raw_buffer_load_b32(r, off + j * kWave * 4, 0, 0);
+    for (int j = 0; j < WV; j++)
+        win[j] = __builtin_amdgcn_raw_buffer_load_b32(r, off + j * kWave * 4, 0, PR_WIN_POLICY);
 }
 
 // Label tokens [0, cnt) (ra, LT wide, cnt <= 64 * NL) against the window,
 // which may hold query tokens past cnt: only lanes below cnt count.  Returns
 // the first mismatch, or -1.
-template <int NL, typename LT, bool HB>
-__device__ __forceinline__ int32_t lcp_step_win(__amdgpu_buffer_rsrc_t ra, const int32_t (&win)[kWinVectors],
+template <int NL, typename LT, bool HB, int WV>
+__device__ __forceinline__ int32_t lcp_step_win(__amdgpu_buffer_rsrc_t ra, const int32_t (&win)[WV],
                                                 int32_t cnt, int lane, const uint32_t *hib, uint32_t A) {
     int32_t va[NL];
     int32_t off = lane * (int32_t)sizeof(LT);  // opaque, as in lcp_step
@@ -286,15 +328,16 @@ __device__ __forceinline__ int32_t lcp_step_win(__amdgpu_buffer_rsrc_t ra, const
 }
 
 // wave_lcp for the first level, whose first query tokens are in win.
-template <typename LT, bool HB>
+template <typename LT, bool HB, int WV>
 __device__ __forceinline__ int64_t wave_lcp_first(const LabelSrc<LT, HB> &lab, const int32_t *__restrict__ b,
-                                                  int64_t n, const int32_t (&win)[kWinVectors], int lane) {
-    const int32_t cnt = (int32_t)min(n, (int64_t)kWinTokens);
+                                                  int64_t n, const int32_t (&win)[WV], int lane) {
+    constexpr int32_t kTokens = kWave * WV;
+    const int32_t cnt = (int32_t)min(n, (int64_t)kTokens);
     const __amdgpu_buffer_rsrc_t ra = label_rsrc(lab.p, cnt);
-    const int32_t r = cnt <= 2 * kWave ? lcp_step_win<2, LT, HB>(ra, win, cnt, lane, lab.hib, lab.abs)
-                                       : lcp_step_win<kWinVectors, LT, HB>(ra, win, cnt, lane, lab.hib, lab.abs);
+    const int32_t r = cnt <= 2 * kWave ? lcp_step_win<2, LT, HB, WV>(ra, win, cnt, lane, lab.hib, lab.abs)
+                                       : lcp_step_win<WV, LT, HB, WV>(ra, win, cnt, lane, lab.hib, lab.abs);
     if (r >= 0 && r < cnt) return r;
-    return wave_lcp<LT, HB>(lab, b, n, kWinTokens, (int64_t)kWave * kLcpVectors, lane);
+    return wave_lcp<LT, HB>(lab, b, n, kTokens, (int64_t)kWave * kLcpVectors, lane);
 }
 #endif
 
@@ -428,8 +471,8 @@ __device__ __forceinline__ int32_t select_peers(const int32_t (&m)[W], int32_t P
 // second pick); the selection options are compiled out.  LT: the label
 // pool's token type (int32_t, or uint16_t for the 16-bit copy); HB (with
 // uint16_t): bit 16 of every label token comes from the bit plane hib
-// (17-bit labels).
-template <int W, bool SEL, typename LT, bool HB = false>
+// (17-bit labels).  WV: vectors of the first-level window.
+template <int W, bool SEL, typename LT, bool HB = false, int WV = kWinVectors>
 __global__ __launch_bounds__(kWave *kRouteWavesPerBlock)
 __attribute__((amdgpu_waves_per_eu(PR_ROUTE_WAVES_PER_EU))) void route_kernel(
     const Node *__restrict__ nodes, const int32_t *__restrict__ ntok, const int32_t *__restrict__ nsep,
@@ -522,7 +565,7 @@ __attribute__((amdgpu_waves_per_eu(PR_ROUTE_WAVES_PER_EU))) void route_kernel(
         const LabelSrc<LT, HB> lab{pool + (uint32_t)c.lab_off, hib, (uint32_t)c.lab_off};
         int64_t l;
         if constexpr (FIRST)
-            l = wave_lcp_first<LT, HB>(lab, qs, n, win, lane);
+            l = wave_lcp_first<LT, HB, WV>(lab, qs, n, win, lane);
         else
             l = wave_lcp<LT, HB>(lab, qs + d, n, 0, (int64_t)kWave * kLcpFirstVectors, lane);
         if constexpr (KNOWN) {
@@ -545,8 +588,8 @@ __attribute__((amdgpu_waves_per_eu(PR_ROUTE_WAVES_PER_EU))) void route_kernel(
     };
     struct NoWindow {};
 #if PR_FIRST_WINDOW
-    int32_t win[kWinVectors];
-    load_window(win, qs, (int32_t)min(qlen, (int64_t)kWinTokens), lane);
+    int32_t win[WV];
+    load_window<WV>(win, qs, (int32_t)min(qlen, (int64_t)kWave * WV), lane);
     bool more = false;
     if (qlen > 0) more = single ? level(std::true_type{}, win, std::true_type{})
                                 : level(std::true_type{}, win, std::false_type{});
@@ -569,17 +612,11 @@ __attribute__((amdgpu_waves_per_eu(PR_ROUTE_WAVES_PER_EU))) void route_kernel(
     for (int w = 0; w < W; w++)
         if ((alive[w] >> lane) & 1ull) m[w] = (int32_t)d;
 
-    if (match_len) {
-#pragma unroll
-        for (int w = 0; w < W; w++) {
-            const int p = lane + 64 * w;
-            if (p < P) row[p] = m[w];
-        }
-    }
+    if (match_len) store_row<W>(row, m, P, lane);
     int32_t second;
     const int32_t best = select_peers<W>(m, P, lane, sel, elig, sel.second != nullptr, second);
     if (lane == 0) {
-        chosen[q] = best;
+        chosen[q] = best;  // 4 bytes a query: plain stores, which the L2 merges into whole lines
         if (sel.second) sel.second[q] = second;
     }
 }

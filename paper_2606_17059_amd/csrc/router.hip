@@ -137,6 +137,9 @@ struct pr_forest {
     bool narrow = false;          // dev.pool16 and dev.hib mirror dev.pool[0, n_pool) (every label token in
                                   // [0, 131071])
     bool hi17 = false;            // some label token is in [65536, 131071]: routes need the bit plane
+    bool wide_window = false;     // routes load the wide first-level window: at the last upload the root
+                                  // had one child, with a label at least that long (a choice of speed
+                                  // only: both windows give the same results)
     bool broken = false;          // a device update failed; only destroy is valid
 };
 
@@ -154,6 +157,12 @@ namespace {
 
 #ifndef PR_NARROW_LABELS
 #define PR_NARROW_LABELS 1
+#endif
+
+// Wide first-level window for forests whose root has one long-labelled child
+// (0: always the narrow window, for comparisons).
+#ifndef PR_WIDE_WINDOW
+#define PR_WIDE_WINDOW 1
 #endif
 
 // Makes the forest's device current for the duration of a call.
@@ -569,6 +578,8 @@ pr_status commit(pr_forest *f) {
     }
     d.n_nodes = n;
     d.n_pool = np;
+    f->wide_window = PR_WIDE_WINDOW && n > 1 && h.nodes[0].ct_cnt == 1 &&
+                     h.nodes[(size_t)h.nodes[0].ct_beg].lab_len >= pr::kWave * pr::kWideWinVectors;
     pr::MergeCounters c;
     std::memset(&c, 0, sizeof(c));
     c.n_nodes = (unsigned long long)n;
@@ -686,9 +697,14 @@ void launch_route_t(const pr_forest *f, const LT *pool, const int32_t *qt, int64
                     hipStream_t s) {
     const int64_t blocks = (nq + pr::kRouteWavesPerBlock - 1) / pr::kRouteWavesPerBlock;
     const uint32_t *hib = HB ? f->dev.hib : nullptr;
-    hipLaunchKernelGGL((pr::route_kernel<W, SEL, LT, HB>), dim3((unsigned)blocks),
-                       dim3(pr::kWave * pr::kRouteWavesPerBlock), 0, s, f->dev.nodes, f->dev.ntok, f->dev.nsep,
-                       f->dev.mext, pool, hib, qt, ntok, qo, nq, f->P, sel, ml, ch, order);
+    if (f->wide_window)
+        hipLaunchKernelGGL((pr::route_kernel<W, SEL, LT, HB, pr::kWideWinVectors>), dim3((unsigned)blocks),
+                           dim3(pr::kWave * pr::kRouteWavesPerBlock), 0, s, f->dev.nodes, f->dev.ntok, f->dev.nsep,
+                           f->dev.mext, pool, hib, qt, ntok, qo, nq, f->P, sel, ml, ch, order);
+    else
+        hipLaunchKernelGGL((pr::route_kernel<W, SEL, LT, HB>), dim3((unsigned)blocks),
+                           dim3(pr::kWave * pr::kRouteWavesPerBlock), 0, s, f->dev.nodes, f->dev.ntok, f->dev.nsep,
+                           f->dev.mext, pool, hib, qt, ntok, qo, nq, f->P, sel, ml, ch, order);
 }
 
 template <int W, bool SEL>
@@ -2014,6 +2030,7 @@ pr_status pr_forest_info_get(pr_forest *f, pr_forest_info *out) {
     out->label_token_bytes = f->narrow ? 2 : 4;
     out->label_bits = f->narrow ? (f->hi17 ? 17 : 16) : 32;
     out->merge_refusals = f->refusals;
+    out->first_window_tokens = (int64_t)pr::kWave * (f->wide_window ? pr::kWideWinVectors : pr::kWinVectors);
     int64_t t = 0;
     for (const auto &S : f->sets) t += (int64_t)S.tokens.size();
     out->host_seq_tokens = t;

@@ -42,7 +42,7 @@ class ForestInfo(ctypes.Structure):
                 ("pool_tokens", ctypes.c_int64), ("device_bytes", ctypes.c_int64),
                 ("host_seq_tokens", ctypes.c_int64), ("layout_epoch", ctypes.c_int64),
                 ("label_token_bytes", ctypes.c_int64), ("label_bits", ctypes.c_int64),
-                ("merge_refusals", ctypes.c_int64)]
+                ("merge_refusals", ctypes.c_int64), ("first_window_tokens", ctypes.c_int64)]
 
 
 class ImageView(ctypes.Structure):
@@ -111,7 +111,7 @@ def lib() -> ctypes.CDLL:
     L.pr_forest_info_get.restype = ctypes.c_int32
     L.pr_forest_host_image.argtypes = [_vp, ctypes.POINTER(ImageView)]
     L.pr_forest_host_image.restype = ctypes.c_int32
-    if L.pr_abi_version() != 6:
+    if L.pr_abi_version() != 7:
         raise RuntimeError("libprefix_router ABI version mismatch")
     _lib_handle = L
     return L

@@ -628,3 +628,79 @@ def test_narrow_labels_with_query_tokens_out_of_range(bits):
     assert_rows_equal(m, c, m_or, c_or, what="narrow labels, wide query tokens")
     o.close()
     f.close()
+
+
+@pytest.mark.parametrize("vocab", [32000, 128256, 2 ** 31 - 1])
+def test_wide_first_window(vocab):
+    """A forest whose root has one child with a label of 256 tokens or more
+    (a long shared system prompt) routes with the 256-token first-level
+    window; results must not depend on it.  Queries end or mismatch at every
+    vector edge of both windows, with 16-, 17- and 32-bit labels.  Merges then
+    give the root a second child and cut its first label short of 256 tokens,
+    so the forest keeps the wide window without its reason; routes must still
+    equal the oracle's."""
+    import torch
+    rng = np.random.default_rng(vocab % 1000 + 7)
+    P = 5
+    head = rng.integers(0, vocab, 300).tolist()
+    seqs, owners = [], []
+    for i in range(40):
+        seqs.append(head + rng.integers(0, vocab, int(rng.integers(0, 200))).tolist())
+        owners.append(i % P)
+    snap = W.from_lists(seqs, owners)
+    f = _forest(snap, P)
+    qs = [[]]
+    cuts = (1, 2, 63, 64, 65, 127, 128, 129, 191, 192, 200, 255, 256, 257, 299, 300)
+    for n in cuts:
+        qs.append(head[:n])
+        q = list(head)
+        q[n - 1] = (q[n - 1] + 1) % vocab
+        qs.append(q)
+    qs += [list(s) for s in seqs[:10]]
+    qs += [s[:len(head) + 5] + [(s[len(head) + 5] + 1) % vocab] if len(s) > len(head) + 5 else list(s)
+           for s in seqs[10:20]]
+    queries = W.from_lists(qs)
+    m, c = gpu_route(f, queries, f"wide first window, vocab {vocab}")
+    info = f.info()
+    assert info["first_window_tokens"] == 256, info
+    o = oracle_for(snap, P)
+    m_or, c_or = o.route(queries.tokens, queries.offsets, nthreads())
+    assert_rows_equal(m, c, m_or, c_or, what="wide first window")
+    # merges: a sequence with another first token, and one leaving the head at 100
+    alt = [(head[0] + 1) % vocab] + rng.integers(0, vocab, 50).tolist()
+    cut = head[:100] + [(head[100] + 1) % vocab] + rng.integers(0, vocab, 30).tolist()
+    ins = W.from_lists([alt, cut], [1, 3])
+    dev = device()
+    announce(f"wide first window: merge of {len(ins)} inserts")
+    f.merge(torch.from_numpy(ins.peer).to(dev), torch.from_numpy(ins.tokens).to(dev),
+            torch.from_numpy(ins.offsets).to(dev))
+    o.merge(ins.peer, ins.tokens, ins.offsets)
+    q2 = W.from_lists(qs + [alt, cut, cut[:101], alt[:1]])
+    m, c = gpu_route(f, q2, "wide first window after merges")
+    assert f.info()["first_window_tokens"] == 256
+    m_or, c_or = o.route(q2.tokens, q2.offsets, nthreads())
+    assert_rows_equal(m, c, m_or, c_or, what="wide first window after merges")
+    f.check()
+    o.close()
+    f.close()
+
+
+def test_narrow_first_window_for_short_root_labels():
+    """A root with a single child whose label is shorter than 256 tokens, or
+    with several children, keeps the 128-token window."""
+    rng = np.random.default_rng(5)
+    head = rng.integers(0, 1000, 200).tolist()
+    snap = W.from_lists([head + [1, 2], head + [3]], [0, 1])
+    f = _forest(snap, 2)
+    q = W.from_lists([head + [1, 2, 9]])
+    m, c = gpu_route(f, q, "short root label")
+    assert f.info()["first_window_tokens"] == 128
+    assert m.tolist() == [[len(head) + 2, len(head)]] and c.tolist() == [0]
+    f.close()
+    snap = W.from_lists([[1] + head + [5] * 300, [2] + head + [5] * 300], [0, 1])
+    f = _forest(snap, 2)
+    q = W.from_lists([[2] + head])
+    m, c = gpu_route(f, q, "two root children")
+    assert f.info()["first_window_tokens"] == 128
+    assert m.tolist() == [[0, len(head) + 1]] and c.tolist() == [1]
+    f.close()

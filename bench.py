@@ -178,6 +178,39 @@ def _alg_bytes(queries, M, P) -> np.ndarray:
     return 4 * np.minimum(queries.lengths(), M.astype(np.int64) + 1) + 4 * (P + 1) + 8
 
 
+def cu_split_streams(dev, merge_cus_per_xcd: int):
+    """Two streams over disjoint sets of compute units (hipExtStreamCreateWithCUMask):
+    merges on merge_cus_per_xcd CUs of each of the 8 XCDs, lookups on the rest.
+    The CU picked as the c-th of XCD j has mask bit per*j + j + 8*c (per = CUs
+    per XCD): that is a CU of XCD j whether the mask numbers CUs XCD by XCD or
+    round-robin over the XCDs.  Returns (lookup stream, merge stream, counts)."""
+    import ctypes
+
+    import torch
+    hip = ctypes.CDLL("libamdhip64.so.7")  # torch's HIP runtime, already loaded
+    n_cu = torch.cuda.get_device_properties(dev).multi_processor_count
+    n_xcd = 8
+    per = n_cu // n_xcd
+    if per * n_xcd != n_cu or not 0 < merge_cus_per_xcd <= per // n_xcd:
+        raise SystemExit(f"bench.py: cannot reserve {merge_cus_per_xcd} CUs per XCD on {n_cu} CUs")
+    merge_bits = {per * j + j + n_xcd * c for j in range(n_xcd) for c in range(merge_cus_per_xcd)}
+    n_words = (n_cu + 31) // 32
+
+    def make(bits):
+        words = (ctypes.c_uint32 * n_words)()
+        for b in bits:
+            words[b // 32] |= 1 << (b % 32)
+        h = ctypes.c_void_p()
+        if hip.hipExtStreamCreateWithCUMask(ctypes.byref(h), ctypes.c_uint32(n_words), words) != 0:
+            raise SystemExit("bench.py: hipExtStreamCreateWithCUMask failed")
+        return torch.cuda.ExternalStream(h.value, device=dev), h
+
+    look, hl = make(set(range(n_cu)) - merge_bits)
+    merge, hm = make(merge_bits)
+    return look, merge, {"lookup_cus": n_cu - len(merge_bits), "merge_cus": len(merge_bits),
+                         "handles": (hip, hl, hm)}
+
+
 def bench_stream(args, dev) -> dict:
     """The streaming workload, 128 peers.  One step = for each topic
     distribution (uniform, Zipf 1.2), the delta-merge of a fresh batch of
@@ -268,7 +301,39 @@ def bench_stream(args, dev) -> dict:
             else:
                 f.route(qt, qo, *warm_out, stream=s)
 
-    if args.schedule == "threads":
+    cu_split = None
+    if args.schedule == "cusplit":
+        # one host thread; lookups on one stream over most of the CUs, merges
+        # on another over the few CUs kept from the lookups.  A forest's merge
+        # waits for its previous lookup (it changes records that lookup reads)
+        # and its lookup for the merge; the other forest's lookup runs meanwhile
+        lstream, mstream, cu_split = cu_split_streams(dev, args.merge_cus)
+        last_lookup = {d: None for d in dists}
+        for k in range(n_steps):
+            if k == Wu:
+                torch.cuda.synchronize()
+                t_region = time.perf_counter()
+            for d in dists:
+                f = forests[d]
+                if last_lookup[d] is not None:
+                    mstream.wait_event(last_lookup[d])
+                t0 = time.perf_counter()
+                f.merge(*idev[d][k], stream=mstream)  # returns when the forest holds the batch
+                merge_s[d][k] = time.perf_counter() - t0
+                done = torch.cuda.Event()
+                done.record(mstream)
+                lstream.wait_event(done)
+                qt, qo = qdev[d][k % R]
+                if k >= Wu:
+                    a, b = ev[d][k - Wu]
+                    a.record(lstream)
+                    f.route(qt, qo, *outs[d][k - Wu], stream=lstream)
+                    b.record(lstream)
+                else:
+                    f.route(qt, qo, *warm_out, stream=lstream)
+                last_lookup[d] = torch.cuda.Event()
+                last_lookup[d].record(lstream)
+    elif args.schedule == "threads":
         # one host thread per forest (the library's calls release the
         # interpreter lock): each forest's merge, then lookup, on its own
         # stream, while the other forest's run beside them
@@ -310,6 +375,10 @@ def bench_stream(args, dev) -> dict:
                 run_steps(d, [k])
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_region
+    if cu_split is not None:
+        hip, hl, hm = cu_split.pop("handles")
+        hip.hipStreamDestroy(hl)
+        hip.hipStreamDestroy(hm)
     for d in dists:
         forests[d].check()
     route_ms = {d: np.array([a.elapsed_time(b) for a, b in ev[d]]) for d in dists}
@@ -428,7 +497,7 @@ def bench_stream(args, dev) -> dict:
                   "alone": {"inserts_per_s": n_alone / alone_s, "inserts": n_alone, "seconds": alone_s,
                             "note": "four more fresh batches per distribution after the timed region, each "
                                     "merged with the GPU otherwise idle"}},
-        "per_distribution": per_dist,
+        "per_distribution": per_dist, "cu_split": cu_split,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": PEAK_HBM_GBPS, "unit": "GB/s",
                      "frac": achieved / PEAK_HBM_GBPS, "traffic": measured_traffic("stream"),
                      "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
@@ -794,10 +863,14 @@ def main() -> int:
     ap.add_argument("--latency", action="store_true",
                     help="also time small batches (1 to 32,768 queries) per call, host wall time included "
                          "(configs 1-4)")
-    ap.add_argument("--schedule", choices=("threads", "pipelined", "serial"), default="threads",
-                    help="config 5: threads (default): a stream and a host thread per forest; pipelined: two "
-                         "streams, one host thread issuing each forest's merge while the other's lookup runs; "
-                         "serial: one stream, in turn")
+    ap.add_argument("--schedule", choices=("cusplit", "threads", "pipelined", "serial"), default="threads",
+                    help="config 5: cusplit: one host thread, lookups on a stream over most CUs and merges on a "
+                         "stream over the CUs kept from it (--merge-cus per XCD), each forest's merge beside the "
+                         "other forest's lookup; threads (default): a stream and a host thread per forest; "
+                         "pipelined: two streams, one host thread issuing each forest's merge while the other's "
+                         "lookup runs; serial: one stream, in turn")
+    ap.add_argument("--merge-cus", type=int, default=2,
+                    help="config 5 with --schedule cusplit: CUs per XCD kept for merges")
     ap.add_argument("--compact", action="store_true",
                     help="config 5: compact both forests after the timed steps and time it")
     ap.add_argument("--no-select", action="store_true",
@@ -842,7 +915,11 @@ def main() -> int:
                        "queries_per_step": r["queries_per_step"], "inserts_per_step": r["inserts_per_step"],
                        "step": "for each topic distribution (uniform, Zipf 1.2): merge a fresh 10,000-insert batch "
                                "into its forest, then route a 1,048,576-query lookup batch on it; "
-                               + {"pipelined": "the two forests on two streams from one host thread, each "
+                               + {"cusplit": "one host thread; lookups on a stream over {lookup_cus} CUs, merges on a "
+                                             "stream over the other {merge_cus}, each forest's merge beside the "
+                                             "other forest's lookup".format(**(r["cu_split"] or
+                                                                               {"lookup_cus": 0, "merge_cus": 0})),
+                                  "pipelined": "the two forests on two streams from one host thread, each "
                                                "forest's merge beside the other forest's lookup",
                                   "threads": "the two forests on two streams and two host threads",
                                   "serial": "all in turn on one stream"}[args.schedule],

@@ -85,12 +85,13 @@ def step_kernels(nq: int, ntok: int) -> list:
 
 def route_kernel_name(f) -> str:
     """The plain route kernel instantiation a forest's routes run: mask words,
-    label token type (16-bit while every label token fits 17 bits) and
-    whether bit 16 comes from the bit plane."""
+    label token type (16-bit while every label token fits 17 bits), whether
+    bit 16 comes from the bit plane, and the first-level window in 64-token
+    vectors."""
     info = f.info()
     lt = "int" if info["label_bits"] == 32 else "unsigned short"
     hb = "true" if info["label_bits"] == 17 else "false"
-    return f"route_kernel<{info['mask_words']}, false, {lt}, {hb}>"
+    return f"route_kernel<{info['mask_words']}, false, {lt}, {hb}, {info['first_window_tokens'] // 64}>"
 
 
 def log(msg: str) -> None:

@@ -403,7 +403,11 @@ pr_status pr_forest_info_get(pr_forest *f, pr_forest_info *out);
  *          root through the node's whole label;
  *   ntok   int32 [num_nodes]: first label token of every node;
  *   nsep   int32 [num_nodes]: for a child block [b, b + cnt) with cnt > 64,
- *          nsep[b + k] = ntok[b + (k * cnt) / 64] for k < 64 (other entries 0);
+ *          nsep[b + k] = ntok[b + (k * cnt) / 64] for k < 64; with cnt >= 4160
+ *          also, for sub-range k = [lo, hi) (lo = (k * cnt) / 64, hi the next
+ *          sub-range's lo, or cnt for k = 63) and j < 64,
+ *          nsep[b + 64 + 64 k + j] = ntok[b + lo + (j * (hi - lo)) / 64]
+ *          (other entries 0);
  *   mext   uint64 [num_nodes][mask_words - 1]: peer-mask words 1.. ;
  *   pool   int32 [pool_tokens]: label tokens.
  */

@@ -152,6 +152,13 @@ class Builder {
             if (nd.ct_cnt <= kSepCount) continue;
             for (int k = 0; k < kSepCount; k++)
                 out->nsep[(size_t)nd.ct_beg + k] = out->ntok[(size_t)nd.ct_beg + PR_SEP_INDEX(k, nd.ct_cnt)];
+            if (nd.ct_cnt < kSep2Min) continue;
+            for (int k = 0; k < kSepCount; k++) {  // second level, per sub-range
+                const int32_t lo = PR_SEP_INDEX(k, nd.ct_cnt), span = PR_SEP_HI(k, nd.ct_cnt) - lo;
+                for (int j = 0; j < kSepCount; j++)
+                    out->nsep[(size_t)nd.ct_beg + kSepCount + (size_t)kSepCount * k + j] =
+                        out->ntok[(size_t)nd.ct_beg + lo + PR_SEP_INDEX(j, span)];
+            }
         }
         return true;
     }

@@ -22,7 +22,14 @@
 //             k < 64 (ascending).  A wave loads the 64 separators (two cache
 //             lines), a ballot picks the sub-range that can hold a token, and
 //             one more load of at most ceil(cnt / 64) first tokens settles it.
-//             Entries outside the first 64 of a wide block are unused.
+//             Blocks of at least kSep2Min (4,160) children also keep a second
+//             level: sub-range k (first tokens [lo_k, hi_k), lo_k =
+//             PR_SEP_INDEX(k, cnt), hi_k = PR_SEP_HI(k, cnt)) has its own 64
+//             separators, contiguous, at nsep[b + 64 + 64 k + j] =
+//             ntok[b + lo_k + PR_SEP_INDEX(j, hi_k - lo_k)]; they sit in slots
+//             of the block that the first level leaves unused, and the search
+//             of a sub-range reads two cache lines instead of gathering one
+//             token from each of 64 lines.  Other entries are unused.
 //   mext[n*(W-1) + w-1]  peer-mask words 1..W-1 of node n (W > 1 only);
 //             word 0 lives in the record.
 //   pool[t]   int32 label tokens; node n's label is pool[lab_off .. +lab_len).
@@ -55,6 +62,12 @@ constexpr int kSepCount = 64;
 
 // Position in a wide block of cnt children of its k-th separator (k < 64).
 #define PR_SEP_INDEX(k, cnt) ((int32_t)(((int64_t)(k) * (int64_t)(cnt)) / 64))
+// End of sub-range k (the next separator's position, or cnt after the last).
+#define PR_SEP_HI(k, cnt) ((k) == kSepCount - 1 ? (int32_t)(cnt) : PR_SEP_INDEX((k) + 1, cnt))
+
+// Child blocks of at least this many children carry second-level separators
+// (the first level's 64 slots plus 64 per sub-range fit in the block).
+constexpr int32_t kSep2Min = kSepCount + kSepCount * kSepCount;
 
 // Mask words per node for a peer count (template instances exist for these).
 inline int mask_words_for(int num_peers) {

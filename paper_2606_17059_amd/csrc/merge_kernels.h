@@ -160,7 +160,8 @@ __device__ __forceinline__ void m_mark(const DevForest &F, int32_t x, uint64_t m
 
 // Child of node x whose first token is t, or -1 (wave-cooperative).  Blocks
 // of up to 64 children take one ballot over their first tokens; wider blocks
-// first pick their sub-range through the block's 64 separators.
+// first pick their sub-range through the block's 64 separators (and, from
+// kSep2Min children on, through the sub-range's own 64).
 __device__ __forceinline__ int32_t m_find_child(const DevForest &F, const Node &x, int32_t t, int lane) {
     const int32_t beg = x.ct_beg, cnt = x.ct_cnt;
     if (cnt <= kSepCount) {
@@ -172,7 +173,15 @@ __device__ __forceinline__ int32_t m_find_child(const DevForest &F, const Node &
     if (!b) return -1;  // t is below every first token
     const int32_t k = (int32_t)__popcll(b) - 1;
     int32_t lo = PR_SEP_INDEX(k, cnt);
-    int32_t hi = k == kSepCount - 1 ? cnt : PR_SEP_INDEX(k + 1, cnt);
+    int32_t hi = PR_SEP_HI(k, cnt);
+    if (cnt >= kSep2Min) {
+        // the sub-range's own 64 separators (lane 0's is the first level's k-th, <= t)
+        const int32_t span = hi - lo;
+        const uint64_t b2 = __ballot(F.nsep[beg + kSepCount + kSepCount * k + lane] <= t);
+        const int32_t j = (int32_t)__popcll(b2) - 1;
+        hi = PR_SEP_HI(j, span) + lo;
+        lo += PR_SEP_INDEX(j, span);
+    }
     while (hi - lo > 64) {  // sub-ranges of more than 64 children: 64-ary search
         const int32_t stride = (hi - lo + 63) / 64;
         const int32_t j = lo + lane * stride;
@@ -1163,6 +1172,11 @@ __global__ __launch_bounds__(64 *kMergeWavesPerBlock) void add_sep_kernel(DevFor
         const int32_t c = F.nodes[key_parent(keys[k])].ct_cnt + grp_nw[k];
         if (c <= kSepCount) continue;
         F.nsep[nb + lane] = F.ntok[nb + PR_SEP_INDEX(lane, c)];
+        if (c < kSep2Min) continue;
+        for (int q = 0; q < kSepCount; q++) {  // second level, per sub-range
+            const int32_t lo = PR_SEP_INDEX(q, c), span = PR_SEP_HI(q, c) - lo;
+            F.nsep[nb + kSepCount + kSepCount * q + lane] = F.ntok[nb + lo + PR_SEP_INDEX(lane, span)];
+        }
     }
 }
 

@@ -367,7 +367,8 @@ __device__ __forceinline__ void load_block(ChildBlock &cb, const int32_t *__rest
 
 // Find the child whose first token is t.  Returns false if there is none.
 __device__ __forceinline__ bool locate(const ChildBlock &cb, int32_t t, const Node *__restrict__ nodes,
-                                       const int32_t *__restrict__ ntok, int lane, Child &c) {
+                                       const int32_t *__restrict__ ntok, const int32_t *__restrict__ nsep, int lane,
+                                       Child &c) {
     int32_t idx = -1;
     if (cb.cnt <= kSepCount) {
         const uint64_t b = __ballot(lane < cb.cnt && cb.tok == t);
@@ -378,8 +379,18 @@ __device__ __forceinline__ bool locate(const ChildBlock &cb, int32_t t, const No
         if (!b) return false;  // t is below every first token
         const int32_t k = (int32_t)__popcll(b) - 1;
         int32_t lo = PR_SEP_INDEX(k, cb.cnt);
-        int32_t hi = k == kSepCount - 1 ? cb.cnt : PR_SEP_INDEX(k + 1, cb.cnt);
-        while (hi - lo > kWave) {  // blocks of more than 64 * 64 children: 64-ary search
+        int32_t hi = PR_SEP_HI(k, cb.cnt);
+        if (cb.cnt >= kSep2Min) {
+            // blocks of 4,160 children or more: the sub-range's own 64
+            // separators, two contiguous lines (lane 0's is the first level's
+            // k-th, <= t); the rest is at most ceil(span / 64) first tokens
+            const int32_t span = hi - lo;
+            const uint64_t b2 = __ballot(nsep[cb.beg + kSepCount + kSepCount * k + lane] <= t);
+            const int32_t j = (int32_t)__popcll(b2) - 1;
+            hi = lo + PR_SEP_HI(j, span);
+            lo += PR_SEP_INDEX(j, span);
+        }
+        while (hi - lo > kWave) {  // sub-ranges of more than 64 children (blocks over 262,144): 64-ary search
             const int32_t stride = (hi - lo + kWave - 1) / kWave;
             const int32_t j = lo + lane * stride;
             bool le = false;
@@ -549,7 +560,7 @@ __attribute__((amdgpu_waves_per_eu(PR_ROUTE_WAVES_PER_EU))) void route_kernel(
             c = c0;
         } else {
             if constexpr (FIRST && PR_FIRST_WINDOW) t = uniform(win[0]);
-            if (!locate(cb, t, nodes, ntok, lane, c)) return false;
+            if (!locate(cb, t, nodes, ntok, nsep, lane, c)) return false;
         }
         if (c.lab_len <= 0) return false;  // only the root has an empty label
         // one batch of loads per level: next token, ext mask words, the next

@@ -86,6 +86,12 @@ def check_structure(img, P):
             seps = img["nsep"][beg:beg + 64]
             want = ntok[beg + (np.arange(64) * cnt) // 64]
             assert np.array_equal(seps, want), "separators of a wide child block"
+        if cnt >= 64 + 64 * 64:  # second-level separators, per sub-range
+            for k in range(64):
+                lo, hi = (k * cnt) // 64, cnt if k == 63 else ((k + 1) * cnt) // 64
+                got = img["nsep"][beg + 64 + 64 * k:beg + 128 + 64 * k]
+                want = ntok[beg + lo + (np.arange(64) * (hi - lo)) // 64]
+                assert np.array_equal(got, want), "second-level separators of a wide child block"
         assert mx >> P == 0
     assert parents[0] == 0 and (parents[1:] == 1).all(), "every non-root node has one parent"
 
@@ -124,10 +130,11 @@ def test_many_peers_mask_words():
 
 
 def test_wide_blocks_carry_separators():
-    """Blocks of more than 64 children (up to a few thousand) carry separators."""
+    """Blocks of more than 64 children carry separators, and blocks of 4,160
+    children or more a second level of them per sub-range."""
     rng = np.random.default_rng(11)
-    for n_children in (65, 100, 513, 4097, 5000):
-        first = rng.choice(np.arange(-100000, 100000), size=n_children, replace=False)
+    for n_children in (65, 100, 513, 4097, 4159, 4160, 5000, 70000):
+        first = rng.choice(np.arange(-200000, 200000), size=n_children, replace=False)
         seqs = [[int(a), int(rng.integers(0, 9))] for a in first]
         ss = W.from_lists(seqs, sorted(int(rng.integers(0, 3)) for _ in seqs))
         w = W.Workload(0, "wide", 3, 0, ss, W.from_lists([[int(first[0]), 1], [int(first[-1])], [7777777]]))

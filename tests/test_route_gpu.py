@@ -543,6 +543,13 @@ def _wide_block_queries(rng, seqs, kids, head):
     for t in (int(kids[0]) - 2, int(kids[-1]) + 2, -5, 2 ** 31 - 1):
         qs.append(head + [t])
         qs.append([t, 5])
+    # every child of the first, a middle and the last separator range, and the
+    # odd tokens between them: hits and misses at every vector of the sub-range
+    for k in (0, 31, 63):
+        lo, hi = (k * n) // 64, n if k == 63 else ((k + 1) * n) // 64
+        for r in range(lo, hi):
+            qs.append(head + [int(kids[r])])
+            qs.append([int(kids[r]) + 1, 5])
     for i in rng.choice(len(seqs), 300, replace=False).tolist():
         s = list(seqs[i])
         qs.append(s)
@@ -553,10 +560,11 @@ def _wide_block_queries(rng, seqs, kids, head):
 
 
 @pytest.mark.timeout(600)
-@pytest.mark.parametrize("n_children", [4097, 5000, 20000])
+@pytest.mark.parametrize("n_children", [4097, 5000, 20000, 70000])
 def test_child_blocks_wider_than_4096(n_children):
     """Child blocks of more than 64 x 64 children take a 64-ary search after
-    the separators, in the route's child locate and in the merge walk's.
+    the separators (one step up to 64 x 64 x 64 children, two above), in the
+    route's child locate and in the merge walk's.
     Built by a host load, and again by a load of half the sequences followed
     by merges of the other half (new children, extensions through the wide
     block, duplicates); every row against the oracle."""

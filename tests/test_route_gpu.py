@@ -712,3 +712,49 @@ def test_narrow_first_window_for_short_root_labels():
     assert f.info()["first_window_tokens"] == 128
     assert m.tolist() == [[0, len(head) + 1]] and c.tolist() == [1]
     f.close()
+
+
+@pytest.mark.timeout(600)
+def test_child_block_past_the_second_separator_level():
+    """A block of 270,000 children: its sub-ranges of about 4,219 first tokens
+    leave second-level ranges of 66 children, which take one step of the
+    64-ary search; every child of two sub-ranges, the odd tokens between them
+    and the block's ends, by host load and after a merge, against the
+    radix-tree oracle."""
+    import torch
+    rng = np.random.default_rng(270000)
+    n = 270000
+    P = 2
+    kids = np.sort(rng.choice(np.arange(0, 4 * n, 2), n, replace=False)).astype(np.int64)
+    head = [77, 78]
+    seqs = [head + [int(t), 9] for t in kids.tolist()]
+    owners = [i % P for i in range(n)]
+    snap = W.from_lists(seqs, owners)
+    qs = []
+    for k in (5, 63):
+        lo, hi = (k * n) // 64, n if k == 63 else ((k + 1) * n) // 64
+        for r in range(lo, hi):
+            qs.append(head + [int(kids[r]), 9])
+            qs.append(head + [int(kids[r]) + 1])
+    qs += [head + [int(kids[0]) - 1], head + [int(kids[-1]) + 1], head + [int(kids[0])], head]
+    queries = W.from_lists(qs)
+    o = radix_for(snap, P)
+    m_or, c_or = o.route(queries.tokens, queries.offsets, nthreads())
+    f = _forest(snap, P)
+    m, c = gpu_route(f, queries, "block of 270,000 children: host load")
+    assert_rows_equal(m, c, m_or, c_or, what="270,000 children, host load")
+    # a merge rebuilds the block (new children between the old ones)
+    new = [head + [int(t) + 1, 4] for t in kids[::97].tolist()]
+    ins = W.from_lists(new, [1] * len(new))
+    announce(f"block of 270,000 children: merge of {len(ins)}")
+    dev = device()
+    f.merge(torch.from_numpy(ins.peer).to(dev), torch.from_numpy(ins.tokens).to(dev),
+            torch.from_numpy(ins.offsets).to(dev))
+    o.merge(ins.peer, ins.tokens, ins.offsets)
+    q2 = W.from_lists(qs + new[:2000])
+    m, c = gpu_route(f, q2, "block of 270,000 children after a merge")
+    m_or, c_or = o.route(q2.tokens, q2.offsets, nthreads())
+    assert_rows_equal(m, c, m_or, c_or, what="270,000 children after a merge")
+    f.check()
+    o.close()
+    f.close()

@@ -2,12 +2,12 @@
 serving loop of small batches: the launch reads its inputs from fixed
 buffers, so each replay routes whatever batch was copied there.  Every
 replay, with eager routes and host waits between them, must equal the eager
-route of the same batch."""
+route of the same batch and the CPU oracle's."""
 import numpy as np
 import pytest
 
 import workloads as W
-from gpu_util import announce, assert_rows_equal, device, gpu_route, to_dev
+from gpu_util import announce, assert_rows_equal, device, gpu_route, nthreads, oracle_for, radix_for, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -50,6 +50,7 @@ def test_route_replayed_from_a_graph():
         qt[:int(x.offsets[-1])].copy_(torch.from_numpy(x.tokens))
         qo.copy_(torch.from_numpy(x.offsets))
 
+    o = oracle_for(w.snapshot, P)
     # the first route builds and uploads the forest; capture needs it built
     fill(batches[0])
     f.route(qt, qo, ml, ch)
@@ -66,6 +67,9 @@ def test_route_replayed_from_a_graph():
         m, c = ml.cpu().numpy().copy(), ch.cpu().numpy().copy()
         m_ref, c_ref = gpu_route(f, x, f"eager reference of replay {i}")
         assert_rows_equal(m, c, m_ref, c_ref, what=f"graph replay {i}")
+        m_or, c_or = o.route(x.tokens, x.offsets, 4)
+        assert_rows_equal(m, c, m_or, c_or, what=f"graph replay {i} against the oracle")
+    o.close()
     f.close()
 
 
@@ -114,7 +118,8 @@ def test_select_replayed_from_a_graph():
 @pytest.mark.timeout(600)
 def test_long_batch_captured_in_index_order():
     """A batch that an eager route takes longest first is captured in index
-    order (no order buffer, event or wait under capture): same rows."""
+    order (no order buffer, event or wait under capture): same rows, which
+    equal the radix-tree oracle's."""
     import torch
     from test_route_gpu import _forest, _long_batch, _long_forest
     rng = np.random.default_rng(808)
@@ -123,6 +128,10 @@ def test_long_batch_captured_in_index_order():
     x = _long_batch(rng, prefixes, 8192 + 40, 4096, 6000)
     f = _forest(snap, P)
     m_ref, c_ref = gpu_route(f, x, "eager, longest first")
+    o = radix_for(snap, P)
+    m_or, c_or = o.route(x.tokens, x.offsets, nthreads())
+    o.close()
+    assert_rows_equal(m_ref, c_ref, m_or, c_or, what="long batch, eager route against the oracle")
     qt, qo = to_dev(x)
     ml = torch.empty((len(x), P), dtype=torch.int32, device=device())
     ch = torch.empty(len(x), dtype=torch.int32, device=device())

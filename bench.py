@@ -101,7 +101,7 @@ def log(msg: str) -> None:
 
 def cpu_threads() -> int:
     """Threads for the CPU oracle: the CPUs this process may run on, at most 16
-    (one GPU's share of the host on the GPU machines)."""
+    (one GPU's share of a host with several GPUs)."""
     return max(1, min(16, host_cpus()["affinity"]))
 
 

@@ -285,22 +285,35 @@ def bench_stream(args, dev) -> dict:
     merge_s = {d: np.zeros(n_steps) for d in dists}
     t_region = time.perf_counter()
 
+    # lookups: each forest's own stream, or one stream both forests' lookups
+    # queue on in turn (--schedule shared)
+    look_s = torch.cuda.Stream(device=dev) if args.schedule == "shared" else None
+    last_lookup = {d: None for d in dists}
+
     def run_steps(d, ks):
         f, s = forests[d], streams[d]
+        ls = look_s if look_s is not None else s
         for k in ks:
             if args.schedule == "serial":
                 s.synchronize()  # the previous lookup is done: the merge's wall time is its own
+            if look_s is not None and last_lookup[d] is not None:
+                s.wait_event(last_lookup[d])  # the merge changes records that lookup reads
             t0 = time.perf_counter()
             f.merge(*idev[d][k], stream=s)  # returns when the forest holds the batch
             merge_s[d][k] = time.perf_counter() - t0
+            if look_s is not None:
+                ls.wait_stream(s)
             qt, qo = qdev[d][k % R]
             if k >= Wu:
                 a, b = ev[d][k - Wu]
-                a.record(s)
-                f.route(qt, qo, *outs[d][k - Wu], stream=s)
-                b.record(s)
+                a.record(ls)
+                f.route(qt, qo, *outs[d][k - Wu], stream=ls)
+                b.record(ls)
             else:
-                f.route(qt, qo, *warm_out, stream=s)
+                f.route(qt, qo, *warm_out, stream=ls)
+            if look_s is not None:
+                last_lookup[d] = torch.cuda.Event()
+                last_lookup[d].record(ls)
 
     cu_split = None
     if args.schedule == "cusplit":
@@ -334,7 +347,7 @@ def bench_stream(args, dev) -> dict:
                     f.route(qt, qo, *warm_out, stream=lstream)
                 last_lookup[d] = torch.cuda.Event()
                 last_lookup[d].record(lstream)
-    elif args.schedule == "threads":
+    elif args.schedule in ("threads", "shared"):
         # one host thread per forest (the library's calls release the
         # interpreter lock): each forest's merge, then lookup, on its own
         # stream, while the other forest's run beside them
@@ -345,7 +358,7 @@ def bench_stream(args, dev) -> dict:
         def worker(d):
             try:
                 run_steps(d, range(Wu))
-                streams[d].synchronize()
+                torch.cuda.synchronize()
                 barrier.wait()
                 barrier.wait()  # the main thread has started the clock
                 run_steps(d, range(Wu, n_steps))
@@ -864,8 +877,10 @@ def main() -> int:
     ap.add_argument("--latency", action="store_true",
                     help="also time small batches (1 to 32,768 queries) per call, host wall time included "
                          "(configs 1-4)")
-    ap.add_argument("--schedule", choices=("cusplit", "threads", "pipelined", "serial"), default="threads",
-                    help="config 5: cusplit: one host thread, lookups on a stream over most CUs and merges on a "
+    ap.add_argument("--schedule", choices=("shared", "cusplit", "threads", "pipelined", "serial"), default="threads",
+                    help="config 5: shared: a host thread and merge stream per forest, both forests' lookups "
+                         "queued in turn on one stream, so each merge runs beside the other forest's lookup; "
+                         "cusplit: one host thread, lookups on a stream over most CUs and merges on a "
                          "stream over the CUs kept from it (--merge-cus per XCD), each forest's merge beside the "
                          "other forest's lookup; threads (default): a stream and a host thread per forest; "
                          "pipelined: two streams, one host thread issuing each forest's merge while the other's "
@@ -916,7 +931,9 @@ def main() -> int:
                        "queries_per_step": r["queries_per_step"], "inserts_per_step": r["inserts_per_step"],
                        "step": "for each topic distribution (uniform, Zipf 1.2): merge a fresh 10,000-insert batch "
                                "into its forest, then route a 1,048,576-query lookup batch on it; "
-                               + {"cusplit": "one host thread; lookups on a stream over {lookup_cus} CUs, merges on a "
+                               + {"shared": "a host thread and a merge stream per forest; both forests' lookups "
+                                            "queued in turn on one stream",
+                                  "cusplit": "one host thread; lookups on a stream over {lookup_cus} CUs, merges on a "
                                              "stream over the other {merge_cus}, each forest's merge beside the "
                                              "other forest's lookup".format(**(r["cu_split"] or
                                                                                {"lookup_cus": 0, "merge_cus": 0})),

@@ -129,11 +129,7 @@ __global__ __launch_bounds__(64 * kCompactWavesPerBlock) void compact_sep_kernel
     if (i >= n) return;
     const Node r = N.nodes[i];
     if (r.ct_cnt > kSepCount) N.nsep[r.ct_beg + lane] = N.ntok[r.ct_beg + PR_SEP_INDEX(lane, r.ct_cnt)];
-    if (r.ct_cnt >= kSep2Min)
-        for (int k = 0; k < kSepCount; k++) {
-            const int32_t lo = PR_SEP_INDEX(k, r.ct_cnt), span = PR_SEP_HI(k, r.ct_cnt) - lo;
-            N.nsep[r.ct_beg + kSepCount + kSepCount * k + lane] = N.ntok[r.ct_beg + lo + PR_SEP_INDEX(lane, span)];
-        }
+    if (r.ct_cnt >= kSep2Min) sep2_write(N.nsep + r.ct_beg, N.ntok + r.ct_beg, r.ct_cnt, lane);
 }
 
 }  // namespace pr

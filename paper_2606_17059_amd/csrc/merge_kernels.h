@@ -158,6 +158,23 @@ __device__ __forceinline__ void m_mark(const DevForest &F, int32_t x, uint64_t m
         atomicMax(&F.ltime[x], F.now);
 }
 
+// Second-level separators of a block of cnt >= kSep2Min children whose first
+// tokens are tok[0, cnt): every sub-range's 64, sixteen sub-ranges' loads
+// issued before their stores (the two arrays share an allocation, so the
+// compiler would otherwise wait for each store before the next load).
+__device__ __forceinline__ void sep2_write(int32_t *sep, const int32_t *tok, int32_t cnt, int lane) {
+    for (int q0 = 0; q0 < kSepCount; q0 += 16) {
+        int32_t v[16];
+#pragma unroll
+        for (int u = 0; u < 16; u++) {
+            const int32_t lo = PR_SEP_INDEX(q0 + u, cnt), span = PR_SEP_HI(q0 + u, cnt) - lo;
+            v[u] = tok[lo + PR_SEP_INDEX(lane, span)];
+        }
+#pragma unroll
+        for (int u = 0; u < 16; u++) sep[kSepCount + kSepCount * (q0 + u) + lane] = v[u];
+    }
+}
+
 // Child of node x whose first token is t, or -1 (wave-cooperative).  Blocks
 // of up to 64 children take one ballot over their first tokens; wider blocks
 // first pick their sub-range through the block's 64 separators (and, from
@@ -350,12 +367,20 @@ __device__ __forceinline__ void copy_tokens(int32_t *dst, const int32_t *src, in
 // block, which the lower part of the edge takes along.  reset_round: also
 // clear the round's counters for the next walk (every kernel that reads them
 // has finished; this one only allocates), which saves a launch per round.
-__global__ __launch_bounds__(64 *kMergeWavesPerBlock) void split_apply_kernel(DevForest F, Batch B,
-                                                                             InsState *st,
-                                                                             MergeCounters *ctr,
-                                                                             long long stamp, int reset_round) {
+// Waves per workgroup of split_apply_kernel: a workgroup takes one allocation
+// of records and one of pool tokens for all its winners (two atomics on the
+// merge's counters instead of two per winner, which serialise on their two
+// addresses when a batch cuts thousands of edges).
+constexpr int kSplitWaves = 16;
+
+__global__ __launch_bounds__(64 *kSplitWaves) void split_apply_kernel(DevForest F, Batch B, InsState *st,
+                                                                     MergeCounters *ctr, long long stamp,
+                                                                     int reset_round) {
+    __shared__ unsigned long long s_need[2][kSplitWaves];  // records, pool tokens per wave
+    __shared__ unsigned long long s_base[2];
     const int lane = (int)(threadIdx.x & 63);
-    const int64_t i = m_wave_index();
+    const int wv = uniform((int32_t)(threadIdx.x / 64));
+    const int64_t i = (int64_t)blockIdx.x * kSplitWaves + wv;
     if (reset_round && blockIdx.x == 0 && threadIdx.x == 0) {
         ctr->n_add = 0;
         ctr->n_split = 0;
@@ -365,20 +390,48 @@ __global__ __launch_bounds__(64 *kMergeWavesPerBlock) void split_apply_kernel(De
         ctr->plan_n = 0;
         ctr->plan_fallback = 0;
     }
-    if (i >= B.n || st[i].kind != kInsSplit) return;
-    InsState r = st[i];
-    r.c = current_pos(F, r.c, stamp);
-    if (F.nodes[r.c].aux != (int32_t)(INT32_MAX - i)) return;  // another insert cuts c this round
-    const int32_t *s = B.tokens + B.offsets[i];
-    const int64_t len = B.offsets[i + 1] - B.offsets[i];
-    const int64_t rest = len - (int64_t)r.d - r.l;  // tokens after the cut (0: ends at the cut)
-    const int32_t k = rest > 0 ? 2 : 1;
-    if (r.l <= 0) {  // a first-token match guarantees l >= 1; refuse anything else
-        if (lane == 0) atomicAdd(&ctr->overflow, 1ull);
-        return;
+    // every wave reaches the workgroup's allocation below; only the winner of
+    // its edge's claim takes a share
+    bool win = false;
+    InsState r{};
+    const int32_t *s = nullptr;
+    int64_t rest = 0;  // tokens after the cut (0: the insert ends at the cut)
+    int32_t k = 0;
+    if (i < B.n && st[i].kind == kInsSplit) {
+        r = st[i];
+        r.c = current_pos(F, r.c, stamp);
+        if (F.nodes[r.c].aux == (int32_t)(INT32_MAX - i)) {  // else another insert cuts c this round
+            s = B.tokens + B.offsets[i];
+            rest = B.offsets[i + 1] - B.offsets[i] - (int64_t)r.d - r.l;
+            k = rest > 0 ? 2 : 1;
+            if (r.l > 0)
+                win = true;
+            else if (lane == 0)  // a first-token match guarantees l >= 1; refuse anything else
+                atomicAdd(&ctr->overflow, 1ull);
+        }
     }
-    const int64_t nb = (int64_t)wave_atomic_add(&ctr->n_nodes, (unsigned long long)k, lane);
-    const int64_t pb = rest > 0 ? (int64_t)wave_atomic_add(&ctr->n_pool, (unsigned long long)rest, lane) : 0;
+    if (lane == 0) {
+        s_need[0][wv] = win ? (unsigned long long)k : 0ull;
+        s_need[1][wv] = win && rest > 0 ? (unsigned long long)rest : 0ull;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        unsigned long long tn = 0, tp = 0;
+        for (int w = 0; w < kSplitWaves; w++) {
+            tn += s_need[0][w];
+            tp += s_need[1][w];
+        }
+        s_base[0] = tn ? atomicAdd(&ctr->n_nodes, tn) : 0ull;
+        s_base[1] = tp ? atomicAdd(&ctr->n_pool, tp) : 0ull;
+    }
+    __syncthreads();
+    if (!win) return;
+    int64_t nb = (int64_t)s_base[0], pb = (int64_t)s_base[1];
+    for (int w = 0; w < wv; w++) {
+        nb += (int64_t)s_need[0][w];
+        pb += (int64_t)s_need[1][w];
+    }
+    if (rest <= 0) pb = 0;  // no pool span
     if (nb + k > F.cap_nodes || pb + rest > F.cap_pool) {
         // refused: nothing is written, the claim is withdrawn, and the insert
         // walks again once the host has grown the forest
@@ -1173,10 +1226,7 @@ __global__ __launch_bounds__(64 *kMergeWavesPerBlock) void add_sep_kernel(DevFor
         if (c <= kSepCount) continue;
         F.nsep[nb + lane] = F.ntok[nb + PR_SEP_INDEX(lane, c)];
         if (c < kSep2Min) continue;
-        for (int q = 0; q < kSepCount; q++) {  // second level, per sub-range
-            const int32_t lo = PR_SEP_INDEX(q, c), span = PR_SEP_HI(q, c) - lo;
-            F.nsep[nb + kSepCount + kSepCount * q + lane] = F.ntok[nb + lo + PR_SEP_INDEX(lane, span)];
-        }
+        sep2_write(F.nsep + nb, F.ntok + nb, c, lane);
     }
 }
 

@@ -193,6 +193,7 @@ constexpr int kDeviceRounds = 2;     // merge rounds queued before the first rea
 
 unsigned grid_threads(int64_t n, int bs) { return (unsigned)((n + bs - 1) / bs); }
 unsigned grid_waves(int64_t n) { return (unsigned)((n + pr::kMergeWavesPerBlock - 1) / pr::kMergeWavesPerBlock); }
+unsigned grid_split(int64_t n) { return (unsigned)((n + pr::kSplitWaves - 1) / pr::kSplitWaves); }
 
 template <typename T>
 bool dalloc(pr_forest *f, T **p, int64_t count) {
@@ -999,8 +1000,8 @@ pr_status run_merge(pr_forest *f, const int32_t *peer_of, const int32_t *tokens,
             hipLaunchKernelGGL(pr::add_fix_kernel, dim3(grid_threads(std::min<int64_t>(n, pr::kPlanMax), bs)),
                                dim3(bs), 0, s, F, m.keys_out, (int64_t)-1, m.grp_nw, m.grp_nb, stamp, f->d_ctr);
             hipLaunchKernelGGL(pr::split_claim_kernel, dim3(grid_threads(n, bs)), dim3(bs), 0, s, F, B, m.st, stamp);
-            hipLaunchKernelGGL(pr::split_apply_kernel, dim3(grid_waves(n)), dim3(wb), 0, s, F, B, m.st, f->d_ctr,
-                               stamp, 1);
+            hipLaunchKernelGGL(pr::split_apply_kernel, dim3(grid_split(n)), dim3(64 * pr::kSplitWaves), 0, s, F, B,
+                               m.st, f->d_ctr, stamp, 1);
         }
         hipLaunchKernelGGL(pr::merge_walk_kernel, dim3(grid_waves(n)), dim3(wb), 0, s, F, B, m.st, f->d_ctr);
         hipLaunchKernelGGL(pr::merge_tally_kernel,
@@ -1118,8 +1119,8 @@ pr_status run_merge(pr_forest *f, const int32_t *peer_of, const int32_t *tokens,
             const pr::DevForest F = dev_view(f);
             hipLaunchKernelGGL(pr::split_claim_kernel, dim3(grid_threads(n, bs)), dim3(bs), 0, s, F, B, m.st,
                                add_stamp);
-            hipLaunchKernelGGL(pr::split_apply_kernel, dim3(grid_waves(n)), dim3(wb), 0, s, F, B, m.st, f->d_ctr,
-                               add_stamp, 0);
+            hipLaunchKernelGGL(pr::split_apply_kernel, dim3(grid_split(n)), dim3(64 * pr::kSplitWaves), 0, s, F, B,
+                               m.st, f->d_ctr, add_stamp, 0);
         }
         if (hipGetLastError() != hipSuccess) return fail(PR_EDEVICE, "merge launch failed");
     }

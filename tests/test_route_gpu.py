@@ -758,3 +758,59 @@ def test_child_block_past_the_second_separator_level():
     f.check()
     o.close()
     f.close()
+
+
+@pytest.mark.parametrize("P", [32, 96, 160])
+def test_rows_of_whole_lines_with_a_partial_mask_word(P):
+    """Rows of P a multiple of 32 are stored non-temporally through a buffer
+    range of the row; with P = 96 or 160 the last mask word is only partly
+    used, and its lanes past the row must store nothing (the next row is
+    another query's).  Every row against the oracle, also through the route
+    without allocation."""
+    import torch
+    for sd in range(3):
+        w = W.tiny_random(sd, num_peers=P, vocab=3, max_seqs=4, n_queries=131)
+        f = _forest(w.snapshot, P)
+        m, c = gpu_route(f, w.queries, f"rows of whole lines P={P} seed={sd}")
+        o = oracle_for(w.snapshot, P)
+        m_or, c_or = o.route(w.queries.tokens, w.queries.offsets, 2)
+        assert_rows_equal(m, c, m_or, c_or, what=f"P={P} seed={sd}")
+        qt, qo = to_dev(w.queries)
+        ml = torch.full((len(w.queries), P), -7, dtype=torch.int32, device=device())
+        ch = torch.full((len(w.queries),), -7, dtype=torch.int32, device=device())
+        announce(f"rows of whole lines P={P} seed={sd}: route without allocation")
+        f.route_noalloc(qt, qo, ml, ch)
+        torch.cuda.synchronize()
+        assert_rows_equal(ml.cpu().numpy(), ch.cpu().numpy(), m_or, c_or, what=f"P={P} seed={sd} noalloc")
+        o.close()
+        f.close()
+
+
+def test_route_without_allocation_on_the_wide_first_window():
+    """pr_route_noalloc on a forest that takes the 256-token first window:
+    every row equals pr_route's and the oracle's."""
+    import torch
+    rng = np.random.default_rng(2561)
+    V = 128256
+    head = rng.integers(0, V, 280).tolist()
+    seqs = [head + rng.integers(0, V, int(rng.integers(0, 90))).tolist() for _ in range(40)]
+    snap = W.from_lists(seqs, [i % 4 for i in range(40)])
+    qs = [head[:n] for n in (5, 128, 255, 256, 257, 280)]
+    qs += [s[:k] + [(s[k] + 1) % V] for s in seqs[:20] for k in (100, 260) if k < len(s)]
+    qs += [list(s) for s in seqs[20:]]
+    queries = W.from_lists(qs)
+    f = _forest(snap, 4)
+    m, c = gpu_route(f, queries, "wide first window: pr_route")
+    assert f.info()["first_window_tokens"] == 256
+    qt, qo = to_dev(queries)
+    ml = torch.full((len(queries), 4), -7, dtype=torch.int32, device=device())
+    ch = torch.full((len(queries),), -7, dtype=torch.int32, device=device())
+    announce("wide first window: route without allocation")
+    f.route_noalloc(qt, qo, ml, ch)
+    torch.cuda.synchronize()
+    assert_rows_equal(ml.cpu().numpy(), ch.cpu().numpy(), m, c, what="noalloc against pr_route")
+    o = oracle_for(snap, 4)
+    m_or, c_or = o.route(queries.tokens, queries.offsets, 2)
+    assert_rows_equal(m, c, m_or, c_or, what="wide window against the oracle")
+    o.close()
+    f.close()

@@ -153,3 +153,39 @@ def test_select_invalid_offsets_and_arguments():
     with pytest.raises(RouterError):
         f.route_select(t, torch.from_numpy(w.queries.offsets).to(dev), None, 4, False)
     f.close()
+
+
+@pytest.mark.parametrize("P", [5, 70])
+def test_select_with_the_wide_first_window(P):
+    """Selection on a forest whose root has one child with a 300-token label,
+    so routes take the 256-token first window: every row against the oracle,
+    under random eligibility, with and without a preferred local peer;
+    queries end and mismatch around both windows' edges."""
+    rng = np.random.default_rng(300 + P)
+    V = 1000 if P < 64 else 128256  # 16-bit labels, then 17-bit ones
+    head = rng.integers(0, V, 300).tolist()
+    seqs = [head + rng.integers(0, V, int(rng.integers(0, 60))).tolist() for _ in range(6 * P)]
+    owners = [i % P for i in range(len(seqs))]
+    snap = W.from_lists(seqs, owners)
+    qs = []
+    for n in (1, 64, 127, 128, 129, 200, 255, 256, 257, 300):
+        qs.append(head[:n])
+        q = list(head)
+        q[n - 1] = (q[n - 1] + 1) % V
+        qs.append(q)
+    qs += [list(s) + [3] for s in seqs[:30]]
+    queries = W.from_lists(qs)
+    f = _forest(snap, P)
+    o = oracle_for(snap, P)
+    for trial in range(3):
+        el = (rng.random(P) < [0.3, 0.7, 1.0][trial]).astype(np.uint8)
+        local = int(rng.integers(-1, P))
+        prefer = bool(trial % 2)
+        m, b1, b2 = _gpu_select(f, queries, el, local, prefer, f"wide window P={P} trial={trial}")
+        m_or, b1_or, b2_or = o.route_select(queries.tokens, queries.offsets, el, local, prefer, 2)
+        assert np.array_equal(m, m_or), f"P={P} trial={trial}: match lengths differ"
+        assert np.array_equal(b1, b1_or), f"P={P} trial={trial}: best differs"
+        assert np.array_equal(b2, b2_or), f"P={P} trial={trial}: second differs"
+    assert f.info()["first_window_tokens"] == 256
+    o.close()
+    f.close()

@@ -567,7 +567,7 @@ def test_child_blocks_wider_than_4096(n_children):
     route's child locate and in the merge walk's.
     Built by a host load, and again by a load of half the sequences followed
     by merges of the other half (new children, extensions through the wide
-    block, duplicates); every row against the oracle."""
+    block, duplicates), then compacted; every row against the oracle."""
     import torch
     rng = np.random.default_rng(n_children)
     P = 3
@@ -600,6 +600,12 @@ def test_child_blocks_wider_than_4096(n_children):
         m, c = gpu_route(g, qs, f"wide block {n_children}: after merge {k}")
         m_or, c_or = og.route(qs.tokens, qs.offsets, nthreads())
         assert_rows_equal(m, c, m_or, c_or, what=f"wide block {n_children} merge {k}")
+    # compaction rebuilds the image, separators (both levels) included
+    announce(f"wide block {n_children}: compaction")
+    before, after = g.compact()
+    assert after <= before
+    m, c = gpu_route(g, qs, f"wide block {n_children}: after compaction")
+    assert_rows_equal(m, c, m_or, c_or, what=f"wide block {n_children} compacted")
     g.check()
     g.close()
     og.close()

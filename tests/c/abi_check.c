@@ -104,6 +104,7 @@ static int device_checks(void) {
     CHECK(pr_forest_info_get(f, &info) == PR_OK);
     CHECK(info.num_peers == 3 && info.mask_words == 1 && info.num_nodes > 1 && info.pool_tokens > 0);
     CHECK(info.layout_epoch >= 1 && info.label_token_bytes == 2);
+    CHECK(info.first_window_tokens == 128); /* the root has two children (1 and 7) */
     /* merge [3 4 1] into peer 1 and [1 2 3 4 5 6] into peer 2 */
     const int32_t mt[9] = {3, 4, 1, 1, 2, 3, 4, 5, 6};
     const int64_t mo[3] = {0, 3, 9};
